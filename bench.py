@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""Benchmark of the rollout hot path on one MI355X.
+
+One step = the whole hot path over one batch: env reset, the fused L-step
+rollout (actor MLP + Gaussian sampling + env step + trajectory store) and
+GAE, on the 100-stock minute workload (4,096 envs at random day offsets,
+390-minute episodes, 1001-512-512-100 bf16 actor, market resident in HBM).
+Inputs are seeded synthetic data generated and uploaded before timing.
+
+Prints one JSON line:
+  value      env-steps/s = E * L / (time per step)
+  roofline   the fused rollout kernel against the bf16 MFMA peak (its
+             algorithmic FLOPs / its average duration, measured with HIP
+             events on its stream), plus its HBM figure (algorithmic bytes)
+  cpu_baseline  the oracle on the host cores on a bounded sample of the same
+             workload (32 envs x one 390-step episode)
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "env-steps/sec (step+actor fwd+GAE) at NASDAQ-100-minute shape; %HBM & %MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+SEED = 0x5EED0FF12C
+
+
+def algorithmic_bytes_rollout(cfg) -> int:
+    """Bytes the fused rollout must move per env-step: the next market row
+    (n prices + n*I indicators, fp32), the observation row (S elements), the
+    action (n fp32), logp, reward (fp32) and done (u8)."""
+    osz = 2 if cfg.dtype == "bf16" else 4
+    return 4 * cfg.n * (1 + cfg.n_ind) + cfg.S * osz + 4 * cfg.n + 4 + 4 + 1
+
+
+def algorithmic_bytes_gae() -> int:
+    """Per env-step: reward, value, done in; advantage, return out."""
+    return 4 + 4 + 1 + 4 + 4
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="nasdaq100",
+                    choices=["nasdaq100", "ensemble", "stress", "dow30", "tiny"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-envs", type=int, default=32)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}): the rollout "
+              "shards by env with no communication on the hot path, and this build "
+              "runs and reports the single-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2111_05188_amd import problem, tp
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    tp.load()                       # fails loudly if libtp.so is missing
+
+    cfg = W.get_config(args.workload)
+    print(f"[bench] generating {cfg.name} market ({cfg.T1} rows x {cfg.n} stocks)",
+          file=sys.stderr, flush=True)
+    t_gen = time.time()
+    mk = W.make_market(cfg)
+    t0 = W.make_t0(cfg)
+    params = W.make_actor(cfg)
+    values = W.make_values(cfg)
+    print(f"[bench] inputs ready in {time.time() - t_gen:.1f}s; uploading",
+          file=sys.stderr, flush=True)
+    pb = problem.Problem(cfg, mk, params, t0, store_obs=True, taps=False)
+    pb.set_values(values)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    for k in range(args.warmup):
+        pb.step(SEED + k)
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(K)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(K):
+        e = ev[k]
+        e[0].record(stream)
+        pb.reset(stream)
+        e[1].record(stream)
+        pb.rollout(SEED + 100 + k, 0, None, stream)
+        e[2].record(stream)
+        pb.gae(stream)
+        e[3].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_step = total_ms / K
+    t_roll = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) * 1e-3
+    t_gae = float(np.mean([e[2].elapsed_time(e[3]) for e in ev])) * 1e-3
+    t_reset = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e-3
+
+    EL = cfg.E * cfg.L
+    value = EL / (ms_step * 1e-3)
+    flops = cfg.flops_per_env_step() * EL
+    achieved_tflops = flops / t_roll / 1e12
+    roll_bytes = algorithmic_bytes_rollout(cfg) * EL
+    gae_bytes = algorithmic_bytes_gae() * EL
+    dtype = "bf16" if cfg.dtype == "bf16" else "f32"
+    peak_flops = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else 157.3
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, mk, params, t0, args.cpu_envs)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "env-steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic (seeded GBM prices, N(0,1) indicators, random-init actor)",
+        "config": {
+            "workload": {"nasdaq100": "NASDAQ-100-like minute", "ensemble": "ensemble 16 agents",
+                         "stress": "stress 65536 envs", "dow30": "DOW-30-like daily",
+                         "tiny": "tiny"}[cfg.name],
+            "stocks": cfg.n, "indicators": cfg.n_ind, "market_rows": cfg.T1,
+            "envs": cfg.E, "agents": cfg.n_agents, "rollout_len": cfg.L,
+            "actor": "-".join(str(d) for d in cfg.dims), "global_batch": cfg.E,
+            "seq_len": cfg.L, "parallelism": "envs (1 GPU)",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "rollout_kernel (fused actor + sampling + env step + store)",
+            "achieved": achieved_tflops,
+            "peak": peak_flops,
+            "unit": "TFLOP/s",
+            "frac": achieved_tflops / peak_flops,
+            "traffic": None,
+            "launch_ms": t_roll * 1e3,
+            "flops_per_launch": flops,
+            "hbm_achieved_GBs": roll_bytes / t_roll / 1e9,
+            "hbm_frac": roll_bytes / t_roll / 1e9 / PEAK_HBM_GBS,
+            "bytes_per_launch": roll_bytes,
+        },
+        "gae": {"launch_ms": t_gae * 1e3, "GBs": gae_bytes / t_gae / 1e9,
+                "hbm_frac": gae_bytes / t_gae / 1e9 / PEAK_HBM_GBS},
+        "reset_ms": t_reset * 1e3,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(cfg, mk, params, t0, n_envs):
+    """The oracle, as it stands, on a bounded sample: n_envs envs of the same
+    workload for one full episode (free-running, single thread)."""
+    import numpy as np
+
+    import oracle
+    m = oracle.market(mk.price, mk.ind, mk.row0)
+    ec = oracle.env_cfg(cfg)
+    act = oracle.actor(*params, cfg.dims, cfg.dtype == "bf16", cfg.envs_per_agent)
+    ids = np.arange(n_envs)
+    cash, sh, t = oracle.env_reset(ec, t0[ids], cfg.n)
+    print(f"[bench] oracle sample: {n_envs} envs x {cfg.L} steps", file=sys.stderr, flush=True)
+    t1 = time.time()
+    out = oracle.rollout(m, ec, act, cash, sh, t, SEED, 0, cfg.L, cfg.K_pad, env_ids=ids,
+                         want=("reward", "done"))
+    v = np.zeros((cfg.L + 1, n_envs), np.float32)
+    oracle.gae(out["reward"], v, out["done"], cfg.gamma, cfg.lam)
+    dt = time.time() - t1
+    return {"value": n_envs * cfg.L / dt, "unit": "env-steps/s", "cores": 1,
+            "kind": "oracle", "seconds": dt,
+            "sample": f"{n_envs} envs x {cfg.L} steps of the same workload (full actor), "
+                      f"free-running rollout + GAE, one thread"}
+
+
+if __name__ == "__main__":
+    main()

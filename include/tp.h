@@ -1,0 +1,229 @@
+/*
+ * tp.h -- C ABI of the MI355X (gfx950) rollout library for the
+ * FinRL-Podracer stock-trading hot path (arXiv 2111.05188).
+ *
+ * The library steps thousands of copies of the paper's stock-trading MDP in
+ * lockstep on one GPU (the batched environment of Section 4.4, "Market
+ * simulation with GPU-acceleration"), runs the actor MLP that picks every
+ * env's action, samples Gaussian actions from a counter-based Philox
+ * stream, records the trajectories in GPU memory (Section 4.4, "Replay
+ * buffer on GPU") and computes GAE advantages and returns over them.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every pointer is a DEVICE pointer owned by the caller, unless its
+ *    comment says "host".  The library never frees or retains caller
+ *    memory past the call.
+ *  - Every call only enqueues work on `stream` (a hipStream_t passed as
+ *    void*; NULL = the null stream) and returns without synchronising.
+ *  - Return value: TP_OK (0) or a negative tp_status.  On a negative return
+ *    nothing was enqueued, and tp_last_error() returns a message for the
+ *    calling thread.  Argument checks run on the host before any launch;
+ *    a launch failure reported by the HIP runtime gives TP_EHIP.  Faults
+ *    inside a kernel surface at the caller's next synchronisation.
+ *  - Pointers must be 16-byte aligned.  Input and output buffers must not
+ *    overlap, except the env state, which is read and updated in place.
+ *  - Calls on different streams with disjoint buffers are independent.
+ *    Results are deterministic: the same inputs give bitwise identical
+ *    outputs (no floating-point atomics).
+ *
+ * Layout of the market (Section 3, "State space"; row = one bar)
+ * --------------------------------------------------------------
+ *  price [T1][n]      fp32 closing prices, row-major, one row per timestep
+ *  ind   [T1][n][I]   fp32 technical indicators, stock-major within a row
+ *  Prices must lie in [2^-2, 2^13): inside that range every traded value
+ *  p*q (q <= 128) and every sum of up to 128 such values is exact in fp64,
+ *  so share counts and balances are reproducible bit for bit.
+ *
+ * Observation row (Section 3, "State space"), K_pad = S rounded up to 32,
+ * S = 1 + 2n + n*I:
+ *  [ b*cash_scale, p_t*price_scale (n), h_t*share_scale (n), ind_t (n*I),
+ *    zeros up to K_pad ]
+ *  stored as fp32 (TP_F32) or bf16 round-to-nearest-even (TP_BF16).
+ */
+#ifndef TP_H
+#define TP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TP_VERSION 1
+
+typedef enum {
+    TP_OK = 0,
+    TP_EINVAL = -1,        /* bad pointer, size, alignment or value        */
+    TP_ERANGE = -2,        /* a time index would leave the market / episode */
+    TP_EUNSUPPORTED = -3,  /* valid request outside what the kernels handle */
+    TP_EHIP = -4           /* HIP runtime error (launch, device query)      */
+} tp_status;
+
+typedef enum { TP_F32 = 0, TP_BF16 = 1 } tp_dtype;
+
+/* Market tensor resident in device memory (see layout above). */
+typedef struct tp_market {
+    const float *price;    /* [T1][n]                                       */
+    const float *ind;      /* [T1][n][n_ind]                                */
+    int64_t T1;            /* rows                                          */
+    int32_t n;             /* stocks, 1..128                                */
+    int32_t n_ind;         /* indicators per stock, 0..; n*n_ind <= 1024    */
+} tp_market;
+
+/* MDP constants (Section 3; fee and initial capital: Figs. 4-5 captions). */
+typedef struct tp_env_cfg {
+    int32_t hmax;          /* max shares per stock and step (Section 3,
+                              "Action space"), 1..128                       */
+    int32_t horizon;       /* episode length in steps; done is raised on the
+                              step whose index (step0 + j) equals horizon-1 */
+    double fee;            /* proportional cost, 0 <= fee < 1: a sale
+                              credits p*s*(1-fee), a purchase debits
+                              p*q*(1+fee) (the c_t of eq. (2))              */
+    double cash0;          /* initial balance b_0 >= 0                       */
+    double reward_scale;   /* r = reward_scale * (V' - V), V = b + p^T h    */
+    float cash_scale;      /* observation scales                             */
+    float price_scale;
+    float share_scale;
+} tp_env_cfg;
+
+/* Batched env state, read and updated in place (structure of arrays). */
+typedef struct tp_env_state {
+    double *cash;          /* [E] balance b                                 */
+    int32_t *shares;       /* [E][n] holdings h (>= 0)                       */
+    int64_t *t;            /* [E] current market row                         */
+    int32_t E;             /* envs, >= 1                                     */
+} tp_env_state;
+
+/* Actor: the PPO Gaussian policy (PPO is named in Section 5.2):
+ *   mu = W3 tanh(W2 tanh(W1 x + b1) + b2) + b3,  a = mu + exp(log_std) z.
+ * Parameters are fp32 masters stacked per agent; env e belongs to agent
+ * e / envs_per_agent (population of agents, Section 4.2).
+ *   W[0] [A][H1][S], W[1] [A][H2][H1], W[2] [A][n][H2]  row-major [out][in]
+ *   b[0] [A][H1],    b[1] [A][H2],     b[2] [A][n];     log_std [A][n]
+ * dtype TP_BF16 computes with bf16 (round-to-nearest-even) copies of the
+ * weights, bf16 observations and bf16 hidden activations, fp32
+ * accumulation; TP_F32 computes in fp32 throughout. */
+typedef struct tp_actor {
+    int32_t n_agents;      /* A >= 1                                         */
+    int32_t envs_per_agent;/* A * envs_per_agent == E                        */
+    int32_t dims[4];       /* {S, H1, H2, n}                                 */
+    int32_t dtype;         /* tp_dtype                                       */
+    const float *W[3];
+    const float *b[3];
+    const float *log_std;
+} tp_actor;
+
+/* Trajectory store, time-major (Section 4.4, "Replay buffer on GPU").
+ * Row j holds (obs_j, a_j, logp_j, r_j, done_j): the observation before
+ * action j, the raw sampled action, its log-probability, the reward and
+ * the episode-end flag.  Every pointer except action/logp/reward/done may
+ * be NULL to skip that output. */
+typedef struct tp_traj {
+    void *obs;             /* [L][E][ld_obs], dtype = actor dtype, or NULL   */
+    int64_t ld_obs;        /* row stride in elements: >= K_pad, % 8 == 0     */
+    float *action;         /* [L][E][n] raw actions a (before clipping)      */
+    float *logp;           /* [L][E] log pi(a_j | obs_j)                     */
+    float *reward;         /* [L][E]                                         */
+    uint8_t *done;         /* [L][E] 1 on the last step of an episode       */
+    double *cash_tap;      /* [L][E] balance after step j, or NULL          */
+    int32_t *shares_tap;   /* [L][E][n] holdings after step j, or NULL      */
+    void *obs_last;        /* [E][ld_obs] observation after the last step
+                              (the bootstrap state), or NULL                 */
+} tp_traj;
+
+/*
+ * tp_env_reset -- start an episode in every env (Section 3: the state is
+ * balance, shares, prices, indicators).
+ *   Sets cash[e] = cash0, shares[e][:] = 0, t[e] = t0[e] and, if obs0 is
+ *   not NULL, writes the observation at row t0[e] to obs0[e][0:K_pad) (pad
+ *   columns zero).  t0 is a device int64 [E].  The host cannot read t0, so
+ *   the kernel checks it: an env with t0[e] outside [0, T1-1) gets
+ *   t[e] = -1 (an invalid env: every later step or rollout leaves it
+ *   untouched and reports NaN for it) and a zero observation row.
+ *   obs_dtype: tp_dtype of obs0.
+ */
+int tp_env_reset(const tp_market *mkt, const tp_env_cfg *cfg,
+                 const tp_env_state *st, const int64_t *t0, void *obs0,
+                 int64_t ld_obs, int32_t obs_dtype, void *stream);
+
+/*
+ * tp_env_step -- one transition of every env with caller-supplied raw
+ * actions (Section 3, eqs. (2)-(4); teacher forcing).
+ *   action [E][n] fp32 raw actions; u = clip(a, -1, 1) (NaN -> 0),
+ *   k = trunc(u * hmax) shares (fp32 product, toward zero).  All sells
+ *   (s = min(-k, h)) execute first at p_t, then buys in ascending stock
+ *   index, each the largest q <= k the balance still covers with fees.
+ *   reward [E] = reward_scale * (V(t+1) - V(t)); the state advances one
+ *   row; if obs_next is not NULL the new observation is written there
+ *   ([E][ld_obs], obs_dtype).
+ *   Every t[e] + 1 must be < T1: the host cannot read device t, so the
+ *   kernel checks it; an env with t[e] < 0 or t[e] + 1 >= T1 is left
+ *   unchanged, gets reward NaN and (if requested) a NaN observation row.
+ */
+int tp_env_step(const tp_market *mkt, const tp_env_cfg *cfg,
+                const tp_env_state *st, const float *action, float *reward,
+                void *obs_next, int64_t ld_obs, int32_t obs_dtype,
+                void *stream);
+
+/*
+ * tp_actor_packed_bytes / tp_actor_pack -- convert the actor's fp32 masters
+ * into the kernel's tiled layout (bf16 round-to-nearest-even copies for
+ * TP_BF16) in a caller-owned device buffer of tp_actor_packed_bytes()
+ * bytes.  Call again after every parameter update: tp_rollout reads only
+ * the packed copy.  tp_actor_packed_bytes returns 0 for an invalid actor.
+ */
+size_t tp_actor_packed_bytes(const tp_actor *actor);
+int tp_actor_pack(const tp_actor *actor, void *packed, size_t packed_bytes,
+                  void *stream);
+
+/*
+ * tp_rollout -- L lockstep steps of the batched env driven by the actor
+ * (the worker's exploration pass, Section 4.3; batch mode, Section 4.4).
+ *   For j = 0..L-1 and every env e (agent g = e / envs_per_agent):
+ *     obs_j  from the current state and market row t;
+ *     mu     = actor_g(obs_j);
+ *     z_i    = Box-Muller normals from Philox4x32-10 with counter
+ *              (i/4, e, step0+j, g) and key (seed low 32, seed high 32);
+ *              the 4 uniforms u = ((w >> 9) + 0.5) 2^-23 of one counter
+ *              give two pairs (u0,u1), (u2,u3); stock i takes z_{i mod 4};
+ *     a      = mu + exp(log_std) z;  logp = sum(-z^2/2 - log_std)
+ *              - (n/2) ln(2 pi);
+ *     the env step of tp_env_step with a;  done = (step0+j+1 == horizon).
+ *   One kernel launch runs all L steps.  step0 is the episode step of the
+ *   state on entry (it selects the random stream), so a rollout split into
+ *   pieces with matching step0 reproduces the unsplit one bit for bit.
+ *   Requires step0 + L <= horizon.  Device-side t is not visible to the
+ *   host: an env with t < 0 or t + L > T1 - 1 is not stepped (its state is
+ *   left unchanged and its trajectory rows are NaN / done = 0).  `packed` must come from tp_actor_pack with the same
+ *   actor shape.
+ */
+int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg,
+               const tp_env_state *st, const tp_actor *actor,
+               const void *packed, size_t packed_bytes, uint64_t seed,
+               uint64_t step0, int32_t L, const tp_traj *traj, void *stream);
+
+/*
+ * tp_gae -- generalized advantage estimation over a rollout (PPO's
+ * estimator; discounting as in eq. (1), gamma from Table 2).
+ *   reward, done, adv, ret [L][E]; value [L+1][E] (row L = bootstrap).
+ *   delta_j = r_j + gamma (1-d_j) V_{j+1} - V_j;
+ *   A_j = delta_j + gamma lambda (1-d_j) A_{j+1} (A_L = 0);  ret_j = A_j + V_j.
+ *   Accumulates in fp64, stores fp32.  0 < gamma <= 1, 0 <= lambda <= 1.
+ */
+int tp_gae(const float *reward, const float *value, const uint8_t *done,
+           int32_t L, int32_t E, float gamma, float lambda, float *adv,
+           float *ret, void *stream);
+
+/* Message for the last non-OK return on the calling thread ("" if none). */
+const char *tp_last_error(void);
+
+/* TP_VERSION of the built library. */
+int tp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TP_H */

@@ -1,0 +1,365 @@
+// C-ABI entry points (include/tp.h): host-side argument checks, error
+// reporting, parameter layout and kernel dispatch.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <map>
+#include <mutex>
+#include <string>
+
+#include "internal.hpp"
+#include "tp.h"
+
+using namespace tpk;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int ok()
+{
+    g_err.clear();
+    return TP_OK;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    return fail(TP_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int check_market(const tp_market *m)
+{
+    if (!m) return fail(TP_EINVAL, "market is NULL");
+    if (!m->price) return fail(TP_EINVAL, "market.price is NULL");
+    if (m->n < 1 || m->n > 128) return fail(TP_EINVAL, "market.n = %d outside 1..128", m->n);
+    if (m->n_ind < 0) return fail(TP_EINVAL, "market.n_ind = %d < 0", m->n_ind);
+    if ((int64_t)m->n * m->n_ind > 16384)
+        return fail(TP_EUNSUPPORTED, "market.n * n_ind = %lld > 16384", (long long)m->n * m->n_ind);
+    if (m->n_ind > 0 && !m->ind) return fail(TP_EINVAL, "market.ind is NULL");
+    if (m->T1 < 2) return fail(TP_EINVAL, "market.T1 = %lld < 2", (long long)m->T1);
+    if (!aligned(m->price, 4) || !aligned(m->ind, 4))
+        return fail(TP_EINVAL, "market arrays are not 4-byte aligned");
+    return TP_OK;
+}
+
+int check_cfg(const tp_env_cfg *c)
+{
+    if (!c) return fail(TP_EINVAL, "env cfg is NULL");
+    if (c->hmax < 1 || c->hmax > 128) return fail(TP_EINVAL, "cfg.hmax = %d outside 1..128", c->hmax);
+    if (c->horizon < 1) return fail(TP_EINVAL, "cfg.horizon = %d < 1", c->horizon);
+    if (!(c->fee >= 0.0 && c->fee < 1.0)) return fail(TP_EINVAL, "cfg.fee = %g outside [0,1)", c->fee);
+    if (!(c->cash0 >= 0.0) || !std::isfinite(c->cash0))
+        return fail(TP_EINVAL, "cfg.cash0 = %g is negative or not finite", c->cash0);
+    if (!std::isfinite(c->reward_scale)) return fail(TP_EINVAL, "cfg.reward_scale is not finite");
+    if (!std::isfinite(c->cash_scale) || !std::isfinite(c->price_scale) ||
+        !std::isfinite(c->share_scale))
+        return fail(TP_EINVAL, "cfg observation scales are not finite");
+    return TP_OK;
+}
+
+int check_state(const tp_env_state *s, int n)
+{
+    if (!s) return fail(TP_EINVAL, "state is NULL");
+    if (s->E < 1) return fail(TP_EINVAL, "state.E = %d < 1", s->E);
+    if (!s->cash || !s->shares || !s->t) return fail(TP_EINVAL, "state array is NULL");
+    if (!aligned(s->cash, 8) || !aligned(s->t, 8) || !aligned(s->shares, 4))
+        return fail(TP_EINVAL, "state arrays are not naturally aligned");
+    (void)n;
+    return TP_OK;
+}
+
+int K_pad_of(const tp_market *m) { return (1 + 2 * m->n + m->n * m->n_ind + 31) / 32 * 32; }
+
+int check_obs(const void *obs, int64_t ld, int dtype, int K_pad, const char *what)
+{
+    if (!obs) return TP_OK;
+    if (dtype != TP_F32 && dtype != TP_BF16) return fail(TP_EINVAL, "%s: bad dtype %d", what, dtype);
+    if (ld < K_pad || ld % 8 != 0)
+        return fail(TP_EINVAL, "%s: ld_obs = %lld must be >= K_pad = %d and a multiple of 8", what,
+                    (long long)ld, K_pad);
+    if (!aligned(obs, 16)) return fail(TP_EINVAL, "%s: not 16-byte aligned", what);
+    return TP_OK;
+}
+
+EnvConst make_env(const tp_market *m, const tp_env_cfg *c)
+{
+    EnvConst e;
+    e.price = m->price;
+    e.ind = m->ind;
+    e.T1 = m->T1;
+    e.n = m->n;
+    e.nI = m->n * m->n_ind;
+    e.K_pad = K_pad_of(m);
+    e.hmax = c->hmax;
+    e.horizon = c->horizon;
+    e.f_s = 1.0 - c->fee;
+    e.f_b = 1.0 + c->fee;
+    e.reward_scale = c->reward_scale;
+    e.cash0 = c->cash0;
+    e.cash_scale = c->cash_scale;
+    e.price_scale = c->price_scale;
+    e.share_scale = c->share_scale;
+    return e;
+}
+
+struct PackSig {
+    int dims[4], dtype, n_agents;
+    size_t total;
+};
+
+std::mutex g_mu;
+std::map<const void *, PackSig> g_packed;
+
+int check_actor(const tp_actor *a, PackedLayout *lay)
+{
+    if (!a) return fail(TP_EINVAL, "actor is NULL");
+    if (a->n_agents < 1 || a->envs_per_agent < 1)
+        return fail(TP_EINVAL, "actor.n_agents = %d, envs_per_agent = %d must be >= 1", a->n_agents,
+                    a->envs_per_agent);
+    if (a->dtype != TP_F32 && a->dtype != TP_BF16)
+        return fail(TP_EINVAL, "actor.dtype = %d", a->dtype);
+    for (int l = 0; l < 3; ++l)
+        if (!a->W[l] || !a->b[l]) return fail(TP_EINVAL, "actor W[%d] or b[%d] is NULL", l, l);
+    if (!a->log_std) return fail(TP_EINVAL, "actor.log_std is NULL");
+    const int S = a->dims[0], H1 = a->dims[1], H2 = a->dims[2], n = a->dims[3];
+    if (S < 1 || H1 < 1 || H2 < 1 || n < 1 || n > 128)
+        return fail(TP_EINVAL, "actor dims {%d,%d,%d,%d} invalid", S, H1, H2, n);
+    if (a->dtype == TP_BF16 && (H1 % 128 || H2 % 128))
+        return fail(TP_EUNSUPPORTED, "bf16 actor needs H1, H2 multiples of 128 (got %d, %d)", H1, H2);
+    if (a->dtype == TP_F32 && (H1 % 4 || H2 % 4))
+        return fail(TP_EUNSUPPORTED, "fp32 actor needs H1, H2 multiples of 4 (got %d, %d)", H1, H2);
+    if (!packed_layout(a, lay)) return fail(TP_EINVAL, "actor layout failed");
+    return TP_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// packed parameter layout
+// ---------------------------------------------------------------------------
+namespace tpk {
+
+bool packed_layout(const tp_actor *a, PackedLayout *L)
+{
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    L->dtype = a->dtype;
+    L->S = a->dims[0];
+    L->H1 = a->dims[1];
+    L->H2 = a->dims[2];
+    L->n = a->dims[3];
+    L->K_pad = (L->S + 31) / 32 * 32;
+    // bf16: layer-1 inputs padded to whole pipeline rounds (4 k-steps of 32)
+    const int K1 = a->dtype == TP_BF16 ? (L->S + 127) / 128 * 128 : L->K_pad;
+    const int ins[3] = {K1, L->H1, L->H2};
+    const int outs[3] = {L->H1, L->H2, L->n};
+    size_t off = 0;
+    for (int l = 0; l < 3; ++l) {
+        size_t wbytes;
+        if (a->dtype == TP_BF16) {
+            L->NT[l] = (outs[l] + 15) / 16;
+            L->KS[l] = ins[l] / 32;
+            wbytes = (size_t)L->NT[l] * L->KS[l] * 64 * 16;
+        } else {
+            L->NT[l] = outs[l];
+            L->KS[l] = ins[l] / 4;
+            wbytes = (size_t)L->KS[l] * outs[l] * 16;
+        }
+        L->off_W[l] = off;
+        // guard: the MFMA pipeline reads up to 4 k-steps (4 KiB per wave
+        // lane group) past a layer's last fragment
+        off = al(off + wbytes + (a->dtype == TP_BF16 ? 4 * 1024 : 0));
+    }
+    for (int l = 0; l < 3; ++l) {
+        const int padded = a->dtype == TP_BF16 ? L->NT[l] * 16 : outs[l];
+        L->off_b[l] = off;
+        off = al(off + (size_t)padded * 4);
+    }
+    L->off_ls = off;
+    off = al(off + (size_t)(a->dtype == TP_BF16 ? L->NT[2] * 16 : L->n) * 4);
+    L->agent_stride = off;
+    L->total = off * (size_t)a->n_agents;
+    return true;
+}
+
+}  // namespace tpk
+
+// ---------------------------------------------------------------------------
+// entry points
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char *tp_last_error(void) { return g_err.c_str(); }
+
+int tp_version(void) { return TP_VERSION; }
+
+int tp_env_reset(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *st,
+                 const int64_t *t0, void *obs0, int64_t ld_obs, int32_t obs_dtype, void *stream)
+{
+    int rc;
+    if ((rc = check_market(mkt)) || (rc = check_cfg(cfg)) || (rc = check_state(st, mkt->n)))
+        return rc;
+    if (!t0 || !aligned(t0, 8)) return fail(TP_EINVAL, "t0 is NULL or misaligned");
+    if ((rc = check_obs(obs0, ld_obs, obs_dtype, K_pad_of(mkt), "obs0"))) return rc;
+    const EnvConst c = make_env(mkt, cfg);
+    hipError_t e = launch_env_reset(c, st->cash, st->shares, st->t, t0, st->E, obs0, ld_obs,
+                                    obs_dtype == TP_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "env_reset launch");
+    return ok();
+}
+
+int tp_env_step(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *st,
+                const float *action, float *reward, void *obs_next, int64_t ld_obs,
+                int32_t obs_dtype, void *stream)
+{
+    int rc;
+    if ((rc = check_market(mkt)) || (rc = check_cfg(cfg)) || (rc = check_state(st, mkt->n)))
+        return rc;
+    if (!action || !reward) return fail(TP_EINVAL, "action or reward is NULL");
+    if (!aligned(action, 4) || !aligned(reward, 4))
+        return fail(TP_EINVAL, "action or reward misaligned");
+    if ((rc = check_obs(obs_next, ld_obs, obs_dtype, K_pad_of(mkt), "obs_next"))) return rc;
+    const EnvConst c = make_env(mkt, cfg);
+    hipError_t e = launch_env_step(c, st->cash, st->shares, st->t, action, reward, st->E, obs_next,
+                                   ld_obs, obs_dtype == TP_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "env_step launch");
+    return ok();
+}
+
+size_t tp_actor_packed_bytes(const tp_actor *actor)
+{
+    PackedLayout L;
+    if (check_actor(actor, &L)) return 0;
+    g_err.clear();
+    return L.total;
+}
+
+int tp_actor_pack(const tp_actor *actor, void *packed, size_t packed_bytes, void *stream)
+{
+    PackedLayout L;
+    int rc;
+    if ((rc = check_actor(actor, &L))) return rc;
+    if (!packed || !aligned(packed, 256)) return fail(TP_EINVAL, "packed is NULL or not 256-byte aligned");
+    if (packed_bytes < L.total)
+        return fail(TP_EINVAL, "packed_bytes = %zu < required %zu", packed_bytes, L.total);
+    hipError_t e = launch_pack(actor, L, packed, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "pack launch");
+    {
+        std::lock_guard<std::mutex> g(g_mu);
+        PackSig sig;
+        for (int i = 0; i < 4; ++i) sig.dims[i] = actor->dims[i];
+        sig.dtype = actor->dtype;
+        sig.n_agents = actor->n_agents;
+        sig.total = L.total;
+        g_packed[packed] = sig;
+    }
+    return ok();
+}
+
+int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *st,
+               const tp_actor *actor, const void *packed, size_t packed_bytes, uint64_t seed,
+               uint64_t step0, int32_t L, const tp_traj *traj, void *stream)
+{
+    int rc;
+    PackedLayout lay;
+    if ((rc = check_market(mkt)) || (rc = check_cfg(cfg)) || (rc = check_state(st, mkt->n)) ||
+        (rc = check_actor(actor, &lay)))
+        return rc;
+    const int n = mkt->n, S = 1 + 2 * n + n * mkt->n_ind;
+    if (actor->dims[0] != S || actor->dims[3] != n)
+        return fail(TP_EINVAL, "actor dims {%d,..,%d} do not match the market (S = %d, n = %d)",
+                    actor->dims[0], actor->dims[3], S, n);
+    if ((int64_t)actor->n_agents * actor->envs_per_agent != st->E)
+        return fail(TP_EINVAL, "n_agents * envs_per_agent = %lld != E = %d",
+                    (long long)actor->n_agents * actor->envs_per_agent, st->E);
+    if (L < 1) return fail(TP_EINVAL, "L = %d < 1", L);
+    if (step0 + (uint64_t)L > (uint64_t)cfg->horizon)
+        return fail(TP_ERANGE, "step0 + L = %llu exceeds the horizon %d",
+                    (unsigned long long)(step0 + L), cfg->horizon);
+    if (!traj) return fail(TP_EINVAL, "traj is NULL");
+    if (!traj->action || !traj->logp || !traj->reward || !traj->done)
+        return fail(TP_EINVAL, "traj.action/logp/reward/done must not be NULL");
+    if (!aligned(traj->action, 4) || !aligned(traj->logp, 4) || !aligned(traj->reward, 4) ||
+        !aligned(traj->cash_tap, 8) || !aligned(traj->shares_tap, 4))
+        return fail(TP_EINVAL, "traj arrays are not naturally aligned");
+    const int K_pad = K_pad_of(mkt);
+    if ((rc = check_obs(traj->obs, traj->ld_obs, actor->dtype, K_pad, "traj.obs")) ||
+        (rc = check_obs(traj->obs_last, traj->ld_obs, actor->dtype, K_pad, "traj.obs_last")))
+        return rc;
+    if (!packed) return fail(TP_EINVAL, "packed is NULL");
+    {
+        std::lock_guard<std::mutex> g(g_mu);
+        auto it = g_packed.find(packed);
+        if (it == g_packed.end())
+            return fail(TP_EINVAL, "packed buffer was not filled by tp_actor_pack");
+        const PackSig &sg = it->second;
+        for (int i = 0; i < 4; ++i)
+            if (sg.dims[i] != actor->dims[i])
+                return fail(TP_EINVAL, "packed buffer holds a different actor shape");
+        if (sg.dtype != actor->dtype || sg.n_agents != actor->n_agents)
+            return fail(TP_EINVAL, "packed buffer holds a different dtype / agent count");
+    }
+    if (packed_bytes < lay.total)
+        return fail(TP_EINVAL, "packed_bytes = %zu < required %zu", packed_bytes, lay.total);
+
+    RolloutArgs a{};
+    a.env = make_env(mkt, cfg);
+    a.cash = st->cash;
+    a.shares = st->shares;
+    a.t = st->t;
+    a.E = st->E;
+    a.packed = (const uint8_t *)packed;
+    a.lay = lay;
+    a.n_agents = actor->n_agents;
+    a.envs_per_agent = actor->envs_per_agent;
+    a.key_lo = (uint32_t)seed;
+    a.key_hi = (uint32_t)(seed >> 32);
+    a.step0 = step0;
+    a.L = L;
+    a.obs = traj->obs;
+    a.ld_obs = traj->ld_obs;
+    a.action = traj->action;
+    a.logp = traj->logp;
+    a.reward = traj->reward;
+    a.done = traj->done;
+    a.cash_tap = traj->cash_tap;
+    a.shares_tap = traj->shares_tap;
+    a.obs_last = traj->obs_last;
+    hipError_t e = launch_rollout(a, (hipStream_t)stream);
+    if (e == hipErrorInvalidConfiguration)
+        return fail(TP_EUNSUPPORTED, "rollout working set (%zu bytes of LDS) exceeds the limit",
+                    a.lds_bytes);
+    if (e != hipSuccess) return hip_fail(e, "rollout launch");
+    return ok();
+}
+
+int tp_gae(const float *reward, const float *value, const uint8_t *done, int32_t L, int32_t E,
+           float gamma, float lambda, float *adv, float *ret, void *stream)
+{
+    if (!reward || !value || !done || !adv || !ret) return fail(TP_EINVAL, "a gae array is NULL");
+    if (!aligned(reward, 4) || !aligned(value, 4) || !aligned(adv, 4) || !aligned(ret, 4))
+        return fail(TP_EINVAL, "gae arrays are not 4-byte aligned");
+    if (L < 1 || E < 1) return fail(TP_EINVAL, "L = %d, E = %d must be >= 1", L, E);
+    if (!(gamma > 0.0f && gamma <= 1.0f)) return fail(TP_EINVAL, "gamma = %g outside (0,1]", gamma);
+    if (!(lambda >= 0.0f && lambda <= 1.0f)) return fail(TP_EINVAL, "lambda = %g outside [0,1]", lambda);
+    hipError_t e = launch_gae(reward, value, done, L, E, (double)gamma,
+                              (double)gamma * (double)lambda, adv, ret, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "gae launch");
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,92 @@
+// Internal interface between the C-ABI layer (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "tp.h"
+
+namespace tpk {
+
+// MDP constants as the kernels use them (fees folded into the two factors
+// f_s = 1 - fee and f_b = 1 + fee, each rounded once to fp64).
+struct EnvConst {
+    const float *price;   // [T1][n]
+    const float *ind;     // [T1][nI]
+    int64_t T1;
+    int n;
+    int nI;               // n * n_ind
+    int K_pad;            // observation row length (multiple of 32)
+    int hmax;
+    int horizon;
+    double f_s, f_b;
+    double reward_scale;
+    double cash0;
+    float cash_scale, price_scale, share_scale;
+};
+
+// Byte layout of one agent's packed parameters inside the packed buffer.
+//  bf16: W_l as MFMA A-fragments, [NT][KS][64 lanes][8 bf16]; lane l of the
+//        block (tile t, k-step s) holds W[16t + l%16][32s + 8(l/16) + 0..7].
+//  f32 : W_l as k-blocked transposes, [in_pad/4][out][4]: entry
+//        (k4, o, e) = W[o][4 k4 + e].
+//  Biases fp32 [out padded to whole tiles]; log_std fp32 [NT3 * 16].
+struct PackedLayout {
+    int dtype;
+    int S, H1, H2, n;
+    int K_pad;
+    int NT[3];            // output tiles of 16 (bf16)
+    int KS[3];            // k-steps of 32 (bf16) / k-blocks of 4 (f32)
+    size_t off_W[3], off_b[3], off_ls;
+    size_t agent_stride;
+    size_t total;
+};
+
+bool packed_layout(const tp_actor *a, PackedLayout *out);
+
+struct RolloutArgs {
+    EnvConst env;
+    double *cash;
+    int32_t *shares;
+    int64_t *t;
+    int E;
+    const uint8_t *packed;
+    PackedLayout lay;
+    int n_agents, envs_per_agent, blocks_per_agent;
+    uint32_t key_lo, key_hi;
+    uint64_t step0;
+    int L;
+    void *obs;
+    int64_t ld_obs;
+    float *action;
+    float *logp;
+    float *reward;
+    uint8_t *done;
+    double *cash_tap;
+    int32_t *shares_tap;
+    void *obs_last;
+    // LDS carve-up (bytes / elements), filled by the launcher
+    int ldx, ldh, ldmu, ldmk;
+    int mk_vec;           // market rows are 16-byte aligned: dwordx4 DMA
+    size_t lds_X, lds_H, lds_MU, lds_MK, lds_OA, lds_OS, lds_scal, lds_bytes;
+};
+
+hipError_t launch_rollout(RolloutArgs &a, hipStream_t s);
+hipError_t launch_env_reset(const EnvConst &c, double *cash, int32_t *shares,
+                            int64_t *t, const int64_t *t0, int E, void *obs,
+                            int64_t ld_obs, int obs_bf16, hipStream_t s);
+hipError_t launch_env_step(const EnvConst &c, double *cash, int32_t *shares,
+                           int64_t *t, const float *action, float *reward,
+                           int E, void *obs, int64_t ld_obs, int obs_bf16,
+                           hipStream_t s);
+hipError_t launch_gae(const float *r, const float *v, const uint8_t *d, int L,
+                      int E, double g, double gl, float *adv, float *ret,
+                      hipStream_t s);
+hipError_t launch_pack(const tp_actor *a, const PackedLayout &lay, void *dst,
+                       hipStream_t s);
+
+// Maximum LDS per workgroup on gfx950.
+constexpr size_t LDS_LIMIT = 160 * 1024;
+
+}  // namespace tpk

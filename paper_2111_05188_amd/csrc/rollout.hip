@@ -1,0 +1,471 @@
+// Fused rollout kernel: L lockstep steps of a block of envs in one launch.
+//
+// A workgroup owns MB envs of one agent for the whole rollout (envs are
+// independent, so workgroups never synchronise with each other).  Per step:
+//   layer 1..3 of the actor on the block's observations (bf16 MFMA or fp32
+//   VALU), Philox + Box-Muller sampling, the env step, the next observation.
+// Observations, hidden activations and the action means stay in LDS; the
+// only HBM traffic is the market row of the next bar, the weights (served
+// from L2 after the first block reads them), the trajectory writes and the
+// state at entry/exit.
+//
+// Wave roles: NWM compute waves run the MLP and the per-env work (EPW envs
+// each); one IO wave moves the next market rows into LDS with
+// global_load_lds DMA and writes the previous step's trajectory rows from
+// LDS staging to HBM.  Keeping every non-weight global access in the IO
+// wave means the compute waves' in-order vmcnt waits only ever wait for
+// weight loads.
+#include "device.hpp"
+#include "env.hpp"
+#include "internal.hpp"
+
+namespace tpk {
+
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+
+// ---------------------------------------------------------------------------
+// Actor layers
+// ---------------------------------------------------------------------------
+
+// bf16 MFMA layer: Y[env][o] = act(sum_k W[o][k] X[env][k] + b[o]).
+// A operand = packed weight fragment (16 outputs x 32 k), B operand = the
+// observations (32 k x 16 envs) read from LDS; the 16x16 fp32 result gives
+// each lane 4 consecutive outputs of one env.  Wave w computes tile groups
+// g = w, w + nwaves, ... of G tiles each (NT % G == 0).  Weight fragments are
+// software-pipelined D k-steps ahead in a register ring (KS % D == 0), so a
+// wave keeps D*G KiB of weight loads in flight while its MFMAs run.
+constexpr int PIPE = 4;
+
+template <int MT, int G, bool HIDDEN, int KSC>
+__device__ __forceinline__ void mfma_layer(const bf16x8 *__restrict__ W,
+                                           const float *__restrict__ bias,
+                                           int NT, int KSr, const __bf16 *Xs,
+                                           int ldx, void *Y, int ldy, int wave,
+                                           int nwaves, int lane)
+{
+    constexpr int D = PIPE;
+    // KSC > 0: k-steps known at compile time, the k loop unrolls completely
+    // and every wait for a weight fragment is exact
+    const int KS = KSC > 0 ? KSC : KSr;
+    const int r16 = lane & 15, kq = lane >> 4;
+    for (int g0 = wave * G; g0 < NT; g0 += nwaves * G) {
+        floatx4 acc[MT][G];
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int t = 0; t < G; ++t) acc[m][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        const bf16x8 *wt[G];
+#pragma unroll
+        for (int t = 0; t < G; ++t) wt[t] = W + ((size_t)(g0 + t) * KS) * WAVE + lane;
+        const __bf16 *xb = Xs + r16 * ldx + kq * 8;
+        bf16x8 buf[D][G];
+#pragma unroll
+        for (int d = 0; d < D; ++d)
+#pragma unroll
+            for (int t = 0; t < G; ++t) buf[d][t] = wt[t][d * WAVE];
+#pragma unroll
+        for (int ks0 = 0; ks0 < (KSC > 0 ? KSC : KS); ks0 += D) {
+#pragma unroll
+            for (int d = 0; d < D; ++d) {
+                const int ks = ks0 + d;
+                bf16x8 xf[MT];
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+                    xf[m] = *(const bf16x8 *)(xb + m * 16 * ldx + ks * 32);
+#pragma unroll
+                for (int t = 0; t < G; ++t)
+#pragma unroll
+                    for (int m = 0; m < MT; ++m)
+                        acc[m][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(buf[d][t], xf[m], acc[m][t], 0, 0, 0);
+                // refill this slot with k-step ks + D.  Past a tile's last
+                // k-step this reads the next tile (or the guard the layout
+                // leaves after every layer); those values are never used.
+#pragma unroll
+                for (int t = 0; t < G; ++t) buf[d][t] = wt[t][(size_t)(ks + D) * WAVE];
+                // keep the refill here: the scheduler must not sink it next
+                // to its use D k-steps later
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < G; ++t) {
+            const int o = (g0 + t) * 16 + kq * 4;
+            const float4 bv = *(const float4 *)(bias + o);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const int env = m * 16 + r16;
+                float v0 = acc[m][t][0] + bv.x, v1 = acc[m][t][1] + bv.y;
+                float v2 = acc[m][t][2] + bv.z, v3 = acc[m][t][3] + bv.w;
+                if (HIDDEN) {
+                    bf16x4 h = {to_bf16(tanhf(v0)), to_bf16(tanhf(v1)),
+                                to_bf16(tanhf(v2)), to_bf16(tanhf(v3))};
+                    *(bf16x4 *)((__bf16 *)Y + env * ldy + o) = h;
+                } else {
+                    *(float4 *)((float *)Y + env * ldy + o) = float4{v0, v1, v2, v3};
+                }
+            }
+        }
+    }
+}
+
+// fp32 VALU layer: thread o computes output o for all MB envs; weights are
+// k-blocked transposes so consecutive threads read consecutive 16 bytes.
+template <int MB, bool HIDDEN>
+__device__ __forceinline__ void valu_layer(const float4 *__restrict__ Wt,
+                                           const float *__restrict__ bias,
+                                           int K4, int out, const float *Xs,
+                                           int ldx, float *Y, int ldy, int tid,
+                                           int nthr)
+{
+    for (int o = tid; o < out; o += nthr) {
+        float acc[MB];
+#pragma unroll
+        for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+#pragma unroll 4
+        for (int k4 = 0; k4 < K4; ++k4) {
+            const float4 w = Wt[(size_t)k4 * out + o];
+#pragma unroll
+            for (int m = 0; m < MB; ++m) {
+                const float4 x = *(const float4 *)(Xs + m * ldx + 4 * k4);
+                acc[m] = fmaf(w.x, x.x, acc[m]);
+                acc[m] = fmaf(w.y, x.y, acc[m]);
+                acc[m] = fmaf(w.z, x.z, acc[m]);
+                acc[m] = fmaf(w.w, x.w, acc[m]);
+            }
+        }
+        const float bo = bias[o];
+#pragma unroll
+        for (int m = 0; m < MB; ++m) {
+            const float v = acc[m] + bo;
+            Y[m * ldy + o] = HIDDEN ? tanhf(v) : v;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// The rollout kernel.  OT = observation element type (__bf16 with the MFMA
+// actor, float with the VALU actor).
+// ---------------------------------------------------------------------------
+template <typename OT, int EPW, int NWM, int KS1, int KS2, int KS3>
+__global__ __launch_bounds__((NWM + 1) * WAVE) void rollout_kernel(RolloutArgs A)
+{
+    constexpr int MB = EPW * NWM;
+    constexpr bool BF16 = sizeof(OT) == 2;
+    extern __shared__ __align__(16) uint8_t smem[];
+
+    const EnvConst &C = A.env;
+    const PackedLayout &P = A.lay;
+    const int n = C.n, nI = C.nI;
+    const int tid = threadIdx.x, wave = tid / WAVE, lane = tid % WAVE;
+    const bool io = wave == NWM;
+
+    // XCD-aware block order: consecutive dispatch slots of one XCD (block id
+    // mod 8) take consecutive logical blocks, so one agent's blocks share an
+    // XCD and its L2.
+    const int nb = gridDim.x;
+    const int logical = (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8;
+    if (logical >= A.n_agents * A.blocks_per_agent) return;
+    const int agent = logical / A.blocks_per_agent;
+    const int blk = logical % A.blocks_per_agent;
+    const int ebase = agent * A.envs_per_agent + blk * MB;
+    const int nenv = min(MB, A.envs_per_agent - blk * MB);
+
+    const uint8_t *pk = A.packed + (size_t)agent * P.agent_stride;
+    const float *b1 = (const float *)(pk + P.off_b[0]);
+    const float *b2 = (const float *)(pk + P.off_b[1]);
+    const float *b3 = (const float *)(pk + P.off_b[2]);
+    const float *lsd = (const float *)(pk + P.off_ls);
+
+    OT *X = (OT *)(smem + A.lds_X);            // [MB][ldx] observations (H2 aliases it)
+    OT *Hd = (OT *)(smem + A.lds_H);           // [MB][ldh] hidden layer 1
+    float *MU = (float *)(smem + A.lds_MU);    // [MB][ldmu] action means
+    float *MK = (float *)(smem + A.lds_MK);    // [MB][ldmk] next-row prices+indicators
+    float *OA = (float *)(smem + A.lds_OA);    // [MB][n] staged actions
+    int32_t *OS = (int32_t *)(smem + A.lds_OS);// [MB][n] staged holdings
+    int64_t *T0 = (int64_t *)(smem + A.lds_scal);   // [MB] start rows
+    double *OC = (double *)(T0 + MB);          // [MB] staged cash
+    float *OL = (float *)(OC + MB);            // [MB] staged logp
+    float *OR = (float *)(OL + MB);            // [MB] staged reward
+    int *ACT = (int *)(OR + MB);               // [MB] env is stepped
+
+    const int ldx = A.ldx, ldh = A.ldh, ldmu = A.ldmu, ldmk = A.ldmk;
+
+    // ---- prologue ---------------------------------------------------------
+    for (int i = tid; i < MB * ldx * (int)sizeof(OT) / 16; i += blockDim.x)
+        ((uint4 *)X)[i] = uint4{0, 0, 0, 0};
+    if (tid < MB) {
+        int64_t tt = -1;
+        int act = 0;
+        if (tid < nenv) {
+            tt = A.t[ebase + tid];
+            act = tt >= 0 && tt + A.L <= C.T1 - 1;
+        }
+        T0[tid] = tt;
+        ACT[tid] = act;
+    }
+    __syncthreads();
+
+    LaneEnv st[EPW];
+    float ls0 = 0.f, ls1 = 0.f, sg0 = 0.f, sg1 = 0.f;
+    const int i0 = 2 * lane, i1 = i0 + 1;
+    if (!io) {
+        if (i0 < n) { ls0 = lsd[i0]; sg0 = expf(ls0); }
+        if (i1 < n) { ls1 = lsd[i1]; sg1 = expf(ls1); }
+#pragma unroll
+        for (int k = 0; k < EPW; ++k) {
+            const int s = wave * EPW + k;
+            st[k] = LaneEnv{0.0, 0, 0, 0.f, 0.f};
+            if (!ACT[s]) continue;
+            const int e = ebase + s;
+            const int64_t t = T0[s];
+            const float *prow = C.price + (size_t)t * n;
+            st[k].cash = A.cash[e];
+            if (i0 < n) { st[k].h0 = A.shares[(size_t)e * n + i0]; st[k].p0 = prow[i0]; }
+            if (i1 < n) { st[k].h1 = A.shares[(size_t)e * n + i1]; st[k].p1 = prow[i1]; }
+            write_obs_row<OT>(X + s * ldx, C, st[k].cash, st[k].h0, st[k].h1, prow,
+                              C.ind + (size_t)t * nI, lane);
+        }
+    }
+    __syncthreads();
+
+    const double half_log2pi_n = 0.5 * (double)n * 1.8378770664093454836;
+    const size_t E = (size_t)A.E;
+    const size_t obs_row_bytes = (size_t)C.K_pad * sizeof(OT);
+
+    for (int j = 0; j <= A.L; ++j) {
+        // ---- IO wave: previous step's trajectory rows, next market rows ---
+        if (io) {
+            if (j > 0) {
+                const size_t row0 = (size_t)(j - 1) * E + ebase;
+                float *ga = A.action + row0 * n;
+                for (int i = lane; i < nenv * n; i += WAVE)
+                    if (ACT[i / n]) ga[i] = OA[i];
+                for (int s = lane; s < nenv; s += WAVE) {
+                    if (!ACT[s]) continue;
+                    A.logp[row0 + s] = OL[s];
+                    A.reward[row0 + s] = OR[s];
+                    A.done[row0 + s] = (uint8_t)(A.step0 + (uint64_t)(j - 1) + 1 == (uint64_t)C.horizon);
+                    if (A.cash_tap) A.cash_tap[row0 + s] = OC[s];
+                }
+                if (A.shares_tap) {
+                    int32_t *gs = A.shares_tap + row0 * n;
+                    for (int i = lane; i < nenv * n; i += WAVE)
+                        if (ACT[i / n]) gs[i] = OS[i];
+                }
+            }
+            if (j < A.L) {
+                // DMA market rows T0 + j + 1 into MK (one row per active env)
+                if (A.mk_vec) {
+                    const int cps = ldmk / 4, np4 = n / 4;
+                    const int total = MB * cps;
+                    for (int c0 = 0; c0 < total; c0 += WAVE) {
+                        const int c = c0 + lane;
+                        const int s = c / cps, part = c - s * cps;
+                        if (c < total && ACT[s]) {
+                            const int64_t t = T0[s] + j + 1;
+                            const float *src = part < np4 ? C.price + (size_t)t * n + 4 * part
+                                                          : C.ind + (size_t)t * nI + 4 * (part - np4);
+                            __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(MK + 4 * c0), 16, 0, 0);
+                        }
+                    }
+                } else {
+                    const int total = MB * ldmk;
+                    for (int c0 = 0; c0 < total; c0 += WAVE) {
+                        const int c = c0 + lane;
+                        const int s = c / ldmk, part = c - s * ldmk;
+                        if (c < total && ACT[s] && part < n + nI) {
+                            const int64_t t = T0[s] + j + 1;
+                            const float *src = part < n ? C.price + (size_t)t * n + part
+                                                        : C.ind + (size_t)t * nI + (part - n);
+                            __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(MK + c0), 4, 0, 0);
+                        }
+                    }
+                }
+            }
+            // observation rows: obs_j (j < L) or the bootstrap observation
+            OT *dst = nullptr;
+            if (j < A.L && A.obs) dst = (OT *)A.obs + ((size_t)j * E + ebase) * A.ld_obs;
+            if (j == A.L && A.obs_last) dst = (OT *)A.obs_last + (size_t)ebase * A.ld_obs;
+            if (dst) {
+                const int cpr = (int)(obs_row_bytes / 16);
+                for (int c = lane; c < nenv * cpr; c += WAVE) {
+                    const int s = c / cpr, part = c - s * cpr;
+                    if (!ACT[s]) continue;
+                    ((uint4 *)(dst + (size_t)s * A.ld_obs))[part] =
+                        ((const uint4 *)(X + s * ldx))[part];
+                }
+            }
+        }
+        if (j == A.L) break;
+
+        // ---- actor ---------------------------------------------------------
+        if constexpr (BF16) {
+            constexpr int MT = MB / 16;
+            if (!io)
+                mfma_layer<MT, 4, true, KS1>((const bf16x8 *)(pk + P.off_W[0]), b1, P.NT[0], P.KS[0],
+                                        (const __bf16 *)X, ldx, Hd, ldh, wave, NWM, lane);
+            __syncthreads();
+            if (!io)
+                mfma_layer<MT, 4, true, KS2>((const bf16x8 *)(pk + P.off_W[1]), b2, P.NT[1], P.KS[1],
+                                        (const __bf16 *)Hd, ldh, X, ldx, wave, NWM, lane);
+            __syncthreads();
+            if (!io)
+                mfma_layer<MT, 1, false, KS3>((const bf16x8 *)(pk + P.off_W[2]), b3, P.NT[2], P.KS[2],
+                                         (const __bf16 *)X, ldx, MU, ldmu, wave, NWM, lane);
+        } else {
+            if (!io)
+                valu_layer<MB, true>((const float4 *)(pk + P.off_W[0]), b1, P.KS[0], P.H1,
+                                     (const float *)X, ldx, (float *)Hd, ldh, tid, NWM * WAVE);
+            __syncthreads();
+            if (!io)
+                valu_layer<MB, true>((const float4 *)(pk + P.off_W[1]), b2, P.KS[1], P.H2,
+                                     (const float *)Hd, ldh, (float *)X, ldx, tid, NWM * WAVE);
+            __syncthreads();
+            if (!io)
+                valu_layer<MB, false>((const float4 *)(pk + P.off_W[2]), b3, P.KS[2], P.n,
+                                      (const float *)X, ldx, MU, ldmu, tid, NWM * WAVE);
+        }
+        if (io) __builtin_amdgcn_s_waitcnt(0);   // market DMA landed in MK
+        __syncthreads();
+
+        // ---- sampling, env step, next observation ---------------------------
+        if (!io) {
+            const uint32_t step = (uint32_t)(A.step0 + (uint64_t)j);
+#pragma unroll
+            for (int k = 0; k < EPW; ++k) {
+                const int s = wave * EPW + k;
+                if (!ACT[s]) continue;
+                const int e = ebase + s;
+                // Philox counter (i/4, env, step, agent): lane l owns stocks
+                // 2l, 2l+1 = counter l/2, Box-Muller pair l%2
+                const U4 w = philox4x32_10(U4{(uint32_t)(lane >> 1), (uint32_t)e, step, (uint32_t)agent},
+                                           A.key_lo, A.key_hi);
+                const bool second = lane & 1;
+                float z0, z1;
+                box_muller(uniform_open01(second ? w.z : w.x),
+                           uniform_open01(second ? w.w : w.y), z0, z1);
+                const float *mu = MU + s * ldmu;
+                float a0 = 0.f, a1 = 0.f;
+                double lp = 0.0;
+                if (i0 < n) {
+                    const float sz = sg0 * z0;
+                    a0 = mu[i0] + sz;
+                    lp += -0.5 * (double)z0 * (double)z0 - (double)ls0;
+                    OA[s * n + i0] = a0;
+                }
+                if (i1 < n) {
+                    const float sz = sg1 * z1;
+                    a1 = mu[i1] + sz;
+                    lp += -0.5 * (double)z1 * (double)z1 - (double)ls1;
+                    OA[s * n + i1] = a1;
+                }
+                lp = wave_sum(lp) - half_log2pi_n;
+                const float *mk = MK + s * ldmk;
+                const float q0 = i0 < n ? mk[i0] : 0.f, q1 = i1 < n ? mk[i1] : 0.f;
+                const float r = env_step_wave(C, st[k], a0, a1, q0, q1, lane);
+                if (lane == 0) {
+                    OL[s] = (float)lp;
+                    OR[s] = r;
+                    OC[s] = st[k].cash;
+                }
+                if (i0 < n) OS[s * n + i0] = st[k].h0;
+                if (i1 < n) OS[s * n + i1] = st[k].h1;
+                write_obs_row<OT>(X + s * ldx, C, st[k].cash, st[k].h0, st[k].h1, mk, mk + n, lane);
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- epilogue: state back to HBM; envs that were not stepped get NaN ---
+    if (!io) {
+#pragma unroll
+        for (int k = 0; k < EPW; ++k) {
+            const int s = wave * EPW + k;
+            if (!ACT[s]) continue;
+            const int e = ebase + s;
+            if (lane == 0) {
+                A.cash[e] = st[k].cash;
+                A.t[e] = T0[s] + A.L;
+            }
+            if (i0 < n) A.shares[(size_t)e * n + i0] = st[k].h0;
+            if (i1 < n) A.shares[(size_t)e * n + i1] = st[k].h1;
+        }
+    } else {
+        const float qnan = __builtin_nanf("");
+        for (int s = 0; s < nenv; ++s) {
+            if (ACT[s]) continue;
+            for (int j = 0; j < A.L; ++j) {
+                const size_t row = (size_t)j * E + ebase + s;
+                for (int i = lane; i < n; i += WAVE) A.action[row * n + i] = qnan;
+                if (lane == 0) {
+                    A.logp[row] = qnan;
+                    A.reward[row] = qnan;
+                    A.done[row] = 0;
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Launcher
+// ---------------------------------------------------------------------------
+static size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
+
+template <typename OT, int EPW, int NWM, int KS1 = 0, int KS2 = 0, int KS3 = 0>
+static hipError_t launch_cfg(RolloutArgs &a, hipStream_t s)
+{
+    constexpr int MB = EPW * NWM;
+    const EnvConst &C = a.env;
+    const PackedLayout &P = a.lay;
+    const int esz = (int)sizeof(OT);
+    if (esz == 2) {
+        const int K1 = P.KS[0] * 32;  // layer-1 inputs incl. pipeline padding
+        a.ldx = (K1 > P.H2 ? K1 : P.H2) + 8;
+        a.ldh = P.H1 + 8;
+        a.ldmu = P.NT[2] * 16;
+    } else {
+        a.ldx = (P.K_pad > P.H2 ? P.K_pad : P.H2) + 4;
+        a.ldh = P.H1 + 4;
+        a.ldmu = P.n + (4 - P.n % 4) % 4;
+    }
+    a.mk_vec = (C.n % 4 == 0) && (C.nI % 4 == 0) && ((uintptr_t)C.price % 16 == 0) &&
+               ((uintptr_t)C.ind % 16 == 0);
+    a.ldmk = C.n + C.nI;
+    if (!a.mk_vec) a.ldmk = (a.ldmk + 3) & ~3;
+    size_t off = 0;
+    a.lds_X = off;   off = align16(off + (size_t)MB * a.ldx * esz);
+    a.lds_H = off;   off = align16(off + (size_t)MB * a.ldh * esz);
+    a.lds_MU = off;  off = align16(off + (size_t)MB * a.ldmu * 4);
+    a.lds_MK = off;  off = align16(off + (size_t)MB * a.ldmk * 4);
+    a.lds_OA = off;  off = align16(off + (size_t)MB * C.n * 4);
+    a.lds_OS = off;  off = align16(off + (size_t)MB * C.n * 4);
+    a.lds_scal = off;
+    off = align16(off + (size_t)MB * (8 + 8 + 4 + 4 + 4));
+    a.lds_bytes = off;
+    if (off > LDS_LIMIT) return hipErrorInvalidConfiguration;
+    a.blocks_per_agent = (a.envs_per_agent + MB - 1) / MB;
+    int nblk = a.n_agents * a.blocks_per_agent;
+    nblk = (nblk + 7) & ~7;
+    auto k = rollout_kernel<OT, EPW, NWM, KS1, KS2, KS3>;
+    hipError_t e = hipFuncSetAttribute((const void *)k,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)off);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, dim3(nblk), dim3((NWM + 1) * WAVE), off, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_rollout(RolloutArgs &a, hipStream_t s)
+{
+    if (a.lay.dtype == TP_BF16) {
+        const int *k = a.lay.KS;
+        // fully unrolled variants for the actor shapes in use
+        if (k[0] == 32 && k[1] == 16 && k[2] == 16) return launch_cfg<__bf16, 2, 8, 32, 16, 16>(a, s);
+        if (k[0] == 32 && k[1] == 32 && k[2] == 32) return launch_cfg<__bf16, 2, 8, 32, 32, 32>(a, s);
+        return launch_cfg<__bf16, 2, 8>(a, s);
+    }
+    return launch_cfg<float, 1, 4>(a, s);
+}
+
+}  // namespace tpk

@@ -1,0 +1,266 @@
+"""Python binding of libtp.so (include/tp.h): argument marshalling only.
+
+Every function takes torch CUDA (HIP) tensors, passes their device pointers
+and the current stream to the C ABI, and raises ``TPError`` on a negative
+status.  No computation happens here; the library must be built
+(``paper_2111_05188_amd.build``) -- a missing library is an error, never a
+fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtp.so")
+
+TP_OK, TP_EINVAL, TP_ERANGE, TP_EUNSUPPORTED, TP_EHIP = 0, -1, -2, -3, -4
+TP_F32, TP_BF16 = 0, 1
+_NAMES = {TP_EINVAL: "TP_EINVAL", TP_ERANGE: "TP_ERANGE",
+          TP_EUNSUPPORTED: "TP_EUNSUPPORTED", TP_EHIP: "TP_EHIP"}
+
+
+class TPError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Market(C.Structure):
+    _fields_ = [("price", C.c_void_p), ("ind", C.c_void_p), ("T1", C.c_int64),
+                ("n", C.c_int32), ("n_ind", C.c_int32)]
+
+
+class EnvCfg(C.Structure):
+    _fields_ = [("hmax", C.c_int32), ("horizon", C.c_int32),
+                ("fee", C.c_double), ("cash0", C.c_double),
+                ("reward_scale", C.c_double), ("cash_scale", C.c_float),
+                ("price_scale", C.c_float), ("share_scale", C.c_float)]
+
+
+class EnvState(C.Structure):
+    _fields_ = [("cash", C.c_void_p), ("shares", C.c_void_p),
+                ("t", C.c_void_p), ("E", C.c_int32)]
+
+
+class Actor(C.Structure):
+    _fields_ = [("n_agents", C.c_int32), ("envs_per_agent", C.c_int32),
+                ("dims", C.c_int32 * 4), ("dtype", C.c_int32),
+                ("W", C.c_void_p * 3), ("b", C.c_void_p * 3),
+                ("log_std", C.c_void_p)]
+
+
+class Traj(C.Structure):
+    _fields_ = [("obs", C.c_void_p), ("ld_obs", C.c_int64),
+                ("action", C.c_void_p), ("logp", C.c_void_p),
+                ("reward", C.c_void_p), ("done", C.c_void_p),
+                ("cash_tap", C.c_void_p), ("shares_tap", C.c_void_p),
+                ("obs_last", C.c_void_p)]
+
+
+EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
+           "tp_actor_pack", "tp_rollout", "tp_gae", "tp_last_error",
+           "tp_version")
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libtp.so and declare its signatures (no GPU work)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run paper_2111_05188_amd/build.py")
+    L = C.CDLL(path)
+    vp, i32, i64, u64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_size_t
+    L.tp_env_reset.argtypes = [vp, vp, vp, vp, vp, i64, i32, vp]
+    L.tp_env_step.argtypes = [vp, vp, vp, vp, vp, vp, i64, i32, vp]
+    L.tp_actor_packed_bytes.argtypes = [vp]
+    L.tp_actor_packed_bytes.restype = sz
+    L.tp_actor_pack.argtypes = [vp, vp, sz, vp]
+    L.tp_rollout.argtypes = [vp, vp, vp, vp, vp, sz, u64, u64, i32, vp, vp]
+    L.tp_gae.argtypes = [vp, vp, vp, i32, i32, C.c_float, C.c_float, vp, vp, vp]
+    L.tp_last_error.restype = C.c_char_p
+    L.tp_version.restype = C.c_int
+    for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae"):
+        getattr(L, f).restype = C.c_int
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != TP_OK:
+        raise TPError(rc, load().tp_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+# --------------------------------------------------------------------------
+# structure helpers (hold references to the tensors they point at)
+# --------------------------------------------------------------------------
+
+class MarketT:
+    def __init__(self, price: torch.Tensor, ind: torch.Tensor):
+        assert price.dim() == 2 and ind.dim() == 3
+        self.price, self.ind = price, ind
+        self.s = Market(_ptr(price), _ptr(ind), price.shape[0], price.shape[1],
+                        ind.shape[2])
+
+    @property
+    def n(self):
+        return self.s.n
+
+    @property
+    def K_pad(self):
+        S = 1 + 2 * self.s.n + self.s.n * self.s.n_ind
+        return (S + 31) // 32 * 32
+
+
+def env_cfg(hmax, horizon, fee, cash0, reward_scale, cash_scale, price_scale,
+            share_scale) -> EnvCfg:
+    return EnvCfg(hmax, horizon, fee, cash0, reward_scale, cash_scale,
+                  price_scale, share_scale)
+
+
+class StateT:
+    def __init__(self, cash: torch.Tensor, shares: torch.Tensor, t: torch.Tensor):
+        self.cash, self.shares, self.t = cash, shares, t
+        self.s = EnvState(_ptr(cash), _ptr(shares), _ptr(t), cash.shape[0])
+
+    @staticmethod
+    def empty(E: int, n: int, device="cuda"):
+        return StateT(torch.zeros(E, dtype=torch.float64, device=device),
+                      torch.zeros(E, n, dtype=torch.int32, device=device),
+                      torch.zeros(E, dtype=torch.int64, device=device))
+
+
+class ActorT:
+    """fp32 master parameters stacked per agent (see tp_actor)."""
+
+    def __init__(self, W, b, log_std, dims, dtype: int, envs_per_agent: int):
+        self.W, self.b, self.log_std = list(W), list(b), log_std
+        s = Actor()
+        s.n_agents = W[0].shape[0]
+        s.envs_per_agent = envs_per_agent
+        for i in range(4):
+            s.dims[i] = dims[i]
+        s.dtype = dtype
+        for l in range(3):
+            s.W[l] = _ptr(self.W[l])
+            s.b[l] = _ptr(self.b[l])
+        s.log_std = _ptr(log_std)
+        self.s = s
+        self.packed = None
+
+    def packed_bytes(self) -> int:
+        nb = load().tp_actor_packed_bytes(C.byref(self.s))
+        if nb == 0:
+            _check(TP_EINVAL)
+        return nb
+
+    def pack(self, stream=None):
+        """(Re)build the packed copy the rollout kernel reads."""
+        nb = self.packed_bytes()
+        if self.packed is None or self.packed.numel() < nb:
+            self.packed = torch.empty(nb, dtype=torch.uint8, device=self.W[0].device)
+        _check(load().tp_actor_pack(C.byref(self.s), _ptr(self.packed), nb,
+                                    _stream(stream)))
+        return self.packed
+
+
+class TrajT:
+    def __init__(self, action, logp, reward, done, obs=None, ld_obs=0,
+                 cash_tap=None, shares_tap=None, obs_last=None):
+        self.t = (action, logp, reward, done, obs, cash_tap, shares_tap, obs_last)
+        self.s = Traj(_ptr(obs), ld_obs, _ptr(action), _ptr(logp), _ptr(reward),
+                      _ptr(done), _ptr(cash_tap), _ptr(shares_tap), _ptr(obs_last))
+
+    @staticmethod
+    def alloc(L, E, n, K_pad=None, obs_dtype=None, taps=False, obs_last=False,
+              device="cuda"):
+        kw = {}
+        if K_pad is not None:
+            ld = (K_pad + 7) // 8 * 8
+            kw["obs"] = torch.empty(L, E, ld, dtype=obs_dtype, device=device)
+            kw["ld_obs"] = ld
+            if obs_last:
+                kw["obs_last"] = torch.empty(E, ld, dtype=obs_dtype, device=device)
+        if taps:
+            kw["cash_tap"] = torch.empty(L, E, dtype=torch.float64, device=device)
+            kw["shares_tap"] = torch.empty(L, E, n, dtype=torch.int32, device=device)
+        return TrajT(torch.empty(L, E, n, dtype=torch.float32, device=device),
+                     torch.empty(L, E, dtype=torch.float32, device=device),
+                     torch.empty(L, E, dtype=torch.float32, device=device),
+                     torch.empty(L, E, dtype=torch.uint8, device=device), **kw)
+
+    action = property(lambda self: self.t[0])
+    logp = property(lambda self: self.t[1])
+    reward = property(lambda self: self.t[2])
+    done = property(lambda self: self.t[3])
+    obs = property(lambda self: self.t[4])
+    cash_tap = property(lambda self: self.t[5])
+    shares_tap = property(lambda self: self.t[6])
+    obs_last = property(lambda self: self.t[7])
+
+
+def _dtype_code(t: torch.Tensor | None, default=TP_F32) -> int:
+    if t is None:
+        return default
+    return TP_BF16 if t.dtype == torch.bfloat16 else TP_F32
+
+
+# --------------------------------------------------------------------------
+# entry points (same names as the C ABI, without the tp_ prefix)
+# --------------------------------------------------------------------------
+
+def env_reset(mkt: MarketT, cfg: EnvCfg, st: StateT, t0: torch.Tensor,
+              obs0: torch.Tensor | None = None, stream=None):
+    ld = obs0.shape[-1] if obs0 is not None else 0
+    _check(load().tp_env_reset(C.byref(mkt.s), C.byref(cfg), C.byref(st.s),
+                               _ptr(t0), _ptr(obs0), ld, _dtype_code(obs0),
+                               _stream(stream)))
+
+
+def env_step(mkt: MarketT, cfg: EnvCfg, st: StateT, action: torch.Tensor,
+             reward: torch.Tensor, obs_next: torch.Tensor | None = None,
+             stream=None):
+    ld = obs_next.shape[-1] if obs_next is not None else 0
+    _check(load().tp_env_step(C.byref(mkt.s), C.byref(cfg), C.byref(st.s),
+                              _ptr(action), _ptr(reward), _ptr(obs_next), ld,
+                              _dtype_code(obs_next), _stream(stream)))
+
+
+def rollout(mkt: MarketT, cfg: EnvCfg, st: StateT, actor: ActorT, seed: int,
+            step0: int, L: int, traj: TrajT, stream=None):
+    if actor.packed is None:
+        raise TPError(TP_EINVAL, "actor is not packed: call actor.pack()")
+    _check(load().tp_rollout(C.byref(mkt.s), C.byref(cfg), C.byref(st.s),
+                             C.byref(actor.s), _ptr(actor.packed),
+                             actor.packed.numel(), seed & (2 ** 64 - 1),
+                             step0, L, C.byref(traj.s), _stream(stream)))
+
+
+def gae(reward, value, done, gamma, lam, adv, ret, stream=None):
+    L, E = reward.shape
+    _check(load().tp_gae(_ptr(reward), _ptr(value), _ptr(done), L, E, gamma,
+                         lam, _ptr(adv), _ptr(ret), _stream(stream)))
+
+
+def last_error() -> str:
+    return load().tp_last_error().decode()
+
+
+def version() -> int:
+    return load().tp_version()

@@ -1,0 +1,99 @@
+"""C-ABI contract checks that need no GPU: every function declared in
+include/tp.h is exported by libtp.so, and host-side argument checks return
+the documented status codes before anything is launched."""
+
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2111_05188_amd import tp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tp.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tp_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_declares_the_abi():
+    assert set(declared_functions()) == set(tp.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.check_output(["nm", "-D", "--defined-only", tp.LIB_PATH]).decode()
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    missing = [f for f in declared_functions() if f not in exported]
+    assert not missing, missing
+    L = tp.load()
+    for f in declared_functions():
+        assert hasattr(L, f)
+    assert L.tp_version() == 1
+
+
+def _nasdaq_actor(dtype=tp.TP_BF16, dims=(1001, 512, 512, 100), A=1):
+    a = tp.Actor()
+    a.n_agents, a.envs_per_agent, a.dtype = A, 4096, dtype
+    for i, d in enumerate(dims):
+        a.dims[i] = d
+    for l in range(3):
+        a.W[l] = 0x1000
+        a.b[l] = 0x2000
+    a.log_std = 0x3000
+    return a
+
+
+def test_packed_bytes_host_only():
+    L = tp.load()
+    a = _nasdaq_actor()
+    nb = L.tp_actor_packed_bytes(C.byref(a))
+    # 3 layers of bf16 fragments + guards + biases + log_std
+    frag = (32 * 32 + 32 * 16 + 7 * 16) * 1024
+    assert frag < nb < frag + 64 * 1024
+    a16 = _nasdaq_actor(A=16)
+    assert L.tp_actor_packed_bytes(C.byref(a16)) == 16 * nb
+    bad = _nasdaq_actor(dims=(1001, 500, 512, 100))
+    assert L.tp_actor_packed_bytes(C.byref(bad)) == 0
+    assert "multiples of 128" in tp.last_error()
+
+
+def test_argument_errors_without_gpu():
+    L = tp.load()
+    assert L.tp_gae(None, None, None, 1, 1, 0.99, 0.95, None, None, None) == tp.TP_EINVAL
+    assert "NULL" in tp.last_error()
+    x = 0x100000
+    assert L.tp_gae(x, x, x, 0, 4, 0.99, 0.95, x, x, None) == tp.TP_EINVAL
+    assert L.tp_gae(x, x, x, 4, 4, 1.5, 0.95, x, x, None) == tp.TP_EINVAL
+    assert L.tp_gae(x, x, x, 4, 4, 0.99, -0.1, x, x, None) == tp.TP_EINVAL
+    m = tp.Market(x, x, 100, 200, 8)
+    assert L.tp_env_step(C.byref(m), None, None, None, None, None, 0, 0, None) == tp.TP_EINVAL
+    assert "market.n" in tp.last_error()
+    m = tp.Market(x, x, 100, 10, 8)
+    cfg = tp.env_cfg(100, 10, 1e-3, 1e6, 2 ** -12, 2 ** -20, 2 ** -7, 2 ** -7)
+    bad_cfg = tp.env_cfg(0, 10, 1e-3, 1e6, 2 ** -12, 2 ** -20, 2 ** -7, 2 ** -7)
+    st = tp.EnvState(x, x, x, 4)
+    assert L.tp_env_step(C.byref(m), C.byref(bad_cfg), C.byref(st), x, x, None, 0, 0, None) == tp.TP_EINVAL
+    assert "hmax" in tp.last_error()
+    # obs stride must cover K_pad and be a multiple of 8
+    assert L.tp_env_reset(C.byref(m), C.byref(cfg), C.byref(st), x, x, 100, 1, None) == tp.TP_EINVAL
+    assert "ld_obs" in tp.last_error()
+    # rollout: horizon exceeded -> TP_ERANGE; unpacked buffer -> TP_EINVAL
+    a = _nasdaq_actor(dims=(1 + 20 + 80, 128, 128, 10))
+    a.envs_per_agent = 4
+    tr = tp.Traj(None, 0, x, x, x, x, None, None, None)
+    assert L.tp_rollout(C.byref(m), C.byref(cfg), C.byref(st), C.byref(a), x, 1 << 30,
+                        1, 5, 10, C.byref(tr), None) == tp.TP_ERANGE
+    assert L.tp_rollout(C.byref(m), C.byref(cfg), C.byref(st), C.byref(a), x, 1 << 30,
+                        1, 0, 10, C.byref(tr), None) == tp.TP_EINVAL
+    assert "tp_actor_pack" in tp.last_error()
+    # actor that does not match the market
+    a2 = _nasdaq_actor(dims=(999, 128, 128, 10))
+    a2.envs_per_agent = 4
+    assert L.tp_rollout(C.byref(m), C.byref(cfg), C.byref(st), C.byref(a2), x, 1 << 30,
+                        1, 0, 10, C.byref(tr), None) == tp.TP_EINVAL
+    assert "match the market" in tp.last_error()

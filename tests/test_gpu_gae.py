@@ -1,0 +1,70 @@
+"""GPU parity of tp_gae against the oracle (seeded generator inputs), at
+small and full sizes, ragged env counts, L = 1, episode ends inside the
+rollout, and the lambda = 0 / 1 special cases."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_common import rel_check, say, TOL_GAE
+from paper_2111_05188_amd import tp
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(L, E, seed, p_done=0.02):
+    rng = np.random.default_rng(seed)
+    r = (rng.standard_normal((L, E)) * 0.3).astype(np.float32)
+    v = rng.standard_normal((L + 1, E)).astype(np.float32)
+    d = (rng.random((L, E)) < p_done).astype(np.uint8)
+    return r, v, d
+
+
+@pytest.mark.parametrize("L,E,gamma,lam", [
+    (1, 1, 0.99, 0.95), (3, 5, 0.9, 0.5), (256, 64, 0.99, 0.95),
+    (390, 100, 0.99, 0.95), (390, 4096, 0.99, 0.95), (2520, 1024, 0.99, 0.95),
+    (17, 130, 0.99, 0.0), (45, 65, 0.97, 1.0), (1000, 3, 1.0, 1.0)])
+def test_gae_parity(L, E, gamma, lam):
+    say(f"[gae] L={L} E={E} gamma={gamma} lambda={lam}")
+    r, v, d = _inputs(L, E, L * 7 + E)
+    dev = "cuda"
+    gr, gv, gd = (torch.from_numpy(x).to(dev) for x in (r, v, d))
+    adv = torch.empty(L, E, device=dev)
+    ret = torch.empty(L, E, device=dev)
+    tp.gae(gr, gv, gd, gamma, lam, adv, ret)
+    torch.cuda.synchronize()
+    a_o, r_o = oracle.gae(r, v, d, gamma, lam)
+    rel_check("adv", adv.cpu().numpy(), a_o, TOL_GAE)
+    rel_check("ret", ret.cpu().numpy(), r_o, TOL_GAE)
+
+
+def test_gae_stress_shape_sampled():
+    """Full stress size (L=390, E=65536): GPU vs oracle on sampled columns."""
+    L, E = 390, 65536
+    say(f"[gae] stress L={L} E={E}")
+    r, v, d = _inputs(L, E, 5)
+    dev = "cuda"
+    gr, gv, gd = (torch.from_numpy(x).to(dev) for x in (r, v, d))
+    adv = torch.empty(L, E, device=dev)
+    ret = torch.empty(L, E, device=dev)
+    tp.gae(gr, gv, gd, 0.99, 0.95, adv, ret)
+    torch.cuda.synchronize()
+    cols = np.random.default_rng(1).choice(E, 64, replace=False)
+    cols = np.sort(np.concatenate([cols, [0, E - 1]]))
+    a_o, r_o = oracle.gae(r[:, cols], v[:, cols], d[:, cols], 0.99, 0.95)
+    rel_check("adv", adv.cpu().numpy()[:, cols], a_o, TOL_GAE)
+    rel_check("ret", ret.cpu().numpy()[:, cols], r_o, TOL_GAE)
+
+
+def test_gae_deterministic():
+    r, v, d = _inputs(390, 777, 3)
+    dev = "cuda"
+    gr, gv, gd = (torch.from_numpy(x).to(dev) for x in (r, v, d))
+    outs = []
+    for _ in range(2):
+        adv = torch.empty(390, 777, device=dev)
+        ret = torch.empty(390, 777, device=dev)
+        tp.gae(gr, gv, gd, 0.99, 0.95, adv, ret)
+        outs.append((adv.cpu(), ret.cpu()))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])

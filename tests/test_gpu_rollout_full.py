@@ -1,0 +1,69 @@
+"""Full-size GPU parity: every workload at its real shape and in the launch
+configuration the benchmark times, checked against the teacher-forced oracle
+on sampled envs (the oracle replays them one by one), plus GAE over the
+full rollout on sampled columns."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from gpu_common import (build_problem, compare_rollout, oracle_replay,
+                        rel_check, say, TOL_GAE)
+
+pytestmark = pytest.mark.gpu
+
+SEED = 0x5EED0FF12C
+
+
+@pytest.fixture(scope="module")
+def minute_market():
+    say("[full] generating the 100-stock minute market")
+    return W.make_market(W.get_config("nasdaq100"))
+
+
+def _full(cfg, mk, ids, store_obs=True, taps=True):
+    t0 = W.make_t0(cfg)
+    pb, params = build_problem(cfg, mk, t0, store_obs=store_obs, taps=taps,
+                               obs_last=store_obs)
+    pb.set_values(W.make_values(cfg))
+    say(f"[full] {cfg.name} E={cfg.E} L={cfg.L}: reset + rollout + gae")
+    pb.step(SEED)
+    torch.cuda.synchronize()
+    ids = np.asarray(ids)
+    teacher = pb.traj.action.index_select(1, torch.as_tensor(ids, device="cuda")).cpu().numpy()
+    out = oracle_replay(cfg, mk, params, t0[ids], ids, SEED, cfg.L, teacher,
+                        cfg.envs_per_agent)
+    compare_rollout(cfg, pb, out, ids, cfg.L)
+    # GAE on the GPU rewards/done at sampled columns
+    cols = torch.as_tensor(ids, device="cuda")
+    r = pb.traj.reward.index_select(1, cols).cpu().numpy()
+    d = pb.traj.done.index_select(1, cols).cpu().numpy()
+    v = pb.values.index_select(1, cols).cpu().numpy()
+    a_o, r_o = oracle.gae(r, v, d, cfg.gamma, cfg.lam)
+    rel_check("adv", pb.adv.index_select(1, cols).cpu().numpy(), a_o, TOL_GAE)
+    rel_check("ret", pb.ret.index_select(1, cols).cpu().numpy(), r_o, TOL_GAE)
+    return pb
+
+
+def test_dow30_full():
+    cfg = W.get_config("dow30")
+    mk = W.make_market(cfg)
+    _full(cfg, mk, [0, 1, 511, 777, 1023])
+
+
+def test_nasdaq100_full(minute_market):
+    cfg = W.get_config("nasdaq100")
+    _full(cfg, minute_market, [0, 15, 16, 2047, 4095])
+
+
+def test_ensemble_full(minute_market):
+    cfg = W.get_config("ensemble")
+    # envs of agents 0, 5, 15 (first/last env of an agent, mid-block env)
+    _full(cfg, minute_market, [0, 5 * 1024 + 17, 16 * 1024 - 1], store_obs=True)
+
+
+def test_stress_full(minute_market):
+    cfg = W.get_config("stress")
+    _full(cfg, minute_market, [0, 40000, 65535], store_obs=False, taps=True)
