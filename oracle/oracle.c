@@ -269,11 +269,20 @@ int32_t orc_shares_from_action(float a, int32_t hmax)
 /* b_s (balance after sells)}.                                               */
 /* ------------------------------------------------------------------------ */
 
+/* An env whose next row is not in the market (t < row0 or t + 1 beyond the
+ * last row) is not stepped: its state is left as it is and the reward is
+ * NaN (the library's documented behaviour for such an env). */
+static int has_rows(const orc_market *m, int64_t t, int64_t steps)
+{
+    return t >= m->row0 && t + steps <= m->row0 + m->rows - 1;
+}
+
 float orc_env_step_one(const orc_market *m, const orc_env_cfg *cfg,
                        double *cash, int32_t *shares, int64_t *t,
                        const float *action, double *diag)
 {
     const int32_t n = m->n;
+    if (!has_rows(m, *t, 1)) return NAN;
     const double f_s = 1.0 - cfg->fee, f_b = 1.0 + cfg->fee;
     const float *p = price_row(m, *t);
     const float *p1 = price_row(m, *t + 1);
@@ -327,11 +336,19 @@ void orc_env_step(const orc_market *m, const orc_env_cfg *cfg, int32_t E,
 {
     const int32_t n = m->n;
     for (int32_t e = 0; e < E; ++e) {
+        const int ok = has_rows(m, t[e], 1);
         reward[e] = orc_env_step_one(m, cfg, &cash[e], &shares[(size_t)e * n],
                                      &t[e], &action[(size_t)e * n], NULL);
-        orc_obs(m, cfg, t[e], cash[e], &shares[(size_t)e * n], K_pad,
-                obs_f32 ? obs_f32 + (size_t)e * K_pad : NULL,
-                obs_bf16 ? obs_bf16 + (size_t)e * K_pad : NULL);
+        if (ok) {
+            orc_obs(m, cfg, t[e], cash[e], &shares[(size_t)e * n], K_pad,
+                    obs_f32 ? obs_f32 + (size_t)e * K_pad : NULL,
+                    obs_bf16 ? obs_bf16 + (size_t)e * K_pad : NULL);
+        } else {
+            for (int32_t k = 0; k < K_pad; ++k) {
+                if (obs_f32) obs_f32[(size_t)e * K_pad + k] = NAN;
+                if (obs_bf16) obs_bf16[(size_t)e * K_pad + k] = orc_bf16_bits(NAN);
+            }
+        }
     }
 }
 
@@ -458,6 +475,11 @@ void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
     float *z = (float *)malloc(sizeof(float) * n);
     float *act = (float *)malloc(sizeof(float) * n);
 
+    /* an env without market rows for all L steps is not stepped: its
+     * state stays, its rows hold NaN (done = 0, obs untouched) */
+    uint8_t *active = (uint8_t *)malloc((size_t)E + 1);
+    for (int32_t e = 0; e < E; ++e) active[e] = (uint8_t)has_rows(m, t[e], L);
+
     for (int32_t j = 0; j < L; ++j) {
         const uint32_t step = (uint32_t)(step0 + (uint64_t)j);
         for (int32_t e = 0; e < E; ++e) {
@@ -465,6 +487,18 @@ void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
             const int32_t ag = gid / a->envs_per_agent;
             int32_t *h = &shares[(size_t)e * n];
             const size_t row = (size_t)j * E + e;
+            if (!active[e]) {
+                for (int32_t i = 0; i < n; ++i) {
+                    if (tr->act) tr->act[row * n + i] = NAN;
+                    if (tr->mu) tr->mu[row * n + i] = NAN;
+                }
+                if (tr->logp) tr->logp[row] = NAN;
+                if (tr->reward) tr->reward[row] = NAN;
+                if (tr->done) tr->done[row] = 0;
+                if (tr->cash_tap) tr->cash_tap[row] = cash[e];
+                if (tr->shares_tap) memcpy(tr->shares_tap + row * n, h, sizeof(int32_t) * n);
+                continue;
+            }
 
             /* observation */
             orc_obs(m, cfg, t[e], cash[e], h, K_pad, x, a->bf16 ? xb : NULL);
@@ -505,6 +539,7 @@ void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
             if (tr->shares_tap) memcpy(tr->shares_tap + row * n, h, sizeof(int32_t) * n);
         }
     }
+    free(active);
     free(x); free(xb); free(h1); free(h2); free(mu); free(z); free(act);
     for (int32_t i = 0; i < 3 * A; ++i) free(W[i]);
     free(W);

@@ -21,7 +21,8 @@ def _setup(name, E, rows, seed):
     cash = np.concatenate([rng.uniform(0, 2e6, E - E // 4), rng.uniform(0, 200, E // 4)])
     shares = rng.integers(0, 400, (E, cfg.n)).astype(np.int32)
     shares[rng.random((E, cfg.n)) < 0.3] = 0
-    t = rng.integers(0, rows - 2, E).astype(np.int64)
+    # room for the four chained steps of the test
+    t = rng.integers(0, rows - 1 - 4, E).astype(np.int64)
     act = W.make_actions(seed + 1, E, cfg.n)
     return cfg, mk, cash, shares, t, act
 

@@ -86,8 +86,9 @@ def test_deterministic_and_resumable():
         torch.cuda.synchronize()
         runs.append(pb)
     a, b = runs
+    # only the first L rows were written (the store holds a full episode)
     for name in ("action", "logp", "reward", "done", "cash_tap", "shares_tap", "obs"):
-        assert torch.equal(getattr(a.traj, name), getattr(b.traj, name)), name
+        assert torch.equal(getattr(a.traj, name)[:L], getattr(b.traj, name)[:L]), name
     # split run
     pb, _ = build_problem(cfg, mk, t0)
     pb.reset()
@@ -98,7 +99,7 @@ def test_deterministic_and_resumable():
     pb.rollout(SEED, j, L - j, traj=t2)
     torch.cuda.synchronize()
     for name in ("action", "logp", "reward", "done", "cash_tap", "shares_tap", "obs"):
-        full = getattr(a.traj, name)
+        full = getattr(a.traj, name)[:L]
         assert torch.equal(full[:j], getattr(t1, name)), name
         assert torch.equal(full[j:], getattr(t2, name)), name
     assert torch.equal(t1.obs_last, a.traj.obs[j])
@@ -119,10 +120,11 @@ def test_env_without_room_is_not_stepped():
     say("[rollout] envs without room")
     pb.rollout(SEED, 0, 50)
     torch.cuda.synchronize()
-    r = pb.traj.reward.cpu().numpy()
+    r = pb.traj.reward[:50].cpu().numpy()
     assert np.isnan(r[:, 3]).all() and np.isnan(r[:, 4]).all()
     assert np.isfinite(r[:, [0, 1, 2, 5]]).all()
-    assert (pb.traj.done.cpu().numpy()[:, 3] == 0).all()
+    assert (pb.traj.done[:50].cpu().numpy()[:, 3] == 0).all()
+    assert np.isnan(pb.traj.action[:50, 3].cpu().numpy()).all()
     assert pb.state.t[3].item() == cfg.T1 - 10 and pb.state.t[4].item() == -1
     assert pb.state.t[0].item() == 50
 

@@ -296,3 +296,14 @@ def test_reset():
     t0 = np.array([0, 390, 780], np.int64)
     cash, shares, t = oracle.env_reset(c, t0, 7)
     assert (cash == 1e6).all() and (shares == 0).all() and np.array_equal(t, t0)
+
+
+def test_env_without_next_row_is_not_stepped():
+    """An env at the last market row (or before the first) keeps its state
+    and reports a NaN reward instead of reading past the market."""
+    m = mk_market([[10, 20], [11, 19]])
+    c = ecfg(hmax=64)
+    for t in (1, -1, 5):
+        r, nb, h1, t1, _ = oracle.env_step_one(m, c, 100.0, [3, 4], t,
+                                               actions_for([5, -5], 64))
+        assert np.isnan(r) and nb == 100.0 and list(h1) == [3, 4] and t1 == t
