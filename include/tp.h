@@ -195,8 +195,9 @@ int tp_actor_pack(const tp_actor *actor, void *packed, size_t packed_bytes,
  *   state on entry (it selects the random stream), so a rollout split into
  *   pieces with matching step0 reproduces the unsplit one bit for bit.
  *   Requires step0 + L <= horizon.  Device-side t is not visible to the
- *   host: an env with t < 0 or t + L > T1 - 1 is not stepped (its state is
- *   left unchanged and its trajectory rows are NaN / done = 0).  `packed` must come from tp_actor_pack with the same
+ *   host: an env with t < 0 or t + L > T1 - 1 is not stepped: its state is
+ *   left unchanged, its action / logp / reward rows are NaN, done is 0, the
+ *   taps hold the unchanged state and its observation rows are not written.  `packed` must come from tp_actor_pack with the same
  *   actor shape.
  */
 int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg,

@@ -57,31 +57,55 @@ __device__ __forceinline__ void box_muller(float u0, float u1, float &z0,
 }
 
 // ---------------------------------------------------------------------------
-// Wavefront collectives (all 64 lanes active).
+// Wavefront collectives (all 64 lanes active), built on DPP lane moves:
+// row_shr:k shifts within 16-lane rows, row_bcast:15 / row_bcast:31 carry
+// row totals into the following rows.  A lane whose DPP source does not
+// exist (or whose row is masked off) receives 0.
 // ---------------------------------------------------------------------------
+enum : int { DPP_ROW_SHR = 0x110, DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143 };
+
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ double dpp_f64(double x)
+{
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, ROWS, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, ROWS, 0xF, false);
+    return __hiloint2double(hi, lo);
+}
+
+// Inclusive prefix sum across the 64 lanes in lane order (Hillis-Steele in
+// rows of 16, then row totals carried forward).
+__device__ __forceinline__ double wave_inclusive_scan(double v)
+{
+    v += dpp_f64<DPP_ROW_SHR + 1>(v);
+    v += dpp_f64<DPP_ROW_SHR + 2>(v);
+    v += dpp_f64<DPP_ROW_SHR + 4>(v);
+    v += dpp_f64<DPP_ROW_SHR + 8>(v);
+    v += dpp_f64<DPP_ROW_BCAST15, 0xA>(v);
+    v += dpp_f64<DPP_ROW_BCAST31, 0xC>(v);
+    return v;
+}
+
+__device__ __forceinline__ double lane_value(double v, int lane)
+{
+    const int lo = __builtin_amdgcn_readlane(__double2loint(v), lane);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(v), lane);
+    return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ int lane_value(int v, int lane)
+{
+    return __builtin_amdgcn_readlane(v, lane);
+}
+
+__device__ __forceinline__ float lane_value(float v, int lane)
+{
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// Sum over the 64 lanes (same value returned to every lane).
 __device__ __forceinline__ double wave_sum(double v)
 {
-#pragma unroll
-    for (int o = WAVE / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
-    return v;
-}
-
-__device__ __forceinline__ float wave_sum(float v)
-{
-#pragma unroll
-    for (int o = WAVE / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, WAVE);
-    return v;
-}
-
-// Inclusive prefix sum across lanes in lane order.
-__device__ __forceinline__ double wave_inclusive_scan(double v, int lane)
-{
-#pragma unroll
-    for (int o = 1; o < WAVE; o <<= 1) {
-        const double t = __shfl_up(v, o, WAVE);
-        if (lane >= o) v += t;
-    }
-    return v;
+    return lane_value(wave_inclusive_scan(v), WAVE - 1);
 }
 
 // fp32 -> bf16, IEEE round to nearest even (v_cvt_pk_bf16_f32 on gfx950).

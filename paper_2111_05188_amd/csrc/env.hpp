@@ -59,33 +59,41 @@ __device__ __forceinline__ float env_step_wave(const EnvConst &C, LaneEnv &s,
     int h0 = s.h0 - sa, h1 = s.h1 - sb;
     const double S = wave_sum(pa * (double)sa + pb * (double)sb);  // exact
     const double b_s = fma(S, C.f_s, s.cash);
+    const double fb = C.f_b;
 
-    // buys: resolve the greedy in ascending stock order.  Each round finds
-    // the first pending stock whose full order no longer fits; every pending
-    // stock before it fits in full, that stock gets its largest affordable
-    // q, and the round repeats on the stocks after it.
+    // buys: resolve the greedy in ascending stock order in rounds.  A round
+    // first drops every pending stock that cannot pay for one share at the
+    // current G (G only grows, so it never will), then finds the first
+    // pending stock whose full order no longer fits: every pending stock
+    // before it is bought in full, it gets its largest affordable q, and the
+    // next round continues after it.
     const double c0 = k0 > 0 ? pa * (double)k0 : 0.0;
     const double c1 = k1 > 0 ? pb * (double)k1 : 0.0;
     bool pend0 = k0 > 0, pend1 = k1 > 0;
     int q0n = 0, q1n = 0;
     double G = 0.0;
-    for (;;) {
+    for (bool first = true;; first = false) {
+        if (!first) {
+            if (pend0 && fma(fb, G + pa, -b_s) > 0.0) pend0 = false;
+            if (pend1 && fma(fb, G + pb, -b_s) > 0.0) pend1 = false;
+        }
+        if (__ballot(pend0 || pend1) == 0) break;
         const double cc0 = pend0 ? c0 : 0.0, cc1 = pend1 ? c1 : 0.0;
         const double tot = cc0 + cc1;
-        const double incl = wave_inclusive_scan(tot, lane);
+        const double incl = wave_inclusive_scan(tot);
         const double base = G + (incl - tot);  // exact
         const double P0 = base + cc0, P1 = P0 + cc1;
-        const bool bad0 = pend0 && fma(C.f_b, P0, -b_s) > 0.0;
-        const bool bad1 = pend1 && fma(C.f_b, P1, -b_s) > 0.0;
+        const bool bad0 = pend0 && fma(fb, P0, -b_s) > 0.0;
+        const bool bad1 = pend1 && fma(fb, P1, -b_s) > 0.0;
         const uint64_t m = __ballot(bad0 || bad1);
         if (m == 0) {
             if (pend0) q0n = k0;
             if (pend1) q1n = k1;
-            G = __shfl(base + tot, WAVE - 1, WAVE);
+            G = lane_value(base + tot, WAVE - 1);
             break;
         }
         const int fl = __ffsll((unsigned long long)m) - 1;
-        const bool f_is_1 = __shfl(bad0 ? 0 : 1, fl, WAVE) != 0;
+        const bool f_is_1 = lane_value(bad0 ? 0 : 1, fl) != 0;
         // stocks before the first misfit are bought in full
         if (lane < fl) {
             if (pend0) q0n = k0;
@@ -95,17 +103,17 @@ __device__ __forceinline__ float env_step_wave(const EnvConst &C, LaneEnv &s,
             q0n = k0;
             pend0 = false;
         }
-        const double Gf = __shfl(f_is_1 ? P1 - cc1 : P0 - cc0, fl, WAVE);
-        const double pf = __shfl(f_is_1 ? pb : pa, fl, WAVE);
-        const int kf = __shfl(f_is_1 ? k1 : k0, fl, WAVE);
+        const double Gf = lane_value(f_is_1 ? P1 - cc1 : P0 - cc0, fl);
+        const double pf = lane_value(f_is_1 ? pb : pa, fl);
+        const int kf = lane_value(f_is_1 ? k1 : k0, fl);
         // largest q in [0, kf-1] with f_b (Gf + pf q) <= b_s: estimate, then
         // step to the exact boundary with the sign-exact test
-        const double rem = fma(-C.f_b, Gf, b_s);
-        double est = floor(rem / (pf * C.f_b));
+        const double rem = fma(-fb, Gf, b_s);
+        double est = floor(rem / (pf * fb));
         est = fmin(fmax(est, 0.0), (double)(kf - 1));
         int q = (int)est;
-        while (q < kf - 1 && fma(C.f_b, Gf + pf * (double)(q + 1), -b_s) <= 0.0) ++q;
-        while (q > 0 && fma(C.f_b, Gf + pf * (double)q, -b_s) > 0.0) --q;
+        while (q < kf - 1 && fma(fb, Gf + pf * (double)(q + 1), -b_s) <= 0.0) ++q;
+        while (q > 0 && fma(fb, Gf + pf * (double)q, -b_s) > 0.0) --q;
         G = Gf + pf * (double)q;
         if (lane == fl) {
             if (f_is_1) {
@@ -119,7 +127,7 @@ __device__ __forceinline__ float env_step_wave(const EnvConst &C, LaneEnv &s,
     }
     h0 += q0n;
     h1 += q1n;
-    double nb = fma(-C.f_b, G, b_s);
+    double nb = fma(-fb, G, b_s);
     if (nb < 0.0) nb = 0.0;
 
     const double V1 = nb + wave_sum((double)h0 * (double)q0 + (double)h1 * (double)q1);
@@ -156,6 +164,37 @@ __device__ __forceinline__ void write_obs_row(T *row, const EnvConst &C,
         row[1 + n + i1] = obs_cvt<T>((float)h1 * C.share_scale);
     }
     for (int k = lane; k < nI; k += WAVE) row[1 + 2 * n + k] = obs_cvt<T>(irow[k]);
+    for (int k = S + lane; k < C.K_pad; k += WAVE) row[k] = obs_cvt<T>(0.0f);
+}
+
+// The same row with the next-row prices and the first 64*IPL indicators
+// already in registers (q0/q1: prices of this lane's stocks; ind[m]:
+// indicator lane + 64 m); indicators beyond that are read from irow.
+template <typename T, int IPL>
+__device__ __forceinline__ void write_obs_row_regs(T *row, const EnvConst &C,
+                                                   double cash, int h0, int h1,
+                                                   float q0, float q1,
+                                                   const float (&ind)[IPL],
+                                                   const float *irow, int lane)
+{
+    const int n = C.n, nI = C.nI, S = 1 + 2 * n + nI;
+    const int i0 = 2 * lane, i1 = i0 + 1;
+    if (lane == 0) row[0] = obs_cvt<T>((float)(cash * (double)C.cash_scale));
+    if (i0 < n) {
+        row[1 + i0] = obs_cvt<T>(q0 * C.price_scale);
+        row[1 + n + i0] = obs_cvt<T>((float)h0 * C.share_scale);
+    }
+    if (i1 < n) {
+        row[1 + i1] = obs_cvt<T>(q1 * C.price_scale);
+        row[1 + n + i1] = obs_cvt<T>((float)h1 * C.share_scale);
+    }
+    T *ri = row + 1 + 2 * n;
+#pragma unroll
+    for (int m = 0; m < IPL; ++m) {
+        const int k = lane + WAVE * m;
+        if (k < nI) ri[k] = obs_cvt<T>(ind[m]);
+    }
+    for (int k = WAVE * IPL + lane; k < nI; k += WAVE) ri[k] = obs_cvt<T>(irow[k]);
     for (int k = S + lane; k < C.K_pad; k += WAVE) row[k] = obs_cvt<T>(0.0f);
 }
 

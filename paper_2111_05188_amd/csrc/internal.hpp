@@ -67,9 +67,8 @@ struct RolloutArgs {
     int32_t *shares_tap;
     void *obs_last;
     // LDS carve-up (bytes / elements), filled by the launcher
-    int ldx, ldh, ldmu, ldmk;
-    int mk_vec;           // market rows are 16-byte aligned: dwordx4 DMA
-    size_t lds_X, lds_H, lds_MU, lds_MK, lds_OA, lds_OS, lds_scal, lds_bytes;
+    int ldx, ldh, ldmu;
+    size_t lds_X, lds_H, lds_MU, lds_OS, lds_PT, lds_scal, lds_bytes;
 };
 
 hipError_t launch_rollout(RolloutArgs &a, hipStream_t s);

@@ -9,19 +9,18 @@
 // from L2 after the first block reads them), the trajectory writes and the
 // state at entry/exit.
 //
-// Wave roles: NWM compute waves run the MLP and the per-env work (EPW envs
-// each); one IO wave moves the next market rows into LDS with
-// global_load_lds DMA and writes the previous step's trajectory rows from
-// LDS staging to HBM.  Keeping every non-weight global access in the IO
-// wave means the compute waves' in-order vmcnt waits only ever wait for
-// weight loads.
+// Every wave owns EPW envs for the per-env work and computes a share of the
+// output tiles of every actor layer.  Within a step the waves' global memory
+// traffic is phased: the actor layers stream weights only; the per-env phase
+// loads the next market row at its start (the weight stream is over, so its
+// latency hides behind the sampling and trade logic) and stores the
+// trajectory rows at its end (their acknowledgements overlap the barrier and
+// the next layer's first weight loads).
 #include "device.hpp"
 #include "env.hpp"
 #include "internal.hpp"
 
 namespace tpk {
-
-typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
 // ---------------------------------------------------------------------------
 // Actor layers
@@ -147,17 +146,17 @@ __device__ __forceinline__ void valu_layer(const float4 *__restrict__ Wt,
 // actor, float with the VALU actor).
 // ---------------------------------------------------------------------------
 template <typename OT, int EPW, int NWM, int KS1, int KS2, int KS3>
-__global__ __launch_bounds__((NWM + 1) * WAVE) void rollout_kernel(RolloutArgs A)
+__global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
 {
     constexpr int MB = EPW * NWM;
     constexpr bool BF16 = sizeof(OT) == 2;
+    constexpr int IPL = 16;  // indicators held per lane (n * n_ind <= 1024)
     extern __shared__ __align__(16) uint8_t smem[];
 
     const EnvConst &C = A.env;
     const PackedLayout &P = A.lay;
     const int n = C.n, nI = C.nI;
     const int tid = threadIdx.x, wave = tid / WAVE, lane = tid % WAVE;
-    const bool io = wave == NWM;
 
     // XCD-aware block order: consecutive dispatch slots of one XCD (block id
     // mod 8) take consecutive logical blocks, so one agent's blocks share an
@@ -176,234 +175,208 @@ __global__ __launch_bounds__((NWM + 1) * WAVE) void rollout_kernel(RolloutArgs A
     const float *b3 = (const float *)(pk + P.off_b[2]);
     const float *lsd = (const float *)(pk + P.off_ls);
 
-    OT *X = (OT *)(smem + A.lds_X);            // [MB][ldx] observations (H2 aliases it)
-    OT *Hd = (OT *)(smem + A.lds_H);           // [MB][ldh] hidden layer 1
-    float *MU = (float *)(smem + A.lds_MU);    // [MB][ldmu] action means
-    float *MK = (float *)(smem + A.lds_MK);    // [MB][ldmk] next-row prices+indicators
-    float *OA = (float *)(smem + A.lds_OA);    // [MB][n] staged actions
-    int32_t *OS = (int32_t *)(smem + A.lds_OS);// [MB][n] staged holdings
-    int64_t *T0 = (int64_t *)(smem + A.lds_scal);   // [MB] start rows
-    double *OC = (double *)(T0 + MB);          // [MB] staged cash
-    float *OL = (float *)(OC + MB);            // [MB] staged logp
-    float *OR = (float *)(OL + MB);            // [MB] staged reward
-    int *ACT = (int *)(OR + MB);               // [MB] env is stepped
+    OT *X = (OT *)(smem + A.lds_X);              // [MB][ldx] observations (H2 aliases it)
+    OT *Hd = (OT *)(smem + A.lds_H);             // [MB][ldh] hidden layer 1
+    float *MU = (float *)(smem + A.lds_MU);      // [MB][ldmu] action means
+    int32_t *OS = (int32_t *)(smem + A.lds_OS);  // [MB][n] holdings
+    float *PT = (float *)(smem + A.lds_PT);      // [MB][n] prices at the current row
+    int64_t *T0 = (int64_t *)(smem + A.lds_scal);  // [MB] start rows
+    double *OC = (double *)(T0 + MB);            // [MB] balances
+    int *ACT = (int *)(OC + MB);                 // [MB] env is stepped
 
-    const int ldx = A.ldx, ldh = A.ldh, ldmu = A.ldmu, ldmk = A.ldmk;
+    const int ldx = A.ldx, ldh = A.ldh, ldmu = A.ldmu;
+    const size_t E = (size_t)A.E;
+    const int obs_chunks = C.K_pad * (int)sizeof(OT) / 16;
 
-    // ---- prologue ---------------------------------------------------------
+    // copy the observation row of slot s from X to global row `dst`
+    auto store_obs_row = [&](OT *dst, int s) {
+        const uint4 *x = (const uint4 *)(X + s * ldx);
+        for (int c = lane; c < obs_chunks; c += WAVE) ((uint4 *)dst)[c] = x[c];
+    };
+
+    // ---- prologue: state of the wave's envs into LDS, obs_0 into X and HBM --
     for (int i = tid; i < MB * ldx * (int)sizeof(OT) / 16; i += blockDim.x)
         ((uint4 *)X)[i] = uint4{0, 0, 0, 0};
-    if (tid < MB) {
-        int64_t tt = -1;
-        int act = 0;
-        if (tid < nenv) {
-            tt = A.t[ebase + tid];
-            act = tt >= 0 && tt + A.L <= C.T1 - 1;
-        }
-        T0[tid] = tt;
-        ACT[tid] = act;
-    }
     __syncthreads();
-
-    LaneEnv st[EPW];
     float ls0 = 0.f, ls1 = 0.f, sg0 = 0.f, sg1 = 0.f;
     const int i0 = 2 * lane, i1 = i0 + 1;
-    if (!io) {
-        if (i0 < n) { ls0 = lsd[i0]; sg0 = expf(ls0); }
-        if (i1 < n) { ls1 = lsd[i1]; sg1 = expf(ls1); }
-#pragma unroll
-        for (int k = 0; k < EPW; ++k) {
-            const int s = wave * EPW + k;
-            st[k] = LaneEnv{0.0, 0, 0, 0.f, 0.f};
-            if (!ACT[s]) continue;
+    if (i0 < n) { ls0 = lsd[i0]; sg0 = expf(ls0); }
+    if (i1 < n) { ls1 = lsd[i1]; sg1 = expf(ls1); }
+    for (int k = 0; k < EPW; ++k) {
+        const int s = wave * EPW + k;
+        int64_t tt = -1;
+        int act = 0;
+        if (s < nenv) {
             const int e = ebase + s;
-            const int64_t t = T0[s];
-            const float *prow = C.price + (size_t)t * n;
-            st[k].cash = A.cash[e];
-            if (i0 < n) { st[k].h0 = A.shares[(size_t)e * n + i0]; st[k].p0 = prow[i0]; }
-            if (i1 < n) { st[k].h1 = A.shares[(size_t)e * n + i1]; st[k].p1 = prow[i1]; }
-            write_obs_row<OT>(X + s * ldx, C, st[k].cash, st[k].h0, st[k].h1, prow,
-                              C.ind + (size_t)t * nI, lane);
+            tt = A.t[e];
+            act = tt >= 0 && tt + A.L <= C.T1 - 1;
+            // state (also for envs that are not stepped: their taps repeat it)
+            for (int i = lane; i < n; i += WAVE) OS[s * n + i] = A.shares[(size_t)e * n + i];
+            if (lane == 0) OC[s] = A.cash[e];
+        }
+        if (lane == 0) {
+            T0[s] = tt;
+            ACT[s] = act;
+        }
+        if (act) {
+            const float *prow = C.price + (size_t)tt * n;
+            int h0 = 0, h1 = 0;
+            if (i0 < n) { h0 = OS[s * n + i0]; PT[s * n + i0] = prow[i0]; }
+            if (i1 < n) { h1 = OS[s * n + i1]; PT[s * n + i1] = prow[i1]; }
+            write_obs_row<OT>(X + s * ldx, C, OC[s], h0, h1, prow, C.ind + (size_t)tt * nI, lane);
+            if (A.obs) store_obs_row((OT *)A.obs + ((size_t)ebase + s) * A.ld_obs, s);
         }
     }
     __syncthreads();
 
     const double half_log2pi_n = 0.5 * (double)n * 1.8378770664093454836;
-    const size_t E = (size_t)A.E;
-    const size_t obs_row_bytes = (size_t)C.K_pad * sizeof(OT);
+    const float qnan = __builtin_nanf("");
+    (void)qnan;
 
-    for (int j = 0; j <= A.L; ++j) {
-        // ---- IO wave: previous step's trajectory rows, next market rows ---
-        if (io) {
-            if (j > 0) {
-                const size_t row0 = (size_t)(j - 1) * E + ebase;
-                float *ga = A.action + row0 * n;
-                for (int i = lane; i < nenv * n; i += WAVE)
-                    if (ACT[i / n]) ga[i] = OA[i];
-                for (int s = lane; s < nenv; s += WAVE) {
-                    if (!ACT[s]) continue;
-                    A.logp[row0 + s] = OL[s];
-                    A.reward[row0 + s] = OR[s];
-                    A.done[row0 + s] = (uint8_t)(A.step0 + (uint64_t)(j - 1) + 1 == (uint64_t)C.horizon);
-                    if (A.cash_tap) A.cash_tap[row0 + s] = OC[s];
-                }
-                if (A.shares_tap) {
-                    int32_t *gs = A.shares_tap + row0 * n;
-                    for (int i = lane; i < nenv * n; i += WAVE)
-                        if (ACT[i / n]) gs[i] = OS[i];
-                }
-            }
-            if (j < A.L) {
-                // DMA market rows T0 + j + 1 into MK (one row per active env)
-                if (A.mk_vec) {
-                    const int cps = ldmk / 4, np4 = n / 4;
-                    const int total = MB * cps;
-                    for (int c0 = 0; c0 < total; c0 += WAVE) {
-                        const int c = c0 + lane;
-                        const int s = c / cps, part = c - s * cps;
-                        if (c < total && ACT[s]) {
-                            const int64_t t = T0[s] + j + 1;
-                            const float *src = part < np4 ? C.price + (size_t)t * n + 4 * part
-                                                          : C.ind + (size_t)t * nI + 4 * (part - np4);
-                            __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(MK + 4 * c0), 16, 0, 0);
-                        }
-                    }
-                } else {
-                    const int total = MB * ldmk;
-                    for (int c0 = 0; c0 < total; c0 += WAVE) {
-                        const int c = c0 + lane;
-                        const int s = c / ldmk, part = c - s * ldmk;
-                        if (c < total && ACT[s] && part < n + nI) {
-                            const int64_t t = T0[s] + j + 1;
-                            const float *src = part < n ? C.price + (size_t)t * n + part
-                                                        : C.ind + (size_t)t * nI + (part - n);
-                            __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(MK + c0), 4, 0, 0);
-                        }
-                    }
-                }
-            }
-            // observation rows: obs_j (j < L) or the bootstrap observation
-            OT *dst = nullptr;
-            if (j < A.L && A.obs) dst = (OT *)A.obs + ((size_t)j * E + ebase) * A.ld_obs;
-            if (j == A.L && A.obs_last) dst = (OT *)A.obs_last + (size_t)ebase * A.ld_obs;
-            if (dst) {
-                const int cpr = (int)(obs_row_bytes / 16);
-                for (int c = lane; c < nenv * cpr; c += WAVE) {
-                    const int s = c / cpr, part = c - s * cpr;
-                    if (!ACT[s]) continue;
-                    ((uint4 *)(dst + (size_t)s * A.ld_obs))[part] =
-                        ((const uint4 *)(X + s * ldx))[part];
-                }
-            }
-        }
-        if (j == A.L) break;
-
+    for (int j = 0; j < A.L; ++j) {
         // ---- actor ---------------------------------------------------------
         if constexpr (BF16) {
             constexpr int MT = MB / 16;
-            if (!io)
-                mfma_layer<MT, 4, true, KS1>((const bf16x8 *)(pk + P.off_W[0]), b1, P.NT[0], P.KS[0],
-                                        (const __bf16 *)X, ldx, Hd, ldh, wave, NWM, lane);
+            mfma_layer<MT, 4, true, KS1>((const bf16x8 *)(pk + P.off_W[0]), b1, P.NT[0], P.KS[0],
+                                         (const __bf16 *)X, ldx, Hd, ldh, wave, NWM, lane);
             __syncthreads();
-            if (!io)
-                mfma_layer<MT, 4, true, KS2>((const bf16x8 *)(pk + P.off_W[1]), b2, P.NT[1], P.KS[1],
-                                        (const __bf16 *)Hd, ldh, X, ldx, wave, NWM, lane);
+            mfma_layer<MT, 4, true, KS2>((const bf16x8 *)(pk + P.off_W[1]), b2, P.NT[1], P.KS[1],
+                                         (const __bf16 *)Hd, ldh, X, ldx, wave, NWM, lane);
             __syncthreads();
-            if (!io)
-                mfma_layer<MT, 1, false, KS3>((const bf16x8 *)(pk + P.off_W[2]), b3, P.NT[2], P.KS[2],
-                                         (const __bf16 *)X, ldx, MU, ldmu, wave, NWM, lane);
+            mfma_layer<MT, 1, false, KS3>((const bf16x8 *)(pk + P.off_W[2]), b3, P.NT[2], P.KS[2],
+                                          (const __bf16 *)X, ldx, MU, ldmu, wave, NWM, lane);
         } else {
-            if (!io)
-                valu_layer<MB, true>((const float4 *)(pk + P.off_W[0]), b1, P.KS[0], P.H1,
-                                     (const float *)X, ldx, (float *)Hd, ldh, tid, NWM * WAVE);
+            valu_layer<MB, true>((const float4 *)(pk + P.off_W[0]), b1, P.KS[0], P.H1,
+                                 (const float *)X, ldx, (float *)Hd, ldh, tid, NWM * WAVE);
             __syncthreads();
-            if (!io)
-                valu_layer<MB, true>((const float4 *)(pk + P.off_W[1]), b2, P.KS[1], P.H2,
-                                     (const float *)Hd, ldh, (float *)X, ldx, tid, NWM * WAVE);
+            valu_layer<MB, true>((const float4 *)(pk + P.off_W[1]), b2, P.KS[1], P.H2,
+                                 (const float *)Hd, ldh, (float *)X, ldx, tid, NWM * WAVE);
             __syncthreads();
-            if (!io)
-                valu_layer<MB, false>((const float4 *)(pk + P.off_W[2]), b3, P.KS[2], P.n,
-                                      (const float *)X, ldx, MU, ldmu, tid, NWM * WAVE);
+            valu_layer<MB, false>((const float4 *)(pk + P.off_W[2]), b3, P.KS[2], P.n,
+                                  (const float *)X, ldx, MU, ldmu, tid, NWM * WAVE);
         }
-        if (io) __builtin_amdgcn_s_waitcnt(0);   // market DMA landed in MK
         __syncthreads();
 
-        // ---- sampling, env step, next observation ---------------------------
-        if (!io) {
-            const uint32_t step = (uint32_t)(A.step0 + (uint64_t)j);
+        // ---- sampling, env step, trajectory rows, next observation ---------
+        // Three passes over the wave's envs so that every load is issued
+        // before any store (vmcnt counts both, in issue order): next-row
+        // market loads; sampling, trade and the next observation in LDS;
+        // trajectory stores.
+        const uint32_t step = (uint32_t)(A.step0 + (uint64_t)j);
+        const uint8_t done = (uint8_t)(A.step0 + (uint64_t)j + 1 == (uint64_t)C.horizon);
+        float q0[EPW], q1[EPW], ind[EPW][IPL];
+        // branch-free: every lane loads from a valid address (clamped index,
+        // row 0 for an env that is not stepped), so the loads issue back to
+        // back instead of each waiting at a branch join
 #pragma unroll
-            for (int k = 0; k < EPW; ++k) {
-                const int s = wave * EPW + k;
-                if (!ACT[s]) continue;
-                const int e = ebase + s;
-                // Philox counter (i/4, env, step, agent): lane l owns stocks
-                // 2l, 2l+1 = counter l/2, Box-Muller pair l%2
-                const U4 w = philox4x32_10(U4{(uint32_t)(lane >> 1), (uint32_t)e, step, (uint32_t)agent},
-                                           A.key_lo, A.key_hi);
-                const bool second = lane & 1;
-                float z0, z1;
-                box_muller(uniform_open01(second ? w.z : w.x),
-                           uniform_open01(second ? w.w : w.y), z0, z1);
-                const float *mu = MU + s * ldmu;
-                float a0 = 0.f, a1 = 0.f;
-                double lp = 0.0;
-                if (i0 < n) {
-                    const float sz = sg0 * z0;
-                    a0 = mu[i0] + sz;
-                    lp += -0.5 * (double)z0 * (double)z0 - (double)ls0;
-                    OA[s * n + i0] = a0;
+        for (int k = 0; k < EPW; ++k) {
+            const int s = wave * EPW + k;
+            const int64_t t1 = ACT[s] ? T0[s] + j + 1 : 0;
+            const float *pr = C.price + (size_t)t1 * n;
+            const float *ir = nI > 0 ? C.ind + (size_t)t1 * nI : pr;
+            const int last = (nI > 0 ? nI : n) - 1;
+            q0[k] = pr[min(i0, n - 1)];
+            q1[k] = pr[min(i1, n - 1)];
+#pragma unroll
+            for (int m = 0; m < IPL; ++m) ind[k][m] = ir[min(lane + WAVE * m, last)];
+        }
+        float a0[EPW], a1[EPW], rw[EPW];
+        double lpv[EPW];
+#pragma unroll
+        for (int k = 0; k < EPW; ++k) {
+            const int s = wave * EPW + k;
+            a0[k] = a1[k] = rw[k] = 0.f;
+            lpv[k] = 0.0;
+            if (!ACT[s]) continue;
+            const int e = ebase + s;
+            // Philox counter (i/4, env, step, agent): lane l owns stocks 2l,
+            // 2l+1 = counter l/2, Box-Muller pair l%2
+            const U4 w = philox4x32_10(U4{(uint32_t)(lane >> 1), (uint32_t)e, step, (uint32_t)agent},
+                                       A.key_lo, A.key_hi);
+            const bool second = lane & 1;
+            float z0, z1;
+            box_muller(uniform_open01(second ? w.z : w.x), uniform_open01(second ? w.w : w.y), z0, z1);
+            const float *mu = MU + s * ldmu;
+            LaneEnv st{OC[s], 0, 0, 0.f, 0.f};
+            double lp = 0.0;
+            if (i0 < n) {
+                const float sz = sg0 * z0;
+                a0[k] = mu[i0] + sz;
+                lp += -0.5 * (double)z0 * (double)z0 - (double)ls0;
+                st.h0 = OS[s * n + i0];
+                st.p0 = PT[s * n + i0];
+            }
+            if (i1 < n) {
+                const float sz = sg1 * z1;
+                a1[k] = mu[i1] + sz;
+                lp += -0.5 * (double)z1 * (double)z1 - (double)ls1;
+                st.h1 = OS[s * n + i1];
+                st.p1 = PT[s * n + i1];
+            }
+            lpv[k] = wave_sum(lp) - half_log2pi_n;
+            if (i0 >= n) q0[k] = 0.f;
+            if (i1 >= n) q1[k] = 0.f;
+            rw[k] = env_step_wave(C, st, a0[k], a1[k], q0[k], q1[k], lane);
+            if (lane == 0) OC[s] = st.cash;
+            if (i0 < n) { OS[s * n + i0] = st.h0; PT[s * n + i0] = q0[k]; }
+            if (i1 < n) { OS[s * n + i1] = st.h1; PT[s * n + i1] = q1[k]; }
+            write_obs_row_regs<OT, IPL>(X + s * ldx, C, st.cash, st.h0, st.h1, q0[k], q1[k], ind[k],
+                                        C.ind + (size_t)(T0[s] + j + 1) * nI, lane);
+        }
+#pragma unroll
+        for (int k = 0; k < EPW; ++k) {
+            const int s = wave * EPW + k;
+            if (s >= nenv) continue;
+            const int e = ebase + s;
+            const size_t row = (size_t)j * E + e;
+            float *ga = A.action + row * n;
+            int32_t *gs = A.shares_tap ? A.shares_tap + row * n : nullptr;
+            if (!ACT[s]) {
+                // not stepped: NaN rows, done = 0, taps repeat the state
+                for (int i = lane; i < n; i += WAVE) {
+                    ga[i] = qnan;
+                    if (gs) gs[i] = OS[s * n + i];
                 }
-                if (i1 < n) {
-                    const float sz = sg1 * z1;
-                    a1 = mu[i1] + sz;
-                    lp += -0.5 * (double)z1 * (double)z1 - (double)ls1;
-                    OA[s * n + i1] = a1;
-                }
-                lp = wave_sum(lp) - half_log2pi_n;
-                const float *mk = MK + s * ldmk;
-                const float q0 = i0 < n ? mk[i0] : 0.f, q1 = i1 < n ? mk[i1] : 0.f;
-                const float r = env_step_wave(C, st[k], a0, a1, q0, q1, lane);
                 if (lane == 0) {
-                    OL[s] = (float)lp;
-                    OR[s] = r;
-                    OC[s] = st[k].cash;
+                    A.logp[row] = qnan;
+                    A.reward[row] = qnan;
+                    A.done[row] = 0;
+                    if (A.cash_tap) A.cash_tap[row] = OC[s];
                 }
-                if (i0 < n) OS[s * n + i0] = st[k].h0;
-                if (i1 < n) OS[s * n + i1] = st[k].h1;
-                write_obs_row<OT>(X + s * ldx, C, st[k].cash, st[k].h0, st[k].h1, mk, mk + n, lane);
+                continue;
+            }
+            if (i0 < n) ga[i0] = a0[k];
+            if (i1 < n) ga[i1] = a1[k];
+            if (gs) {
+                if (i0 < n) gs[i0] = OS[s * n + i0];
+                if (i1 < n) gs[i1] = OS[s * n + i1];
+            }
+            if (lane == 0) {
+                A.logp[row] = (float)lpv[k];
+                A.reward[row] = rw[k];
+                A.done[row] = done;
+                if (A.cash_tap) A.cash_tap[row] = OC[s];
+            }
+            // observation row j+1 (or the bootstrap observation)
+            if (j + 1 < A.L) {
+                if (A.obs) store_obs_row((OT *)A.obs + (row + E) * A.ld_obs, s);
+            } else if (A.obs_last) {
+                store_obs_row((OT *)A.obs_last + (size_t)e * A.ld_obs, s);
             }
         }
         __syncthreads();
     }
 
-    // ---- epilogue: state back to HBM; envs that were not stepped get NaN ---
-    if (!io) {
-#pragma unroll
-        for (int k = 0; k < EPW; ++k) {
-            const int s = wave * EPW + k;
-            if (!ACT[s]) continue;
-            const int e = ebase + s;
-            if (lane == 0) {
-                A.cash[e] = st[k].cash;
-                A.t[e] = T0[s] + A.L;
-            }
-            if (i0 < n) A.shares[(size_t)e * n + i0] = st[k].h0;
-            if (i1 < n) A.shares[(size_t)e * n + i1] = st[k].h1;
+    // ---- epilogue: state back to HBM -----------------------------------------
+    for (int k = 0; k < EPW; ++k) {
+        const int s = wave * EPW + k;
+        if (s >= nenv || !ACT[s]) continue;
+        const int e = ebase + s;
+        if (lane == 0) {
+            A.cash[e] = OC[s];
+            A.t[e] = T0[s] + A.L;
         }
-    } else {
-        const float qnan = __builtin_nanf("");
-        for (int s = 0; s < nenv; ++s) {
-            if (ACT[s]) continue;
-            for (int j = 0; j < A.L; ++j) {
-                const size_t row = (size_t)j * E + ebase + s;
-                for (int i = lane; i < n; i += WAVE) A.action[row * n + i] = qnan;
-                if (lane == 0) {
-                    A.logp[row] = qnan;
-                    A.reward[row] = qnan;
-                    A.done[row] = 0;
-                }
-            }
-        }
+        for (int i = lane; i < n; i += WAVE) A.shares[(size_t)e * n + i] = OS[s * n + i];
     }
 }
 
@@ -429,19 +402,14 @@ static hipError_t launch_cfg(RolloutArgs &a, hipStream_t s)
         a.ldh = P.H1 + 4;
         a.ldmu = P.n + (4 - P.n % 4) % 4;
     }
-    a.mk_vec = (C.n % 4 == 0) && (C.nI % 4 == 0) && ((uintptr_t)C.price % 16 == 0) &&
-               ((uintptr_t)C.ind % 16 == 0);
-    a.ldmk = C.n + C.nI;
-    if (!a.mk_vec) a.ldmk = (a.ldmk + 3) & ~3;
     size_t off = 0;
     a.lds_X = off;   off = align16(off + (size_t)MB * a.ldx * esz);
     a.lds_H = off;   off = align16(off + (size_t)MB * a.ldh * esz);
     a.lds_MU = off;  off = align16(off + (size_t)MB * a.ldmu * 4);
-    a.lds_MK = off;  off = align16(off + (size_t)MB * a.ldmk * 4);
-    a.lds_OA = off;  off = align16(off + (size_t)MB * C.n * 4);
     a.lds_OS = off;  off = align16(off + (size_t)MB * C.n * 4);
+    a.lds_PT = off;  off = align16(off + (size_t)MB * C.n * 4);
     a.lds_scal = off;
-    off = align16(off + (size_t)MB * (8 + 8 + 4 + 4 + 4));
+    off = align16(off + (size_t)MB * (8 + 8 + 4));
     a.lds_bytes = off;
     if (off > LDS_LIMIT) return hipErrorInvalidConfiguration;
     a.blocks_per_agent = (a.envs_per_agent + MB - 1) / MB;
@@ -452,7 +420,7 @@ static hipError_t launch_cfg(RolloutArgs &a, hipStream_t s)
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)off);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k, dim3(nblk), dim3((NWM + 1) * WAVE), off, s, a);
+    hipLaunchKernelGGL(k, dim3(nblk), dim3(NWM * WAVE), off, s, a);
     return hipGetLastError();
 }
 
