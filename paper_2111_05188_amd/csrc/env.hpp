@@ -1,8 +1,11 @@
-// The stock-trading env step on one wavefront (paper Section 3, eqs. (2)-(4)).
+// The stock-trading env step (paper Section 3, eqs. (2)-(4)) on half a
+// wavefront.
 //
-// One 64-lane wavefront owns one env.  Lane l holds stocks 2l and 2l+1
-// (n <= 128), so stock order equals (lane, slot) order and lane-order prefix
-// sums are prefix sums in stock index order.
+// A 64-lane wavefront steps two envs at once: lanes 0-31 own env A, lanes
+// 32-63 env B.  Lane h of a half holds stocks 4h .. 4h+3 (n <= 128), so stock
+// order equals (lane, slot) order and a half's lane-order prefix sum is a
+// prefix sum in stock index order.  Every collective below works on both
+// halves independently, so the two envs share one instruction stream.
 //
 //   k_i  = trunc(clip(a_i, -1, 1) * hmax)   (fp32 product, NaN -> 0)
 //   sells: s_i = min(-k_i, h_i) at p_t, credit S*(1 - fee)
@@ -13,7 +16,7 @@
 //
 // Every p*q with q <= 128 and p in [2^-2, 2^13) is a multiple of 2^-25 below
 // 2^20, so S, G and every partial sum of them are exact in fp64 in any order:
-// the wave-level sums and scans below give the same bits as a serial loop.
+// the lane-level sums and scans below give the same bits as a serial loop.
 // The buy test fma(f_b, X, -b_s) <= 0 rounds once, so its sign is the sign
 // of the exact f_b*X - b_s.  Balances therefore agree bit for bit with a
 // serial implementation, and so do share counts.
@@ -24,118 +27,193 @@
 
 namespace tpk {
 
+constexpr int HALF = 32;   // lanes per env
+constexpr int SPL = 4;     // stocks per lane
+
 __device__ __forceinline__ int shares_from_action(float a, int hmax)
 {
     const float u = isnan(a) ? 0.0f : fminf(fmaxf(a, -1.0f), 1.0f);
     return (int)truncf(u * (float)hmax);
 }
 
-// Per-env state held by the owning wave: lane l keeps stocks 2l, 2l+1.
-struct LaneEnv {
-    double cash;   // balance (same on every lane)
-    int h0, h1;    // holdings (0 for stocks >= n)
-    float p0, p1;  // prices at the current row (0 for stocks >= n)
+// ---------------------------------------------------------------------------
+// Half-wave collectives (all 64 lanes active; each half independent)
+// ---------------------------------------------------------------------------
+
+// Inclusive prefix sum within each 32-lane half, in lane order.
+__device__ __forceinline__ double half_inclusive_scan(double v)
+{
+    v += dpp_f64<DPP_ROW_SHR + 1>(v);
+    v += dpp_f64<DPP_ROW_SHR + 2>(v);
+    v += dpp_f64<DPP_ROW_SHR + 4>(v);
+    v += dpp_f64<DPP_ROW_SHR + 8>(v);
+    v += dpp_f64<DPP_ROW_BCAST15, 0xA>(v);   // row 0 -> row 1, row 2 -> row 3
+    return v;
+}
+
+// The value of lane `la` (half A) or 32 + `lb` (half B), seen by its half.
+template <typename T>
+__device__ __forceinline__ T half_value(T v, int la, int lb, bool upper)
+{
+    const T a = lane_value(v, la), b = lane_value(v, HALF + lb);
+    return upper ? b : a;
+}
+
+__device__ __forceinline__ double half_sum(double v, bool upper)
+{
+    v = half_inclusive_scan(v);
+    return half_value(v, HALF - 1, HALF - 1, upper);
+}
+
+// Per-env state held by the owning half: lane h keeps stocks 4h .. 4h+3.
+struct HalfEnv {
+    double cash;      // balance (same on every lane of the half)
+    int h[SPL];       // holdings (0 for stocks >= n)
+    float p[SPL];     // prices at the current row (0 for stocks >= n)
 };
 
-// One transition.  a0/a1: raw actions of this lane's stocks; q0/q1: their
-// prices at the next row.  Returns the reward (same on every lane).  Must be
-// called by all 64 lanes.
-__device__ __forceinline__ float env_step_wave(const EnvConst &C, LaneEnv &s,
-                                               float a0, float a1, float q0,
-                                               float q1, int lane)
+// One transition of the env owned by this lane's half.  a[c]: raw actions of
+// this lane's stocks; q[c]: their prices at the next row (0 for stocks >= n).
+// `live`: this half holds an env to step (an idle half trades nothing).
+// Returns the reward (same on every lane of the half).  All 64 lanes call it.
+__device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
+                                               const float (&a)[SPL],
+                                               const float (&q)[SPL], bool live,
+                                               int lane)
 {
-    const int n = C.n;
-    const bool v0 = 2 * lane < n, v1 = 2 * lane + 1 < n;
-    const int k0 = v0 ? shares_from_action(a0, C.hmax) : 0;
-    const int k1 = v1 ? shares_from_action(a1, C.hmax) : 0;
-    const double pa = (double)s.p0, pb = (double)s.p1;
+    const bool upper = lane >= HALF;
+    const int hl = lane & (HALF - 1);
+    const double fb = C.f_b;
+    int k[SPL];
+    double pd[SPL];
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        const bool v = live && SPL * hl + c < C.n;
+        k[c] = v ? shares_from_action(a[c], C.hmax) : 0;
+        pd[c] = (double)s.p[c];
+    }
 
     // total asset before the step (fp64; products h*p are exact)
-    const double V = s.cash + wave_sum((double)s.h0 * pa + (double)s.h1 * pb);
+    double hv = 0.0;
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) hv += (double)s.h[c] * pd[c];
+    const double V = s.cash + half_sum(hv, upper);
 
     // sells
-    const int sa = k0 < 0 ? min(-k0, s.h0) : 0;
-    const int sb = k1 < 0 ? min(-k1, s.h1) : 0;
-    int h0 = s.h0 - sa, h1 = s.h1 - sb;
-    const double S = wave_sum(pa * (double)sa + pb * (double)sb);  // exact
+    double sv = 0.0;
+    int h[SPL];
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        const int sc = k[c] < 0 ? min(-k[c], s.h[c]) : 0;
+        h[c] = s.h[c] - sc;
+        sv += pd[c] * (double)sc;
+    }
+    const double S = half_sum(sv, upper);   // exact
     const double b_s = fma(S, C.f_s, s.cash);
-    const double fb = C.f_b;
 
     // buys: resolve the greedy in ascending stock order in rounds.  A round
     // first drops every pending stock that cannot pay for one share at the
     // current G (G only grows, so it never will), then finds the first
     // pending stock whose full order no longer fits: every pending stock
     // before it is bought in full, it gets its largest affordable q, and the
-    // next round continues after it.
-    const double c0 = k0 > 0 ? pa * (double)k0 : 0.0;
-    const double c1 = k1 > 0 ? pb * (double)k1 : 0.0;
-    bool pend0 = k0 > 0, pend1 = k1 > 0;
-    int q0n = 0, q1n = 0;
+    // next round continues after it.  Both halves run their rounds together;
+    // a half without pending stocks idles.
+    double cost[SPL];
+    bool pend[SPL];
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        cost[c] = k[c] > 0 ? pd[c] * (double)k[c] : 0.0;
+        pend[c] = k[c] > 0;
+    }
     double G = 0.0;
     for (bool first = true;; first = false) {
-        if (!first) {
-            if (pend0 && fma(fb, G + pa, -b_s) > 0.0) pend0 = false;
-            if (pend1 && fma(fb, G + pb, -b_s) > 0.0) pend1 = false;
+        bool any = false;
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            if (!first && pend[c] && fma(fb, G + pd[c], -b_s) > 0.0) pend[c] = false;
+            any |= pend[c];
         }
-        if (__ballot(pend0 || pend1) == 0) break;
-        const double cc0 = pend0 ? c0 : 0.0, cc1 = pend1 ? c1 : 0.0;
-        const double tot = cc0 + cc1;
-        const double incl = wave_inclusive_scan(tot);
-        const double base = G + (incl - tot);  // exact
-        const double P0 = base + cc0, P1 = P0 + cc1;
-        const bool bad0 = pend0 && fma(fb, P0, -b_s) > 0.0;
-        const bool bad1 = pend1 && fma(fb, P1, -b_s) > 0.0;
-        const uint64_t m = __ballot(bad0 || bad1);
-        if (m == 0) {
-            if (pend0) q0n = k0;
-            if (pend1) q1n = k1;
-            G = lane_value(base + tot, WAVE - 1);
-            break;
+        if (__ballot(any) == 0) break;
+        // lane-local inclusive prefix of the pending full costs, then the
+        // half's exclusive prefix of lane totals (all exact)
+        double pre[SPL], acc = 0.0;
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            acc += pend[c] ? cost[c] : 0.0;
+            pre[c] = acc;
         }
-        const int fl = __ffsll((unsigned long long)m) - 1;
-        const bool f_is_1 = lane_value(bad0 ? 0 : 1, fl) != 0;
+        const double incl = half_inclusive_scan(acc);
+        const double base = G + (incl - acc);
+        int firstbad = SPL;
+#pragma unroll
+        for (int c = SPL - 1; c >= 0; --c)
+            if (pend[c] && fma(fb, base + pre[c], -b_s) > 0.0) firstbad = c;
+        const uint64_t m = __ballot(firstbad < SPL);
+        const uint32_t ma = (uint32_t)m, mb = (uint32_t)(m >> 32);
+        const uint32_t mine = upper ? mb : ma;
+        // a half with no misfit buys every pending stock in full
+        const double total = half_value(base + acc, HALF - 1, HALF - 1, upper);
+        const int fla = ma ? __ffs(ma) - 1 : 0, flb = mb ? __ffs(mb) - 1 : 0;
+        const int fl = upper ? flb : fla;
+        const int cf = half_value(firstbad, fla, flb, upper);
         // stocks before the first misfit are bought in full
-        if (lane < fl) {
-            if (pend0) q0n = k0;
-            if (pend1) q1n = k1;
-            pend0 = pend1 = false;
-        } else if (lane == fl && f_is_1 && pend0) {
-            q0n = k0;
-            pend0 = false;
-        }
-        const double Gf = lane_value(f_is_1 ? P1 - cc1 : P0 - cc0, fl);
-        const double pf = lane_value(f_is_1 ? pb : pa, fl);
-        const int kf = lane_value(f_is_1 ? k1 : k0, fl);
-        // largest q in [0, kf-1] with f_b (Gf + pf q) <= b_s: estimate, then
-        // step to the exact boundary with the sign-exact test
-        const double rem = fma(-fb, Gf, b_s);
-        double est = floor(rem / (pf * fb));
-        est = fmin(fmax(est, 0.0), (double)(kf - 1));
-        int q = (int)est;
-        while (q < kf - 1 && fma(fb, Gf + pf * (double)(q + 1), -b_s) <= 0.0) ++q;
-        while (q > 0 && fma(fb, Gf + pf * (double)q, -b_s) > 0.0) --q;
-        G = Gf + pf * (double)q;
-        if (lane == fl) {
-            if (f_is_1) {
-                q1n = q;
-                pend1 = false;
-            } else {
-                q0n = q;
-                pend0 = false;
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            if (pend[c] && (mine == 0 || hl < fl || (hl == fl && c < cf))) {
+                h[c] += k[c];
+                pend[c] = false;
             }
         }
+        // the misfit stock: largest q in [0, kf-1] with f_b (Gf + pf q) <= b_s
+        double gf_l = base, pf_l = pd[0];
+        int kf_l = k[0];
+#pragma unroll
+        for (int c = 0; c < SPL; ++c)
+            if (c == firstbad) {
+                gf_l = base + pre[c] - cost[c];
+                pf_l = pd[c];
+                kf_l = k[c];
+            }
+        const double Gf = half_value(gf_l, fla, flb, upper);
+        const double pf = half_value(pf_l, fla, flb, upper);
+        const int kf = mine ? half_value(kf_l, fla, flb, upper) : 1;
+        int qf = 0;
+        if (mine) {
+            const double rem = fma(-fb, Gf, b_s);
+            double est = floor(rem / (pf * fb));
+            est = fmin(fmax(est, 0.0), (double)(kf - 1));
+            qf = (int)est;
+        }
+        // the two halves step their estimates to the exact boundary together
+        for (;;) {
+            const bool up = mine && qf < kf - 1 && fma(fb, Gf + pf * (double)(qf + 1), -b_s) <= 0.0;
+            const bool dn = mine && !up && qf > 0 && fma(fb, Gf + pf * (double)qf, -b_s) > 0.0;
+            if (__ballot(up || dn) == 0) break;
+            qf += up ? 1 : (dn ? -1 : 0);
+        }
+        G = mine ? Gf + pf * (double)qf : total;
+        if (mine && hl == fl) {
+#pragma unroll
+            for (int c = 0; c < SPL; ++c)
+                if (c == cf) {
+                    h[c] += qf;
+                    pend[c] = false;
+                }
+        }
     }
-    h0 += q0n;
-    h1 += q1n;
     double nb = fma(-fb, G, b_s);
     if (nb < 0.0) nb = 0.0;
 
-    const double V1 = nb + wave_sum((double)h0 * (double)q0 + (double)h1 * (double)q1);
+    double hv1 = 0.0;
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) hv1 += (double)h[c] * (double)q[c];
+    const double V1 = nb + half_sum(hv1, upper);
     s.cash = nb;
-    s.h0 = h0;
-    s.h1 = h1;
-    s.p0 = q0;
-    s.p1 = q1;
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        s.h[c] = h[c];
+        s.p[c] = q[c];
+    }
     return (float)(C.reward_scale * (V1 - V));
 }
 
@@ -144,62 +222,37 @@ template <> __device__ __forceinline__ float obs_cvt<float>(float x) { return x;
 template <> __device__ __forceinline__ __bf16 obs_cvt<__bf16>(float x) { return to_bf16(x); }
 
 // Observation row [b*cs, p*ps (n), h*ss (n), ind (nI), 0 ... K_pad) written
-// to `row` (LDS or global).  prow: the n prices of the observed row; irow:
-// its nI indicators.  All 64 lanes call it.
-template <typename T>
-__device__ __forceinline__ void write_obs_row(T *row, const EnvConst &C,
-                                              double cash, int h0, int h1,
-                                              const float *prow,
-                                              const float *irow, int lane)
-{
-    const int n = C.n, nI = C.nI, S = 1 + 2 * n + nI;
-    const int i0 = 2 * lane, i1 = i0 + 1;
-    if (lane == 0) row[0] = obs_cvt<T>((float)(cash * (double)C.cash_scale));
-    if (i0 < n) {
-        row[1 + i0] = obs_cvt<T>(prow[i0] * C.price_scale);
-        row[1 + n + i0] = obs_cvt<T>((float)h0 * C.share_scale);
-    }
-    if (i1 < n) {
-        row[1 + i1] = obs_cvt<T>(prow[i1] * C.price_scale);
-        row[1 + n + i1] = obs_cvt<T>((float)h1 * C.share_scale);
-    }
-    for (int k = lane; k < nI; k += WAVE) row[1 + 2 * n + k] = obs_cvt<T>(irow[k]);
-    for (int k = S + lane; k < C.K_pad; k += WAVE) row[k] = obs_cvt<T>(0.0f);
-}
-
-// The same row with the next-row prices and the first 64*IPL indicators
-// already in registers (q0/q1: prices of this lane's stocks; ind[m]:
-// indicator lane + 64 m); indicators beyond that are read from irow.
+// by one half: prices and holdings of the lane's stocks, `ind[m]` =
+// indicator hl + 32 m for m < IPL, the rest read from `irow` (LDS or
+// global).  All lanes of the half call it.
 template <typename T, int IPL>
-__device__ __forceinline__ void write_obs_row_regs(T *row, const EnvConst &C,
-                                                   double cash, int h0, int h1,
-                                                   float q0, float q1,
-                                                   const float (&ind)[IPL],
-                                                   const float *irow, int lane)
+__device__ __forceinline__ void write_obs_half(T *row, const EnvConst &C, double cash,
+                                               const int (&h)[SPL], const float (&p)[SPL],
+                                               const float (&ind)[IPL], const float *irow,
+                                               int hl)
 {
     const int n = C.n, nI = C.nI, S = 1 + 2 * n + nI;
-    const int i0 = 2 * lane, i1 = i0 + 1;
-    if (lane == 0) row[0] = obs_cvt<T>((float)(cash * (double)C.cash_scale));
-    if (i0 < n) {
-        row[1 + i0] = obs_cvt<T>(q0 * C.price_scale);
-        row[1 + n + i0] = obs_cvt<T>((float)h0 * C.share_scale);
-    }
-    if (i1 < n) {
-        row[1 + i1] = obs_cvt<T>(q1 * C.price_scale);
-        row[1 + n + i1] = obs_cvt<T>((float)h1 * C.share_scale);
+    if (hl == 0) row[0] = obs_cvt<T>((float)(cash * (double)C.cash_scale));
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        const int i = SPL * hl + c;
+        if (i < n) {
+            row[1 + i] = obs_cvt<T>(p[c] * C.price_scale);
+            row[1 + n + i] = obs_cvt<T>((float)h[c] * C.share_scale);
+        }
     }
     T *ri = row + 1 + 2 * n;
 #pragma unroll
     for (int m = 0; m < IPL; ++m) {
-        const int k = lane + WAVE * m;
-        if (k < nI) ri[k] = obs_cvt<T>(ind[m]);
+        const int kk = hl + HALF * m;
+        if (kk < nI) ri[kk] = obs_cvt<T>(ind[m]);
     }
-    for (int k = WAVE * IPL + lane; k < nI; k += WAVE) ri[k] = obs_cvt<T>(irow[k]);
-    for (int k = S + lane; k < C.K_pad; k += WAVE) row[k] = obs_cvt<T>(0.0f);
+    for (int kk = HALF * IPL + hl; kk < nI; kk += HALF) ri[kk] = obs_cvt<T>(irow[kk]);
+    for (int kk = S + hl; kk < C.K_pad; kk += HALF) row[kk] = obs_cvt<T>(0.0f);
 }
 
-// Copy `bytes` (a multiple of 16) from LDS to global with 16-byte accesses,
-// lanes [l0, l0 + nl) of the calling group participating.
+// Copy `bytes` (a multiple of 16) with 16-byte accesses, lanes l = 0..nl-1
+// of the calling group participating.
 __device__ __forceinline__ void copy16(void *dst, const void *src, size_t bytes,
                                        int l, int nl)
 {

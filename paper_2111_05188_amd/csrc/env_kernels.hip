@@ -1,13 +1,20 @@
 // Standalone env kernels: reset and one teacher-forced step.
-// One 64-lane wave per env; the observation row is assembled in LDS and
-// written to HBM with 16-byte stores.
+// Each 64-lane wave owns two envs (one per 32-lane half, 4 stocks per lane);
+// observation rows are assembled in LDS and written with 16-byte stores.
 #include "device.hpp"
 #include "env.hpp"
 #include "internal.hpp"
 
 namespace tpk {
 
-constexpr int ENV_WPB = 4;  // envs (waves) per workgroup
+constexpr int ENV_WPB = 4;              // waves per workgroup
+constexpr int ENV_EPB = 2 * ENV_WPB;    // envs per workgroup
+
+template <typename OT>
+__device__ __forceinline__ int obs_ld_lds(const EnvConst &C)
+{
+    return (C.K_pad * (int)sizeof(OT) + 15) / 16 * 16 / (int)sizeof(OT);
+}
 
 template <typename OT>
 __global__ __launch_bounds__(ENV_WPB *WAVE) void env_reset_kernel(
@@ -15,31 +22,41 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_reset_kernel(
     int E, OT *obs, int64_t ld_obs)
 {
     extern __shared__ __align__(16) uint8_t smem[];
-    const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-    const int e = blockIdx.x * ENV_WPB + wave;
-    const int ldr = (C.K_pad * (int)sizeof(OT) + 15) / 16 * 16 / (int)sizeof(OT);
-    OT *row = (OT *)smem + wave * ldr;
+    const int lane = threadIdx.x % WAVE, hl = lane % HALF;
+    const int slot = threadIdx.x / HALF;               // env of this half in the block
+    const int e = blockIdx.x * ENV_EPB + slot;
+    OT *row = (OT *)smem + slot * obs_ld_lds<OT>(C);
     if (e < E) {
         const int n = C.n;
         const int64_t tt = t0[e];
         const bool ok = tt >= 0 && tt < C.T1 - 1;
-        for (int i = lane; i < n; i += WAVE) shares[(size_t)e * n + i] = 0;
-        if (lane == 0) {
+        for (int i = hl; i < n; i += HALF) shares[(size_t)e * n + i] = 0;
+        if (hl == 0) {
             cash[e] = C.cash0;
             t[e] = ok ? tt : -1;
         }
         if (obs) {
             if (ok) {
-                write_obs_row<OT>(row, C, C.cash0, 0, 0, C.price + (size_t)tt * n,
-                                  C.ind + (size_t)tt * C.nI, lane);
+                const float *prow = C.price + (size_t)tt * n;
+                const float *irow = C.ind + (size_t)tt * C.nI;
+                int h[SPL];
+                float p[SPL], ind1[1];
+#pragma unroll
+                for (int c = 0; c < SPL; ++c) {
+                    const int i = SPL * hl + c;
+                    h[c] = 0;
+                    p[c] = i < n ? prow[i] : 0.f;
+                }
+                ind1[0] = hl < C.nI ? irow[hl] : 0.f;
+                write_obs_half<OT, 1>(row, C, C.cash0, h, p, ind1, irow, hl);
             } else {
-                for (int k = lane; k < C.K_pad; k += WAVE) row[k] = obs_cvt<OT>(0.0f);
+                for (int k = hl; k < C.K_pad; k += HALF) row[k] = obs_cvt<OT>(0.0f);
             }
         }
     }
     __syncthreads();
     if (e < E && obs)
-        copy16(obs + (size_t)e * ld_obs, row, (size_t)C.K_pad * sizeof(OT), lane, WAVE);
+        copy16(obs + (size_t)e * ld_obs, row, (size_t)C.K_pad * sizeof(OT), hl, HALF);
 }
 
 template <typename OT>
@@ -48,55 +65,69 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
     float *reward, int E, OT *obs, int64_t ld_obs)
 {
     extern __shared__ __align__(16) uint8_t smem[];
-    const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-    const int e = blockIdx.x * ENV_WPB + wave;
-    const int ldr = (C.K_pad * (int)sizeof(OT) + 15) / 16 * 16 / (int)sizeof(OT);
-    OT *row = (OT *)smem + wave * ldr;
-    if (e < E) {
-        const int n = C.n;
-        const int i0 = 2 * lane, i1 = i0 + 1;
-        const int64_t tt = t[e];
-        if (tt >= 0 && tt + 1 < C.T1) {
-            const float *p = C.price + (size_t)tt * n;
-            const float *p1 = p + n;
-            const float *ar = action + (size_t)e * n;
-            int32_t *hr = shares + (size_t)e * n;
-            LaneEnv s{cash[e], 0, 0, 0.f, 0.f};
-            float a0 = 0.f, a1 = 0.f, q0 = 0.f, q1 = 0.f;
-            if (i0 < n) { s.h0 = hr[i0]; s.p0 = p[i0]; a0 = ar[i0]; q0 = p1[i0]; }
-            if (i1 < n) { s.h1 = hr[i1]; s.p1 = p[i1]; a1 = ar[i1]; q1 = p1[i1]; }
-            const float r = env_step_wave(C, s, a0, a1, q0, q1, lane);
-            if (i0 < n) hr[i0] = s.h0;
-            if (i1 < n) hr[i1] = s.h1;
-            if (lane == 0) {
-                cash[e] = s.cash;
-                t[e] = tt + 1;
-                reward[e] = r;
-            }
-            if (obs)
-                write_obs_row<OT>(row, C, s.cash, s.h0, s.h1, p1,
-                                  C.ind + (size_t)(tt + 1) * C.nI, lane);
-        } else {
-            if (lane == 0) reward[e] = __builtin_nanf("");
-            if (obs)
-                for (int k = lane; k < C.K_pad; k += WAVE) row[k] = obs_cvt<OT>(__builtin_nanf(""));
+    const int lane = threadIdx.x % WAVE, hl = lane % HALF;
+    const int slot = threadIdx.x / HALF;
+    const int e = blockIdx.x * ENV_EPB + slot;
+    OT *row = (OT *)smem + slot * obs_ld_lds<OT>(C);
+    const int n = C.n;
+    // every lane of the wave runs the half-wave step (idle halves trade
+    // nothing); loads use valid addresses only
+    const bool in = e < E;
+    const int64_t tt = in ? t[e] : -1;
+    const bool live = in && tt >= 0 && tt + 1 < C.T1;
+    const int64_t trow = live ? tt : 0;
+    const float *p0 = C.price + (size_t)trow * n;
+    const float *p1 = p0 + (live ? n : 0);
+    HalfEnv s;
+    s.cash = live ? cash[e] : 0.0;
+    float a[SPL], q[SPL];
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        const int i = SPL * hl + c;
+        const bool v = live && i < n;
+        s.h[c] = v ? shares[(size_t)e * n + i] : 0;
+        s.p[c] = v ? p0[i] : 0.f;
+        a[c] = v ? action[(size_t)e * n + i] : 0.f;
+        q[c] = v ? p1[i] : 0.f;
+    }
+    const float r = env_step_half(C, s, a, q, live, lane);
+    if (live) {
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            const int i = SPL * hl + c;
+            if (i < n) shares[(size_t)e * n + i] = s.h[c];
         }
+        if (hl == 0) {
+            cash[e] = s.cash;
+            t[e] = tt + 1;
+            reward[e] = r;
+        }
+        if (obs) {
+            const float *irow = C.ind + (size_t)(tt + 1) * C.nI;
+            float ind1[1];
+            ind1[0] = hl < C.nI ? irow[hl] : 0.f;
+            write_obs_half<OT, 1>(row, C, s.cash, s.h, q, ind1, irow, hl);
+        }
+    } else if (in) {
+        if (hl == 0) reward[e] = __builtin_nanf("");
+        if (obs)
+            for (int k = hl; k < C.K_pad; k += HALF) row[k] = obs_cvt<OT>(__builtin_nanf(""));
     }
     __syncthreads();
-    if (e < E && obs)
-        copy16(obs + (size_t)e * ld_obs, row, (size_t)C.K_pad * sizeof(OT), lane, WAVE);
+    if (in && obs)
+        copy16(obs + (size_t)e * ld_obs, row, (size_t)C.K_pad * sizeof(OT), hl, HALF);
 }
 
 static size_t row_lds(const EnvConst &c, int esz)
 {
-    return (size_t)ENV_WPB * (((size_t)c.K_pad * esz + 15) / 16 * 16);
+    return (size_t)ENV_EPB * (((size_t)c.K_pad * esz + 15) / 16 * 16);
 }
 
 hipError_t launch_env_reset(const EnvConst &c, double *cash, int32_t *shares,
                             int64_t *t, const int64_t *t0, int E, void *obs,
                             int64_t ld_obs, int obs_bf16, hipStream_t s)
 {
-    const dim3 grid((E + ENV_WPB - 1) / ENV_WPB), block(ENV_WPB * WAVE);
+    const dim3 grid((E + ENV_EPB - 1) / ENV_EPB), block(ENV_WPB * WAVE);
     if (obs_bf16)
         hipLaunchKernelGGL(env_reset_kernel<__bf16>, grid, block, row_lds(c, 2), s, c,
                            cash, shares, t, t0, E, (__bf16 *)obs, ld_obs);
@@ -111,7 +142,7 @@ hipError_t launch_env_step(const EnvConst &c, double *cash, int32_t *shares,
                            int E, void *obs, int64_t ld_obs, int obs_bf16,
                            hipStream_t s)
 {
-    const dim3 grid((E + ENV_WPB - 1) / ENV_WPB), block(ENV_WPB * WAVE);
+    const dim3 grid((E + ENV_EPB - 1) / ENV_EPB), block(ENV_WPB * WAVE);
     if (obs_bf16)
         hipLaunchKernelGGL(env_step_kernel<__bf16>, grid, block, row_lds(c, 2), s, c,
                            cash, shares, t, action, reward, E, (__bf16 *)obs, ld_obs);

@@ -150,7 +150,8 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
 {
     constexpr int MB = EPW * NWM;
     constexpr bool BF16 = sizeof(OT) == 2;
-    constexpr int IPL = 16;  // indicators held per lane (n * n_ind <= 1024)
+    constexpr int IPL = 32;  // indicators held per lane (n * n_ind <= 1024)
+    static_assert(EPW == 1 || EPW == 2, "one env per half wave");
     extern __shared__ __align__(16) uint8_t smem[];
 
     const EnvConst &C = A.env;
@@ -188,50 +189,62 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
     const size_t E = (size_t)A.E;
     const int obs_chunks = C.K_pad * (int)sizeof(OT) / 16;
 
-    // copy the observation row of slot s from X to global row `dst`
-    auto store_obs_row = [&](OT *dst, int s) {
-        const uint4 *x = (const uint4 *)(X + s * ldx);
-        for (int c = lane; c < obs_chunks; c += WAVE) ((uint4 *)dst)[c] = x[c];
+    // this lane's half of the wave: env slot `sl` (EPW == 1 leaves the upper
+    // half idle), lane `hl` within it, stocks 4 hl .. 4 hl + 3
+    const int half = lane / HALF, hl = lane % HALF;
+    const int sl = wave * EPW + (half < EPW ? half : 0);
+    const bool mine = half < EPW && sl < nenv;
+
+    // copy slot sl's observation row from X to the global row `dst`
+    auto store_obs_row = [&](OT *dst) {
+        const uint4 *x = (const uint4 *)(X + sl * ldx);
+        for (int c = hl; c < obs_chunks; c += HALF) ((uint4 *)dst)[c] = x[c];
     };
 
-    // ---- prologue: state of the wave's envs into LDS, obs_0 into X and HBM --
+    // ---- prologue: state into LDS, obs_0 into X and HBM ----------------------
     for (int i = tid; i < MB * ldx * (int)sizeof(OT) / 16; i += blockDim.x)
         ((uint4 *)X)[i] = uint4{0, 0, 0, 0};
     __syncthreads();
-    float ls0 = 0.f, ls1 = 0.f, sg0 = 0.f, sg1 = 0.f;
-    const int i0 = 2 * lane, i1 = i0 + 1;
-    if (i0 < n) { ls0 = lsd[i0]; sg0 = expf(ls0); }
-    if (i1 < n) { ls1 = lsd[i1]; sg1 = expf(ls1); }
-    for (int k = 0; k < EPW; ++k) {
-        const int s = wave * EPW + k;
-        int64_t tt = -1;
-        int act = 0;
-        if (s < nenv) {
-            const int e = ebase + s;
-            tt = A.t[e];
-            act = tt >= 0 && tt + A.L <= C.T1 - 1;
-            // state (also for envs that are not stepped: their taps repeat it)
-            for (int i = lane; i < n; i += WAVE) OS[s * n + i] = A.shares[(size_t)e * n + i];
-            if (lane == 0) OC[s] = A.cash[e];
+    float ls[SPL], sg[SPL];
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        const int i = SPL * hl + c;
+        ls[c] = i < n ? lsd[i] : 0.f;
+        sg[c] = expf(ls[c]);
+    }
+    bool live = false;   // this half's env is stepped
+    if (mine) {
+        const int e = ebase + sl;
+        const int64_t tt = A.t[e];
+        live = tt >= 0 && tt + A.L <= C.T1 - 1;
+        // state (also for envs that are not stepped: their taps repeat it)
+        for (int i = hl; i < n; i += HALF) OS[sl * n + i] = A.shares[(size_t)e * n + i];
+        if (hl == 0) {
+            OC[sl] = A.cash[e];
+            T0[sl] = tt;
+            ACT[sl] = live;
         }
-        if (lane == 0) {
-            T0[s] = tt;
-            ACT[s] = act;
-        }
-        if (act) {
+        if (live) {
             const float *prow = C.price + (size_t)tt * n;
-            int h0 = 0, h1 = 0;
-            if (i0 < n) { h0 = OS[s * n + i0]; PT[s * n + i0] = prow[i0]; }
-            if (i1 < n) { h1 = OS[s * n + i1]; PT[s * n + i1] = prow[i1]; }
-            write_obs_row<OT>(X + s * ldx, C, OC[s], h0, h1, prow, C.ind + (size_t)tt * nI, lane);
-            if (A.obs) store_obs_row((OT *)A.obs + ((size_t)ebase + s) * A.ld_obs, s);
+            int h[SPL];
+            float p[SPL], ind1[1];
+#pragma unroll
+            for (int c = 0; c < SPL; ++c) {
+                const int i = SPL * hl + c;
+                h[c] = i < n ? OS[sl * n + i] : 0;
+                p[c] = i < n ? prow[i] : 0.f;
+                if (i < n) PT[sl * n + i] = p[c];
+            }
+            const float *irow = C.ind + (size_t)tt * nI;
+            ind1[0] = hl < nI ? irow[hl] : 0.f;
+            write_obs_half<OT, 1>(X + sl * ldx, C, OC[sl], h, p, ind1, irow, hl);
+            if (A.obs) store_obs_row((OT *)A.obs + ((size_t)ebase + sl) * A.ld_obs);
         }
     }
     __syncthreads();
 
     const double half_log2pi_n = 0.5 * (double)n * 1.8378770664093454836;
     const float qnan = __builtin_nanf("");
-    (void)qnan;
 
     for (int j = 0; j < A.L; ++j) {
         // ---- actor ---------------------------------------------------------
@@ -258,125 +271,112 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
         __syncthreads();
 
         // ---- sampling, env step, trajectory rows, next observation ---------
-        // Three passes over the wave's envs so that every load is issued
-        // before any store (vmcnt counts both, in issue order): next-row
-        // market loads; sampling, trade and the next observation in LDS;
-        // trajectory stores.
+        // Both envs of the wave are stepped together (one per half).  Order:
+        // next-row market loads first, then the compute, then the stores, so
+        // that every load is issued before any store (vmcnt counts both, in
+        // issue order).
         const uint32_t step = (uint32_t)(A.step0 + (uint64_t)j);
         const uint8_t done = (uint8_t)(A.step0 + (uint64_t)j + 1 == (uint64_t)C.horizon);
-        float q0[EPW], q1[EPW], ind[EPW][IPL];
-        // branch-free: every lane loads from a valid address (clamped index,
-        // row 0 for an env that is not stepped), so the loads issue back to
-        // back instead of each waiting at a branch join
+        // branch-free loads from valid addresses (clamped index; row 0 for a
+        // half without a stepped env), so they issue back to back
+        const int64_t t1 = live ? T0[sl] + j + 1 : 0;
+        const float *pr = C.price + (size_t)t1 * n;
+        const float *ir = nI > 0 ? C.ind + (size_t)t1 * nI : pr;
+        const int last = (nI > 0 ? nI : n) - 1;
+        float q[SPL], ind[IPL];
 #pragma unroll
-        for (int k = 0; k < EPW; ++k) {
-            const int s = wave * EPW + k;
-            const int64_t t1 = ACT[s] ? T0[s] + j + 1 : 0;
-            const float *pr = C.price + (size_t)t1 * n;
-            const float *ir = nI > 0 ? C.ind + (size_t)t1 * nI : pr;
-            const int last = (nI > 0 ? nI : n) - 1;
-            q0[k] = pr[min(i0, n - 1)];
-            q1[k] = pr[min(i1, n - 1)];
+        for (int c = 0; c < SPL; ++c) q[c] = pr[min(SPL * hl + c, n - 1)];
 #pragma unroll
-            for (int m = 0; m < IPL; ++m) ind[k][m] = ir[min(lane + WAVE * m, last)];
+        for (int m = 0; m < IPL; ++m) ind[m] = ir[min(hl + HALF * m, last)];
+
+        // Philox counter (i/4, env, step, agent): lane hl owns stocks 4 hl ..
+        // 4 hl + 3 = counter hl, the two Box-Muller pairs of its 4 words
+        const int e = ebase + sl;
+        const U4 w = philox4x32_10(U4{(uint32_t)hl, (uint32_t)e, step, (uint32_t)agent},
+                                   A.key_lo, A.key_hi);
+        float z[SPL];
+        box_muller(uniform_open01(w.x), uniform_open01(w.y), z[0], z[1]);
+        box_muller(uniform_open01(w.z), uniform_open01(w.w), z[2], z[3]);
+        const float *mu = MU + sl * ldmu;
+        HalfEnv st;
+        st.cash = live ? OC[sl] : 0.0;
+        float a[SPL];
+        double lp = 0.0;
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            const int i = SPL * hl + c;
+            const bool v = live && i < n;
+            a[c] = v ? mu[i] + sg[c] * z[c] : 0.f;
+            if (v) lp += -0.5 * (double)z[c] * (double)z[c] - (double)ls[c];
+            st.h[c] = v ? OS[sl * n + i] : 0;
+            st.p[c] = v ? PT[sl * n + i] : 0.f;
+            if (!v) q[c] = 0.f;
         }
-        float a0[EPW], a1[EPW], rw[EPW];
-        double lpv[EPW];
+        lp = half_sum(lp, half != 0) - half_log2pi_n;
+        const float r = env_step_half(C, st, a, q, live, lane);
+        if (live) {
+            if (hl == 0) OC[sl] = st.cash;
 #pragma unroll
-        for (int k = 0; k < EPW; ++k) {
-            const int s = wave * EPW + k;
-            a0[k] = a1[k] = rw[k] = 0.f;
-            lpv[k] = 0.0;
-            if (!ACT[s]) continue;
-            const int e = ebase + s;
-            // Philox counter (i/4, env, step, agent): lane l owns stocks 2l,
-            // 2l+1 = counter l/2, Box-Muller pair l%2
-            const U4 w = philox4x32_10(U4{(uint32_t)(lane >> 1), (uint32_t)e, step, (uint32_t)agent},
-                                       A.key_lo, A.key_hi);
-            const bool second = lane & 1;
-            float z0, z1;
-            box_muller(uniform_open01(second ? w.z : w.x), uniform_open01(second ? w.w : w.y), z0, z1);
-            const float *mu = MU + s * ldmu;
-            LaneEnv st{OC[s], 0, 0, 0.f, 0.f};
-            double lp = 0.0;
-            if (i0 < n) {
-                const float sz = sg0 * z0;
-                a0[k] = mu[i0] + sz;
-                lp += -0.5 * (double)z0 * (double)z0 - (double)ls0;
-                st.h0 = OS[s * n + i0];
-                st.p0 = PT[s * n + i0];
+            for (int c = 0; c < SPL; ++c) {
+                const int i = SPL * hl + c;
+                if (i < n) {
+                    OS[sl * n + i] = st.h[c];
+                    PT[sl * n + i] = q[c];
+                }
             }
-            if (i1 < n) {
-                const float sz = sg1 * z1;
-                a1[k] = mu[i1] + sz;
-                lp += -0.5 * (double)z1 * (double)z1 - (double)ls1;
-                st.h1 = OS[s * n + i1];
-                st.p1 = PT[s * n + i1];
-            }
-            lpv[k] = wave_sum(lp) - half_log2pi_n;
-            if (i0 >= n) q0[k] = 0.f;
-            if (i1 >= n) q1[k] = 0.f;
-            rw[k] = env_step_wave(C, st, a0[k], a1[k], q0[k], q1[k], lane);
-            if (lane == 0) OC[s] = st.cash;
-            if (i0 < n) { OS[s * n + i0] = st.h0; PT[s * n + i0] = q0[k]; }
-            if (i1 < n) { OS[s * n + i1] = st.h1; PT[s * n + i1] = q1[k]; }
-            write_obs_row_regs<OT, IPL>(X + s * ldx, C, st.cash, st.h0, st.h1, q0[k], q1[k], ind[k],
-                                        C.ind + (size_t)(T0[s] + j + 1) * nI, lane);
+            write_obs_half<OT, IPL>(X + sl * ldx, C, st.cash, st.h, q, ind, ir, hl);
         }
-#pragma unroll
-        for (int k = 0; k < EPW; ++k) {
-            const int s = wave * EPW + k;
-            if (s >= nenv) continue;
-            const int e = ebase + s;
+
+        // trajectory row j; observation row j+1 (or the bootstrap one)
+        if (mine) {
             const size_t row = (size_t)j * E + e;
             float *ga = A.action + row * n;
             int32_t *gs = A.shares_tap ? A.shares_tap + row * n : nullptr;
-            if (!ACT[s]) {
+            if (!live) {
                 // not stepped: NaN rows, done = 0, taps repeat the state
-                for (int i = lane; i < n; i += WAVE) {
+                for (int i = hl; i < n; i += HALF) {
                     ga[i] = qnan;
-                    if (gs) gs[i] = OS[s * n + i];
+                    if (gs) gs[i] = OS[sl * n + i];
                 }
-                if (lane == 0) {
+                if (hl == 0) {
                     A.logp[row] = qnan;
                     A.reward[row] = qnan;
                     A.done[row] = 0;
-                    if (A.cash_tap) A.cash_tap[row] = OC[s];
+                    if (A.cash_tap) A.cash_tap[row] = OC[sl];
                 }
-                continue;
-            }
-            if (i0 < n) ga[i0] = a0[k];
-            if (i1 < n) ga[i1] = a1[k];
-            if (gs) {
-                if (i0 < n) gs[i0] = OS[s * n + i0];
-                if (i1 < n) gs[i1] = OS[s * n + i1];
-            }
-            if (lane == 0) {
-                A.logp[row] = (float)lpv[k];
-                A.reward[row] = rw[k];
-                A.done[row] = done;
-                if (A.cash_tap) A.cash_tap[row] = OC[s];
-            }
-            // observation row j+1 (or the bootstrap observation)
-            if (j + 1 < A.L) {
-                if (A.obs) store_obs_row((OT *)A.obs + (row + E) * A.ld_obs, s);
-            } else if (A.obs_last) {
-                store_obs_row((OT *)A.obs_last + (size_t)e * A.ld_obs, s);
+            } else {
+#pragma unroll
+                for (int c = 0; c < SPL; ++c) {
+                    const int i = SPL * hl + c;
+                    if (i < n) {
+                        ga[i] = a[c];
+                        if (gs) gs[i] = st.h[c];
+                    }
+                }
+                if (hl == 0) {
+                    A.logp[row] = (float)lp;
+                    A.reward[row] = r;
+                    A.done[row] = done;
+                    if (A.cash_tap) A.cash_tap[row] = st.cash;
+                }
+                if (j + 1 < A.L) {
+                    if (A.obs) store_obs_row((OT *)A.obs + (row + E) * A.ld_obs);
+                } else if (A.obs_last) {
+                    store_obs_row((OT *)A.obs_last + (size_t)e * A.ld_obs);
+                }
             }
         }
         __syncthreads();
     }
 
     // ---- epilogue: state back to HBM -----------------------------------------
-    for (int k = 0; k < EPW; ++k) {
-        const int s = wave * EPW + k;
-        if (s >= nenv || !ACT[s]) continue;
-        const int e = ebase + s;
-        if (lane == 0) {
-            A.cash[e] = OC[s];
-            A.t[e] = T0[s] + A.L;
+    if (mine && live) {
+        const int e = ebase + sl;
+        if (hl == 0) {
+            A.cash[e] = OC[sl];
+            A.t[e] = T0[sl] + A.L;
         }
-        for (int i = lane; i < n; i += WAVE) A.shares[(size_t)e * n + i] = OS[s * n + i];
+        for (int i = hl; i < n; i += HALF) A.shares[(size_t)e * n + i] = OS[sl * n + i];
     }
 }
 
