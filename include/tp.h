@@ -21,8 +21,11 @@
  *    calling thread.  Argument checks run on the host before any launch;
  *    a launch failure reported by the HIP runtime gives TP_EHIP.  Faults
  *    inside a kernel surface at the caller's next synchronisation.
- *  - Pointers must be 16-byte aligned.  Input and output buffers must not
- *    overlap, except the env state, which is read and updated in place.
+ *  - Pointers must be aligned to their element size; observation buffers
+ *    to 16 bytes with a row pitch ld_obs that is a multiple of 8 elements,
+ *    the packed actor buffer to 256 bytes.  Misalignment gives TP_EINVAL.
+ *    Input and output buffers must not overlap, except the env state,
+ *    which is read and updated in place.
  *  - Calls on different streams with disjoint buffers are independent.
  *    Results are deterministic: the same inputs give bitwise identical
  *    outputs (no floating-point atomics).

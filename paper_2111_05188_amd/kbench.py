@@ -1,0 +1,108 @@
+"""Per-kernel bandwidth benchmark of the standalone HBM-bound kernels.
+
+    python -m paper_2111_05188_amd.kbench [--envs 65536] [--iters 20]
+
+Times, with HIP events on the launch stream:
+  * env_step: one teacher-forced transition of every env of the 100-stock
+    minute workload (bf16 observation written), at the 65,536-env stress
+    shape by default, where the rows touched per launch exceed the 256 MB
+    last-level cache;
+  * gae: the GAE scan over a 390 x E rollout;
+  * copy: a plain device-to-device copy of 1 GiB (the reference kernel used
+    to calibrate HBM byte counters: FETCH_SIZE and WRITE_SIZE of this copy
+    should each read 1 GiB per launch).
+
+Algorithmic bytes per env (env_step): action n*4 in; holdings 2*n*4 and
+balance/time 2*(8+8) in and out; prices of rows t and t+1 2*n*4; indicators
+of row t+1 n*I*4; observation S*2 out; reward 4 out.
+GAE per env-step: reward, value, done in; advantage, return out (17 B).
+Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import sys
+
+import numpy as np
+import torch
+
+from . import problem, tp
+
+PEAK_HBM_GBS = 8000.0
+
+
+def _time(fn, iters, stream):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    fn()
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for _ in range(iters):
+        fn()
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[1]) / iters * 1e-3
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--envs", type=int, default=65536)
+    ap.add_argument("--iters", type=int, default=20)
+    ap.add_argument("--only", choices=["env_step", "gae", "copy"], default=None)
+    args = ap.parse_args()
+    sys.path.insert(0, __file__.rsplit("/", 2)[0])
+    import workloads as W
+
+    tp.load()
+    dev = "cuda"
+    stream = torch.cuda.current_stream()
+    cfg = W.get_config("stress").with_(E=args.envs)
+    out = {"kernel_bench": "standalone kernels", "envs": cfg.E}
+    E, n, I = cfg.E, cfg.n, cfg.n_ind
+
+    if args.only in (None, "env_step"):
+        print("[kbench] env_step: generating the 100-stock minute market", file=sys.stderr, flush=True)
+        mk = W.make_market(cfg)
+        mkt = tp.MarketT(torch.from_numpy(mk.price).to(dev), torch.from_numpy(mk.ind).to(dev))
+        ecfg = problem.env_cfg(cfg)
+        rng = np.random.default_rng(1)
+        t0 = torch.from_numpy(rng.integers(0, cfg.T1 - 1 - 2 * (args.iters + 2), E)).to(dev)
+        st = tp.StateT.empty(E, n)
+        tp.env_reset(mkt, ecfg, st, t0)
+        act = torch.from_numpy(W.make_actions(2, E, n, special=False)).to(dev)
+        rew = torch.empty(E, device=dev)
+        obs = torch.empty(E, cfg.K_pad, dtype=torch.bfloat16, device=dev)
+        sec = _time(lambda: tp.env_step(mkt, ecfg, st, act, rew, obs), args.iters, stream)
+        per_env = 4 * n + 2 * 4 * n + 2 * 16 + 2 * 4 * n + 4 * n * I + 2 * cfg.S + 4
+        gbs = per_env * E / sec / 1e9
+        out["env_step"] = {"launch_ms": sec * 1e3, "bytes_per_launch": per_env * E,
+                           "GBs": gbs, "hbm_frac": gbs / PEAK_HBM_GBS}
+        del mkt, st, act, rew, obs
+        torch.cuda.empty_cache()
+
+    if args.only in (None, "gae"):
+        L = cfg.L
+        print(f"[kbench] gae L={L} E={E}", file=sys.stderr, flush=True)
+        r = torch.randn(L, E, device=dev)
+        v = torch.randn(L + 1, E, device=dev)
+        d = (torch.rand(L, E, device=dev) < 0.01).to(torch.uint8)
+        adv = torch.empty(L, E, device=dev)
+        ret = torch.empty(L, E, device=dev)
+        sec = _time(lambda: tp.gae(r, v, d, cfg.gamma, cfg.lam, adv, ret), args.iters, stream)
+        nbytes = 17 * L * E
+        out["gae"] = {"launch_ms": sec * 1e3, "bytes_per_launch": nbytes,
+                      "GBs": nbytes / sec / 1e9, "hbm_frac": nbytes / sec / 1e9 / PEAK_HBM_GBS}
+
+    if args.only in (None, "copy"):
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        sec = _time(lambda: b.copy_(a), args.iters, stream)
+        out["copy_1GiB"] = {"launch_ms": sec * 1e3, "GBs": 2 * a.numel() * 4 / sec / 1e9}
+
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
