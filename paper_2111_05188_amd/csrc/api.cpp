@@ -172,6 +172,8 @@ bool packed_layout(const tp_actor *a, PackedLayout *L)
         size_t wbytes;
         if (a->dtype == TP_BF16) {
             L->NT[l] = (outs[l] + 15) / 16;
+            // action tiles in whole groups of 4 (one per matrix wave)
+            if (l == 2) L->NT[l] = (L->NT[l] + 3) / 4 * 4;
             L->KS[l] = ins[l] / 32;
             wbytes = (size_t)L->NT[l] * L->KS[l] * 64 * 16;
         } else {

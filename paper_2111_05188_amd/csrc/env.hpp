@@ -76,6 +76,8 @@ struct HalfEnv {
 // this lane's stocks; q[c]: their prices at the next row (0 for stocks >= n).
 // `live`: this half holds an env to step (an idle half trades nothing).
 // Returns the reward (same on every lane of the half).  All 64 lanes call it.
+// NC > 0 fixes the stock count at compile time (C.n otherwise).
+template <int NC = 0>
 __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
                                                const float (&a)[SPL],
                                                const float (&q)[SPL], bool live,
@@ -83,12 +85,13 @@ __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
 {
     const bool upper = lane >= HALF;
     const int hl = lane & (HALF - 1);
+    const int n = NC > 0 ? NC : C.n;
     const double fb = C.f_b;
     int k[SPL];
     double pd[SPL];
 #pragma unroll
     for (int c = 0; c < SPL; ++c) {
-        const bool v = live && SPL * hl + c < C.n;
+        const bool v = live && SPL * hl + c < n;
         k[c] = v ? shares_from_action(a[c], C.hmax) : 0;
         pd[c] = (double)s.p[c];
     }

@@ -67,11 +67,12 @@ struct RolloutArgs {
     int32_t *shares_tap;
     void *obs_last;
     // LDS carve-up (bytes / elements), filled by the launcher
-    int ldx, ldh, ldmu;
-    size_t lds_X, lds_H, lds_MU, lds_OS, lds_PT, lds_scal, lds_bytes;
+    int ldx, ldh, ldmu, ldz, ldh2;
+    size_t lds_X, lds_H, lds_MU, lds_OS, lds_PT, lds_scal, lds_Z, lds_B, lds_bytes;
 };
 
 hipError_t launch_rollout(RolloutArgs &a, hipStream_t s);
+hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s);
 hipError_t launch_env_reset(const EnvConst &c, double *cash, int32_t *shares,
                             int64_t *t, const int64_t *t0, int E, void *obs,
                             int64_t ld_obs, int obs_bf16, hipStream_t s);

@@ -427,6 +427,8 @@ static hipError_t launch_cfg(RolloutArgs &a, hipStream_t s)
 hipError_t launch_rollout(RolloutArgs &a, hipStream_t s)
 {
     if (a.lay.dtype == TP_BF16) {
+        const hipError_t e = launch_rollout_rs(a, s);
+        if (e != hipErrorNotSupported) return e;
         const int *k = a.lay.KS;
         // fully unrolled variants for the actor shapes in use
         if (k[0] == 32 && k[1] == 16 && k[2] == 16) return launch_cfg<__bf16, 2, 8, 32, 16, 16>(a, s);

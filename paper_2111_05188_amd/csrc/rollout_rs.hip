@@ -1,0 +1,596 @@
+// Role-split fused rollout kernel for bf16 actors of the shapes in use
+// (1001 inputs from 100 stocks with 8 indicators each, 512- or 1024-wide
+// hidden layers).  One launch runs all L lockstep steps of a block of 16 envs.
+//
+// Why split roles.  A workgroup owns 16 envs, the N dimension of one MFMA
+// tile, so every step streams the whole actor (1.65 MB at 1001-512-512-100)
+// from L2 into the CU.  That stream, not the MFMAs, bounds the actor, and the
+// env step is VALU work of about the same length.  Run back to back they add
+// up; here they overlap.  The observation is [balance, prices, holdings,
+// indicators] (Section 3, "State space"), and layer 1's columns past the
+// first KSB k-steps of 32 hold only indicators of the market row.  Those do
+// not depend on the actions, so their share of layer 1 for step j+1 can be
+// computed while the env step of step j runs.  Only the first KSB k-steps of
+// layer 1, layers 2 and 3 remain on the step-to-step chain.
+//
+// Waves.  Four matrix waves (one per SIMD) compute every actor layer; eight
+// env waves (two per SIMD) own two envs each, one per 32-lane half, four
+// stocks per lane.  Each role runs its own loop with the same barrier
+// sequence: per step, four slots separated by workgroup barriers:
+//
+//   slot   matrix waves                         env waves
+//   A      Z = W1[:, KSB..] x_j  (indicators)   env step j-1, trajectory row j-1,
+//                                               balance/prices/holdings of x_j
+//   B      h1 = tanh(Z + W1[:, ..KSB] x_j + b1) x_j to HBM; loads of row t+j+1;
+//                                               Philox + Box-Muller normals of step j
+//   L2     h2 = tanh(W2 h1 + b2)                indicators of row t+j+1 into x_{j+1}
+//   L3     mu = W3 h2 + b3                      -
+//
+// LDS: x rows (bf16), h1 (bf16), Z (fp32) sharing its space with h2 (their
+// lifetimes, slots A->B and L2->L3, do not overlap), mu (fp32), biases.
+//
+// Weight stream.  A matrix wave consumes a fixed sequence of F weight
+// fragments per step (1 KiB each: one 16x32 A-operand of
+// v_mfma_f32_16x16x32_bf16, 16 bytes per lane) through a ring of R fragment
+// registers: consuming fragment f issues the load of fragment f + R, wrapping
+// into the next step's sequence (the weights do not change during a
+// rollout), so loads stay in flight across group ends, layer ends and
+// barriers, and nothing is read twice.  Fragments come through buffer loads
+// with a wave-uniform scalar offset.
+#include <type_traits>
+
+#include "device.hpp"
+#include "env.hpp"
+#include "internal.hpp"
+
+namespace tpk {
+namespace rs {
+
+constexpr int MW = 4;            // matrix waves
+constexpr int VW = 8;            // env waves
+constexpr int NWAVES = MW + VW;
+constexpr int MB = 2 * VW;       // envs per workgroup
+constexpr int G = 4;             // output tiles per group in layers 1 and 2
+constexpr int R = 16;            // weight fragments in flight per matrix wave
+
+template <int I> using ic = std::integral_constant<int, I>;
+
+template <int B, int E, typename Fn>
+__device__ __forceinline__ void static_for(Fn &&fn)
+{
+    if constexpr (B < E) {
+        fn(ic<B>{});
+        static_for<B + 1, E>(fn);
+    }
+}
+
+// Actor shape.  NS stocks with NI indicator values per market row; KS1 k-steps of 32 inputs in layer 1, the first KSB of which
+// hold the balance, prices and holdings; NT1, NT2, NT3 output tiles of 16.
+template <int NS_, int NI_, int KS1_, int KSB_, int NT1_, int NT2_, int NT3_>
+struct Shape {
+    static constexpr int NS = NS_, NI = NI_;   // stocks, indicator values per row
+    static constexpr int KS1 = KS1_, KSB = KSB_, KSA = KS1_ - KSB_;
+    static constexpr int NT1 = NT1_, NT2 = NT2_, NT3 = NT3_;
+    static constexpr int KS2 = NT1 / 2, KS3 = NT2 / 2;
+    static constexpr int NG1 = NT1 / (MW * G), NG2 = NT2 / (MW * G), NG3 = NT3 / MW;
+    static_assert(NT1 % (MW * G) == 0 && NT2 % (MW * G) == 0 && NT3 % MW == 0,
+                  "tiles must split evenly over the matrix waves");
+    // fragments per step of one matrix wave, in consumption order A, B, L2, L3
+    static constexpr int FA = NG1 * KSA * G, FB = NG1 * KSB * G;
+    static constexpr int F2 = NG2 * KS2 * G, F3 = NG3 * KS3;
+    static constexpr int F = FA + FB + F2 + F3;
+    static_assert(F % R == 0, "the ring must map every fragment to a fixed slot");
+
+    // layer of fragment f, and its byte offset from the wave's base in that
+    // layer (the wave's first tile; groups are MW * G tiles apart in layers
+    // 1 and 2, MW tiles apart in layer 3)
+    static constexpr int layer(int f) { return f < FA + FB ? 0 : (f < FA + FB + F2 ? 1 : 2); }
+    static constexpr int offset(int f)
+    {
+        if (f < FA) {
+            const int g = f / (KSA * G), r = f % (KSA * G);
+            return ((g * MW * G + r % G) * KS1 + KSB + r / G) * 1024;
+        }
+        f -= FA;
+        if (f < FB) {
+            const int g = f / (KSB * G), r = f % (KSB * G);
+            return ((g * MW * G + r % G) * KS1 + r / G) * 1024;
+        }
+        f -= FB;
+        if (f < F2) {
+            const int g = f / (KS2 * G), r = f % (KS2 * G);
+            return ((g * MW * G + r % G) * KS2 + r / G) * 1024;
+        }
+        f -= F2;
+        return ((f / KS3) * MW * KS3 + f % KS3) * 1024;
+    }
+};
+
+// tanh from the identity tanh|x| = 1 - 2 / (exp(2|x|) + 1), with the odd
+// Taylor series x - x^3/3 + 2x^5/15 - 17x^7/315 below |x| = 1/16, where the
+// identity would cancel.  Absolute error below 1e-6 everywhere (hardware
+// exp2 and reciprocal, each within a few ulp).
+__device__ __forceinline__ float tanh_fast(float x)
+{
+    const float ax = fabsf(x);
+    const float e = __builtin_amdgcn_exp2f(ax * 2.8853900817779268f);   // 2 log2(e)
+    const float big = fmaf(-2.0f, __builtin_amdgcn_rcpf(e + 1.0f), 1.0f);
+    const float x2 = x * x;
+    const float poly = ax * fmaf(x2, fmaf(x2, fmaf(x2, -17.0f / 315.0f, 2.0f / 15.0f), -1.0f / 3.0f), 1.0f);
+    return copysignf(ax < 0.0625f ? poly : big, x);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint32_t __attribute__((ext_vector_type(4))) v)
+{
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+struct Lds {
+    __bf16 *X;      // [MB][ldx]   observations
+    __bf16 *H1;     // [MB][ldh1]  hidden layer 1
+    float *Z;       // [MB][ldz]   indicator part of layer 1 (shares space with H2)
+    __bf16 *H2;     // [MB][ldh2]  hidden layer 2
+    float *MU;      // [MB][ldmu]  action means
+    float *BIAS;    // b1 | b2 | b3
+    int ldx, ldh1, ldz, ldh2, ldmu;
+};
+
+// ---------------------------------------------------------------------------
+// Matrix role
+// ---------------------------------------------------------------------------
+template <class S>
+__device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
+                                            const uint8_t *pk, int m, int lane)
+{
+    const PackedLayout &P = A.lay;
+    const int r16 = lane & 15, kq = lane >> 4;
+    const float *b1 = s.BIAS, *b2 = b1 + S::NT1 * 16, *b3 = b2 + S::NT2 * 16;
+
+    // biases into LDS (read by every epilogue)
+    {
+        const float *src = (const float *)(pk + P.off_b[0]);
+        for (int i = m * WAVE + lane; i < S::NT1 * 16; i += MW * WAVE) s.BIAS[i] = src[i];
+        src = (const float *)(pk + P.off_b[1]);
+        for (int i = m * WAVE + lane; i < S::NT2 * 16; i += MW * WAVE) s.BIAS[S::NT1 * 16 + i] = src[i];
+        src = (const float *)(pk + P.off_b[2]);
+        for (int i = m * WAVE + lane; i < S::NT3 * 16; i += MW * WAVE)
+            s.BIAS[(S::NT1 + S::NT2) * 16 + i] = src[i];
+    }
+
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)pk, (short)0, (int)P.agent_stride, 0x00020000);
+    int wb0 = (int)P.off_W[0] + m * G * S::KS1 * 1024;
+    int wb1 = (int)P.off_W[1] + m * G * S::KS2 * 1024;
+    int wb2 = (int)P.off_W[2] + m * S::KS3 * 1024;
+    // The fragment offsets base + constant are loop-invariant; hoisted out
+    // of the step loop they would need one scalar register each.  Hiding
+    // the bases from the optimiser at every slot keeps each offset next to
+    // its load.
+    auto launder = [&]() {
+        asm volatile("" : "+s"(wb0), "+s"(wb1), "+s"(wb2));
+    };
+    const int voff = lane * 16;
+
+    bf16x8 ring[R];
+    // load fragment i (mod F) of the step sequence into its ring slot
+    auto fetch = [&](auto i) {
+        constexpr int f = decltype(i)::value % S::F;
+        constexpr int slot = decltype(i)::value % R;
+        constexpr int L = S::layer(f);
+        const int base = L == 0 ? wb0 : (L == 1 ? wb1 : wb2);
+        ring[slot] = as_bf16x8(
+            __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, base + S::offset(f), 0));
+    };
+    // multiply by fragment i, then refill its slot with fragment i + R
+    auto mma = [&](auto i, const bf16x8 &x, floatx4 &acc) {
+        constexpr int f = decltype(i)::value;
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[f % R], x, acc, 0, 0, 0);
+        fetch(ic<f + R>{});
+    };
+
+    const __bf16 *xb = s.X + r16 * s.ldx + kq * 8;
+    const __bf16 *h1b = s.H1 + r16 * s.ldh1 + kq * 8;
+    const __bf16 *h2b = s.H2 + r16 * s.ldh2 + kq * 8;
+
+    // slot A: Z = W1[:, KSB..] x (fp32, no bias)
+    auto seg_A = [&]() {
+        static_for<0, S::NG1>([&](auto g) {
+            floatx4 acc[G];
+#pragma unroll
+            for (int t = 0; t < G; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+            static_for<0, S::KSA>([&](auto ks) {
+                const bf16x8 x = *(const bf16x8 *)(xb + (S::KSB + decltype(ks)::value) * 32);
+                static_for<0, G>([&](auto t) {
+                    mma(ic<(decltype(g)::value * S::KSA + decltype(ks)::value) * G + decltype(t)::value>{},
+                        x, acc[decltype(t)::value]);
+                });
+                __builtin_amdgcn_sched_barrier(0);
+            });
+#pragma unroll
+            for (int t = 0; t < G; ++t) {
+                const int o = ((decltype(g)::value * MW + m) * G + t) * 16 + kq * 4;
+                *(floatx4 *)(s.Z + r16 * s.ldz + o) = acc[t];
+            }
+        });
+    };
+    // slot B: h1 = tanh(Z + W1[:, ..KSB] x + b1)
+    auto seg_B = [&]() {
+        static_for<0, S::NG1>([&](auto g) {
+            floatx4 acc[G];
+#pragma unroll
+            for (int t = 0; t < G; ++t) {
+                const int o = ((decltype(g)::value * MW + m) * G + t) * 16 + kq * 4;
+                acc[t] = *(const floatx4 *)(s.Z + r16 * s.ldz + o);
+            }
+            static_for<0, S::KSB>([&](auto ks) {
+                const bf16x8 x = *(const bf16x8 *)(xb + decltype(ks)::value * 32);
+                static_for<0, G>([&](auto t) {
+                    mma(ic<S::FA + (decltype(g)::value * S::KSB + decltype(ks)::value) * G +
+                           decltype(t)::value>{},
+                        x, acc[decltype(t)::value]);
+                });
+                __builtin_amdgcn_sched_barrier(0);
+            });
+#pragma unroll
+            for (int t = 0; t < G; ++t) {
+                const int o = ((decltype(g)::value * MW + m) * G + t) * 16 + kq * 4;
+                const floatx4 bv = *(const floatx4 *)(b1 + o);
+                bf16x4 h = {to_bf16(tanh_fast(acc[t][0] + bv[0])), to_bf16(tanh_fast(acc[t][1] + bv[1])),
+                            to_bf16(tanh_fast(acc[t][2] + bv[2])), to_bf16(tanh_fast(acc[t][3] + bv[3]))};
+                *(bf16x4 *)(s.H1 + r16 * s.ldh1 + o) = h;
+            }
+        });
+    };
+    // slot L2: h2 = tanh(W2 h1 + b2)
+    auto seg_L2 = [&]() {
+        static_for<0, S::NG2>([&](auto g) {
+            floatx4 acc[G];
+#pragma unroll
+            for (int t = 0; t < G; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+            static_for<0, S::KS2>([&](auto ks) {
+                const bf16x8 x = *(const bf16x8 *)(h1b + decltype(ks)::value * 32);
+                static_for<0, G>([&](auto t) {
+                    mma(ic<S::FA + S::FB + (decltype(g)::value * S::KS2 + decltype(ks)::value) * G +
+                           decltype(t)::value>{},
+                        x, acc[decltype(t)::value]);
+                });
+                __builtin_amdgcn_sched_barrier(0);
+            });
+#pragma unroll
+            for (int t = 0; t < G; ++t) {
+                const int o = ((decltype(g)::value * MW + m) * G + t) * 16 + kq * 4;
+                const floatx4 bv = *(const floatx4 *)(b2 + o);
+                bf16x4 h = {to_bf16(tanh_fast(acc[t][0] + bv[0])), to_bf16(tanh_fast(acc[t][1] + bv[1])),
+                            to_bf16(tanh_fast(acc[t][2] + bv[2])), to_bf16(tanh_fast(acc[t][3] + bv[3]))};
+                *(bf16x4 *)(s.H2 + r16 * s.ldh2 + o) = h;
+            }
+        });
+    };
+    // slot L3: mu = W3 h2 + b3
+    auto seg_L3 = [&]() {
+        static_for<0, S::NG3>([&](auto g) {
+            floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+            static_for<0, S::KS3>([&](auto ks) {
+                const bf16x8 x = *(const bf16x8 *)(h2b + decltype(ks)::value * 32);
+                mma(ic<S::FA + S::FB + S::F2 + decltype(g)::value * S::KS3 + decltype(ks)::value>{},
+                    x, acc);
+                __builtin_amdgcn_sched_barrier(0);
+            });
+            const int o = (decltype(g)::value * MW + m) * 16 + kq * 4;
+            const floatx4 bv = *(const floatx4 *)(b3 + o);
+            *(floatx4 *)(s.MU + r16 * s.ldmu + o) =
+                floatx4{acc[0] + bv[0], acc[1] + bv[1], acc[2] + bv[2], acc[3] + bv[3]};
+        });
+    };
+
+    static_for<0, R>([&](auto i) { fetch(i); });
+    __syncthreads();   // observations of step 0 and the biases are in LDS
+    for (int j = 0; j < A.L; ++j) {
+        launder();
+        seg_A();
+        __syncthreads();
+        launder();
+        seg_B();
+        __syncthreads();
+        launder();
+        seg_L2();
+        __syncthreads();
+        launder();
+        seg_L3();
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Env role
+// ---------------------------------------------------------------------------
+// Balance, prices and holdings of an observation row (the indicator part is
+// written separately, one slot earlier).
+template <int n>
+__device__ __forceinline__ void write_obs_state(__bf16 *row, const EnvConst &C, double cash,
+                                                const int (&h)[SPL], const float (&p)[SPL],
+                                                int hl)
+{
+    if (hl == 0) row[0] = to_bf16((float)(cash * (double)C.cash_scale));
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        const int i = SPL * hl + c;
+        if (i < n) {
+            row[1 + i] = to_bf16(p[c] * C.price_scale);
+            row[1 + n + i] = to_bf16((float)h[c] * C.share_scale);
+        }
+    }
+}
+
+template <int NS, int NI>
+__device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, const uint8_t *pk,
+                                         int agent, int ebase, int nenv, int v, int lane)
+{
+    // NS stocks (a multiple of 4, at most 128), NI = NS * indicators (a
+    // multiple of 32): every lane's loads are in range without clamping
+    static_assert(NS % SPL == 0 && NS <= SPL * HALF && NI % HALF == 0, "shape");
+    constexpr int IPL = NI / HALF;   // indicator values per lane
+    const EnvConst &C = A.env;
+    const PackedLayout &P = A.lay;
+    constexpr int n = NS, nI = NI;
+    const int half = lane / HALF, hl = lane % HALF;
+    const int sl = 2 * v + half;
+    const bool mine = sl < nenv;
+    const int e = ebase + sl;
+    __bf16 *xrow = s.X + sl * s.ldx;
+    const size_t E = (size_t)A.E;
+    const float qnan = __builtin_nanf("");
+
+    float ls[SPL], sg[SPL];
+    {
+        const float *lsd = (const float *)(pk + P.off_ls);
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            const int i = SPL * hl + c;
+            ls[c] = i < n ? lsd[i] : 0.f;
+            sg[c] = expf(ls[c]);
+        }
+    }
+
+    // state of this half's env, kept in registers for the whole rollout
+    HalfEnv st;
+    st.cash = 0.0;
+    int64_t t0 = 0;
+    bool live = false;
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        st.h[c] = 0;
+        st.p[c] = 0.f;
+    }
+    if (mine) {
+        t0 = A.t[e];
+        live = t0 >= 0 && t0 + A.L <= C.T1 - 1;
+        st.cash = A.cash[e];
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            const int i = SPL * hl + c;
+            st.h[c] = i < n ? A.shares[(size_t)e * n + i] : 0;
+        }
+        if (live) {
+            const float *prow = C.price + (size_t)t0 * n;
+            const float *irow = C.ind + (size_t)t0 * nI;
+#pragma unroll
+            for (int c = 0; c < SPL; ++c) {
+                const int i = SPL * hl + c;
+                st.p[c] = i < n ? prow[i] : 0.f;
+            }
+            float ind1[1];
+            ind1[0] = hl < nI ? irow[hl] : 0.f;
+            write_obs_half<__bf16, 1>(xrow, C, st.cash, st.h, st.p, ind1, irow, hl);
+        }
+    }
+    const bool wave_live = __ballot(live) != 0;
+    const double half_log2pi_n = 0.5 * (double)n * 1.8378770664093454836;
+    const int obs_bytes = C.K_pad * 2;
+
+    float z[SPL], q[SPL];
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) z[c] = q[c] = 0.f;
+
+    // env step of step jj: action, log-density, trade, trajectory row jj and
+    // the balance / prices / holdings of observation jj + 1
+    auto step_env = [&](int jj) {
+        const float *mu = s.MU + sl * s.ldmu;
+        float a[SPL];
+        double lp = 0.0;
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            const int i = SPL * hl + c;
+            const bool ok = live && i < n;
+            a[c] = ok ? mu[i] + sg[c] * z[c] : 0.f;
+            if (ok) lp += -0.5 * (double)z[c] * (double)z[c] - (double)ls[c];
+        }
+        float qq[SPL];
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) qq[c] = (live && SPL * hl + c < n) ? q[c] : 0.f;
+        lp = half_sum(lp, half != 0) - half_log2pi_n;
+        float r = 0.f;
+        if (wave_live) r = env_step_half<NS>(C, st, a, qq, live, lane);
+        if (live) write_obs_state<NS>(xrow, C, st.cash, st.h, st.p, hl);
+        if (!mine) return;
+        const size_t row = (size_t)jj * E + e;
+        float *ga = A.action + row * n;
+        int32_t *gs = A.shares_tap ? A.shares_tap + row * n : nullptr;
+        const uint8_t done = (uint8_t)(A.step0 + (uint64_t)jj + 1 == (uint64_t)C.horizon);
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            const int i = SPL * hl + c;
+            if (i < n) {
+                ga[i] = live ? a[c] : qnan;
+                if (gs) gs[i] = st.h[c];
+            }
+        }
+        if (hl == 0) {
+            A.logp[row] = live ? (float)lp : qnan;
+            A.reward[row] = live ? r : qnan;
+            A.done[row] = live ? done : (uint8_t)0;
+            if (A.cash_tap) A.cash_tap[row] = st.cash;
+        }
+    };
+
+    __syncthreads();   // observations of step 0 are in LDS
+    for (int j = 0; j < A.L; ++j) {
+        // slot A: env step of step j-1 (the matrix waves read only the
+        // indicator columns of x_j meanwhile)
+        if (j > 0) step_env(j - 1);
+        __syncthreads();
+
+        // slot B: x_j to HBM; loads of row t0+j+1; the normals of step j
+        // (row t0+j+1 exists for a stepped env; others read row 0)
+        const int64_t t1 = live ? t0 + j + 1 : 0;
+        const float *pr = C.price + (size_t)t1 * NS;
+        const float *ir = C.ind + (size_t)t1 * NI;
+        float ind[IPL];
+        {
+            const float4 qv = *(const float4 *)(pr + SPL * min(hl, NS / SPL - 1));
+            q[0] = qv.x;
+            q[1] = qv.y;
+            q[2] = qv.z;
+            q[3] = qv.w;
+        }
+#pragma unroll
+        for (int mm = 0; mm < IPL; ++mm) ind[mm] = ir[hl + HALF * mm];
+        if (live && A.obs)
+            copy16((__bf16 *)A.obs + ((size_t)j * E + e) * A.ld_obs, xrow, obs_bytes, hl, HALF);
+        const U4 w = philox4x32_10(U4{(uint32_t)hl, (uint32_t)e, (uint32_t)(A.step0 + (uint64_t)j),
+                                      (uint32_t)agent},
+                                   A.key_lo, A.key_hi);
+        box_muller(uniform_open01(w.x), uniform_open01(w.y), z[0], z[1]);
+        box_muller(uniform_open01(w.z), uniform_open01(w.w), z[2], z[3]);
+        __syncthreads();
+
+        // slot L2: indicators of row t0+j+1 into x_{j+1} (the matrix waves
+        // are done with x_j)
+        if (live) {
+            __bf16 *ri = xrow + 1 + 2 * n;
+#pragma unroll
+            for (int mm = 0; mm < IPL; ++mm) {
+                const int kk = hl + HALF * mm;
+                if (kk < nI) ri[kk] = to_bf16(ind[mm]);
+            }
+        }
+        __syncthreads();
+
+        // slot L3: nothing for the env waves
+        __syncthreads();
+    }
+    step_env(A.L - 1);
+
+    if (mine && live) {
+        if (A.obs_last) copy16((__bf16 *)A.obs_last + (size_t)e * A.ld_obs, xrow, obs_bytes, hl, HALF);
+        if (hl == 0) {
+            A.cash[e] = st.cash;
+            A.t[e] = t0 + A.L;
+        }
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            const int i = SPL * hl + c;
+            if (i < n) A.shares[(size_t)e * n + i] = st.h[c];
+        }
+    }
+}
+
+template <class S>
+__global__ __launch_bounds__(NWAVES *WAVE) void rollout_rs_kernel(RolloutArgs A)
+{
+    extern __shared__ __align__(16) uint8_t smem[];
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / WAVE));
+    const int lane = threadIdx.x % WAVE;
+
+    // XCD-aware block order (consecutive dispatch slots of one XCD take
+    // consecutive logical blocks)
+    const int nb = gridDim.x;
+    const int logical = (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8;
+    if (logical >= A.n_agents * A.blocks_per_agent) return;
+    const int agent = logical / A.blocks_per_agent;
+    const int blk = logical % A.blocks_per_agent;
+    const int ebase = agent * A.envs_per_agent + blk * MB;
+    const int nenv = min(MB, A.envs_per_agent - blk * MB);
+    const uint8_t *pk = A.packed + (size_t)agent * A.lay.agent_stride;
+
+    Lds s;
+    s.X = (__bf16 *)(smem + A.lds_X);
+    s.H1 = (__bf16 *)(smem + A.lds_H);
+    s.Z = (float *)(smem + A.lds_Z);
+    s.H2 = (__bf16 *)(smem + A.lds_Z);
+    s.MU = (float *)(smem + A.lds_MU);
+    s.BIAS = (float *)(smem + A.lds_B);
+    s.ldx = A.ldx;
+    s.ldh1 = A.ldh;
+    s.ldz = A.ldz;
+    s.ldh2 = A.ldh2;
+    s.ldmu = A.ldmu;
+
+    // zero the observation rows (padding columns and rows of absent envs
+    // stay zero)
+    for (int i = threadIdx.x; i < MB * s.ldx * 2 / 16; i += NWAVES * WAVE)
+        ((uint4 *)s.X)[i] = uint4{0, 0, 0, 0};
+    __syncthreads();
+
+    if (wave < MW)
+        matrix_role<S>(A, s, pk, wave, lane);
+    else
+        env_role<S::NS, S::NI>(A, s, pk, agent, ebase, nenv, wave - MW, lane);
+}
+
+template <class S>
+hipError_t launch(RolloutArgs &a, hipStream_t st)
+{
+    const PackedLayout &P = a.lay;
+    a.ldx = S::KS1 * 32 + 8;
+    a.ldh = S::NT1 * 16 + 8;
+    a.ldz = S::NT1 * 16 + 4;
+    a.ldh2 = S::NT2 * 16 + 8;
+    a.ldmu = S::NT3 * 16 + 4;
+    auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
+    size_t off = 0;
+    a.lds_X = off;  off = al(off + (size_t)MB * a.ldx * 2);
+    a.lds_H = off;  off = al(off + (size_t)MB * a.ldh * 2);
+    a.lds_Z = off;
+    {
+        const size_t z = (size_t)MB * a.ldz * 4, h2 = (size_t)MB * a.ldh2 * 2;
+        off = al(off + (z > h2 ? z : h2));
+    }
+    a.lds_MU = off; off = al(off + (size_t)MB * a.ldmu * 4);
+    a.lds_B = off;  off = al(off + (size_t)(S::NT1 + S::NT2 + S::NT3) * 16 * 4);
+    a.lds_bytes = off;
+    if (off > LDS_LIMIT) return hipErrorInvalidConfiguration;
+    if (P.KS[0] != S::KS1 || P.NT[0] != S::NT1 || P.NT[1] != S::NT2 || P.NT[2] != S::NT3 ||
+        P.KS[1] != S::KS2 || P.KS[2] != S::KS3)
+        return hipErrorInvalidValue;
+    a.blocks_per_agent = (a.envs_per_agent + MB - 1) / MB;
+    int nblk = a.n_agents * a.blocks_per_agent;
+    nblk = (nblk + 7) & ~7;
+    auto k = rollout_rs_kernel<S>;
+    hipError_t e = hipFuncSetAttribute((const void *)k,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)off);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, dim3(nblk), dim3(NWAVES * WAVE), off, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace rs
+
+// The role-split kernel covers bf16 actors with 100 stocks of 8 indicators
+// (1001 inputs: KS1 = 32, the balance/prices/holdings in the first 7
+// k-steps) and hidden widths 512 or 1024; returns hipErrorNotSupported for
+// other shapes.
+hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
+{
+    const PackedLayout &P = a.lay;
+    if (P.dtype != TP_BF16 || P.n != 100 || P.S != 1001 || a.env.nI != 800 || P.KS[0] != 32 ||
+        P.NT[2] != 8)
+        return hipErrorNotSupported;
+    // the env waves read each lane's 4 prices as one 16-byte load
+    if ((uintptr_t)a.env.price % 16) return hipErrorNotSupported;
+    if (P.H1 == 512 && P.H2 == 512) return rs::launch<rs::Shape<100, 800, 32, 7, 32, 32, 8>>(a, s);
+    if (P.H1 == 1024 && P.H2 == 1024) return rs::launch<rs::Shape<100, 800, 32, 7, 64, 64, 8>>(a, s);
+    return hipErrorNotSupported;
+}
+
+}  // namespace tpk

@@ -1,7 +1,8 @@
 """GPU parity of tp_rollout (fused actor + sampling + env step + trajectory
 store) against a teacher-forced oracle replay, at sizes the oracle finishes
 in seconds: several workgroups of envs, ragged tails, every actor shape
-family (fp32 VALU, bf16 MFMA 512-wide and 1024-wide, multi-agent), plus
+family (fp32 VALU, bf16 MFMA 512-wide and 1024-wide on the role-split kernel,
+bf16 of another shape on the generic kernel, multi-agent), plus
 determinism, split/resume, and envs whose start row leaves no room."""
 
 import numpy as np
@@ -68,6 +69,12 @@ def test_stress_shape_small():
 
 def test_dow_shape_small():
     _run_case(W.get_config("dow30"), 9, 300, rows=2521)
+
+
+def test_bf16_actor_of_another_shape():
+    # a bf16 actor outside the shapes with a specialised kernel (301 inputs,
+    # 256-wide layers) runs the generic MFMA rollout kernel
+    _run_case(W.get_config("dow30").with_(dtype="bf16"), 21, 120, rows=2521)
 
 
 def test_deterministic_and_resumable():
