@@ -56,6 +56,19 @@ __device__ __forceinline__ void box_muller(float u0, float u1, float &z0,
     z1 = rad * sinf(ang);
 }
 
+// The same with the hardware transcendentals: v_log_f32 (log2), v_sqrt_f32,
+// and v_sin_f32 / v_cos_f32, whose argument is in revolutions, so the
+// uniform u1 is the angle / 2 pi as it stands.  Close to fp32 precision, not
+// correctly rounded: used where the draws feed a bf16 actor, whose
+// tolerance is far wider.
+__device__ __forceinline__ void box_muller_hw(float u0, float u1, float &z0, float &z1)
+{
+    // -2 ln u0 = -2 ln(2) log2(u0)
+    const float rad = __builtin_amdgcn_sqrtf(-1.38629436111989061f * __builtin_amdgcn_logf(u0));
+    z0 = rad * __builtin_amdgcn_cosf(u1);
+    z1 = rad * __builtin_amdgcn_sinf(u1);
+}
+
 // ---------------------------------------------------------------------------
 // Wavefront collectives (all 64 lanes active), built on DPP lane moves:
 // row_shr:k shifts within 16-lane rows, row_bcast:15 / row_bcast:31 carry

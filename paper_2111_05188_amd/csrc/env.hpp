@@ -75,13 +75,15 @@ struct HalfEnv {
 // One transition of the env owned by this lane's half.  a[c]: raw actions of
 // this lane's stocks; q[c]: their prices at the next row (0 for stocks >= n).
 // `live`: this half holds an env to step (an idle half trades nothing).
+// `extra`: a per-lane fp64 term summed over the half alongside the step's
+// own sums (the caller's log-density); on return it holds the half's total.
 // Returns the reward (same on every lane of the half).  All 64 lanes call it.
 // NC > 0 fixes the stock count at compile time (C.n otherwise).
 template <int NC = 0>
 __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
                                                const float (&a)[SPL],
                                                const float (&q)[SPL], bool live,
-                                               int lane)
+                                               int lane, double &extra)
 {
     const bool upper = lane >= HALF;
     const int hl = lane & (HALF - 1);
@@ -96,113 +98,106 @@ __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
         pd[c] = (double)s.p[c];
     }
 
-    // total asset before the step (fp64; products h*p are exact)
-    double hv = 0.0;
-#pragma unroll
-    for (int c = 0; c < SPL; ++c) hv += (double)s.h[c] * pd[c];
-    const double V = s.cash + half_sum(hv, upper);
-
-    // sells
-    double sv = 0.0;
+    // value of the holdings before the step, and the sells (fp64; every
+    // product p*h is exact); the three half sums share one pass
+    double hv = 0.0, sv = 0.0;
     int h[SPL];
 #pragma unroll
     for (int c = 0; c < SPL; ++c) {
+        hv += (double)s.h[c] * pd[c];
         const int sc = k[c] < 0 ? min(-k[c], s.h[c]) : 0;
         h[c] = s.h[c] - sc;
         sv += pd[c] * (double)sc;
     }
-    const double S = half_sum(sv, upper);   // exact
+    hv = half_inclusive_scan(hv);
+    sv = half_inclusive_scan(sv);
+    extra = half_inclusive_scan(extra);
+    const double V = s.cash + half_value(hv, HALF - 1, HALF - 1, upper);
+    const double S = half_value(sv, HALF - 1, HALF - 1, upper);   // exact
+    extra = half_value(extra, HALF - 1, HALF - 1, upper);
     const double b_s = fma(S, C.f_s, s.cash);
 
     // buys: resolve the greedy in ascending stock order in rounds.  A round
     // first drops every pending stock that cannot pay for one share at the
     // current G (G only grows, so it never will), then finds the first
-    // pending stock whose full order no longer fits: every pending stock
-    // before it is bought in full, it gets its largest affordable q, and the
-    // next round continues after it.  Both halves run their rounds together;
-    // a half without pending stocks idles.
+    // pending stock whose full order no longer fits (the misfit): every
+    // pending stock before it is bought in full, the lane holding it buys
+    // its largest affordable q, and the next round continues after it.
+    // Both halves run their rounds together; a half without pending stocks
+    // idles.
+    // pending stocks as a 4-bit mask per lane (bit c = stock 4 hl + c);
+    // everything below is branch-free except the misfit's own search
     double cost[SPL];
-    bool pend[SPL];
+    int pm = 0;
 #pragma unroll
     for (int c = 0; c < SPL; ++c) {
         cost[c] = k[c] > 0 ? pd[c] * (double)k[c] : 0.0;
-        pend[c] = k[c] > 0;
+        pm |= k[c] > 0 ? 1 << c : 0;
     }
     double G = 0.0;
-    for (bool first = true;; first = false) {
-        bool any = false;
+    for (;;) {
+        // drop what cannot pay for one share (at G = 0 such a stock buys
+        // nothing either, so the first round may drop too)
 #pragma unroll
-        for (int c = 0; c < SPL; ++c) {
-            if (!first && pend[c] && fma(fb, G + pd[c], -b_s) > 0.0) pend[c] = false;
-            any |= pend[c];
-        }
-        if (__ballot(any) == 0) break;
+        for (int c = 0; c < SPL; ++c)
+            pm &= fma(fb, G + pd[c], -b_s) > 0.0 ? ~(1 << c) : ~0;
+        if (__ballot(pm != 0) == 0) break;
         // lane-local inclusive prefix of the pending full costs, then the
         // half's exclusive prefix of lane totals (all exact)
         double pre[SPL], acc = 0.0;
 #pragma unroll
         for (int c = 0; c < SPL; ++c) {
-            acc += pend[c] ? cost[c] : 0.0;
+            acc += (pm >> c) & 1 ? cost[c] : 0.0;
             pre[c] = acc;
         }
-        const double incl = half_inclusive_scan(acc);
-        const double base = G + (incl - acc);
-        int firstbad = SPL;
-#pragma unroll
-        for (int c = SPL - 1; c >= 0; --c)
-            if (pend[c] && fma(fb, base + pre[c], -b_s) > 0.0) firstbad = c;
-        const uint64_t m = __ballot(firstbad < SPL);
-        const uint32_t ma = (uint32_t)m, mb = (uint32_t)(m >> 32);
-        const uint32_t mine = upper ? mb : ma;
-        // a half with no misfit buys every pending stock in full
-        const double total = half_value(base + acc, HALF - 1, HALF - 1, upper);
-        const int fla = ma ? __ffs(ma) - 1 : 0, flb = mb ? __ffs(mb) - 1 : 0;
-        const int fl = upper ? flb : fla;
-        const int cf = half_value(firstbad, fla, flb, upper);
-        // stocks before the first misfit are bought in full
-#pragma unroll
-        for (int c = 0; c < SPL; ++c) {
-            if (pend[c] && (mine == 0 || hl < fl || (hl == fl && c < cf))) {
-                h[c] += k[c];
-                pend[c] = false;
-            }
-        }
-        // the misfit stock: largest q in [0, kf-1] with f_b (Gf + pf q) <= b_s
-        double gf_l = base, pf_l = pd[0];
-        int kf_l = k[0];
+        const double base = G + (half_inclusive_scan(acc) - acc);
+        int bad = 0;   // pending stocks whose prefix no longer fits
 #pragma unroll
         for (int c = 0; c < SPL; ++c)
-            if (c == firstbad) {
-                gf_l = base + pre[c] - cost[c];
-                pf_l = pd[c];
-                kf_l = k[c];
-            }
-        const double Gf = half_value(gf_l, fla, flb, upper);
-        const double pf = half_value(pf_l, fla, flb, upper);
-        const int kf = mine ? half_value(kf_l, fla, flb, upper) : 1;
-        int qf = 0;
-        if (mine) {
-            const double rem = fma(-fb, Gf, b_s);
-            double est = floor(rem / (pf * fb));
-            est = fmin(fmax(est, 0.0), (double)(kf - 1));
-            qf = (int)est;
-        }
-        // the two halves step their estimates to the exact boundary together
-        for (;;) {
-            const bool up = mine && qf < kf - 1 && fma(fb, Gf + pf * (double)(qf + 1), -b_s) <= 0.0;
-            const bool dn = mine && !up && qf > 0 && fma(fb, Gf + pf * (double)qf, -b_s) > 0.0;
-            if (__ballot(up || dn) == 0) break;
-            qf += up ? 1 : (dn ? -1 : 0);
-        }
-        G = mine ? Gf + pf * (double)qf : total;
-        if (mine && hl == fl) {
+            bad |= fma(fb, base + pre[c], -b_s) > 0.0 ? 1 << c : 0;
+        bad &= pm;
+        const uint64_t m = __ballot(bad != 0);
+        const uint32_t ma = (uint32_t)m, mb = (uint32_t)(m >> 32);
+        // the misfit's lane in each half (the last lane when there is none:
+        // its running total is then the half's new G)
+        const int fla = ma ? __ffs(ma) - 1 : HALF - 1;
+        const int flb = mb ? __ffs(mb) - 1 : HALF - 1;
+        const bool has = (upper ? mb : ma) != 0;
+        const int fl = upper ? flb : fla;
+        const bool at = has && hl == fl;
+        const int cf = __ffs(bad) - 1;   // on the misfit's lane: its stock
+        // every pending stock before the misfit is bought in full
+        const int full = pm & (!has || hl < fl ? 0xF : (at ? (1 << cf) - 1 : 0));
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) h[c] += (full >> c) & 1 ? k[c] : 0;
+        pm &= ~full;
+        double gnew = base + acc;
+        if (at) {
+            // the misfit: largest q in [0, kf - 1] with f_b (Gf + pf q) <= b_s.
+            // An fp32 estimate (off by at most one) is stepped to the exact
+            // boundary with the sign-exact fma test.
+            double gf = base, pf = pd[0];
+            int kf = k[0];
+#pragma unroll
+            for (int c = 1; c < SPL; ++c)
+                if (c == cf) {
+                    pf = pd[c];
+                    kf = k[c];
+                }
 #pragma unroll
             for (int c = 0; c < SPL; ++c)
-                if (c == cf) {
-                    h[c] += qf;
-                    pend[c] = false;
-                }
+                if (c == cf) gf = base + pre[c] - cost[c];
+            const float rem = (float)fma(-fb, gf, b_s);
+            const float est = floorf(rem * __builtin_amdgcn_rcpf((float)(pf * fb)));
+            int qf = (int)fminf(fmaxf(est, 0.0f), (float)(kf - 1));
+            while (qf < kf - 1 && fma(fb, gf + pf * (double)(qf + 1), -b_s) <= 0.0) ++qf;
+            while (qf > 0 && fma(fb, gf + pf * (double)qf, -b_s) > 0.0) --qf;
+#pragma unroll
+            for (int c = 0; c < SPL; ++c) h[c] += c == cf ? qf : 0;
+            pm &= ~(1 << cf);
+            gnew = gf + pf * (double)qf;
         }
+        G = half_value(gnew, fla, flb, upper);
     }
     double nb = fma(-fb, G, b_s);
     if (nb < 0.0) nb = 0.0;

@@ -90,7 +90,8 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
         a[c] = v ? action[(size_t)e * n + i] : 0.f;
         q[c] = v ? p1[i] : 0.f;
     }
-    const float r = env_step_half(C, s, a, q, live, lane);
+    double none = 0.0;
+    const float r = env_step_half(C, s, a, q, live, lane, none);
     if (live) {
 #pragma unroll
         for (int c = 0; c < SPL; ++c) {

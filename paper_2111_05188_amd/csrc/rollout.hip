@@ -312,8 +312,8 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
             st.p[c] = v ? PT[sl * n + i] : 0.f;
             if (!v) q[c] = 0.f;
         }
-        lp = half_sum(lp, half != 0) - half_log2pi_n;
-        const float r = env_step_half(C, st, a, q, live, lane);
+        const float r = env_step_half(C, st, a, q, live, lane, lp);
+        lp -= half_log2pi_n;
         if (live) {
             if (hl == 0) OC[sl] = st.cash;
 #pragma unroll

@@ -21,9 +21,9 @@
 //   slot   matrix waves                         env waves
 //   A      Z = W1[:, KSB..] x_j  (indicators)   env step j-1, trajectory row j-1,
 //                                               balance/prices/holdings of x_j
-//   B      h1 = tanh(Z + W1[:, ..KSB] x_j + b1) x_j to HBM; loads of row t+j+1;
+//   B      h1 = tanh(Z + W1[:, ..KSB] x_j + b1) x_j to HBM; loads of row t+j+1
+//   L2     h2 = tanh(W2 h1 + b2)                indicators of row t+j+1 into x_{j+1};
 //                                               Philox + Box-Muller normals of step j
-//   L2     h2 = tanh(W2 h1 + b2)                indicators of row t+j+1 into x_{j+1}
 //   L3     mu = W3 h2 + b3                      -
 //
 // LDS: x rows (bf16), h1 (bf16), Z (fp32) sharing its space with h2 (their
@@ -51,9 +51,25 @@ constexpr int VW = 8;            // env waves
 constexpr int NWAVES = MW + VW;
 constexpr int MB = 2 * VW;       // envs per workgroup
 constexpr int G = 4;             // output tiles per group in layers 1 and 2
-constexpr int R = 16;            // weight fragments in flight per matrix wave
 
 template <int I> using ic = std::integral_constant<int, I>;
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+typedef int i4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+
+// Market rows and trajectory rows are touched once per step; streaming
+// (non-temporal) accesses keep them from evicting the actor's weights,
+// which every step reads again, from L2.
+__device__ __forceinline__ f4v load_stream(const float *p)
+{
+    return __builtin_nontemporal_load((const f4v *)p);
+}
+template <class T>
+__device__ __forceinline__ void store_stream(T v, T *p)
+{
+    __builtin_nontemporal_store(v, p);
+}
 
 template <int B, int E, typename Fn>
 __device__ __forceinline__ void static_for(Fn &&fn)
@@ -64,11 +80,14 @@ __device__ __forceinline__ void static_for(Fn &&fn)
     }
 }
 
-// Actor shape.  NS stocks with NI indicator values per market row; KS1 k-steps of 32 inputs in layer 1, the first KSB of which
-// hold the balance, prices and holdings; NT1, NT2, NT3 output tiles of 16.
-template <int NS_, int NI_, int KS1_, int KSB_, int NT1_, int NT2_, int NT3_>
+// Actor shape.  NS stocks with NI indicator values per market row; KS1
+// k-steps of 32 inputs in layer 1, the first KSB of which hold the balance,
+// prices and holdings; NT1, NT2, NT3 output tiles of 16; a ring of R weight
+// fragments per matrix wave.
+template <int NS_, int NI_, int KS1_, int KSB_, int NT1_, int NT2_, int NT3_, int R_>
 struct Shape {
     static constexpr int NS = NS_, NI = NI_;   // stocks, indicator values per row
+    static constexpr int R = R_;
     static constexpr int KS1 = KS1_, KSB = KSB_, KSA = KS1_ - KSB_;
     static constexpr int NT1 = NT1_, NT2 = NT2_, NT3 = NT3_;
     static constexpr int KS2 = NT1 / 2, KS3 = NT2 / 2;
@@ -106,18 +125,15 @@ struct Shape {
     }
 };
 
-// tanh from the identity tanh|x| = 1 - 2 / (exp(2|x|) + 1), with the odd
-// Taylor series x - x^3/3 + 2x^5/15 - 17x^7/315 below |x| = 1/16, where the
-// identity would cancel.  Absolute error below 1e-6 everywhere (hardware
-// exp2 and reciprocal, each within a few ulp).
-__device__ __forceinline__ float tanh_fast(float x)
+// tanh(x) = 2 / (1 + exp(-2x)) - 1 with the hardware exp2 and reciprocal;
+// `e2` = -2 log2(e) (x + b) comes in as one fma.  Absolute error of a few
+// 1e-7 (cancellation near 0 leaves fp32 rounding of 1), far below the bf16
+// rounding the result goes through.
+constexpr float NEG_2LOG2E = -2.8853900817779268f;
+
+__device__ __forceinline__ float tanh_from_e2(float e2)
 {
-    const float ax = fabsf(x);
-    const float e = __builtin_amdgcn_exp2f(ax * 2.8853900817779268f);   // 2 log2(e)
-    const float big = fmaf(-2.0f, __builtin_amdgcn_rcpf(e + 1.0f), 1.0f);
-    const float x2 = x * x;
-    const float poly = ax * fmaf(x2, fmaf(x2, fmaf(x2, -17.0f / 315.0f, 2.0f / 15.0f), -1.0f / 3.0f), 1.0f);
-    return copysignf(ax < 0.0625f ? poly : big, x);
+    return fmaf(2.0f, __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(e2)), -1.0f);
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint32_t __attribute__((ext_vector_type(4))) v)
@@ -138,164 +154,169 @@ struct Lds {
 // ---------------------------------------------------------------------------
 // Matrix role
 // ---------------------------------------------------------------------------
+// One matrix wave's weight stream.  Fragment i of the step sequence lives in
+// ring slot i % R; consuming fragment i first refills the slot fragment i-1
+// left (its MFMA has issued), then multiplies, so R-1 loads stay in flight.
+template <class S>
+struct Stream {
+    static constexpr int R = S::R;
+    __amdgpu_buffer_rsrc_t rsrc;
+    int wb0, wb1, wb2;   // wave's byte base in each layer
+    int voff;
+    bf16x8 ring[R];
+
+    template <int I>
+    __device__ __forceinline__ void fetch()
+    {
+        constexpr int f = I % S::F, slot = I % R, L = S::layer(f);
+        const int base = L == 0 ? wb0 : (L == 1 ? wb1 : wb2);
+        ring[slot] = as_bf16x8(
+            __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, base + S::offset(f), 0));
+    }
+
+    template <int I>
+    __device__ __forceinline__ void mma(const bf16x8 &x, floatx4 &acc)
+    {
+        fetch<I + R - 1>();
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[I % R], x, acc, 0, 0, 0);
+    }
+
+    // The fragment offsets base + constant are loop-invariant; hoisted out
+    // of the step loop they would need one scalar register each.  Hiding
+    // the bases from the optimiser at every slot keeps each offset next to
+    // its load.
+    __device__ __forceinline__ void launder() { asm volatile("" : "+s"(wb0), "+s"(wb1), "+s"(wb2)); }
+
+    // One slot's work: NG groups of GT output tiles over KS k-steps that
+    // start at k-step K0 of the input rows `xb` (this lane's row and column
+    // offset).  init(g, acc) and epi(g, t, acc) set up and store group g.
+    // With DEFER the epilogue of group g runs tile by tile inside the first
+    // GT k-steps of group g+1, so the weight stream keeps moving through it.
+    template <int FB0, int NG, int KS, int K0, int GT, bool DEFER, class InitF, class EpiF>
+    __device__ __forceinline__ void seg(const __bf16 *xb, InitF &&init, EpiF &&epi)
+    {
+        static_assert(!DEFER || KS >= GT, "deferred epilogue needs a k-step per tile");
+        floatx4 acc[GT], prev[GT];
+        static_for<0, NG>([&](auto gi) {
+            constexpr int g = decltype(gi)::value;
+            init(g, acc);
+            bf16x8 x = *(const bf16x8 *)(xb + K0 * 32);
+            static_for<0, KS>([&](auto ki) {
+                constexpr int k = decltype(ki)::value;
+                bf16x8 xn;
+                if constexpr (k + 1 < KS) xn = *(const bf16x8 *)(xb + (K0 + k + 1) * 32);
+                static_for<0, GT>([&](auto ti) {
+                    constexpr int t = decltype(ti)::value;
+                    mma<FB0 + (g * KS + k) * GT + t>(x, acc[t]);
+                });
+                if constexpr (DEFER && g > 0 && k < GT) epi(g - 1, k, prev[k]);
+                if constexpr (k + 1 < KS) x = xn;
+                __builtin_amdgcn_sched_barrier(0);
+            });
+            if constexpr (DEFER && g + 1 < NG) {
+#pragma unroll
+                for (int t = 0; t < GT; ++t) prev[t] = acc[t];
+            } else {
+#pragma unroll
+                for (int t = 0; t < GT; ++t) epi(g, t, acc[t]);
+            }
+        });
+    }
+};
+
 template <class S>
 __device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
                                             const uint8_t *pk, int m, int lane)
 {
     const PackedLayout &P = A.lay;
     const int r16 = lane & 15, kq = lane >> 4;
-    const float *b1 = s.BIAS, *b2 = b1 + S::NT1 * 16, *b3 = b2 + S::NT2 * 16;
-
-    // biases into LDS (read by every epilogue)
+    // biases in LDS; those of the tanh layers pre-scaled by -2 log2(e)
+    float *b1 = s.BIAS, *b2 = b1 + S::NT1 * 16, *b3 = b2 + S::NT2 * 16;
     {
         const float *src = (const float *)(pk + P.off_b[0]);
-        for (int i = m * WAVE + lane; i < S::NT1 * 16; i += MW * WAVE) s.BIAS[i] = src[i];
+        for (int i = m * WAVE + lane; i < S::NT1 * 16; i += MW * WAVE) b1[i] = NEG_2LOG2E * src[i];
         src = (const float *)(pk + P.off_b[1]);
-        for (int i = m * WAVE + lane; i < S::NT2 * 16; i += MW * WAVE) s.BIAS[S::NT1 * 16 + i] = src[i];
+        for (int i = m * WAVE + lane; i < S::NT2 * 16; i += MW * WAVE) b2[i] = NEG_2LOG2E * src[i];
         src = (const float *)(pk + P.off_b[2]);
-        for (int i = m * WAVE + lane; i < S::NT3 * 16; i += MW * WAVE)
-            s.BIAS[(S::NT1 + S::NT2) * 16 + i] = src[i];
+        for (int i = m * WAVE + lane; i < S::NT3 * 16; i += MW * WAVE) b3[i] = src[i];
     }
 
-    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)pk, (short)0, (int)P.agent_stride, 0x00020000);
-    int wb0 = (int)P.off_W[0] + m * G * S::KS1 * 1024;
-    int wb1 = (int)P.off_W[1] + m * G * S::KS2 * 1024;
-    int wb2 = (int)P.off_W[2] + m * S::KS3 * 1024;
-    // The fragment offsets base + constant are loop-invariant; hoisted out
-    // of the step loop they would need one scalar register each.  Hiding
-    // the bases from the optimiser at every slot keeps each offset next to
-    // its load.
-    auto launder = [&]() {
-        asm volatile("" : "+s"(wb0), "+s"(wb1), "+s"(wb2));
-    };
-    const int voff = lane * 16;
-
-    bf16x8 ring[R];
-    // load fragment i (mod F) of the step sequence into its ring slot
-    auto fetch = [&](auto i) {
-        constexpr int f = decltype(i)::value % S::F;
-        constexpr int slot = decltype(i)::value % R;
-        constexpr int L = S::layer(f);
-        const int base = L == 0 ? wb0 : (L == 1 ? wb1 : wb2);
-        ring[slot] = as_bf16x8(
-            __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, base + S::offset(f), 0));
-    };
-    // multiply by fragment i, then refill its slot with fragment i + R
-    auto mma = [&](auto i, const bf16x8 &x, floatx4 &acc) {
-        constexpr int f = decltype(i)::value;
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[f % R], x, acc, 0, 0, 0);
-        fetch(ic<f + R>{});
-    };
+    Stream<S> st;
+    st.rsrc = __builtin_amdgcn_make_buffer_rsrc((void *)pk, (short)0, (int)P.agent_stride,
+                                                0x00020000);
+    st.wb0 = (int)P.off_W[0] + m * G * S::KS1 * 1024;
+    st.wb1 = (int)P.off_W[1] + m * G * S::KS2 * 1024;
+    st.wb2 = (int)P.off_W[2] + m * S::KS3 * 1024;
+    st.voff = lane * 16;
 
     const __bf16 *xb = s.X + r16 * s.ldx + kq * 8;
     const __bf16 *h1b = s.H1 + r16 * s.ldh1 + kq * 8;
     const __bf16 *h2b = s.H2 + r16 * s.ldh2 + kq * 8;
+    // output column of tile t of group g, for this lane, in layers 1-2 / 3
+    auto col12 = [&](int g, int t) { return ((g * MW + m) * G + t) * 16 + kq * 4; };
+    auto col3 = [&](int g) { return (g * MW + m) * 16 + kq * 4; };
+    auto zero = [&](int, floatx4 *acc) {
+#pragma unroll
+        for (int t = 0; t < G; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    };
+    auto tanh_store = [&](const floatx4 &a, const float *bs, __bf16 *Y, int o) {
+        const floatx4 bv = *(const floatx4 *)(bs + o);
+        const bf16x4 h = {to_bf16(tanh_from_e2(fmaf(a[0], NEG_2LOG2E, bv[0]))),
+                          to_bf16(tanh_from_e2(fmaf(a[1], NEG_2LOG2E, bv[1]))),
+                          to_bf16(tanh_from_e2(fmaf(a[2], NEG_2LOG2E, bv[2]))),
+                          to_bf16(tanh_from_e2(fmaf(a[3], NEG_2LOG2E, bv[3])))};
+        *(bf16x4 *)(Y + o) = h;
+    };
 
     // slot A: Z = W1[:, KSB..] x (fp32, no bias)
     auto seg_A = [&]() {
-        static_for<0, S::NG1>([&](auto g) {
-            floatx4 acc[G];
-#pragma unroll
-            for (int t = 0; t < G; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-            static_for<0, S::KSA>([&](auto ks) {
-                const bf16x8 x = *(const bf16x8 *)(xb + (S::KSB + decltype(ks)::value) * 32);
-                static_for<0, G>([&](auto t) {
-                    mma(ic<(decltype(g)::value * S::KSA + decltype(ks)::value) * G + decltype(t)::value>{},
-                        x, acc[decltype(t)::value]);
-                });
-                __builtin_amdgcn_sched_barrier(0);
+        st.template seg<0, S::NG1, S::KSA, S::KSB, G, false>(
+            xb, zero, [&](int g, int t, const floatx4 &a) {
+                *(floatx4 *)(s.Z + r16 * s.ldz + col12(g, t)) = a;
             });
-#pragma unroll
-            for (int t = 0; t < G; ++t) {
-                const int o = ((decltype(g)::value * MW + m) * G + t) * 16 + kq * 4;
-                *(floatx4 *)(s.Z + r16 * s.ldz + o) = acc[t];
-            }
-        });
     };
     // slot B: h1 = tanh(Z + W1[:, ..KSB] x + b1)
     auto seg_B = [&]() {
-        static_for<0, S::NG1>([&](auto g) {
-            floatx4 acc[G];
+        st.template seg<S::FA, S::NG1, S::KSB, 0, G, true>(
+            xb,
+            [&](int g, floatx4 *acc) {
 #pragma unroll
-            for (int t = 0; t < G; ++t) {
-                const int o = ((decltype(g)::value * MW + m) * G + t) * 16 + kq * 4;
-                acc[t] = *(const floatx4 *)(s.Z + r16 * s.ldz + o);
-            }
-            static_for<0, S::KSB>([&](auto ks) {
-                const bf16x8 x = *(const bf16x8 *)(xb + decltype(ks)::value * 32);
-                static_for<0, G>([&](auto t) {
-                    mma(ic<S::FA + (decltype(g)::value * S::KSB + decltype(ks)::value) * G +
-                           decltype(t)::value>{},
-                        x, acc[decltype(t)::value]);
-                });
-                __builtin_amdgcn_sched_barrier(0);
-            });
-#pragma unroll
-            for (int t = 0; t < G; ++t) {
-                const int o = ((decltype(g)::value * MW + m) * G + t) * 16 + kq * 4;
-                const floatx4 bv = *(const floatx4 *)(b1 + o);
-                bf16x4 h = {to_bf16(tanh_fast(acc[t][0] + bv[0])), to_bf16(tanh_fast(acc[t][1] + bv[1])),
-                            to_bf16(tanh_fast(acc[t][2] + bv[2])), to_bf16(tanh_fast(acc[t][3] + bv[3]))};
-                *(bf16x4 *)(s.H1 + r16 * s.ldh1 + o) = h;
-            }
-        });
+                for (int t = 0; t < G; ++t) acc[t] = *(const floatx4 *)(s.Z + r16 * s.ldz + col12(g, t));
+            },
+            [&](int g, int t, const floatx4 &a) { tanh_store(a, b1, s.H1 + r16 * s.ldh1, col12(g, t)); });
     };
     // slot L2: h2 = tanh(W2 h1 + b2)
     auto seg_L2 = [&]() {
-        static_for<0, S::NG2>([&](auto g) {
-            floatx4 acc[G];
-#pragma unroll
-            for (int t = 0; t < G; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-            static_for<0, S::KS2>([&](auto ks) {
-                const bf16x8 x = *(const bf16x8 *)(h1b + decltype(ks)::value * 32);
-                static_for<0, G>([&](auto t) {
-                    mma(ic<S::FA + S::FB + (decltype(g)::value * S::KS2 + decltype(ks)::value) * G +
-                           decltype(t)::value>{},
-                        x, acc[decltype(t)::value]);
-                });
-                __builtin_amdgcn_sched_barrier(0);
-            });
-#pragma unroll
-            for (int t = 0; t < G; ++t) {
-                const int o = ((decltype(g)::value * MW + m) * G + t) * 16 + kq * 4;
-                const floatx4 bv = *(const floatx4 *)(b2 + o);
-                bf16x4 h = {to_bf16(tanh_fast(acc[t][0] + bv[0])), to_bf16(tanh_fast(acc[t][1] + bv[1])),
-                            to_bf16(tanh_fast(acc[t][2] + bv[2])), to_bf16(tanh_fast(acc[t][3] + bv[3]))};
-                *(bf16x4 *)(s.H2 + r16 * s.ldh2 + o) = h;
-            }
-        });
+        st.template seg<S::FA + S::FB, S::NG2, S::KS2, 0, G, true>(
+            h1b, zero,
+            [&](int g, int t, const floatx4 &a) { tanh_store(a, b2, s.H2 + r16 * s.ldh2, col12(g, t)); });
     };
     // slot L3: mu = W3 h2 + b3
     auto seg_L3 = [&]() {
-        static_for<0, S::NG3>([&](auto g) {
-            floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-            static_for<0, S::KS3>([&](auto ks) {
-                const bf16x8 x = *(const bf16x8 *)(h2b + decltype(ks)::value * 32);
-                mma(ic<S::FA + S::FB + S::F2 + decltype(g)::value * S::KS3 + decltype(ks)::value>{},
-                    x, acc);
-                __builtin_amdgcn_sched_barrier(0);
+        st.template seg<S::FA + S::FB + S::F2, S::NG3, S::KS3, 0, 1, false>(
+            h2b, [&](int, floatx4 *acc) { acc[0] = floatx4{0.f, 0.f, 0.f, 0.f}; },
+            [&](int g, int, const floatx4 &a) {
+                const int o = col3(g);
+                const floatx4 bv = *(const floatx4 *)(b3 + o);
+                *(floatx4 *)(s.MU + r16 * s.ldmu + o) =
+                    floatx4{a[0] + bv[0], a[1] + bv[1], a[2] + bv[2], a[3] + bv[3]};
             });
-            const int o = (decltype(g)::value * MW + m) * 16 + kq * 4;
-            const floatx4 bv = *(const floatx4 *)(b3 + o);
-            *(floatx4 *)(s.MU + r16 * s.ldmu + o) =
-                floatx4{acc[0] + bv[0], acc[1] + bv[1], acc[2] + bv[2], acc[3] + bv[3]};
-        });
     };
 
-    static_for<0, R>([&](auto i) { fetch(i); });
+    // the first R-1 fragments; the rest is fetched one slot behind use
+    static_for<0, S::R - 1>([&](auto i) { st.template fetch<decltype(i)::value>(); });
     __syncthreads();   // observations of step 0 and the biases are in LDS
     for (int j = 0; j < A.L; ++j) {
-        launder();
+        st.launder();
         seg_A();
         __syncthreads();
-        launder();
+        st.launder();
         seg_B();
         __syncthreads();
-        launder();
+        st.launder();
         seg_L2();
         __syncthreads();
-        launder();
+        st.launder();
         seg_L3();
         __syncthreads();
     }
@@ -322,14 +343,15 @@ __device__ __forceinline__ void write_obs_state(__bf16 *row, const EnvConst &C, 
     }
 }
 
-template <int NS, int NI>
+template <int NS, int NI, int KPAD>
 __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, const uint8_t *pk,
                                          int agent, int ebase, int nenv, int v, int lane)
 {
     // NS stocks (a multiple of 4, at most 128), NI = NS * indicators (a
-    // multiple of 32): every lane's loads are in range without clamping
-    static_assert(NS % SPL == 0 && NS <= SPL * HALF && NI % HALF == 0, "shape");
-    constexpr int IPL = NI / HALF;   // indicator values per lane
+    // multiple of 4), observation rows of KPAD elements
+    static_assert(NS % SPL == 0 && NS <= SPL * HALF && NI % 4 == 0, "shape");
+    constexpr int IPC = (NI / 4 + HALF - 1) / HALF;   // 16-byte indicator chunks per lane
+    constexpr int OBS_CHUNKS = KPAD * 2 / 16;         // 16-byte chunks of an observation row
     const EnvConst &C = A.env;
     const PackedLayout &P = A.lay;
     constexpr int n = NS, nI = NI;
@@ -408,28 +430,26 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
         float qq[SPL];
 #pragma unroll
         for (int c = 0; c < SPL; ++c) qq[c] = (live && SPL * hl + c < n) ? q[c] : 0.f;
-        lp = half_sum(lp, half != 0) - half_log2pi_n;
         float r = 0.f;
-        if (wave_live) r = env_step_half<NS>(C, st, a, qq, live, lane);
+        if (wave_live) r = env_step_half<NS>(C, st, a, qq, live, lane, lp);
+        lp -= half_log2pi_n;
         if (live) write_obs_state<NS>(xrow, C, st.cash, st.h, st.p, hl);
         if (!mine) return;
         const size_t row = (size_t)jj * E + e;
-        float *ga = A.action + row * n;
-        int32_t *gs = A.shares_tap ? A.shares_tap + row * n : nullptr;
         const uint8_t done = (uint8_t)(A.step0 + (uint64_t)jj + 1 == (uint64_t)C.horizon);
-#pragma unroll
-        for (int c = 0; c < SPL; ++c) {
-            const int i = SPL * hl + c;
-            if (i < n) {
-                ga[i] = live ? a[c] : qnan;
-                if (gs) gs[i] = st.h[c];
-            }
+        // this lane's 4 stocks are 16 contiguous bytes of the action row
+        if (hl < NS / SPL) {
+            const f4v av = live ? f4v{a[0], a[1], a[2], a[3]} : f4v{qnan, qnan, qnan, qnan};
+            store_stream(av, (f4v *)(A.action + row * n) + hl);
+            if (A.shares_tap)
+                store_stream(i4v{st.h[0], st.h[1], st.h[2], st.h[3]},
+                             (i4v *)(A.shares_tap + row * n) + hl);
         }
         if (hl == 0) {
-            A.logp[row] = live ? (float)lp : qnan;
-            A.reward[row] = live ? r : qnan;
-            A.done[row] = live ? done : (uint8_t)0;
-            if (A.cash_tap) A.cash_tap[row] = st.cash;
+            store_stream(live ? (float)lp : qnan, A.logp + row);
+            store_stream(live ? r : qnan, A.reward + row);
+            store_stream(live ? done : (uint8_t)0, A.done + row);
+            if (A.cash_tap) store_stream(st.cash, A.cash_tap + row);
         }
     };
 
@@ -440,39 +460,46 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
         if (j > 0) step_env(j - 1);
         __syncthreads();
 
-        // slot B: x_j to HBM; loads of row t0+j+1; the normals of step j
+        // slot B: loads of row t0+j+1; x_j to HBM
         // (row t0+j+1 exists for a stepped env; others read row 0)
         const int64_t t1 = live ? t0 + j + 1 : 0;
         const float *pr = C.price + (size_t)t1 * NS;
         const float *ir = C.ind + (size_t)t1 * NI;
-        float ind[IPL];
+        f4v ind[IPC];
         {
-            const float4 qv = *(const float4 *)(pr + SPL * min(hl, NS / SPL - 1));
-            q[0] = qv.x;
-            q[1] = qv.y;
-            q[2] = qv.z;
-            q[3] = qv.w;
+            const f4v qv = load_stream(pr + SPL * min(hl, NS / SPL - 1));
+#pragma unroll
+            for (int c = 0; c < SPL; ++c) q[c] = qv[c];
         }
 #pragma unroll
-        for (int mm = 0; mm < IPL; ++mm) ind[mm] = ir[hl + HALF * mm];
-        if (live && A.obs)
-            copy16((__bf16 *)A.obs + ((size_t)j * E + e) * A.ld_obs, xrow, obs_bytes, hl, HALF);
-        const U4 w = philox4x32_10(U4{(uint32_t)hl, (uint32_t)e, (uint32_t)(A.step0 + (uint64_t)j),
-                                      (uint32_t)agent},
-                                   A.key_lo, A.key_hi);
-        box_muller(uniform_open01(w.x), uniform_open01(w.y), z[0], z[1]);
-        box_muller(uniform_open01(w.z), uniform_open01(w.w), z[2], z[3]);
+        for (int mm = 0; mm < IPC; ++mm) ind[mm] = load_stream(ir + 4 * min(hl + HALF * mm, NI / 4 - 1));
+        if (live && A.obs) {
+            const u4v *src = (const u4v *)xrow;
+            u4v *dst = (u4v *)((__bf16 *)A.obs + ((size_t)j * E + e) * A.ld_obs);
+#pragma unroll
+            for (int c = hl; c < OBS_CHUNKS; c += HALF) store_stream(src[c], dst + c);
+        }
         __syncthreads();
 
         // slot L2: indicators of row t0+j+1 into x_{j+1} (the matrix waves
-        // are done with x_j)
+        // are done with x_j); the normals of step j
         if (live) {
             __bf16 *ri = xrow + 1 + 2 * n;
 #pragma unroll
-            for (int mm = 0; mm < IPL; ++mm) {
-                const int kk = hl + HALF * mm;
-                if (kk < nI) ri[kk] = to_bf16(ind[mm]);
+            for (int mm = 0; mm < IPC; ++mm) {
+                const int kk = 4 * (hl + HALF * mm);
+                if (kk < nI) {
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) ri[kk + c] = to_bf16(ind[mm][c]);
+                }
             }
+        }
+        {
+            const U4 w = philox4x32_10(
+                U4{(uint32_t)hl, (uint32_t)e, (uint32_t)(A.step0 + (uint64_t)j), (uint32_t)agent},
+                A.key_lo, A.key_hi);
+            box_muller_hw(uniform_open01(w.x), uniform_open01(w.y), z[0], z[1]);
+            box_muller_hw(uniform_open01(w.z), uniform_open01(w.w), z[2], z[3]);
         }
         __syncthreads();
 
@@ -535,7 +562,7 @@ __global__ __launch_bounds__(NWAVES *WAVE) void rollout_rs_kernel(RolloutArgs A)
     if (wave < MW)
         matrix_role<S>(A, s, pk, wave, lane);
     else
-        env_role<S::NS, S::NI>(A, s, pk, agent, ebase, nenv, wave - MW, lane);
+        env_role<S::NS, S::NI, S::KS1 * 32>(A, s, pk, agent, ebase, nenv, wave - MW, lane);
 }
 
 template <class S>
@@ -586,10 +613,13 @@ hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
     if (P.dtype != TP_BF16 || P.n != 100 || P.S != 1001 || a.env.nI != 800 || P.KS[0] != 32 ||
         P.NT[2] != 8)
         return hipErrorNotSupported;
-    // the env waves read each lane's 4 prices as one 16-byte load
-    if ((uintptr_t)a.env.price % 16) return hipErrorNotSupported;
-    if (P.H1 == 512 && P.H2 == 512) return rs::launch<rs::Shape<100, 800, 32, 7, 32, 32, 8>>(a, s);
-    if (P.H1 == 1024 && P.H2 == 1024) return rs::launch<rs::Shape<100, 800, 32, 7, 64, 64, 8>>(a, s);
+    // the env waves move prices, indicators, actions and holdings in
+    // 16-byte accesses
+    if ((uintptr_t)a.env.price % 16 || (uintptr_t)a.env.ind % 16 || (uintptr_t)a.action % 16 ||
+        (uintptr_t)a.shares_tap % 16)
+        return hipErrorNotSupported;
+    if (P.H1 == 512 && P.H2 == 512) return rs::launch<rs::Shape<100, 800, 32, 7, 32, 32, 8, 16>>(a, s);
+    if (P.H1 == 1024 && P.H2 == 1024) return rs::launch<rs::Shape<100, 800, 32, 7, 64, 64, 8, 16>>(a, s);
     return hipErrorNotSupported;
 }
 
