@@ -20,8 +20,9 @@
 //
 //   slot   matrix waves                         env waves
 //   A      Z = W1[:, KSB..] x_j  (indicators)   env step j-1, trajectory row j-1,
-//                                               balance/prices/holdings of x_j
-//   B      h1 = tanh(Z + W1[:, ..KSB] x_j + b1) x_j to HBM; loads of row t+j+1
+//                                               balance/prices/holdings of x_j;
+//                                               x_j to HBM; loads of row t+j+1
+//   B      h1 = tanh(Z + W1[:, ..KSB] x_j + b1) -
 //   L2     h2 = tanh(W2 h1 + b2)                indicators of row t+j+1 into x_{j+1};
 //                                               Philox + Box-Muller normals of step j
 //   L3     mu = W3 h2 + b3                      -
@@ -454,31 +455,33 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
     };
 
     __syncthreads();   // observations of step 0 are in LDS
+    f4v ind[IPC];
     for (int j = 0; j < A.L; ++j) {
-        // slot A: env step of step j-1 (the matrix waves read only the
-        // indicator columns of x_j meanwhile)
+        // slot A: env step of step j-1, which completes x_j (the matrix
+        // waves read only the indicator columns of x_j meanwhile); then
+        // this step's memory traffic, kept out of the short slot B where
+        // it would hold up the weight stream: x_j to HBM, loads of row
+        // t0+j+1 (which exists for a stepped env; others read row 0)
         if (j > 0) step_env(j - 1);
-        __syncthreads();
-
-        // slot B: loads of row t0+j+1; x_j to HBM
-        // (row t0+j+1 exists for a stepped env; others read row 0)
-        const int64_t t1 = live ? t0 + j + 1 : 0;
-        const float *pr = C.price + (size_t)t1 * NS;
-        const float *ir = C.ind + (size_t)t1 * NI;
-        f4v ind[IPC];
-        {
-            const f4v qv = load_stream(pr + SPL * min(hl, NS / SPL - 1));
-#pragma unroll
-            for (int c = 0; c < SPL; ++c) q[c] = qv[c];
-        }
-#pragma unroll
-        for (int mm = 0; mm < IPC; ++mm) ind[mm] = load_stream(ir + 4 * min(hl + HALF * mm, NI / 4 - 1));
         if (live && A.obs) {
             const u4v *src = (const u4v *)xrow;
             u4v *dst = (u4v *)((__bf16 *)A.obs + ((size_t)j * E + e) * A.ld_obs);
 #pragma unroll
             for (int c = hl; c < OBS_CHUNKS; c += HALF) store_stream(src[c], dst + c);
         }
+        {
+            const int64_t t1 = live ? t0 + j + 1 : 0;
+            const float *pr = C.price + (size_t)t1 * NS;
+            const float *ir = C.ind + (size_t)t1 * NI;
+            const f4v qv = load_stream(pr + SPL * min(hl, NS / SPL - 1));
+#pragma unroll
+            for (int c = 0; c < SPL; ++c) q[c] = qv[c];
+#pragma unroll
+            for (int mm = 0; mm < IPC; ++mm) ind[mm] = load_stream(ir + 4 * min(hl + HALF * mm, NI / 4 - 1));
+        }
+        __syncthreads();
+
+        // slot B: nothing for the env waves
         __syncthreads();
 
         // slot L2: indicators of row t0+j+1 into x_{j+1} (the matrix waves
