@@ -200,8 +200,8 @@ int tp_actor_pack(const tp_actor *actor, void *packed, size_t packed_bytes,
  *   Requires step0 + L <= horizon.  Device-side t is not visible to the
  *   host: an env with t < 0 or t + L > T1 - 1 is not stepped: its state is
  *   left unchanged, its action / logp / reward rows are NaN, done is 0, the
- *   taps hold the unchanged state and its observation rows are not written.  `packed` must come from tp_actor_pack with the same
- *   actor shape.
+ *   taps hold the unchanged state and its observation rows are not written.
+ *   `packed` must come from tp_actor_pack with the same actor shape.
  */
 int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg,
                const tp_env_state *st, const tp_actor *actor,
@@ -219,6 +219,48 @@ int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg,
 int tp_gae(const float *reward, const float *value, const uint8_t *done,
            int32_t L, int32_t E, float gamma, float lambda, float *adv,
            float *ret, void *stream);
+
+/* Critic: the value network of the PPO learner (PPO, Section 5.2; the
+ * learner trains the networks, Section 4.3):
+ *   V(x) = w3 . tanh(W2 tanh(W1 x + b1) + b2) + b3   (a scalar per state).
+ * fp32 masters stacked per agent, env e belongs to agent e / envs_per_agent:
+ *   W[0] [A][H1][S], W[1] [A][H2][H1], W[2] [A][H2] (w3);
+ *   b[0] [A][H1], b[1] [A][H2], b[2] [A].
+ * dtype as for the actor (TP_BF16: bf16 copies of weights, observations and
+ * hidden activations, fp32 accumulation; TP_F32: fp32 throughout). */
+typedef struct tp_critic {
+    int32_t n_agents;      /* A >= 1                                         */
+    int32_t envs_per_agent;/* A * envs_per_agent == E of the observations    */
+    int32_t dims[3];       /* {S, H1, H2}                                    */
+    int32_t dtype;         /* tp_dtype                                       */
+    const float *W[3];
+    const float *b[3];
+} tp_critic;
+
+/*
+ * tp_critic_packed_bytes / tp_critic_pack -- the critic's fp32 masters in
+ * the kernels' layout (as tp_actor_pack), in a caller-owned device buffer
+ * of tp_critic_packed_bytes() bytes (256-byte aligned).  Returns 0 / an
+ * error for an invalid critic.
+ */
+size_t tp_critic_packed_bytes(const tp_critic *critic);
+int tp_critic_pack(const tp_critic *critic, void *packed, size_t packed_bytes,
+                   void *stream);
+
+/*
+ * tp_critic_value -- V of every observation row of a time-major block of
+ * observations (a trajectory's obs, or its bootstrap row obs_last).
+ *   obs   [T][E][ld_obs] rows in the layout tp_rollout writes (dtype =
+ *         critic dtype; the first S = dims[0] columns are the state, the
+ *         rest up to K_pad are ignored);
+ *   value [T][E] fp32 out; row (t, e) uses agent e / envs_per_agent.
+ *   T >= 1, E = n_agents * envs_per_agent; obs 16-byte aligned, ld_obs >=
+ *   K_pad and a multiple of 8; `packed` from tp_critic_pack with the same
+ *   shape.  Rows are independent; results are deterministic.
+ */
+int tp_critic_value(const tp_critic *critic, const void *packed,
+                    size_t packed_bytes, const void *obs, int64_t ld_obs,
+                    int64_t T, int32_t E, float *value, void *stream);
 
 /* Message for the last non-OK return on the calling thread ("" if none). */
 const char *tp_last_error(void);

@@ -147,6 +147,35 @@ int check_actor(const tp_actor *a, PackedLayout *lay)
     return TP_OK;
 }
 
+struct CriticSig {
+    int dims[3], dtype, n_agents;
+    size_t total;
+};
+
+std::map<const void *, CriticSig> g_packed_critic;
+
+int check_critic(const tp_critic *c, CriticLayout *lay)
+{
+    if (!c) return fail(TP_EINVAL, "critic is NULL");
+    if (c->n_agents < 1 || c->envs_per_agent < 1)
+        return fail(TP_EINVAL, "critic.n_agents = %d, envs_per_agent = %d must be >= 1",
+                    c->n_agents, c->envs_per_agent);
+    if (c->dtype != TP_F32 && c->dtype != TP_BF16)
+        return fail(TP_EINVAL, "critic.dtype = %d", c->dtype);
+    for (int l = 0; l < 3; ++l)
+        if (!c->W[l] || !c->b[l]) return fail(TP_EINVAL, "critic W[%d] or b[%d] is NULL", l, l);
+    const int S = c->dims[0], H1 = c->dims[1], H2 = c->dims[2];
+    if (S < 1 || H1 < 1 || H2 < 1 || S > 65536 || H1 > 4096 || H2 > 4096)
+        return fail(TP_EINVAL, "critic dims {%d,%d,%d} invalid", S, H1, H2);
+    if (H1 % 4 || H2 % 4)
+        return fail(TP_EUNSUPPORTED, "critic needs H1, H2 multiples of 4 (got %d, %d)", H1, H2);
+    critic_layout(c, lay);
+    if (!lay->mfma && (size_t)16 * (lay->K_pad + H1 + 256) * 4 > LDS_LIMIT)
+        return fail(TP_EUNSUPPORTED, "critic {%d,%d,%d} exceeds the generic kernel's working set",
+                    S, H1, H2);
+    return TP_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -195,6 +224,38 @@ bool packed_layout(const tp_actor *a, PackedLayout *L)
     off = al(off + (size_t)(a->dtype == TP_BF16 ? L->NT[2] * 16 : L->n) * 4);
     L->agent_stride = off;
     L->total = off * (size_t)a->n_agents;
+    return true;
+}
+
+bool critic_layout(const tp_critic *c, CriticLayout *L)
+{
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    L->dtype = c->dtype;
+    L->S = c->dims[0];
+    L->H1 = c->dims[1];
+    L->H2 = c->dims[2];
+    L->K_pad = (L->S + 31) / 32 * 32;
+    L->mfma = critic_mfma_shape(*L);
+    size_t off = 0;
+    const int outs[2] = {L->H1, L->H2}, ins[2] = {L->K_pad, L->H1};
+    for (int l = 0; l < 2; ++l) {
+        L->NT[l] = (outs[l] + 15) / 16;
+        L->KS[l] = ins[l] / 32;
+        const size_t wbytes = L->mfma ? (size_t)L->NT[l] * L->KS[l] * 64 * 16
+                                      : (size_t)ins[l] * outs[l] * 4;
+        L->off_W[l] = off;
+        off = al(off + wbytes);
+    }
+    L->off_W[2] = off;
+    off = al(off + (size_t)L->H2 * 4);
+    L->off_b[0] = off;
+    off = al(off + (size_t)L->H1 * 4);
+    L->off_b[1] = off;
+    off = al(off + (size_t)L->H2 * 4);
+    L->off_b[2] = off;
+    off = al(off + 4);
+    L->agent_stride = off;
+    L->total = off * (size_t)c->n_agents;
     return true;
 }
 
@@ -346,6 +407,84 @@ int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *
         return fail(TP_EUNSUPPORTED, "rollout working set (%zu bytes of LDS) exceeds the limit",
                     a.lds_bytes);
     if (e != hipSuccess) return hip_fail(e, "rollout launch");
+    return ok();
+}
+
+size_t tp_critic_packed_bytes(const tp_critic *critic)
+{
+    CriticLayout L;
+    if (check_critic(critic, &L)) return 0;
+    g_err.clear();
+    return L.total;
+}
+
+int tp_critic_pack(const tp_critic *critic, void *packed, size_t packed_bytes, void *stream)
+{
+    CriticLayout L;
+    int rc;
+    if ((rc = check_critic(critic, &L))) return rc;
+    if (!packed || !aligned(packed, 256)) return fail(TP_EINVAL, "packed is NULL or not 256-byte aligned");
+    if (packed_bytes < L.total)
+        return fail(TP_EINVAL, "packed_bytes = %zu < required %zu", packed_bytes, L.total);
+    hipError_t e = launch_critic_pack(critic, L, packed, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "critic pack launch");
+    {
+        std::lock_guard<std::mutex> g(g_mu);
+        CriticSig sig;
+        for (int i = 0; i < 3; ++i) sig.dims[i] = critic->dims[i];
+        sig.dtype = critic->dtype;
+        sig.n_agents = critic->n_agents;
+        sig.total = L.total;
+        g_packed_critic[packed] = sig;
+    }
+    return ok();
+}
+
+int tp_critic_value(const tp_critic *critic, const void *packed, size_t packed_bytes,
+                    const void *obs, int64_t ld_obs, int64_t T, int32_t E, float *value,
+                    void *stream)
+{
+    CriticLayout L;
+    int rc;
+    if ((rc = check_critic(critic, &L))) return rc;
+    if (T < 1 || E < 1) return fail(TP_EINVAL, "T = %lld, E = %d must be >= 1", (long long)T, E);
+    if ((int64_t)critic->n_agents * critic->envs_per_agent != E)
+        return fail(TP_EINVAL, "n_agents * envs_per_agent = %lld != E = %d",
+                    (long long)critic->n_agents * critic->envs_per_agent, E);
+    if (!obs || !aligned(obs, 16)) return fail(TP_EINVAL, "obs is NULL or not 16-byte aligned");
+    if (ld_obs < L.K_pad || ld_obs % 8)
+        return fail(TP_EINVAL, "ld_obs = %lld must be >= K_pad = %d and a multiple of 8",
+                    (long long)ld_obs, L.K_pad);
+    if (!value || !aligned(value, 4)) return fail(TP_EINVAL, "value is NULL or misaligned");
+    if (!packed) return fail(TP_EINVAL, "packed is NULL");
+    {
+        std::lock_guard<std::mutex> g(g_mu);
+        auto it = g_packed_critic.find(packed);
+        if (it == g_packed_critic.end())
+            return fail(TP_EINVAL, "packed buffer was not filled by tp_critic_pack");
+        const CriticSig &sg = it->second;
+        for (int i = 0; i < 3; ++i)
+            if (sg.dims[i] != critic->dims[i])
+                return fail(TP_EINVAL, "packed buffer holds a different critic shape");
+        if (sg.dtype != critic->dtype || sg.n_agents != critic->n_agents)
+            return fail(TP_EINVAL, "packed buffer holds a different dtype / agent count");
+    }
+    if (packed_bytes < L.total)
+        return fail(TP_EINVAL, "packed_bytes = %zu < required %zu", packed_bytes, L.total);
+    CriticArgs a;
+    a.packed = (const uint8_t *)packed;
+    a.lay = L;
+    a.obs = obs;
+    a.ld_obs = ld_obs;
+    a.T = T;
+    a.E = E;
+    a.n_agents = critic->n_agents;
+    a.envs_per_agent = critic->envs_per_agent;
+    a.value = value;
+    hipError_t e = launch_critic_value(a, (hipStream_t)stream);
+    if (e == hipErrorInvalidConfiguration)
+        return fail(TP_EUNSUPPORTED, "critic launch exceeds the grid or LDS limits");
+    if (e != hipSuccess) return hip_fail(e, "critic launch");
     return ok();
 }
 

@@ -124,4 +124,15 @@ __device__ __forceinline__ double wave_sum(double v)
 // fp32 -> bf16, IEEE round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }
 
+// tanh(x) = 2 / (1 + exp(-2x)) - 1 with the hardware exp2 and reciprocal;
+// the argument comes in as e2 = -2 log2(e) x (one fma with a pre-scaled
+// bias).  Absolute error of a few 1e-7 (cancellation near 0 leaves the fp32
+// rounding of 1), far below the bf16 rounding the result goes through.
+constexpr float NEG_2LOG2E = -2.8853900817779268f;
+
+__device__ __forceinline__ float tanh_from_e2(float e2)
+{
+    return fmaf(2.0f, __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(e2)), -1.0f);
+}
+
 }  // namespace tpk

@@ -86,6 +86,40 @@ hipError_t launch_gae(const float *r, const float *v, const uint8_t *d, int L,
 hipError_t launch_pack(const tp_actor *a, const PackedLayout &lay, void *dst,
                        hipStream_t s);
 
+// Byte layout of one agent's packed critic inside the packed buffer.
+//  mfma (bf16, H1 == H2 in {512, 1024}, K_pad % 128 == 0): W1, W2 as MFMA
+//       A-fragments [NT][KS][64 lanes][8 bf16] (as the actor's);
+//  otherwise: W1T [K_pad][H1] and W2T [H1][H2] fp32 transposes (values
+//       rounded to bf16 for a bf16 critic), zero rows for k >= S.
+//  Then w3 [H2] fp32 (rounded to bf16 for a bf16 critic), b1 [H1],
+//  b2 [H2], b3 [1] fp32.
+struct CriticLayout {
+    int dtype;
+    int S, H1, H2, K_pad;
+    bool mfma;
+    int NT[2], KS[2];     // fragment tiles and k-steps of layers 1 and 2
+    size_t off_W[3], off_b[3];
+    size_t agent_stride;
+    size_t total;
+};
+
+bool critic_mfma_shape(const CriticLayout &L);
+bool critic_layout(const tp_critic *c, CriticLayout *out);
+
+struct CriticArgs {
+    const uint8_t *packed;
+    CriticLayout lay;
+    const void *obs;
+    int64_t ld_obs;
+    int64_t T;
+    int E, n_agents, envs_per_agent;
+    float *value;
+};
+
+hipError_t launch_critic_value(const CriticArgs &a, hipStream_t s);
+hipError_t launch_critic_pack(const tp_critic *c, const CriticLayout &lay, void *dst,
+                              hipStream_t s);
+
 // Maximum LDS per workgroup on gfx950.
 constexpr size_t LDS_LIMIT = 160 * 1024;
 

@@ -126,17 +126,6 @@ struct Shape {
     }
 };
 
-// tanh(x) = 2 / (1 + exp(-2x)) - 1 with the hardware exp2 and reciprocal;
-// `e2` = -2 log2(e) (x + b) comes in as one fma.  Absolute error of a few
-// 1e-7 (cancellation near 0 leaves fp32 rounding of 1), far below the bf16
-// rounding the result goes through.
-constexpr float NEG_2LOG2E = -2.8853900817779268f;
-
-__device__ __forceinline__ float tanh_from_e2(float e2)
-{
-    return fmaf(2.0f, __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(e2)), -1.0f);
-}
-
 __device__ __forceinline__ bf16x8 as_bf16x8(uint32_t __attribute__((ext_vector_type(4))) v)
 {
     return __builtin_bit_cast(bf16x8, v);

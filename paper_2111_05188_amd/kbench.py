@@ -8,6 +8,9 @@ Times, with HIP events on the launch stream:
     shape by default, where the rows touched per launch exceed the 256 MB
     last-level cache;
   * gae: the GAE scan over a 390 x E rollout;
+  * critic: the critic forward (1001-512-512-1 bf16) over a 100-stock
+    minute trajectory, 391 x 4,096 observation rows, against the bf16 MFMA
+    peak (algorithmic FLOPs 2 (S H1 + H1 H2 + H2) per row);
   * copy: a plain device-to-device copy of 1 GiB (the reference kernel used
     to calibrate HBM byte counters: FETCH_SIZE and WRITE_SIZE of this copy
     should each read 1 GiB per launch).
@@ -31,6 +34,7 @@ import torch
 from . import problem, tp
 
 PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
 
 
 def _time(fn, iters, stream):
@@ -49,7 +53,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--envs", type=int, default=65536)
     ap.add_argument("--iters", type=int, default=20)
-    ap.add_argument("--only", choices=["env_step", "gae", "copy"], default=None)
+    ap.add_argument("--only", choices=["env_step", "gae", "critic", "copy"], default=None)
     args = ap.parse_args()
     sys.path.insert(0, __file__.rsplit("/", 2)[0])
     import workloads as W
@@ -93,6 +97,31 @@ def main():
         nbytes = 17 * L * E
         out["gae"] = {"launch_ms": sec * 1e3, "bytes_per_launch": nbytes,
                       "GBs": nbytes / sec / 1e9, "hbm_frac": nbytes / sec / 1e9 / PEAK_HBM_GBS}
+
+    if args.only in (None, "critic"):
+        # critic forward over a 100-stock minute trajectory: (L+1) x 4096 rows
+        # of bf16 observations, 1001-512-512-1
+        cc = W.get_config("nasdaq100")
+        T, Ec = cc.L + 1, cc.E
+        print(f"[kbench] critic T={T} E={Ec}", file=sys.stderr, flush=True)
+        g = torch.Generator(device=dev).manual_seed(3)
+        obs = torch.randn(T, Ec, cc.K_pad, device=dev, generator=g).to(torch.bfloat16)
+        obs[:, :, cc.S:] = 0
+        Wc, bc = W.make_critic(cc)
+        crit = tp.CriticT([torch.from_numpy(w).to(dev) for w in Wc],
+                          [torch.from_numpy(x).to(dev) for x in bc], cc.dims[:3],
+                          tp.TP_BF16, cc.envs_per_agent)
+        crit.pack()
+        val = torch.empty(T, Ec, dtype=torch.float32, device=dev)
+        sec = _time(lambda: tp.critic_value(crit, obs, val), args.iters, stream)
+        S, H1, H2 = cc.dims[:3]
+        flops = 2.0 * (S * H1 + H1 * H2 + H2) * T * Ec
+        out["critic"] = {"launch_ms": sec * 1e3, "rows": T * Ec, "flops_per_launch": flops,
+                         "TFLOPs": flops / sec / 1e12,
+                         "mfma_frac": flops / sec / 1e12 / PEAK_BF16_TFLOPS,
+                         "obs_GBs": obs.numel() * 2 / sec / 1e9}
+        del obs, crit, val
+        torch.cuda.empty_cache()
 
     if args.only in (None, "copy"):
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB

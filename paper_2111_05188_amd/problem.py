@@ -61,6 +61,25 @@ class Problem:
     def set_values(self, values):
         self.values = torch.from_numpy(values).to(self.device)
 
+    def set_critic(self, critic_params):
+        """Critic S-H1-H2-1 of the actor's dtype (fp32 masters, packed)."""
+        W, b = critic_params
+        cfg = self.cfg
+        self.critic = tp.CriticT([torch.from_numpy(w).to(self.device) for w in W],
+                                 [torch.from_numpy(x).to(self.device) for x in b],
+                                 cfg.dims[:3], actor_dtype(cfg), self.actor.s.envs_per_agent)
+        self.critic.pack()
+        if self.values is None:
+            self.values = torch.empty(cfg.L + 1, self.E, dtype=torch.float32,
+                                      device=self.device)
+
+    def critic_values(self, stream=None):
+        """values [L+1][E] = V(obs_0 .. obs_L) of the stored trajectory."""
+        obs = self.traj.obs_all
+        if obs is None or obs.shape[0] != self.cfg.L + 1:
+            raise ValueError("critic values need the stored observations and obs_last")
+        tp.critic_value(self.critic, obs, self.values, stream)
+
     def reset(self, stream=None):
         tp.env_reset(self.mkt, self.ecfg, self.state, self.t0, None, stream)
 

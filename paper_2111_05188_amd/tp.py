@@ -53,6 +53,12 @@ class Actor(C.Structure):
                 ("log_std", C.c_void_p)]
 
 
+class Critic(C.Structure):
+    _fields_ = [("n_agents", C.c_int32), ("envs_per_agent", C.c_int32),
+                ("dims", C.c_int32 * 3), ("dtype", C.c_int32),
+                ("W", C.c_void_p * 3), ("b", C.c_void_p * 3)]
+
+
 class Traj(C.Structure):
     _fields_ = [("obs", C.c_void_p), ("ld_obs", C.c_int64),
                 ("action", C.c_void_p), ("logp", C.c_void_p),
@@ -62,8 +68,8 @@ class Traj(C.Structure):
 
 
 EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
-           "tp_actor_pack", "tp_rollout", "tp_gae", "tp_last_error",
-           "tp_version")
+           "tp_actor_pack", "tp_rollout", "tp_gae", "tp_critic_packed_bytes",
+           "tp_critic_pack", "tp_critic_value", "tp_last_error", "tp_version")
 
 _lib = None
 
@@ -84,9 +90,14 @@ def load(path: str = LIB_PATH):
     L.tp_actor_pack.argtypes = [vp, vp, sz, vp]
     L.tp_rollout.argtypes = [vp, vp, vp, vp, vp, sz, u64, u64, i32, vp, vp]
     L.tp_gae.argtypes = [vp, vp, vp, i32, i32, C.c_float, C.c_float, vp, vp, vp]
+    L.tp_critic_packed_bytes.argtypes = [vp]
+    L.tp_critic_packed_bytes.restype = sz
+    L.tp_critic_pack.argtypes = [vp, vp, sz, vp]
+    L.tp_critic_value.argtypes = [vp, vp, sz, vp, i64, i64, i32, vp, vp]
     L.tp_last_error.restype = C.c_char_p
     L.tp_version.restype = C.c_int
-    for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae"):
+    for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae",
+              "tp_critic_pack", "tp_critic_value"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -180,6 +191,38 @@ class ActorT:
         return self.packed
 
 
+class CriticT:
+    """fp32 master parameters of the critic stacked per agent (see tp_critic)."""
+
+    def __init__(self, W, b, dims, dtype: int, envs_per_agent: int):
+        self.W, self.b = list(W), list(b)
+        s = Critic()
+        s.n_agents = W[0].shape[0]
+        s.envs_per_agent = envs_per_agent
+        for i in range(3):
+            s.dims[i] = dims[i]
+        s.dtype = dtype
+        for l in range(3):
+            s.W[l] = _ptr(self.W[l])
+            s.b[l] = _ptr(self.b[l])
+        self.s = s
+        self.packed = None
+
+    def packed_bytes(self) -> int:
+        nb = load().tp_critic_packed_bytes(C.byref(self.s))
+        if nb == 0:
+            _check(TP_EINVAL)
+        return nb
+
+    def pack(self, stream=None):
+        nb = self.packed_bytes()
+        if self.packed is None or self.packed.numel() < nb:
+            self.packed = torch.empty(nb, dtype=torch.uint8, device=self.W[0].device)
+        _check(load().tp_critic_pack(C.byref(self.s), _ptr(self.packed), nb,
+                                     _stream(stream)))
+        return self.packed
+
+
 class TrajT:
     def __init__(self, action, logp, reward, done, obs=None, ld_obs=0,
                  cash_tap=None, shares_tap=None, obs_last=None):
@@ -191,19 +234,26 @@ class TrajT:
     def alloc(L, E, n, K_pad=None, obs_dtype=None, taps=False, obs_last=False,
               device="cuda"):
         kw = {}
+        obs_all = None
         if K_pad is not None:
             ld = (K_pad + 7) // 8 * 8
-            kw["obs"] = torch.empty(L, E, ld, dtype=obs_dtype, device=device)
+            # the bootstrap row follows the L rows, so that [L+1][E] is one
+            # block (the critic reads it in one call)
+            obs_all = torch.empty(L + (1 if obs_last else 0), E, ld, dtype=obs_dtype,
+                                  device=device)
+            kw["obs"] = obs_all[:L]
             kw["ld_obs"] = ld
             if obs_last:
-                kw["obs_last"] = torch.empty(E, ld, dtype=obs_dtype, device=device)
+                kw["obs_last"] = obs_all[L]
         if taps:
             kw["cash_tap"] = torch.empty(L, E, dtype=torch.float64, device=device)
             kw["shares_tap"] = torch.empty(L, E, n, dtype=torch.int32, device=device)
-        return TrajT(torch.empty(L, E, n, dtype=torch.float32, device=device),
-                     torch.empty(L, E, dtype=torch.float32, device=device),
-                     torch.empty(L, E, dtype=torch.float32, device=device),
-                     torch.empty(L, E, dtype=torch.uint8, device=device), **kw)
+        tr = TrajT(torch.empty(L, E, n, dtype=torch.float32, device=device),
+                   torch.empty(L, E, dtype=torch.float32, device=device),
+                   torch.empty(L, E, dtype=torch.float32, device=device),
+                   torch.empty(L, E, dtype=torch.uint8, device=device), **kw)
+        tr.obs_all = obs_all
+        return tr
 
     action = property(lambda self: self.t[0])
     logp = property(lambda self: self.t[1])
@@ -264,3 +314,14 @@ def last_error() -> str:
 
 def version() -> int:
     return load().tp_version()
+
+
+def critic_value(critic: CriticT, obs: torch.Tensor, value: torch.Tensor, stream=None):
+    """V of every row of obs [T][E][ld_obs] into value [T][E]."""
+    if critic.packed is None:
+        raise TPError(TP_EINVAL, "critic is not packed: call critic.pack()")
+    T, E, ld = obs.shape
+    assert value.shape == (T, E) and value.dtype == torch.float32
+    _check(load().tp_critic_value(C.byref(critic.s), _ptr(critic.packed),
+                                  critic.packed.numel(), _ptr(obs), ld, T, E,
+                                  _ptr(value), _stream(stream)))

@@ -97,3 +97,45 @@ def test_argument_errors_without_gpu():
     assert L.tp_rollout(C.byref(m), C.byref(cfg), C.byref(st), C.byref(a2), x, 1 << 30,
                         1, 0, 10, C.byref(tr), None) == tp.TP_EINVAL
     assert "match the market" in tp.last_error()
+
+
+def _critic(dims=(1001, 512, 512), dtype=tp.TP_BF16, A=1, epa=4096):
+    c = tp.Critic()
+    c.n_agents, c.envs_per_agent, c.dtype = A, epa, dtype
+    for i, d in enumerate(dims):
+        c.dims[i] = d
+    for l in range(3):
+        c.W[l] = 0x1000
+        c.b[l] = 0x2000
+    return c
+
+
+def test_critic_packed_bytes_host_only():
+    L = tp.load()
+    # MFMA layout: two layers of bf16 fragments, w3 and biases in fp32
+    nb = L.tp_critic_packed_bytes(C.byref(_critic()))
+    frag = (32 * 32 + 32 * 16) * 1024
+    assert frag < nb < frag + 16 * 1024
+    assert L.tp_critic_packed_bytes(C.byref(_critic(A=3))) == 3 * nb
+    # generic layout (fp32 transposes): K_pad x H1 + H1 x H2 floats
+    nb32 = L.tp_critic_packed_bytes(C.byref(_critic(dims=(301, 256, 256), dtype=tp.TP_F32)))
+    assert (320 * 256 + 256 * 256) * 4 < nb32 < (320 * 256 + 256 * 256) * 4 + 8 * 1024
+    assert L.tp_critic_packed_bytes(C.byref(_critic(dims=(301, 250, 256)))) == 0
+    assert "multiples of 4" in tp.last_error()
+
+
+def test_critic_argument_errors_without_gpu():
+    L = tp.load()
+    x = 0x100000
+    c = _critic(A=2, epa=8)
+    # E must equal n_agents * envs_per_agent
+    assert L.tp_critic_value(C.byref(c), x, 1 << 30, x, 1024, 3, 15, x, None) == tp.TP_EINVAL
+    assert "envs_per_agent" in tp.last_error()
+    # observation pitch must cover K_pad
+    assert L.tp_critic_value(C.byref(c), x, 1 << 30, x, 1000, 3, 16, x, None) == tp.TP_EINVAL
+    assert "ld_obs" in tp.last_error()
+    # a buffer that tp_critic_pack did not fill
+    assert L.tp_critic_value(C.byref(c), x, 1 << 30, x, 1024, 3, 16, x, None) == tp.TP_EINVAL
+    assert "tp_critic_pack" in tp.last_error()
+    assert L.tp_critic_value(None, x, 1 << 30, x, 1024, 3, 16, x, None) == tp.TP_EINVAL
+    assert L.tp_critic_value(C.byref(c), x, 1 << 30, x, 1024, 0, 16, x, None) == tp.TP_EINVAL

@@ -29,7 +29,7 @@ import numpy as np
 
 __all__ = [
     "Config", "CONFIGS", "get_config", "Market", "make_market", "make_t0",
-    "make_actor", "make_values", "make_actions", "K_PAD_MULTIPLE",
+    "make_actor", "make_critic", "make_values", "make_actions", "K_PAD_MULTIPLE",
 ]
 
 # Observation rows are padded to a multiple of the bf16 MFMA k-step.
@@ -66,7 +66,8 @@ class Config:
     share_scale: float = 2.0 ** -7
     log_std_init: float = -0.5
     seeds: dict = field(default_factory=lambda: dict(
-        market=20211109, t0=7, actor=1234, values=99, philox=0x5EED_0F_F1_2C))
+        market=20211109, t0=7, actor=1234, values=99, philox=0x5EED_0F_F1_2C,
+        critic=4321))
 
     @property
     def T1(self) -> int:
@@ -241,6 +242,27 @@ def make_actor(cfg: Config, seed: int | None = None, n_agents: int | None = None
             b[l][a] = rng.uniform(-bound, bound, size=o).astype(np.float32)
     log_std = np.full((A, n), cfg.log_std_init, dtype=np.float32)
     return W, b, log_std
+
+
+def make_critic(cfg: Config, seed: int | None = None, n_agents: int | None = None):
+    """fp32 master weights of the critic S-H1-H2-1: W_l [A][out][in] (the last
+    one [A][H2]), b_l [A][out] (the last one [A]) ~ U(+-1/sqrt(in)), one
+    stream per agent."""
+    seed = cfg.seeds["critic"] if seed is None else seed
+    A = cfg.n_agents if n_agents is None else n_agents
+    S, H1, H2, _ = cfg.dims
+    shapes = [(H1, S), (H2, H1), (1, H2)]
+    W = [np.empty((A,) + s, dtype=np.float32) for s in shapes]
+    b = [np.empty((A, s[0]), dtype=np.float32) for s in shapes]
+    for a in range(A):
+        rng = _block_rng(seed, 4, a)
+        for l, (o, i) in enumerate(shapes):
+            bound = 1.0 / math.sqrt(i)
+            W[l][a] = rng.uniform(-bound, bound, size=(o, i)).astype(np.float32)
+            b[l][a] = rng.uniform(-bound, bound, size=o).astype(np.float32)
+    W[2] = W[2].reshape(A, H2)
+    b[2] = b[2].reshape(A)
+    return W, b
 
 
 def make_values(cfg: Config, seed: int | None = None, L: int | None = None,
