@@ -4,11 +4,11 @@
 // A workgroup owns a block of rows of one time step and one agent (envs
 // e0 .. e0 + BM - 1 of that agent), so the weights it streams serve BM rows.
 //
-// MFMA kernel (bf16, hidden widths 512 or 1024, observation rows a multiple
-// of 128 long).  Four waves, one per SIMD, so each may hold 512 registers;
-// wave w owns output tiles w*OT .. w*OT+OT-1 of both hidden layers
-// (OT = H / 64) for all BM = 1024 / OT rows, an 8x8 or 16x4 register block
-// of 16x16 fp32 accumulators (256 registers).  The MFMA is
+// MFMA kernel (bf16, hidden widths 512 or 1024, observation rows of 1024
+// columns).  Eight waves, two per SIMD; wave w owns output tiles
+// w*OT .. w*OT+OT-1 of both hidden layers (OT = H / 128) for all
+// BM = 512 / OT rows, a 4x8 or 8x4 register block of 16x16 fp32
+// accumulators (128 registers).  The MFMA is
 // v_mfma_f32_16x16x32_bf16 with A = a packed weight fragment (16 outputs x
 // 32 inputs, streamed from L2 two k-steps ahead) and B = 32 inputs x 16 rows
 // from LDS.  Layer 1 stages the observation block through LDS in chunks of
@@ -16,7 +16,7 @@
 // while the current one is multiplied); h1 then replaces the staging
 // buffers in LDS.  Layer 2's tanh outputs are rounded to bf16 and reduced
 // with w3 straight from the accumulators: per lane, across the four lane
-// groups of a tile, then across the four waves in LDS, always in the same
+// groups of a tile, then across the eight waves in LDS, always in the same
 // order, so the result is deterministic.
 //
 // Generic kernel (fp32, or bf16 shapes the MFMA kernel does not take):
@@ -24,6 +24,19 @@
 // consecutive threads read consecutive addresses.
 #include "device.hpp"
 #include "internal.hpp"
+
+// MFMA kernel configuration: waves per workgroup and 16x16 accumulator
+// tiles per wave (each 4 registers).
+#ifndef CRITIC_NW
+#define CRITIC_NW 8
+#endif
+#ifndef CRITIC_ACC_TILES
+#define CRITIC_ACC_TILES 32
+#endif
+#ifndef CRITIC_MIN_WAVES
+#define CRITIC_MIN_WAVES 2
+#endif
+
 
 namespace tpk {
 
@@ -53,29 +66,28 @@ __device__ __forceinline__ RowBlock row_block(const CriticArgs &A, int BM)
     return r;
 }
 
-constexpr int CR_WAVES = 4;
-constexpr int CR_THREADS = CR_WAVES * WAVE;
-
-template <int OT>
-__global__ __launch_bounds__(CR_THREADS) void critic_mfma_kernel(CriticArgs A)
+// NW waves, each OT output tiles x RT row tiles of accumulators; KS1
+// k-steps of 32 inputs in layer 1 (a multiple of 4).
+template <int NW, int OT, int RT, int KS1>
+__global__ __launch_bounds__(NW *WAVE, CRITIC_MIN_WAVES) void critic_mfma_kernel(CriticArgs A)
 {
-    constexpr int H = 64 * OT;         // hidden width (both layers)
-    constexpr int BM = 1024 / OT;      // rows per workgroup
-    constexpr int RT = BM / 16;        // row tiles
+    constexpr int NTH = NW * WAVE;
+    constexpr int H = 16 * NW * OT;    // hidden width (both layers)
+    constexpr int BM = 16 * RT;        // rows per workgroup
     constexpr int KC = 128;            // columns per staged chunk (4 k-steps)
+    constexpr int NCH = KS1 / 4;
     constexpr int LDX = KC + 8;        // staged row pitch (conflict-free reads)
     constexpr int LDH = H + 8;
     constexpr int KS2 = H / 32;
-    constexpr int SPT = BM * (KC / 8) / CR_THREADS;   // 16-byte staging loads per thread
+    constexpr int SPT = BM * (KC / 8) / NTH;   // 16-byte staging loads per thread
+    static_assert(KS1 % 4 == 0 && KS2 % 2 == 0 && SPT >= 1, "shape");
     extern __shared__ __align__(16) uint8_t smem[];
     __bf16 *Xs = (__bf16 *)smem;       // [2][BM][LDX]
     __bf16 *H1s = (__bf16 *)smem;      // [BM][LDH] (after layer 1)
     constexpr size_t XBYTES = 2 * BM * LDX * 2, HBYTES = (size_t)BM * LDH * 2;
-    float *vred = (float *)(smem + (XBYTES > HBYTES ? XBYTES : HBYTES));   // [CR_WAVES][BM]
+    float *vred = (float *)(smem + (XBYTES > HBYTES ? XBYTES : HBYTES));   // [NW][BM]
 
     const CriticLayout &P = A.lay;
-    const int KS1 = P.KS[0];
-    const int NCH = KS1 / 4;
     const int tid = threadIdx.x, lane = tid % WAVE;
     const int w = __builtin_amdgcn_readfirstlane(tid / WAVE);
     const int r16 = lane & 15, kq = lane >> 4;
@@ -83,46 +95,51 @@ __global__ __launch_bounds__(CR_THREADS) void critic_mfma_kernel(CriticArgs A)
     const uint8_t *pk = A.packed + (size_t)rb.agent * P.agent_stride;
     const __bf16 *rows = (const __bf16 *)A.obs + ((size_t)rb.t * A.E + rb.e0) * A.ld_obs;
 
-    // weight fragments: layer 1 k-steps 0..KS1-1, then layer 2 0..KS2-1,
-    // read two k-steps ahead (ring slot = global k-step parity)
+    // weight fragments, two k-steps ahead in a ring of two slots
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
         (void *)pk, (short)0, (int)P.agent_stride, 0x00020000);
     const int voff = lane * 16;
     const int base1 = (int)P.off_W[0] + w * OT * KS1 * 1024;
     const int base2 = (int)P.off_W[1] + w * OT * KS2 * 1024;
-    const int G = KS1 + KS2;
     bf16x8 wr[2][OT];
-    auto fetch = [&](int slot, int g) {
-        g = g < G ? g : G - 1;   // past the end: a valid fragment, never used
+    auto fetch1 = [&](int slot, int k) {
 #pragma unroll
-        for (int ot = 0; ot < OT; ++ot) {
-            const int off = g < KS1 ? base1 + (ot * KS1 + g) * 1024
-                                    : base2 + (ot * KS2 + (g - KS1)) * 1024;
-            wr[slot][ot] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, off, 0));
-        }
+        for (int ot = 0; ot < OT; ++ot)
+            wr[slot][ot] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(
+                rsrc, voff, base1 + (ot * KS1 + k) * 1024, 0));
+    };
+    auto fetch2 = [&](int slot, int k) {
+#pragma unroll
+        for (int ot = 0; ot < OT; ++ot)
+            wr[slot][ot] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(
+                rsrc, voff, base2 + (ot * KS2 + k) * 1024, 0));
     };
 
-    // observation staging: thread tid moves chunks tid + 256 i (16 bytes of
-    // row (idx / 16), part idx % 16 of a 128-column chunk)
+    // observation staging: thread tid moves the 16-byte pieces tid + NTH i
+    // of a 128-column chunk (row idx / 16, piece idx % 16); rows past the
+    // block's last read its last row (never stored)
+    const __bf16 *src[SPT];
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+        const int idx = tid + NTH * i, row = min(idx >> 4, rb.nrow - 1), part = idx & 15;
+        src[i] = rows + (size_t)row * A.ld_obs + part * 8;
+    }
     u4v st[SPT];
     auto load_chunk = [&](int c) {
 #pragma unroll
-        for (int i = 0; i < SPT; ++i) {
-            const int idx = tid + CR_THREADS * i, row = idx >> 4, part = idx & 15;
-            const u4v *src = (const u4v *)(rows + (size_t)row * A.ld_obs + c * KC + part * 8);
-            st[i] = row < rb.nrow ? __builtin_nontemporal_load(src) : u4v{0, 0, 0, 0};
-        }
+        for (int i = 0; i < SPT; ++i)
+            st[i] = __builtin_nontemporal_load((const u4v *)(src[i] + c * KC));
     };
     auto store_chunk = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < SPT; ++i) {
-            const int idx = tid + CR_THREADS * i, row = idx >> 4, part = idx & 15;
+            const int idx = tid + NTH * i, row = idx >> 4, part = idx & 15;
             *(u4v *)(Xs + (size_t)buf * BM * LDX + row * LDX + part * 8) = st[i];
         }
     };
 
-    fetch(0, 0);
-    fetch(1, 1);
+    fetch1(0, 0);
+    fetch1(1, 1);
     load_chunk(0);
     store_chunk(0);
     __syncthreads();
@@ -149,14 +166,20 @@ __global__ __launch_bounds__(CR_THREADS) void critic_mfma_kernel(CriticArgs A)
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) acc[ot][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
     for (int c = 0; c < NCH; ++c) {
-        if (c + 1 < NCH) load_chunk(c + 1);
+        const bool more = c + 1 < NCH;
+        if (more) load_chunk(c + 1);
         const __bf16 *xb = Xs + (size_t)(c & 1) * BM * LDX + r16 * LDX + kq * 8;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            mma_kstep(xb + ks * 32, LDX, ks & 1);
-            fetch(ks & 1, c * 4 + ks + 2);
-        }
-        if (c + 1 < NCH) store_chunk((c + 1) & 1);
+        mma_kstep(xb, LDX, 0);
+        fetch1(0, c * 4 + 2);
+        mma_kstep(xb + 32, LDX, 1);
+        fetch1(1, c * 4 + 3);
+        mma_kstep(xb + 64, LDX, 0);
+        if (more) fetch1(0, c * 4 + 4);
+        else fetch2(0, 0);
+        mma_kstep(xb + 96, LDX, 1);
+        if (more) fetch1(1, c * 4 + 5);
+        else fetch2(1, 1);
+        if (more) store_chunk((c + 1) & 1);
         __syncthreads();
     }
 
@@ -185,13 +208,14 @@ __global__ __launch_bounds__(CR_THREADS) void critic_mfma_kernel(CriticArgs A)
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) acc[ot][rt] = floatx4{0.f, 0.f, 0.f, 0.f};
     {
-        // KS1 is a multiple of 4, so layer-2 k-step ks sits in ring slot ks & 1
+        // layer-2 k-step ks sits in ring slot ks & 1
         const __bf16 *hb = H1s + r16 * LDH + kq * 8;
         for (int ks = 0; ks < KS2; ks += 2) {
+            const bool more = ks + 2 < KS2;
             mma_kstep(hb + ks * 32, LDH, 0);
-            fetch(0, KS1 + ks + 2);
+            if (more) fetch2(0, ks + 2);
             mma_kstep(hb + (ks + 1) * 32, LDH, 1);
-            fetch(1, KS1 + ks + 3);
+            if (more) fetch2(1, ks + 3);
         }
     }
 
@@ -228,7 +252,7 @@ __global__ __launch_bounds__(CR_THREADS) void critic_mfma_kernel(CriticArgs A)
     if (tid < rb.nrow) {
         float v = *(const float *)(pk + P.off_b[2]);
 #pragma unroll
-        for (int ww = 0; ww < CR_WAVES; ++ww) v += vred[ww * BM + tid];
+        for (int ww = 0; ww < NW; ++ww) v += vred[ww * BM + tid];
         A.value[(size_t)rb.t * A.E + rb.e0 + tid] = v;
     }
 }
@@ -329,19 +353,24 @@ hipError_t launch_with_lds(K k, size_t nblk, int threads, size_t lds, const Crit
 bool critic_mfma_shape(const CriticLayout &L)
 {
     return L.dtype == TP_BF16 && L.H1 == L.H2 && (L.H1 == 512 || L.H1 == 1024) &&
-           L.K_pad % 128 == 0;
+           L.K_pad == 1024;
 }
 
 hipError_t launch_critic_value(const CriticArgs &a, hipStream_t s)
 {
     const CriticLayout &L = a.lay;
     if (L.mfma) {
-        const int OT = L.H1 / 64, BM = 1024 / OT;
+        constexpr int NW = CRITIC_NW;
+        const int OT = L.H1 / (16 * NW), RT = CRITIC_ACC_TILES / OT, BM = 16 * RT;
         const size_t nblk = (size_t)a.T * a.n_agents * ((a.envs_per_agent + BM - 1) / BM);
         const size_t xb = 2 * (size_t)BM * (128 + 8) * 2, hb = (size_t)BM * (L.H1 + 8) * 2;
-        const size_t lds = (xb > hb ? xb : hb) + CR_WAVES * (size_t)BM * 4;
-        if (OT == 8) return launch_with_lds(critic_mfma_kernel<8>, nblk, CR_THREADS, lds, a, s);
-        return launch_with_lds(critic_mfma_kernel<16>, nblk, CR_THREADS, lds, a, s);
+        const size_t lds = (xb > hb ? xb : hb) + NW * (size_t)BM * 4;
+        constexpr int T512 = 512 / (16 * NW), T1024 = 1024 / (16 * NW);
+        if (L.H1 == 512)
+            return launch_with_lds(critic_mfma_kernel<NW, T512, CRITIC_ACC_TILES / T512, 32>,
+                                   nblk, NW * WAVE, lds, a, s);
+        return launch_with_lds(critic_mfma_kernel<NW, T1024, CRITIC_ACC_TILES / T1024, 32>, nblk,
+                               NW * WAVE, lds, a, s);
     }
     const size_t nblk = (size_t)a.T * a.n_agents * ((a.envs_per_agent + GEN_BM - 1) / GEN_BM);
     const size_t lds = ((size_t)GEN_BM * (L.K_pad + L.H1) + (size_t)GEN_THREADS * GEN_BM) * 4;
