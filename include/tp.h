@@ -134,6 +134,10 @@ typedef struct tp_traj {
     int32_t *shares_tap;   /* [L][E][n] holdings after step j, or NULL      */
     void *obs_last;        /* [E][ld_obs] observation after the last step
                               (the bootstrap state), or NULL                 */
+    double *asset_tap;     /* [L][E] total asset b + p^T h after step j, at
+                              the prices of the new row (the account value
+                              of eq. (2)), or NULL; NaN for an env that is
+                              not stepped                                    */
 } tp_traj;
 
 /*
@@ -261,6 +265,26 @@ int tp_critic_pack(const tp_critic *critic, void *packed, size_t packed_bytes,
 int tp_critic_value(const tp_critic *critic, const void *packed,
                     size_t packed_bytes, const void *obs, int64_t ld_obs,
                     int64_t T, int32_t E, float *value, void *stream);
+
+/*
+ * tp_backtest_metrics -- the evaluator's measurements of a backtest
+ * (Section 5.2, "Evaluation metrics"), per env, from its total-asset series
+ * V_0 = v0[e] and V_t = v[t-1][e], t = 1..T (e.g. a rollout's asset_tap):
+ *   r_t = V_t / V_{t-1} - 1, s = sample standard deviation of r;
+ *   out[e][0] cumulative return  V_T / V_0 - 1
+ *   out[e][1] annual return      (V_T / V_0)^(P / T) - 1
+ *   out[e][2] annual volatility  s sqrt(P)
+ *   out[e][3] Sharpe ratio       (mean(r) - risk_free / P) / s * sqrt(P),
+ *                                0 when s = 0
+ *   out[e][4] max drawdown       max_t (peak_t - V_t) / peak_t, peak_t =
+ *                                max_{u <= t} V_u
+ *   with P = periods_per_year (252 for daily bars, 252 * 390 for minute
+ *   bars) and risk_free the annual rate.  v0 [E], v [T][E], out [E][5] fp64
+ *   device arrays; T, E >= 1, periods_per_year > 0.
+ */
+int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
+                        double periods_per_year, double risk_free, double *out,
+                        void *stream);
 
 /* Message for the last non-OK return on the calling thread ("" if none). */
 const char *tp_last_error(void);

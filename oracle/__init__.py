@@ -60,7 +60,7 @@ class Traj(C.Structure):
                 ("act", C.c_void_p), ("logp", C.c_void_p),
                 ("reward", C.c_void_p), ("done", C.c_void_p),
                 ("cash_tap", C.c_void_p), ("shares_tap", C.c_void_p),
-                ("mu", C.c_void_p)]
+                ("mu", C.c_void_p), ("asset_tap", C.c_void_p)]
 
 
 _lib = None
@@ -96,6 +96,7 @@ def lib():
         L.orc_rollout.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, u64, u64,
                                   i32, i32, vp, vp]
         L.orc_gae.argtypes = [vp, vp, vp, i32, i32, C.c_float, C.c_float, vp, vp]
+        L.orc_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp]
         L.orc_version.restype = C.c_int
         _lib = L
     return _lib
@@ -253,7 +254,8 @@ def mlp(act, agent, x):
 
 def rollout(mkt, ecfg, act, cash, shares, t, seed, step0, L, K_pad,
             env_ids=None, teacher=None, want=("obs", "act", "logp", "reward",
-                                              "done", "cash", "shares", "mu")):
+                                              "done", "cash", "shares", "mu",
+                                              "asset")):
     """Run O9 over the envs in (cash, shares, t) (updated in place).
 
     env_ids: global env index of each row (Philox counter and agent id);
@@ -277,7 +279,8 @@ def rollout(mkt, ecfg, act, cash, shares, t, seed, step0, L, K_pad,
                                 ("done", (L, E), np.uint8, "done"),
                                 ("cash", (L, E), np.float64, "cash_tap"),
                                 ("shares", (L, E, n), np.int32, "shares_tap"),
-                                ("mu", (L, E, n), np.float32, "mu")):
+                                ("mu", (L, E, n), np.float32, "mu"),
+                                ("asset", (L, E), np.float64, "asset_tap")):
         if key in want:
             out[key] = np.zeros(shape, dtype=dt)
             setattr(tr, fld, _p(out[key]))
@@ -297,3 +300,15 @@ def gae(r, v, d, gamma, lam):
     ret = np.zeros((L, E), dtype=np.float32)
     lib().orc_gae(_p(r), _p(v), _p(d), L, E, gamma, lam, _p(adv), _p(ret))
     return adv, ret
+
+
+def backtest_metrics(v0, v, periods_per_year, risk_free=0.0):
+    """Per-env {cumulative, annual return, annual volatility, Sharpe, max
+    drawdown} of the asset series V_0 = v0 [E], V_1..V_T = v [T][E]."""
+    v0 = _c(v0, np.float64)
+    v = _c(v, np.float64)
+    T, E = v.shape
+    assert v0.shape == (E,)
+    out = np.zeros((E, 5), dtype=np.float64)
+    lib().orc_backtest_metrics(_p(v0), _p(v), T, E, periods_per_year, risk_free, _p(out))
+    return out

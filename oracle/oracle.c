@@ -288,8 +288,11 @@ float orc_env_step_one(const orc_market *m, const orc_env_cfg *cfg,
     const float *p1 = price_row(m, *t + 1);
     double b = *cash;
 
-    double V = b;
-    for (int32_t i = 0; i < n; ++i) V += (double)shares[i] * (double)p[i];
+    /* V = b + p^T h: the dot product first (exact, see above), then one
+       rounded addition of the balance */
+    double ph = 0.0;
+    for (int32_t i = 0; i < n; ++i) ph += (double)shares[i] * (double)p[i];
+    const double V = b + ph;
 
     /* sells */
     double S = 0.0;
@@ -319,8 +322,9 @@ float orc_env_step_one(const orc_market *m, const orc_env_cfg *cfg,
     *cash = nb;
     *t += 1;
 
-    double V1 = nb;
-    for (int32_t i = 0; i < n; ++i) V1 += (double)shares[i] * (double)p1[i];
+    double ph1 = 0.0;
+    for (int32_t i = 0; i < n; ++i) ph1 += (double)shares[i] * (double)p1[i];
+    const double V1 = nb + ph1;
 
     if (diag) { diag[0] = V; diag[1] = V1; diag[2] = S; diag[3] = G; diag[4] = b_s; }
     return (float)(cfg->reward_scale * (V1 - V));
@@ -432,7 +436,9 @@ void orc_mlp(const orc_actor *a, int32_t agent, int32_t M, const float *x,
 /*   done = (step0 + j + 1 == horizon).                                      */
 /* Outputs (each optional, time-major): obs [L][E][K_pad] (fp32 or bf16     */
 /* bits), act [L][E][n], logp [L][E], reward [L][E], done [L][E],           */
-/* cash_tap [L][E], shares_tap [L][E][n] (state after step j), mu [L][E][n]. */
+/* cash_tap [L][E], shares_tap [L][E][n] (state after step j), mu [L][E][n], */
+/* asset_tap [L][E] (total asset b + p^T h after step j, at the new prices;  */
+/* NaN for an env that is not stepped).                                      */
 /* ------------------------------------------------------------------------ */
 
 typedef struct {
@@ -445,6 +451,7 @@ typedef struct {
     double *cash_tap;
     int32_t *shares_tap;
     float *mu;
+    double *asset_tap;
 } orc_traj;
 
 void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
@@ -497,6 +504,7 @@ void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
                 if (tr->done) tr->done[row] = 0;
                 if (tr->cash_tap) tr->cash_tap[row] = cash[e];
                 if (tr->shares_tap) memcpy(tr->shares_tap + row * n, h, sizeof(int32_t) * n);
+                if (tr->asset_tap) tr->asset_tap[row] = NAN;
                 continue;
             }
 
@@ -537,6 +545,14 @@ void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
                 tr->done[row] = (uint8_t)((int64_t)(step0 + (uint64_t)j) + 1 == (int64_t)cfg->horizon);
             if (tr->cash_tap) tr->cash_tap[row] = cash[e];
             if (tr->shares_tap) memcpy(tr->shares_tap + row * n, h, sizeof(int32_t) * n);
+            if (tr->asset_tap) {
+                /* V = b + p_t^T h at the row the step moved to (eq. (2)'s
+                   account value) */
+                const float *p = price_row(m, t[e]);
+                double ph = 0.0;
+                for (int32_t i = 0; i < n; ++i) ph += (double)p[i] * (double)h[i];
+                tr->asset_tap[row] = cash[e] + ph;
+            }
         }
     }
     free(active);
@@ -568,5 +584,54 @@ void orc_gae(const float *r, const float *v, const uint8_t *d, int32_t L,
             adv[i] = (float)A;
             ret[i] = (float)(A + (double)v[i]);
         }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Backtest metrics of a total-asset series (Section 5.2, "Evaluation       */
+/* metrics").  Per env e, V_0 = v0[e] and V_t = v[(t-1) E + e], t = 1..T:    */
+/*   per-period returns  r_t = V_t / V_{t-1} - 1;                           */
+/*   cumulative return   V_T / V_0 - 1;                                     */
+/*   annual return       (V_T / V_0)^(P / T) - 1 (geometric, P periods a    */
+/*                       year);                                             */
+/*   annual volatility   s sqrt(P), s the sample standard deviation of r;   */
+/*   Sharpe ratio        (mean(r) - rf / P) / s * sqrt(P) (0 when s = 0);   */
+/*   max drawdown        max_t (max_{u<=t} V_u - V_t) / max_{u<=t} V_u.     */
+/* out [E][5] = {cumulative, annual return, annual volatility, Sharpe,      */
+/* max drawdown}.  T = 1 gives s = 0.                                        */
+/* ------------------------------------------------------------------------ */
+
+void orc_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
+                          double periods_per_year, double risk_free, double *out)
+{
+    for (int32_t e = 0; e < E; ++e) {
+        double *o = out + (size_t)e * 5;
+        /* the series for this env */
+        double *V = (double *)malloc(sizeof(double) * ((size_t)T + 1));
+        V[0] = v0[e];
+        for (int32_t t = 1; t <= T; ++t) V[t] = v[(size_t)(t - 1) * E + e];
+        /* returns, their mean and sample standard deviation (two passes) */
+        double mean = 0.0;
+        for (int32_t t = 1; t <= T; ++t) mean += V[t] / V[t - 1] - 1.0;
+        mean /= (double)T;
+        double ss = 0.0;
+        for (int32_t t = 1; t <= T; ++t) {
+            const double d = (V[t] / V[t - 1] - 1.0) - mean;
+            ss += d * d;
+        }
+        const double sd = T > 1 ? sqrt(ss / (double)(T - 1)) : 0.0;
+        o[0] = V[T] / V[0] - 1.0;
+        o[1] = pow(V[T] / V[0], periods_per_year / (double)T) - 1.0;
+        o[2] = sd * sqrt(periods_per_year);
+        o[3] = sd > 0.0 ? (mean - risk_free / periods_per_year) / sd * sqrt(periods_per_year) : 0.0;
+        /* drawdown against the running peak */
+        double peak = V[0], mdd = 0.0;
+        for (int32_t t = 0; t <= T; ++t) {
+            if (V[t] > peak) peak = V[t];
+            const double dd = (peak - V[t]) / peak;
+            if (dd > mdd) mdd = dd;
+        }
+        o[4] = mdd;
+        free(V);
     }
 }

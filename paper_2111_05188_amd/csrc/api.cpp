@@ -357,7 +357,8 @@ int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *
     if (!traj->action || !traj->logp || !traj->reward || !traj->done)
         return fail(TP_EINVAL, "traj.action/logp/reward/done must not be NULL");
     if (!aligned(traj->action, 4) || !aligned(traj->logp, 4) || !aligned(traj->reward, 4) ||
-        !aligned(traj->cash_tap, 8) || !aligned(traj->shares_tap, 4))
+        !aligned(traj->cash_tap, 8) || !aligned(traj->shares_tap, 4) ||
+        !aligned(traj->asset_tap, 8))
         return fail(TP_EINVAL, "traj arrays are not naturally aligned");
     const int K_pad = K_pad_of(mkt);
     if ((rc = check_obs(traj->obs, traj->ld_obs, actor->dtype, K_pad, "traj.obs")) ||
@@ -402,6 +403,7 @@ int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *
     a.cash_tap = traj->cash_tap;
     a.shares_tap = traj->shares_tap;
     a.obs_last = traj->obs_last;
+    a.asset_tap = traj->asset_tap;
     hipError_t e = launch_rollout(a, (hipStream_t)stream);
     if (e == hipErrorInvalidConfiguration)
         return fail(TP_EUNSUPPORTED, "rollout working set (%zu bytes of LDS) exceeds the limit",
@@ -485,6 +487,22 @@ int tp_critic_value(const tp_critic *critic, const void *packed, size_t packed_b
     if (e == hipErrorInvalidConfiguration)
         return fail(TP_EUNSUPPORTED, "critic launch exceeds the grid or LDS limits");
     if (e != hipSuccess) return hip_fail(e, "critic launch");
+    return ok();
+}
+
+int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
+                        double periods_per_year, double risk_free, double *out, void *stream)
+{
+    if (!v0 || !v || !out) return fail(TP_EINVAL, "a metrics array is NULL");
+    if (!aligned(v0, 8) || !aligned(v, 8) || !aligned(out, 8))
+        return fail(TP_EINVAL, "metrics arrays are not 8-byte aligned");
+    if (T < 1 || E < 1) return fail(TP_EINVAL, "T = %d, E = %d must be >= 1", T, E);
+    if (!(periods_per_year > 0.0))
+        return fail(TP_EINVAL, "periods_per_year = %g must be > 0", periods_per_year);
+    if (!std::isfinite(risk_free)) return fail(TP_EINVAL, "risk_free = %g", risk_free);
+    hipError_t e = launch_backtest_metrics(v0, v, T, E, periods_per_year, risk_free, out,
+                                           (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "metrics launch");
     return ok();
 }
 

@@ -70,6 +70,7 @@ struct HalfEnv {
     double cash;      // balance (same on every lane of the half)
     int h[SPL];       // holdings (0 for stocks >= n)
     float p[SPL];     // prices at the current row (0 for stocks >= n)
+    double value;     // total asset b + p^T h after the last step
 };
 
 // One transition of the env owned by this lane's half.  a[c]: raw actions of
@@ -207,6 +208,7 @@ __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
     for (int c = 0; c < SPL; ++c) hv1 += (double)h[c] * (double)q[c];
     const double V1 = nb + half_sum(hv1, upper);
     s.cash = nb;
+    s.value = V1;
 #pragma unroll
     for (int c = 0; c < SPL; ++c) {
         s.h[c] = h[c];

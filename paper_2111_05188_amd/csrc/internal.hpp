@@ -66,6 +66,7 @@ struct RolloutArgs {
     double *cash_tap;
     int32_t *shares_tap;
     void *obs_last;
+    double *asset_tap;
     // LDS carve-up (bytes / elements), filled by the launcher
     int ldx, ldh, ldmu, ldz, ldh2;
     size_t lds_X, lds_H, lds_MU, lds_OS, lds_PT, lds_scal, lds_Z, lds_B, lds_bytes;
@@ -80,6 +81,9 @@ hipError_t launch_env_step(const EnvConst &c, double *cash, int32_t *shares,
                            int64_t *t, const float *action, float *reward,
                            int E, void *obs, int64_t ld_obs, int obs_bf16,
                            hipStream_t s);
+hipError_t launch_backtest_metrics(const double *v0, const double *v, int T, int E,
+                                   double periods_per_year, double risk_free, double *out,
+                                   hipStream_t s);
 hipError_t launch_gae(const float *r, const float *v, const uint8_t *d, int L,
                       int E, double g, double gl, float *adv, float *ret,
                       hipStream_t s);

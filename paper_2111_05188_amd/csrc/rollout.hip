@@ -343,6 +343,7 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
                     A.reward[row] = qnan;
                     A.done[row] = 0;
                     if (A.cash_tap) A.cash_tap[row] = OC[sl];
+                    if (A.asset_tap) A.asset_tap[row] = (double)qnan;
                 }
             } else {
 #pragma unroll
@@ -358,6 +359,7 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
                     A.reward[row] = r;
                     A.done[row] = done;
                     if (A.cash_tap) A.cash_tap[row] = st.cash;
+                    if (A.asset_tap) A.asset_tap[row] = st.value;
                 }
                 if (j + 1 < A.L) {
                     if (A.obs) store_obs_row((OT *)A.obs + (row + E) * A.ld_obs);

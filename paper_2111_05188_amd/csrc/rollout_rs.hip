@@ -440,6 +440,7 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
             store_stream(live ? r : qnan, A.reward + row);
             store_stream(live ? done : (uint8_t)0, A.done + row);
             if (A.cash_tap) store_stream(st.cash, A.cash_tap + row);
+            if (A.asset_tap) store_stream(live ? st.value : (double)qnan, A.asset_tap + row);
         }
     };
 

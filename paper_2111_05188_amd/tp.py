@@ -64,12 +64,13 @@ class Traj(C.Structure):
                 ("action", C.c_void_p), ("logp", C.c_void_p),
                 ("reward", C.c_void_p), ("done", C.c_void_p),
                 ("cash_tap", C.c_void_p), ("shares_tap", C.c_void_p),
-                ("obs_last", C.c_void_p)]
+                ("obs_last", C.c_void_p), ("asset_tap", C.c_void_p)]
 
 
 EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_actor_pack", "tp_rollout", "tp_gae", "tp_critic_packed_bytes",
-           "tp_critic_pack", "tp_critic_value", "tp_last_error", "tp_version")
+           "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
+           "tp_last_error", "tp_version")
 
 _lib = None
 
@@ -94,10 +95,11 @@ def load(path: str = LIB_PATH):
     L.tp_critic_packed_bytes.restype = sz
     L.tp_critic_pack.argtypes = [vp, vp, sz, vp]
     L.tp_critic_value.argtypes = [vp, vp, sz, vp, i64, i64, i32, vp, vp]
+    L.tp_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp, vp]
     L.tp_last_error.restype = C.c_char_p
     L.tp_version.restype = C.c_int
     for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae",
-              "tp_critic_pack", "tp_critic_value"):
+              "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -225,10 +227,12 @@ class CriticT:
 
 class TrajT:
     def __init__(self, action, logp, reward, done, obs=None, ld_obs=0,
-                 cash_tap=None, shares_tap=None, obs_last=None):
-        self.t = (action, logp, reward, done, obs, cash_tap, shares_tap, obs_last)
+                 cash_tap=None, shares_tap=None, obs_last=None, asset_tap=None):
+        self.t = (action, logp, reward, done, obs, cash_tap, shares_tap, obs_last,
+                  asset_tap)
         self.s = Traj(_ptr(obs), ld_obs, _ptr(action), _ptr(logp), _ptr(reward),
-                      _ptr(done), _ptr(cash_tap), _ptr(shares_tap), _ptr(obs_last))
+                      _ptr(done), _ptr(cash_tap), _ptr(shares_tap), _ptr(obs_last),
+                      _ptr(asset_tap))
 
     @staticmethod
     def alloc(L, E, n, K_pad=None, obs_dtype=None, taps=False, obs_last=False,
@@ -248,6 +252,7 @@ class TrajT:
         if taps:
             kw["cash_tap"] = torch.empty(L, E, dtype=torch.float64, device=device)
             kw["shares_tap"] = torch.empty(L, E, n, dtype=torch.int32, device=device)
+            kw["asset_tap"] = torch.empty(L, E, dtype=torch.float64, device=device)
         tr = TrajT(torch.empty(L, E, n, dtype=torch.float32, device=device),
                    torch.empty(L, E, dtype=torch.float32, device=device),
                    torch.empty(L, E, dtype=torch.float32, device=device),
@@ -263,6 +268,7 @@ class TrajT:
     cash_tap = property(lambda self: self.t[5])
     shares_tap = property(lambda self: self.t[6])
     obs_last = property(lambda self: self.t[7])
+    asset_tap = property(lambda self: self.t[8])
 
 
 def _dtype_code(t: torch.Tensor | None, default=TP_F32) -> int:
@@ -325,3 +331,15 @@ def critic_value(critic: CriticT, obs: torch.Tensor, value: torch.Tensor, stream
     _check(load().tp_critic_value(C.byref(critic.s), _ptr(critic.packed),
                                   critic.packed.numel(), _ptr(obs), ld, T, E,
                                   _ptr(value), _stream(stream)))
+
+
+def backtest_metrics(v0: torch.Tensor, v: torch.Tensor, periods_per_year: float,
+                     risk_free: float = 0.0, out: torch.Tensor | None = None, stream=None):
+    """Per-env [cumulative, annual return, annual volatility, Sharpe, max
+    drawdown] of V_0 = v0 [E], V_1..V_T = v [T][E] (fp64)."""
+    T, E = v.shape
+    if out is None:
+        out = torch.empty(E, 5, dtype=torch.float64, device=v.device)
+    _check(load().tp_backtest_metrics(_ptr(v0), _ptr(v), T, E, periods_per_year,
+                                      risk_free, _ptr(out), _stream(stream)))
+    return out

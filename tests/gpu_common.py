@@ -90,6 +90,10 @@ def compare_rollout(cfg, pb, out, ids, L, check_obs=True):
         g_sh = pb.traj.shares_tap[:L].index_select(1, ids_t).cpu().numpy()
         assert np.array_equal(g_sh, out["shares"]), "share counts differ"
         assert np.array_equal(g_cash, out["cash"]), "balances differ"
+    if pb.traj.asset_tap is not None:
+        # b + p^T h is exact in fp64 (prices in [2^-2, 2^13)), so bit-exact
+        g_as = pb.traj.asset_tap[:L].index_select(1, ids_t).cpu().numpy()
+        assert np.array_equal(g_as, out["asset"], equal_nan=True), "total assets differ"
     if check_obs and pb.traj.obs is not None:
         K = cfg.K_pad
         g_obs = pb.traj.obs[:L].index_select(1, ids_t)[..., :K]

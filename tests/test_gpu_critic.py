@@ -33,7 +33,8 @@ def _obs_f32(obs):
 
 
 def _run(cfg, E, L, rows, n_agents=1, sample=None):
-    c = cfg.with_(N=rows - 1, E=E, n_agents=n_agents)
+    # episode length L, so that the bootstrap row obs_L is row L of the block
+    c = cfg.with_(N=rows - 1, E=E, n_agents=n_agents, L=L)
     mk = W.make_market(c)
     t0 = W.make_t0(c)
     pb, _ = build_problem(c, mk, t0, taps=False)
