@@ -97,6 +97,10 @@ def lib():
                                   i32, i32, vp, vp]
         L.orc_gae.argtypes = [vp, vp, vp, i32, i32, C.c_float, C.c_float, vp, vp]
         L.orc_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp]
+        L.orc_ensemble_fuse.argtypes = [vp, i32, i32, C.c_int64]
+        L.orc_fitness.argtypes = [vp, i32, i32, i32, C.c_double, vp]
+        L.orc_keep_best.argtypes = [vp, vp, vp, vp, vp, i32, C.c_int64]
+        L.orc_select.argtypes = [vp, vp, i32, C.c_int64, i32, vp]
         L.orc_version.restype = C.c_int
         _lib = L
     return _lib
@@ -312,3 +316,42 @@ def backtest_metrics(v0, v, periods_per_year, risk_free=0.0):
     out = np.zeros((E, 5), dtype=np.float64)
     lib().orc_backtest_metrics(_p(v0), _p(v), T, E, periods_per_year, risk_free, _p(out))
     return out
+
+
+def ensemble_fuse(params):
+    """params [N][K][P] fp32 -> every pod of agent g holds the mean of its K pods."""
+    p = np.array(params, dtype=np.float32, order="C", copy=True)
+    N, K, P = p.shape
+    lib().orc_ensemble_fuse(_p(p), N, K, P)
+    return p
+
+
+def fitness(reward, n_agents, gamma):
+    """Per-agent mean over envs of sum_j gamma^j r_j (reward [L][E])."""
+    r = _c(reward, np.float32)
+    L, E = r.shape
+    f = np.zeros(n_agents, dtype=np.float64)
+    lib().orc_fitness(_p(r), L, E, n_agents, gamma, _p(f))
+    return f
+
+
+def keep_best(fit, best, stall, params, best_params):
+    """Evaluator bookkeeping; returns updated copies (best, stall, best_params)."""
+    fit = _c(fit, np.float64)
+    best = np.array(best, dtype=np.float64, copy=True)
+    stall = np.array(stall, dtype=np.int32, copy=True)
+    params = _c(params, np.float32)
+    bp = np.array(best_params, dtype=np.float32, order="C", copy=True)
+    A, P = params.shape
+    lib().orc_keep_best(_p(fit), _p(best), _p(stall), _p(params), _p(bp), A, P)
+    return best, stall, bp
+
+
+def select(fit, params, keep):
+    """Selector: returns (rank [N], new params [N][P])."""
+    fit = _c(fit, np.float64)
+    p = np.array(params, dtype=np.float32, order="C", copy=True)
+    N, P = p.shape
+    rank = np.zeros(N, dtype=np.int32)
+    lib().orc_select(_p(fit), _p(p), N, P, keep, _p(rank))
+    return rank, p

@@ -635,3 +635,108 @@ void orc_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t 
         free(V);
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Evolution layer (Section 4.2).                                            */
+/*                                                                           */
+/* Model ensemble: agent g is trained by K pods that differ only in their   */
+/* random seeds; fusing gives every pod the mean of the agent's K parameter */
+/* vectors.  params [N][K][P], in place; the mean is summed in fp64 over    */
+/* k = 0..K-1 and rounded once.                                              */
+/* ------------------------------------------------------------------------ */
+
+void orc_ensemble_fuse(float *params, int32_t N, int32_t K, int64_t P)
+{
+    for (int32_t g = 0; g < N; ++g) {
+        float *base = params + (size_t)g * K * P;
+        for (int64_t p = 0; p < P; ++p) {
+            double s = 0.0;
+            for (int32_t k = 0; k < K; ++k) s += (double)base[(size_t)k * P + p];
+            const float m = (float)(s / (double)K);
+            for (int32_t k = 0; k < K; ++k) base[(size_t)k * P + p] = m;
+        }
+    }
+}
+
+/* Fitness (the objective J of eq. (1) as the evaluator's score): per agent */
+/* g, the mean over its envs e of sum_j gamma^j r[j][e].  An env with a NaN */
+/* reward (not stepped) is left out; an agent without stepped envs gets NaN.*/
+void orc_fitness(const float *reward, int32_t L, int32_t E, int32_t A,
+                 double gamma, double *fitness)
+{
+    const int32_t epa = E / A;
+    for (int32_t g = 0; g < A; ++g) {
+        double sum = 0.0;
+        int32_t cnt = 0;
+        for (int32_t e = g * epa; e < (g + 1) * epa; ++e) {
+            double ret = 0.0, disc = 1.0;
+            int ok = 1;
+            for (int32_t j = 0; j < L; ++j) {
+                const float r = reward[(size_t)j * E + e];
+                if (isnan(r)) ok = 0;
+                ret += disc * (double)r;
+                disc *= gamma;
+            }
+            if (ok) {
+                sum += ret;
+                ++cnt;
+            }
+        }
+        fitness[g] = cnt ? sum / (double)cnt : NAN;
+    }
+}
+
+/* Keep-best bookkeeping of the evaluator: an agent whose fitness beats its */
+/* best so far (a NaN best counts as beaten; a NaN fitness never beats)     */
+/* takes it as the new best, its parameters become best_params and its     */
+/* stall count resets; otherwise the stall count grows by one (a training   */
+/* loop stops the agent once it reaches the patience: early stopping).      */
+void orc_keep_best(const double *fitness, double *best, int32_t *stall,
+                   const float *params, float *best_params, int32_t A, int64_t P)
+{
+    for (int32_t g = 0; g < A; ++g) {
+        const int better = !isnan(fitness[g]) && (isnan(best[g]) || fitness[g] > best[g]);
+        if (better) {
+            best[g] = fitness[g];
+            memcpy(best_params + (size_t)g * P, params + (size_t)g * P, sizeof(float) * (size_t)P);
+            stall[g] = 0;
+        } else {
+            stall[g] += 1;
+        }
+    }
+}
+
+/* Selector (Section 4.2; the selection step of a genetic algorithm): rank  */
+/* the N agents by fitness, descending, NaN last, ties to the lower index;  */
+/* the `keep` best survive and the agent of rank r >= keep becomes a copy   */
+/* of the survivor of rank (r - keep) mod keep.  rank [N] out; params       */
+/* [N][P] in place.                                                          */
+void orc_select(const double *fitness, float *params, int32_t N, int64_t P,
+                int32_t keep, int32_t *rank)
+{
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)N);
+    for (int32_t i = 0; i < N; ++i) order[i] = i;
+    /* insertion sort by (fitness desc, NaN last, index asc) */
+    for (int32_t a = 1; a < N; ++a) {
+        const int32_t x = order[a];
+        int32_t b = a - 1;
+        while (b >= 0) {
+            const int32_t y = order[b];
+            const double fx = fitness[x], fy = fitness[y];
+            int x_first;
+            if (isnan(fx)) x_first = 0;
+            else if (isnan(fy)) x_first = 1;
+            else x_first = fx > fy;
+            if (!x_first) break;
+            order[b + 1] = y;
+            --b;
+        }
+        order[b + 1] = x;
+    }
+    for (int32_t r = 0; r < N; ++r) rank[order[r]] = r;
+    for (int32_t r = keep; r < N; ++r) {
+        const int32_t dst = order[r], src = order[(r - keep) % keep];
+        memcpy(params + (size_t)dst * P, params + (size_t)src * P, sizeof(float) * (size_t)P);
+    }
+    free(order);
+}
