@@ -286,6 +286,58 @@ int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
                         double periods_per_year, double risk_free, double *out,
                         void *stream);
 
+/*
+ * Evolution layer (Section 4.2): model ensemble, evaluator and selector
+ * over a population of agents whose parameters are flat fp32 vectors of P
+ * values each (e.g. the actor's W and b masters laid end to end).
+ */
+
+/*
+ * tp_ensemble_fuse -- every pod of agent g (K pods trained with different
+ * seeds) takes the mean of the agent's K parameter vectors.
+ *   params [N][K][P] fp32, in place; each mean is summed in fp64 over
+ *   k = 0..K-1 and rounded once.  N, K >= 1, P >= 1.
+ */
+int tp_ensemble_fuse(float *params, int32_t N, int32_t K, int64_t P,
+                     void *stream);
+
+/*
+ * tp_fitness -- the evaluator's fitness score, the objective J of eq. (1)
+ * on an evaluation rollout: env_return[e] = sum_j gamma^j reward[j][e]
+ * (fp64; NaN if any of the env's rewards is NaN, i.e. it was not stepped),
+ * and fitness[g] = the mean of env_return over the envs of agent g that
+ * were stepped (NaN if none), in env order.  Env e belongs to agent
+ * e / (E / n_agents).
+ *   reward [L][E] fp32; env_return [E], fitness [n_agents] fp64 out;
+ *   E % n_agents == 0.
+ */
+int tp_fitness(const float *reward, int32_t L, int32_t E, int32_t n_agents,
+               double gamma, double *env_return, double *fitness, void *stream);
+
+/*
+ * tp_keep_best -- the evaluator's keep-best bookkeeping: for every agent g
+ * whose fitness[g] beats best[g] (a NaN best is always beaten, a NaN
+ * fitness never beats), best[g] = fitness[g], best_params[g] = params[g]
+ * and stall[g] = 0; otherwise stall[g] += 1.  A training loop stops the
+ * agent (early stopping) once stall[g] reaches its patience and keeps
+ * best_params[g] as the final agent.
+ *   fitness, best [A] fp64; stall [A] int32; params, best_params [A][P].
+ */
+int tp_keep_best(const double *fitness, double *best, int32_t *stall,
+                 const float *params, float *best_params, int32_t A, int64_t P,
+                 void *stream);
+
+/*
+ * tp_select -- the selector's step (Section 4.2, the selection of a genetic
+ * algorithm): rank the N agents by fitness, descending, NaN last, ties to
+ * the lower index; the `keep` best survive and the agent of rank r >= keep
+ * becomes a copy of the survivor of rank (r - keep) mod keep.
+ *   fitness [N] fp64; params [N][P] fp32, in place; rank [N] int32 out
+ *   (the rank of each agent).  1 <= keep <= N <= 1024.
+ */
+int tp_select(const double *fitness, float *params, int32_t N, int64_t P,
+              int32_t keep, int32_t *rank, void *stream);
+
 /* Message for the last non-OK return on the calling thread ("" if none). */
 const char *tp_last_error(void);
 

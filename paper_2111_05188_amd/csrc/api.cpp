@@ -506,6 +506,61 @@ int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
     return ok();
 }
 
+int tp_ensemble_fuse(float *params, int32_t N, int32_t K, int64_t P, void *stream)
+{
+    if (!params || !aligned(params, 4)) return fail(TP_EINVAL, "params is NULL or misaligned");
+    if (N < 1 || K < 1 || P < 1)
+        return fail(TP_EINVAL, "N = %d, K = %d, P = %lld must be >= 1", N, K, (long long)P);
+    hipError_t e = launch_ensemble_fuse(params, N, K, P, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "fuse launch");
+    return ok();
+}
+
+int tp_fitness(const float *reward, int32_t L, int32_t E, int32_t n_agents, double gamma,
+               double *env_return, double *fitness, void *stream)
+{
+    if (!reward || !env_return || !fitness) return fail(TP_EINVAL, "a fitness array is NULL");
+    if (!aligned(reward, 4) || !aligned(env_return, 8) || !aligned(fitness, 8))
+        return fail(TP_EINVAL, "fitness arrays are misaligned");
+    if (L < 1 || E < 1 || n_agents < 1 || E % n_agents)
+        return fail(TP_EINVAL, "L = %d, E = %d, n_agents = %d (E must be a multiple)", L, E,
+                    n_agents);
+    if (!(gamma > 0.0 && gamma <= 1.0)) return fail(TP_EINVAL, "gamma = %g outside (0,1]", gamma);
+    hipError_t e = launch_fitness(reward, L, E, n_agents, gamma, fitness, env_return,
+                                  (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "fitness launch");
+    return ok();
+}
+
+int tp_keep_best(const double *fitness, double *best, int32_t *stall, const float *params,
+                 float *best_params, int32_t A, int64_t P, void *stream)
+{
+    if (!fitness || !best || !stall || !params || !best_params)
+        return fail(TP_EINVAL, "a keep-best array is NULL");
+    if (!aligned(fitness, 8) || !aligned(best, 8) || !aligned(stall, 4) || !aligned(params, 4) ||
+        !aligned(best_params, 4))
+        return fail(TP_EINVAL, "keep-best arrays are misaligned");
+    if (A < 1 || P < 1) return fail(TP_EINVAL, "A = %d, P = %lld must be >= 1", A, (long long)P);
+    hipError_t e = launch_keep_best(fitness, best, stall, params, best_params, A, P,
+                                    (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "keep-best launch");
+    return ok();
+}
+
+int tp_select(const double *fitness, float *params, int32_t N, int64_t P, int32_t keep,
+              int32_t *rank, void *stream)
+{
+    if (!fitness || !params || !rank) return fail(TP_EINVAL, "a select array is NULL");
+    if (!aligned(fitness, 8) || !aligned(params, 4) || !aligned(rank, 4))
+        return fail(TP_EINVAL, "select arrays are misaligned");
+    if (N < 1 || N > 1024 || P < 1)
+        return fail(TP_EINVAL, "N = %d (1..1024), P = %lld", N, (long long)P);
+    if (keep < 1 || keep > N) return fail(TP_EINVAL, "keep = %d outside 1..N = %d", keep, N);
+    hipError_t e = launch_select(fitness, params, N, P, keep, rank, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "select launch");
+    return ok();
+}
+
 int tp_gae(const float *reward, const float *value, const uint8_t *done, int32_t L, int32_t E,
            float gamma, float lambda, float *adv, float *ret, void *stream)
 {

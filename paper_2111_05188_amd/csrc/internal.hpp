@@ -84,6 +84,13 @@ hipError_t launch_env_step(const EnvConst &c, double *cash, int32_t *shares,
 hipError_t launch_backtest_metrics(const double *v0, const double *v, int T, int E,
                                    double periods_per_year, double risk_free, double *out,
                                    hipStream_t s);
+hipError_t launch_ensemble_fuse(float *params, int N, int K, int64_t P, hipStream_t s);
+hipError_t launch_fitness(const float *r, int L, int E, int A, double gamma, double *fit,
+                          double *env_return, hipStream_t s);
+hipError_t launch_keep_best(const double *fit, double *best, int32_t *stall, const float *params,
+                            float *best_params, int A, int64_t P, hipStream_t s);
+hipError_t launch_select(const double *fit, float *params, int N, int64_t P, int keep,
+                         int32_t *rank, hipStream_t s);
 hipError_t launch_gae(const float *r, const float *v, const uint8_t *d, int L,
                       int E, double g, double gl, float *adv, float *ret,
                       hipStream_t s);

@@ -70,6 +70,7 @@ class Traj(C.Structure):
 EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_actor_pack", "tp_rollout", "tp_gae", "tp_critic_packed_bytes",
            "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
+           "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
            "tp_last_error", "tp_version")
 
 _lib = None
@@ -96,10 +97,15 @@ def load(path: str = LIB_PATH):
     L.tp_critic_pack.argtypes = [vp, vp, sz, vp]
     L.tp_critic_value.argtypes = [vp, vp, sz, vp, i64, i64, i32, vp, vp]
     L.tp_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp, vp]
+    L.tp_ensemble_fuse.argtypes = [vp, i32, i32, i64, vp]
+    L.tp_fitness.argtypes = [vp, i32, i32, i32, C.c_double, vp, vp, vp]
+    L.tp_keep_best.argtypes = [vp, vp, vp, vp, vp, i32, i64, vp]
+    L.tp_select.argtypes = [vp, vp, i32, i64, i32, vp, vp]
     L.tp_last_error.restype = C.c_char_p
     L.tp_version.restype = C.c_int
     for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae",
-              "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics"):
+              "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
+              "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -343,3 +349,37 @@ def backtest_metrics(v0: torch.Tensor, v: torch.Tensor, periods_per_year: float,
     _check(load().tp_backtest_metrics(_ptr(v0), _ptr(v), T, E, periods_per_year,
                                       risk_free, _ptr(out), _stream(stream)))
     return out
+
+
+def ensemble_fuse(params: torch.Tensor, stream=None):
+    """params [N][K][P] fp32: each pod takes its agent's mean, in place."""
+    N, K, P = params.shape
+    _check(load().tp_ensemble_fuse(_ptr(params), N, K, P, _stream(stream)))
+
+
+def fitness(reward: torch.Tensor, n_agents: int, gamma: float, env_return=None,
+            out=None, stream=None):
+    """Per-agent fitness (fp64 [n_agents]) and per-env returns (fp64 [E])."""
+    L, E = reward.shape
+    if env_return is None:
+        env_return = torch.empty(E, dtype=torch.float64, device=reward.device)
+    if out is None:
+        out = torch.empty(n_agents, dtype=torch.float64, device=reward.device)
+    _check(load().tp_fitness(_ptr(reward), L, E, n_agents, gamma, _ptr(env_return),
+                             _ptr(out), _stream(stream)))
+    return out, env_return
+
+
+def keep_best(fit, best, stall, params, best_params, stream=None):
+    A, P = params.shape
+    _check(load().tp_keep_best(_ptr(fit), _ptr(best), _ptr(stall), _ptr(params),
+                               _ptr(best_params), A, P, _stream(stream)))
+
+
+def select(fit, params, keep: int, rank=None, stream=None):
+    N, P = params.shape
+    if rank is None:
+        rank = torch.empty(N, dtype=torch.int32, device=params.device)
+    _check(load().tp_select(_ptr(fit), _ptr(params), N, P, keep, _ptr(rank),
+                            _stream(stream)))
+    return rank

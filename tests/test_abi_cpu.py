@@ -139,3 +139,22 @@ def test_critic_argument_errors_without_gpu():
     assert "tp_critic_pack" in tp.last_error()
     assert L.tp_critic_value(None, x, 1 << 30, x, 1024, 3, 16, x, None) == tp.TP_EINVAL
     assert L.tp_critic_value(C.byref(c), x, 1 << 30, x, 1024, 0, 16, x, None) == tp.TP_EINVAL
+
+
+def test_evolution_argument_errors_without_gpu():
+    L = tp.load()
+    x = 0x100000
+    assert L.tp_ensemble_fuse(None, 2, 2, 10, None) == tp.TP_EINVAL
+    assert L.tp_ensemble_fuse(x, 2, 0, 10, None) == tp.TP_EINVAL
+    # envs must split evenly over agents
+    assert L.tp_fitness(x, 10, 15, 2, 0.99, x, x, None) == tp.TP_EINVAL
+    assert "multiple" in tp.last_error()
+    assert L.tp_fitness(x, 10, 16, 2, 1.5, x, x, None) == tp.TP_EINVAL
+    assert L.tp_fitness(x, 10, 16, 2, 0.99, None, x, None) == tp.TP_EINVAL
+    assert L.tp_keep_best(x, x, x, x, None, 4, 10, None) == tp.TP_EINVAL
+    assert L.tp_keep_best(x, x, x, x, x, 0, 10, None) == tp.TP_EINVAL
+    # the selector ranks at most 1024 agents and keeps 1..N of them
+    assert L.tp_select(x, x, 1025, 10, 1, x, None) == tp.TP_EINVAL
+    assert L.tp_select(x, x, 8, 10, 0, x, None) == tp.TP_EINVAL
+    assert L.tp_select(x, x, 8, 10, 9, x, None) == tp.TP_EINVAL
+    assert "keep" in tp.last_error()
