@@ -11,6 +11,16 @@ Times, with HIP events on the launch stream:
   * critic: the critic forward (1001-512-512-1 bf16) over a 100-stock
     minute trajectory, 391 x 4,096 observation rows, against the bf16 MFMA
     peak (algorithmic FLOPs 2 (S H1 + H1 H2 + H2) per row);
+  * metrics: the backtest metrics of total-asset series, for 4,096 envs
+    over one 390-minute day and for 16 agents over a year of minute bars
+    (98,280 steps); algorithmic bytes T E 8 (series) + 8 E (V_0) + 40 E
+    (five metrics);
+  * evolution: ensemble fusion of 16 pods (4 agents x 4 pods) over the
+    actor and critic parameters of the 100-stock minute workload (P floats
+    per pod, N K P 4 bytes in and out), the fitness of a 390 x 16,384
+    reward block (L E 4 + 8 E + 8 A bytes), keep-best over 16 agents all
+    improving (A P 4 in and out) and the selector keeping 4 of 16 (12 P 4
+    in and out);
   * copy: a plain device-to-device copy of 1 GiB (the reference kernel used
     to calibrate HBM byte counters: FETCH_SIZE and WRITE_SIZE of this copy
     should each read 1 GiB per launch).
@@ -53,7 +63,8 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--envs", type=int, default=65536)
     ap.add_argument("--iters", type=int, default=20)
-    ap.add_argument("--only", choices=["env_step", "gae", "critic", "copy"], default=None)
+    ap.add_argument("--only", default=None,
+                    choices=["env_step", "gae", "critic", "metrics", "evolution", "copy"])
     args = ap.parse_args()
     sys.path.insert(0, __file__.rsplit("/", 2)[0])
     import workloads as W
@@ -121,6 +132,69 @@ def main():
                          "mfma_frac": flops / sec / 1e12 / PEAK_BF16_TFLOPS,
                          "obs_GBs": obs.numel() * 2 / sec / 1e9}
         del obs, crit, val
+        torch.cuda.empty_cache()
+
+    if args.only in (None, "metrics"):
+        out["metrics"] = {}
+        for T, Em in ((390, 4096), (98280, 16)):
+            print(f"[kbench] metrics T={T} E={Em}", file=sys.stderr, flush=True)
+            g = torch.Generator(device=dev).manual_seed(T)
+            v0 = torch.full((Em,), 1e6, dtype=torch.float64, device=dev)
+            steps = 1.0 + 1e-3 * torch.randn(T, Em, dtype=torch.float64, device=dev, generator=g)
+            v = v0 * torch.cumprod(steps, dim=0)
+            met = torch.empty(Em, 5, dtype=torch.float64, device=dev)
+            sec = _time(lambda: tp.backtest_metrics(v0, v, 252.0 * 390, 0.02, out=met),
+                        args.iters, stream)
+            nbytes = 8 * T * Em + 8 * Em + 40 * Em
+            out["metrics"][f"T{T}_E{Em}"] = {
+                "launch_ms": sec * 1e3, "bytes_per_launch": nbytes, "GBs": nbytes / sec / 1e9,
+                "hbm_frac": nbytes / sec / 1e9 / PEAK_HBM_GBS}
+            del v0, steps, v, met
+        torch.cuda.empty_cache()
+
+    if args.only in (None, "evolution"):
+        cc = W.get_config("nasdaq100")
+        S, H1, H2, A_ = cc.dims
+        P = (S * H1 + H1 + H1 * H2 + H2 + H2 * A_ + 2 * A_) + (S * H1 + H1 + H1 * H2 + H2 + H2 + 1)
+        N, K = 4, 4
+        print(f"[kbench] evolution P={P}", file=sys.stderr, flush=True)
+        ev = {}
+        g = torch.Generator(device=dev).manual_seed(7)
+        pods = torch.randn(N, K, P, device=dev, generator=g)
+        sec = _time(lambda: tp.ensemble_fuse(pods), args.iters, stream)
+        nb = 2 * N * K * P * 4
+        ev["fuse"] = {"launch_ms": sec * 1e3, "bytes_per_launch": nb, "GBs": nb / sec / 1e9,
+                      "hbm_frac": nb / sec / 1e9 / PEAK_HBM_GBS}
+        del pods
+        L, Ef, Af = 390, 16384, 16
+        rew = 2.0 ** -8 * torch.randn(L, Ef, device=dev, generator=g)
+        ret = torch.empty(Ef, dtype=torch.float64, device=dev)
+        fit = torch.empty(Af, dtype=torch.float64, device=dev)
+        sec = _time(lambda: tp.fitness(rew, Af, 0.99, env_return=ret, out=fit), args.iters, stream)
+        nb = L * Ef * 4 + 8 * Ef + 8 * Af
+        ev["fitness"] = {"launch_ms": sec * 1e3, "bytes_per_launch": nb, "GBs": nb / sec / 1e9,
+                         "hbm_frac": nb / sec / 1e9 / PEAK_HBM_GBS}
+        params = torch.randn(Af, P, device=dev, generator=g)
+        bestp = torch.empty_like(params)
+        fit = torch.arange(Af, dtype=torch.float64, device=dev)
+        best = torch.full((Af,), float("nan"), dtype=torch.float64, device=dev)
+        stall = torch.zeros(Af, dtype=torch.int32, device=dev)
+
+        def kb():
+            best.fill_(float("nan"))          # every agent improves: the full copy
+            tp.keep_best(fit, best, stall, params, bestp)
+        sec = _time(kb, args.iters, stream)
+        nb = 2 * Af * P * 4
+        ev["keep_best"] = {"launch_ms": sec * 1e3, "bytes_per_launch": nb, "GBs": nb / sec / 1e9,
+                           "hbm_frac": nb / sec / 1e9 / PEAK_HBM_GBS,
+                           "note": "includes a 16-element fill"}
+        rank = torch.empty(Af, dtype=torch.int32, device=dev)
+        sec = _time(lambda: tp.select(fit, params, 4, rank=rank), args.iters, stream)
+        nb = 2 * (Af - 4) * P * 4
+        ev["select"] = {"launch_ms": sec * 1e3, "bytes_per_launch": nb, "GBs": nb / sec / 1e9,
+                        "hbm_frac": nb / sec / 1e9 / PEAK_HBM_GBS}
+        out["evolution"] = {"P": P, **ev}
+        del rew, ret, fit, params, bestp, best, stall, rank
         torch.cuda.empty_cache()
 
     if args.only in (None, "copy"):
