@@ -287,6 +287,85 @@ int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
                         void *stream);
 
 /*
+ * PPO learner (PPO, Section 5.2; hyper-parameters of Table 2: Adam,
+ * learning rate 2^-14, batch 2^10, repeat 2^3, ratio clip 0.25, entropy
+ * coefficient 0.02; the learner trains the networks on the transitions the
+ * workers stored, Section 4.3): minibatch updates of one agent's actor and
+ * critic, both read from and written to one flat fp32 vector.
+ *
+ * Flat parameters of one agent, fp32 [P] (P = tp_ppo_param_count), in order:
+ *   W1 [H1][S], b1 [H1], W2 [H2][H1], b2 [H2], W3 [n][H2], b3 [n],
+ *   log_std [n], Wc1 [C1][S], bc1 [C1], Wc2 [C2][C1], bc2 [C2], wc3 [C2],
+ *   bc3 [1]
+ * (a tp_actor / tp_critic with agent_stride = P points into [A][P]).
+ *
+ * One update on the minibatch rows idx[0..B-1] of a time-major trajectory
+ * (row r = j E + e of its [L][E] arrays) takes the gradient of
+ *   L = L_clip - ent_coef H + L_critic, where
+ *   logp_i = sum_k [-(a_ik - mu_ik)^2 / (2 sigma_k^2) - log_std_k] - (n/2) ln 2pi,
+ *   rho_i  = exp(logp_i - logp_old_i),
+ *   L_clip = -(1/B) sum_i min(rho_i A_i, clip(rho_i, 1 - clip, 1 + clip) A_i),
+ *   H      = sum_k (log_std_k + (1 + ln 2pi) / 2)   (Gaussian entropy),
+ *   L_critic = (1/B) sum_i (V_i - R_i)^2,
+ * with mu and V the actor and critic of this vector on observation row x_i
+ * (tanh hidden layers as in tp_rollout / tp_critic_value), then one Adam
+ * step (Kingma and Ba) at step number t:
+ *   m = b1 m + (1 - b1) g;  v = b2 v + (1 - b2) g^2;
+ *   theta -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps).
+ */
+typedef struct tp_ppo {
+    int32_t dims[6];       /* S, H1, H2, n (actor), C1, C2 (critic)           */
+    int32_t dtype;         /* TP_BF16: bf16 operands (weights rounded from the
+                              masters, observations as stored, activations and
+                              backpropagated gradients rounded), fp32 sums;
+                              TP_F32: fp32 throughout                        */
+    int32_t batch;         /* B, rows per minibatch: a multiple of 32        */
+    float clip;            /* ratio clip, 0 < clip < 1 (0.25)                */
+    float ent_coef;        /* entropy coefficient >= 0 (0.02)                */
+    float lr;              /* learning rate > 0 (2^-14)                      */
+    float beta1, beta2;    /* Adam decay rates in [0, 1) (0.9, 0.999)        */
+    float eps;             /* Adam epsilon > 0 (1e-8)                        */
+} tp_ppo;
+
+/* P for this configuration, or 0 (tp_last_error says why) when the
+ * configuration is invalid: S >= 1, 1 <= n <= 128, H1, H2, C1, C2 positive
+ * multiples of 32, batch a positive multiple of 32. */
+int64_t tp_ppo_param_count(const tp_ppo *cfg);
+
+/* Bytes of the caller-owned device workspace tp_ppo_update needs (operand
+ * copies of the weights, minibatch activations and gradients), or 0. */
+size_t tp_ppo_workspace_bytes(const tp_ppo *cfg);
+
+/*
+ * tp_ppo_update -- n_updates minibatch updates in sequence on `stream`.
+ *   params, adam_m, adam_v  [P] fp32 device, updated in place (m and v start
+ *                           at zero before step 1);
+ *   step0                   Adam step number of the first update (>= 1);
+ *                           update u uses step0 + u;
+ *   obs [rows][ld_obs]      observation rows (bf16 for TP_BF16, fp32 for
+ *                           TP_F32) as tp_rollout writes them; columns >= S
+ *                           are ignored; ld_obs >= S;
+ *   action [rows][n], logp, adv, ret [rows]  fp32: the stored raw actions,
+ *                           their log-probabilities under the policy that
+ *                           acted, the GAE advantages and returns;
+ *   idx [n_updates][B]      int64 device row indices (values outside
+ *                           [0, rows) are clamped into it; rows of envs that
+ *                           were not stepped hold NaN and must not be drawn);
+ *   grad [P]                optional (NULL): the last update's gradient;
+ *   stats [n_updates][4]    optional fp64: L_clip, H, L_critic and the
+ *                           fraction of rows with |rho - 1| > clip, at the
+ *                           parameters each update starts from;
+ *   workspace               >= tp_ppo_workspace_bytes, 256-byte aligned.
+ * Nothing is allocated.  Returns TP_EINVAL for a bad configuration, NULL or
+ * misaligned pointers, or a short workspace.
+ */
+int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v,
+                  int64_t step0, int32_t n_updates, const void *obs, int64_t ld_obs,
+                  const float *action, const float *logp, const float *adv,
+                  const float *ret, int64_t rows, const int64_t *idx, float *grad,
+                  double *stats, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Evolution layer (Section 4.2): model ensemble, evaluator and selector
  * over a population of agents whose parameters are flat fp32 vectors of P
  * values each (e.g. the actor's W and b masters laid end to end).

@@ -154,6 +154,30 @@ struct CriticSig {
 
 std::map<const void *, CriticSig> g_packed_critic;
 
+int check_ppo(const tp_ppo *c, PpoLayout *lay)
+{
+    if (!c) return fail(TP_EINVAL, "learner configuration is NULL");
+    const int32_t *d = c->dims;
+    if (c->dtype != TP_BF16 && c->dtype != TP_F32)
+        return fail(TP_EINVAL, "learner dtype %d", c->dtype);
+    if (d[0] < 1 || d[3] < 1 || d[3] > 128)
+        return fail(TP_EINVAL, "learner S = %d, n = %d (need S >= 1, 1 <= n <= 128)", d[0], d[3]);
+    for (int i : {1, 2, 4, 5})
+        if (d[i] < 32 || d[i] % 32)
+            return fail(TP_EINVAL, "learner hidden width dims[%d] = %d: positive multiples of 32",
+                        i, d[i]);
+    if (c->batch < 32 || c->batch % 32)
+        return fail(TP_EINVAL, "learner batch = %d: a positive multiple of 32", c->batch);
+    if (!(c->clip > 0.f && c->clip < 1.f)) return fail(TP_EINVAL, "clip = %g", c->clip);
+    if (!(c->ent_coef >= 0.f)) return fail(TP_EINVAL, "ent_coef = %g", c->ent_coef);
+    if (!(c->lr > 0.f)) return fail(TP_EINVAL, "lr = %g", c->lr);
+    if (!(c->beta1 >= 0.f && c->beta1 < 1.f) || !(c->beta2 >= 0.f && c->beta2 < 1.f))
+        return fail(TP_EINVAL, "Adam betas %g, %g outside [0, 1)", c->beta1, c->beta2);
+    if (!(c->eps > 0.f)) return fail(TP_EINVAL, "Adam eps = %g", c->eps);
+    ppo_layout(c, lay);
+    return TP_OK;
+}
+
 int check_critic(const tp_critic *c, CriticLayout *lay)
 {
     if (!c) return fail(TP_EINVAL, "critic is NULL");
@@ -503,6 +527,74 @@ int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
     hipError_t e = launch_backtest_metrics(v0, v, T, E, periods_per_year, risk_free, out,
                                            (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "metrics launch");
+    return ok();
+}
+
+int64_t tp_ppo_param_count(const tp_ppo *cfg)
+{
+    PpoLayout L;
+    if (check_ppo(cfg, &L) != TP_OK) return 0;
+    ok();
+    return L.P;
+}
+
+size_t tp_ppo_workspace_bytes(const tp_ppo *cfg)
+{
+    PpoLayout L;
+    if (check_ppo(cfg, &L) != TP_OK) return 0;
+    ok();
+    return L.total;
+}
+
+int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v, int64_t step0,
+                  int32_t n_updates, const void *obs, int64_t ld_obs, const float *action,
+                  const float *logp, const float *adv, const float *ret, int64_t rows,
+                  const int64_t *idx, float *grad, double *stats, void *workspace,
+                  size_t workspace_bytes, void *stream)
+{
+    PpoArgs a{};
+    int rc = check_ppo(cfg, &a.lay);
+    if (rc != TP_OK) return rc;
+    if (!params || !adam_m || !adam_v || !obs || !action || !logp || !adv || !ret || !idx ||
+        !workspace)
+        return fail(TP_EINVAL, "a learner array is NULL");
+    if (!aligned(params, 4) || !aligned(adam_m, 4) || !aligned(adam_v, 4) ||
+        !aligned(obs, cfg->dtype == TP_BF16 ? 2 : 4) || !aligned(action, 4) ||
+        !aligned(logp, 4) || !aligned(adv, 4) || !aligned(ret, 4) || !aligned(idx, 8) ||
+        (grad && !aligned(grad, 4)) || (stats && !aligned(stats, 8)))
+        return fail(TP_EINVAL, "learner arrays are misaligned");
+    if (!aligned(workspace, 256)) return fail(TP_EINVAL, "workspace must be 256-byte aligned");
+    if (workspace_bytes < a.lay.total)
+        return fail(TP_EINVAL, "workspace of %zu bytes, %zu needed", workspace_bytes, a.lay.total);
+    if (step0 < 1) return fail(TP_EINVAL, "step0 = %lld must be >= 1", (long long)step0);
+    if (n_updates < 1) return fail(TP_EINVAL, "n_updates = %d must be >= 1", n_updates);
+    if (rows < 1) return fail(TP_EINVAL, "rows = %lld must be >= 1", (long long)rows);
+    if (ld_obs < cfg->dims[0])
+        return fail(TP_EINVAL, "ld_obs = %lld < S = %d", (long long)ld_obs, cfg->dims[0]);
+    a.params = params;
+    a.adam_m = adam_m;
+    a.adam_v = adam_v;
+    a.step0 = step0;
+    a.n_updates = n_updates;
+    a.obs = obs;
+    a.ld_obs = ld_obs;
+    a.action = action;
+    a.logp = logp;
+    a.adv = adv;
+    a.ret = ret;
+    a.rows = rows;
+    a.idx = idx;
+    a.grad_out = grad;
+    a.stats = stats;
+    a.workspace = workspace;
+    a.clip = cfg->clip;
+    a.ent_coef = cfg->ent_coef;
+    a.lr = cfg->lr;
+    a.beta1 = cfg->beta1;
+    a.beta2 = cfg->beta2;
+    a.eps = cfg->eps;
+    hipError_t e = launch_ppo_update(a, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "learner launch");
     return ok();
 }
 

@@ -131,6 +131,41 @@ hipError_t launch_critic_value(const CriticArgs &a, hipStream_t s);
 hipError_t launch_critic_pack(const tp_critic *c, const CriticLayout &lay, void *dst,
                               hipStream_t s);
 
+// PPO learner: flat parameter offsets (floats) and workspace carve-up
+// (bytes, 256-byte aligned areas).  Kp = S rounded up to 32, n_pad = n
+// rounded up to 32, HC1 = H1 + C1 (the concatenated first layers).
+struct PpoLayout {
+    int dtype;
+    int S, H1, H2, n, C1, C2, B;
+    int Kp, n_pad, HC1;
+    int64_t oW1, ob1, oW2, ob2, oW3, ob3, ols, oWc1, obc1, oWc2, obc2, owc3, obc3, P;
+    size_t wWcat1, wW2, wW2t, wWc2, wWc2t, wW3, wW3t;
+    size_t wX, wXt, wH1, wH1t, wH2, wH2t, wHc2, wHc2t;
+    size_t wMU, wAg, wRowIn, wRowOut, wdMU, wdMUt, wLSt, wdZc2, wdZc2t, wdZ2, wdZ2t, wdZ1t;
+    size_t wG;
+    size_t total;
+};
+
+bool ppo_layout(const tp_ppo *c, PpoLayout *out);
+
+struct PpoArgs {
+    PpoLayout lay;
+    float *params, *adam_m, *adam_v;
+    int64_t step0;
+    int n_updates;
+    const void *obs;
+    int64_t ld_obs;
+    const float *action, *logp, *adv, *ret;
+    int64_t rows;
+    const int64_t *idx;
+    float *grad_out;
+    double *stats;
+    void *workspace;
+    float clip, ent_coef, lr, beta1, beta2, eps;
+};
+
+hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s);
+
 // Maximum LDS per workgroup on gfx950.
 constexpr size_t LDS_LIMIT = 160 * 1024;
 

@@ -1,0 +1,918 @@
+// PPO learner update (PPO, Section 5.2; hyper-parameters of Table 2; the
+// learner trains the networks on the stored transitions, Section 4.3) for
+// one agent's flat fp32 parameter vector, on minibatches of B transitions
+// gathered from a time-major trajectory.
+//
+// Every matrix product of the forward and backward passes is one "NT"
+// product C[M][N] = A[M][K] B[N][K]^T with both operands K-contiguous:
+//   forward   Z = X W^T                      (A = activations, B = weights)
+//   backward  dH = dZ W   = dZ (W^T)^T       (B = a transposed weight copy)
+//   weights   dW = dZ^T X = (dZ^T)(X^T)^T    (both transposed activations)
+// so the epilogues that produce activations also write their transposes
+// (the MFMA result layout gives each lane four consecutive rows of one
+// column, one 8-byte store).  Actor and critic take the same minibatch
+// rows, so their first layers run as one product over the concatenated
+// weights [W1; Wc1]; the other products of a stage are grouped into one
+// launch.  bf16 configs use bf16 operands (weights rounded from the fp32
+// masters, observations as stored, hidden activations and backpropagated
+// pre-activation gradients rounded to bf16) with fp32 MFMA accumulation;
+// fp32 configs use an LDS-tiled fp32 kernel.  Bias, log-std and critic-head
+// gradients are row sums of the transposed gradient blocks (one wave per
+// row, fixed order).  Adam runs over 32x32 tiles of each weight matrix and
+// rewrites the operand copies (and their transposes, through LDS) in the
+// same pass.
+#include "device.hpp"
+#include "internal.hpp"
+
+namespace tpk {
+
+namespace {
+
+constexpr float LN_2PI_F = 1.8378770664093453f;
+
+template <bool BF>
+using Elem = typename std::conditional<BF, __bf16, float>::type;
+
+template <bool BF>
+__device__ __forceinline__ Elem<BF> to_elem(float x)
+{
+    if constexpr (BF) return to_bf16(x);
+    else return x;
+}
+
+__device__ __forceinline__ float fast_tanh(float x) { return tanh_from_e2(NEG_2LOG2E * x); }
+
+// ---------------------------------------------------------------------------
+// Grouped NT products with fused epilogues
+// ---------------------------------------------------------------------------
+
+enum Epi : int {
+    EPI_TANH = 0,   // h = tanh(acc + bias[col]) -> out[row][col], outT[col][row] (elem)
+    EPI_BIAS = 1,   // out[row][col] = acc + bias[col]                   (fp32)
+    EPI_GRAD = 2,   // gradient rows: row < gsplit -> g0, else g1; cols < gcols (fp32)
+    EPI_DTANH = 3,  // v = acc (1 - h[row][col]^2) -> out, outT            (elem)
+};
+
+struct GemmProb {
+    const void *A;
+    const void *B;
+    int64_t lda, ldb;
+    int M, N, K;
+    int mode;
+    const float *bias0, *bias1;
+    int bsplit;
+    void *out;
+    int64_t ldo;
+    void *outT;
+    int64_t ldt;
+    float *g0, *g1;
+    int64_t ldg;
+    int gsplit, gcols;
+    const void *hsrc;
+    int64_t ldh;
+    int tiles_n, tile0;
+};
+
+constexpr int MAX_PROBS = 4;
+struct GemmBatch {
+    GemmProb p[MAX_PROBS];
+    int np;
+};
+
+constexpr int GT = 64;   // workgroup tile (rows and columns)
+
+template <bool BF>
+__device__ __forceinline__ void epi4(const GemmProb &P, int row0, int col, const float v[4])
+{
+    if (col >= P.N) return;
+    const int mode = P.mode;
+    if (mode == EPI_GRAD) {
+        if (col >= P.gcols) return;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = row0 + i;
+            if (r >= P.M) break;
+            float *d = r < P.gsplit ? P.g0 + (size_t)r * P.ldg : P.g1 + (size_t)(r - P.gsplit) * P.ldg;
+            d[col] = v[i];
+        }
+        return;
+    }
+    if (mode == EPI_BIAS) {
+        const float b = col < P.bsplit ? P.bias0[col] : P.bias1[col - P.bsplit];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = row0 + i;
+            if (r >= P.M) break;
+            ((float *)P.out)[(size_t)r * P.ldo + col] = v[i] + b;
+        }
+        return;
+    }
+    Elem<BF> h[4];
+    if (mode == EPI_TANH) {
+        const float b = col < P.bsplit ? P.bias0[col] : P.bias1[col - P.bsplit];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) h[i] = to_elem<BF>(fast_tanh(v[i] + b));
+    } else {   // EPI_DTANH
+        const Elem<BF> *hs = (const Elem<BF> *)P.hsrc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = min(row0 + i, P.M - 1);
+            const float y = (float)hs[(size_t)r * P.ldh + col];
+            h[i] = to_elem<BF>(v[i] * (1.0f - y * y));
+        }
+    }
+    if (P.out) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = row0 + i;
+            if (r >= P.M) break;
+            ((Elem<BF> *)P.out)[(size_t)r * P.ldo + col] = h[i];
+        }
+    }
+    if (P.outT) {
+        Elem<BF> *t = (Elem<BF> *)P.outT + (size_t)col * P.ldt + row0;
+        if (row0 + 3 < P.M) {
+            if constexpr (BF) {
+                *(bf16x4 *)t = bf16x4{h[0], h[1], h[2], h[3]};
+            } else {
+                *(floatx4 *)t = floatx4{h[0], h[1], h[2], h[3]};
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (row0 + i < P.M) t[i] = h[i];
+        }
+    }
+}
+
+__device__ __forceinline__ int find_prob(const GemmBatch &g, int t)
+{
+    int pi = 0;
+#pragma unroll
+    for (int q = 1; q < MAX_PROBS; ++q)
+        if (q < g.np && t >= g.p[q].tile0) pi = q;
+    return pi;
+}
+
+// bf16: four waves, each a 32x32 block of the 64x64 tile (2x2 MFMA tiles of
+// 16x16, v_mfma_f32_16x16x32_bf16), fragments loaded straight from global
+// memory (operands are small and L2-resident), one k-step ahead.
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
+{
+    int t = blockIdx.x;
+    const int pi = find_prob(gb, t);
+    const GemmProb &P = gb.p[pi];
+    t -= P.tile0;
+    const int tn = t % P.tiles_n, tm = t / P.tiles_n;
+    const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
+    const int m0 = tm * GT + (wave >> 1) * 32, n0 = tn * GT + (wave & 1) * 32;
+    const int r16 = lane & 15, kq = lane >> 4;
+    const __bf16 *A = (const __bf16 *)P.A, *B = (const __bf16 *)P.B;
+    const __bf16 *pa[2], *pb[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        pa[i] = A + (size_t)min(m0 + i * 16 + r16, P.M - 1) * P.lda + kq * 8;
+        pb[i] = B + (size_t)min(n0 + i * 16 + r16, P.N - 1) * P.ldb + kq * 8;
+    }
+    floatx4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    bf16x8 fa[2], fb[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        fa[i] = *(const bf16x8 *)pa[i];
+        fb[i] = *(const bf16x8 *)pb[i];
+    }
+    for (int k = 32; k <= P.K; k += 32) {
+        bf16x8 na[2], nb[2];
+        const bool more = k < P.K;
+        if (more) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                na[i] = *(const bf16x8 *)(pa[i] + k);
+                nb[i] = *(const bf16x8 *)(pb[i] + k);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        if (more) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                fa[i] = na[i];
+                fb[i] = nb[i];
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+            epi4<true>(P, m0 + i * 16 + kq * 4, n0 + j * 16 + r16, v);
+        }
+}
+
+// fp32: 16x16 threads, each a 4x4 block of the 64x64 tile; k-slices of 16
+// staged in LDS, k-major, so the inner loop reads broadcast-free rows.
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmBatch gb)
+{
+    __shared__ float As[16][GT + 4];
+    __shared__ float Bs[16][GT + 4];
+    int t = blockIdx.x;
+    const int pi = find_prob(gb, t);
+    const GemmProb &P = gb.p[pi];
+    t -= P.tile0;
+    const int tn = t % P.tiles_n, tm = t / P.tiles_n;
+    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+    const float *A = (const float *)P.A, *B = (const float *)P.B;
+    // loader: row lr = tid / 4 of the tile, k-quad lq = tid % 4
+    const int lr = tid >> 2, lq = tid & 3;
+    const float *la = A + (size_t)min(tm * GT + lr, P.M - 1) * P.lda + lq * 4;
+    const float *lb = B + (size_t)min(tn * GT + lr, P.N - 1) * P.ldb + lq * 4;
+    float acc[4][4] = {};
+    for (int k = 0; k < P.K; k += 16) {
+        const floatx4 va = *(const floatx4 *)(la + k);
+        const floatx4 vb = *(const floatx4 *)(lb + k);
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            As[lq * 4 + e][lr] = va[e];
+            Bs[lq * 4 + e][lr] = vb[e];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < 16; ++kk) {
+            const floatx4 a = *(const floatx4 *)&As[kk][ty * 4];
+            const floatx4 b = *(const floatx4 *)&Bs[kk][tx * 4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float v[4] = {acc[0][j], acc[1][j], acc[2][j], acc[3][j]};
+        epi4<false>(P, tm * GT + ty * 4, tn * GT + tx * 4 + j, v);
+    }
+}
+
+// Minibatch indices outside [0, rows) are clamped into it (never read out
+// of bounds).
+__device__ __forceinline__ int64_t clamp_row(int64_t r, int64_t rows)
+{
+    return r < 0 ? 0 : (r >= rows ? rows - 1 : r);
+}
+
+// ---------------------------------------------------------------------------
+// Minibatch gather: X [B][Kp] and X^T [Kp][B] from the trajectory's
+// observation rows idx[i] (columns >= S zeroed), plus the per-row
+// transition data.  Tiles of 64 rows x 64 columns through LDS.
+// ---------------------------------------------------------------------------
+template <bool BF>
+__global__ __launch_bounds__(256) void gather_kernel(
+    const Elem<BF> *__restrict__ obs, int64_t ld_obs, const float *__restrict__ action,
+    const float *__restrict__ logp, const float *__restrict__ adv, const float *__restrict__ ret,
+    const int64_t *__restrict__ idx, int64_t rows, int B, int S, int Kp, int n,
+    Elem<BF> *__restrict__ X,
+    Elem<BF> *__restrict__ Xt, float *__restrict__ Ag, float *__restrict__ row_in)
+{
+    __shared__ Elem<BF> tile[64][65];
+    const int i0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    const int tid = threadIdx.x;
+    for (int q = tid; q < 64 * 64; q += 256) {
+        const int r = q >> 6, c = q & 63;
+        const int i = i0 + r, col = c0 + c;
+        Elem<BF> v = to_elem<BF>(0.0f);
+        if (i < B && col < S) v = obs[(size_t)clamp_row(idx[i], rows) * ld_obs + col];
+        if (i < B && col < Kp) X[(size_t)i * Kp + col] = v;
+        tile[r][c] = v;
+    }
+    __syncthreads();
+    for (int q = tid; q < 64 * 64; q += 256) {
+        const int c = q >> 6, r = q & 63;
+        const int i = i0 + r, col = c0 + c;
+        if (i < B && col < Kp) Xt[(size_t)col * B + i] = tile[r][c];
+    }
+    if (blockIdx.y == 0) {
+        for (int q = tid; q < 64 * n; q += 256) {
+            const int r = q / n, k = q % n;
+            const int i = i0 + r;
+            if (i < B) Ag[(size_t)i * n + k] = action[(size_t)clamp_row(idx[i], rows) * n + k];
+        }
+        if (tid < 64 && i0 + tid < B) {
+            const int i = i0 + tid;
+            const int64_t g = clamp_row(idx[i], rows);
+            row_in[i] = logp[g];
+            row_in[B + i] = adv[g];
+            row_in[2 * B + i] = ret[g];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Loss, per row (one wave per row): log-probability, ratio, clip decision,
+// the critic's value, and the per-row factors the gradient tiles use.
+//   row_out[0][i] = dL/dlogp_i (zero on the clipped branch)
+//   row_out[1][i] = dL/dV_i = 2 (V_i - R_i) / B
+//   row_out[2..4][i] = surrogate, squared error, |rho - 1| > clip
+// ---------------------------------------------------------------------------
+template <bool BF>
+__global__ __launch_bounds__(256) void loss_row_kernel(
+    const float *__restrict__ mu, const float *__restrict__ Ag, const float *__restrict__ row_in,
+    const Elem<BF> *__restrict__ Hc2, const float *__restrict__ params, int64_t ols,
+    int64_t owc3, int64_t obc3, int B, int n, int C2, float clip, float *__restrict__ row_out)
+{
+    const int lane = threadIdx.x % WAVE;
+    const int i = blockIdx.x * 4 + threadIdx.x / WAVE;
+    if (i >= B) return;
+    const float *ls = params + ols;
+    double lp = 0.0;
+    for (int k = lane; k < n; k += WAVE) {
+        const float d = Ag[(size_t)i * n + k] - mu[(size_t)i * n + k];
+        const float inv = expf(-2.0f * ls[k]);
+        lp += (double)(-0.5f * (d * d * inv) - ls[k]);
+    }
+    lp = wave_sum(lp) - 0.5 * (double)n * (double)LN_2PI_F;
+    const float *wc3 = params + owc3;
+    double v = 0.0;
+    for (int k = lane; k < C2; k += WAVE)
+        v += (double)((float)to_elem<BF>(wc3[k]) * (float)Hc2[(size_t)i * C2 + k]);
+    v = wave_sum(v);
+    if (lane != 0) return;
+    const float V = (float)(v + (double)params[obc3]);
+    const double lp_old = row_in[i], A = row_in[B + i], R = row_in[2 * B + i];
+    const double rho = exp(lp - lp_old);
+    const double rc = fmin(fmax(rho, 1.0 - clip), 1.0 + clip);
+    const bool unclipped = rho * A <= rc * A;
+    row_out[i] = unclipped ? (float)(-A * rho / (double)B) : 0.0f;
+    const double e = (double)V - R;
+    row_out[B + i] = (float)(2.0 * e / (double)B);
+    row_out[2 * B + i] = (float)(unclipped ? rho * A : rc * A);
+    row_out[3 * B + i] = (float)(e * e);
+    row_out[4 * B + i] = fabs(rho - 1.0) > (double)clip ? 1.0f : 0.0f;
+}
+
+// Gradient tiles over [B] x [vsplit + C2] virtual columns (64 x 64 through
+// LDS; vsplit = n_pad rounded up to a whole tile): columns < vsplit give
+// dmu (row-major and transposed, zero for n <= col < n_pad) and the
+// log-std terms (transposed), the rest the critic's second pre-activation
+// gradient dV wc3 (1 - hc2^2) (row-major and transposed).
+template <bool BF>
+__global__ __launch_bounds__(256) void loss_tile_kernel(
+    const float *__restrict__ mu, const float *__restrict__ Ag, const float *__restrict__ row_out,
+    const Elem<BF> *__restrict__ Hc2, const float *__restrict__ params, int64_t ols,
+    int64_t owc3, int B, int n, int n_pad, int vsplit, int C2, Elem<BF> *__restrict__ dMU,
+    Elem<BF> *__restrict__ dMUt, float *__restrict__ LSt, Elem<BF> *__restrict__ dZc2,
+    Elem<BF> *__restrict__ dZc2t)
+{
+    __shared__ float t1[64][65];
+    __shared__ float t2[64][65];
+    const int i0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    const bool actor = c0 < vsplit;
+    const int tid = threadIdx.x;
+    const float *ls = params + ols, *wc3 = params + owc3;
+    for (int q = tid; q < 64 * 64; q += 256) {
+        const int r = q >> 6, c = q & 63;
+        const int i = i0 + r, col = c0 + c;
+        float a = 0.f, b = 0.f;
+        if (i < B) {
+            if (actor) {
+                if (col < n) {
+                    const float d = Ag[(size_t)i * n + col] - mu[(size_t)i * n + col];
+                    const float inv = expf(-2.0f * ls[col]);
+                    const float g = row_out[i];
+                    a = g * (d * inv);
+                    b = g * (d * d * inv - 1.0f);
+                }
+                if (col < n_pad) dMU[(size_t)i * n_pad + col] = to_elem<BF>(a);
+            } else {
+                const int k = col - vsplit;
+                if (k < C2) {
+                    const float h = (float)Hc2[(size_t)i * C2 + k];
+                    a = row_out[B + i] * (float)to_elem<BF>(wc3[k]) * (1.0f - h * h);
+                    dZc2[(size_t)i * C2 + k] = to_elem<BF>(a);
+                }
+            }
+        }
+        t1[r][c] = a;
+        t2[r][c] = b;
+    }
+    __syncthreads();
+    for (int q = tid; q < 64 * 64; q += 256) {
+        const int c = q >> 6, r = q & 63;
+        const int i = i0 + r, col = c0 + c;
+        if (i >= B) continue;
+        if (actor) {
+            if (col < n_pad) dMUt[(size_t)col * B + i] = to_elem<BF>(t1[r][c]);
+            if (col < n) LSt[(size_t)col * B + i] = t2[r][c];
+        } else if (col - vsplit < C2) {
+            dZc2t[(size_t)(col - vsplit) * B + i] = to_elem<BF>(t1[r][c]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Row sums (one wave per row, fp64 partials, fixed order):
+// dst[r] = scale * sum_b src[r][b] (* w[b]) + add
+// ---------------------------------------------------------------------------
+struct RedSeg {
+    const void *src;
+    int64_t ld;
+    int rows, len;
+    int bf;             // source elements are bf16
+    const float *w;     // optional weights [len]
+    float *dst;         // fp32 destination, or
+    double *dst64;      // fp64 destination (stats)
+    double scale, add;
+    int row0;           // first global row of this segment
+};
+constexpr int MAX_SEGS = 12;
+struct RedBatch {
+    RedSeg s[MAX_SEGS];
+    int ns, total_rows;
+};
+
+__global__ __launch_bounds__(256) void row_reduce_kernel(RedBatch rb)
+{
+    const int lane = threadIdx.x % WAVE;
+    const int g = blockIdx.x * 4 + threadIdx.x / WAVE;
+    if (g >= rb.total_rows) return;
+    int si = 0;
+#pragma unroll
+    for (int q = 1; q < MAX_SEGS; ++q)
+        if (q < rb.ns && g >= rb.s[q].row0) si = q;
+    const RedSeg &S = rb.s[si];
+    const int r = g - S.row0;
+    double acc = 0.0;
+    if (S.bf) {
+        const __bf16 *p = (const __bf16 *)S.src + (size_t)r * S.ld;
+        for (int b = lane; b < S.len; b += WAVE)
+            acc += (double)((float)p[b] * (S.w ? S.w[b] : 1.0f));
+    } else {
+        const float *p = (const float *)S.src + (size_t)r * S.ld;
+        for (int b = lane; b < S.len; b += WAVE)
+            acc += (double)(p[b] * (S.w ? S.w[b] : 1.0f));
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) {
+        const double v = S.scale * acc + S.add;
+        if (S.dst64) S.dst64[r] = v;
+        else S.dst[r] = (float)v;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Adam over the flat vector and the operand copies of the weights.
+// Matrix segments run in 32x32 tiles of the (padded) copy: each element is
+// updated (when do_adam), its master written back, its copy written
+// row-major and, through LDS, transposed.  Vector segments run in chunks.
+// ---------------------------------------------------------------------------
+struct AdamSeg {
+    int64_t off;        // flat offset of the master
+    int rows, cols;     // master shape (vectors: rows = 1)
+    int rows_pad, cols_pad;   // copy shape (zero outside the master)
+    void *copy;         // row-major copy [.][ld_copy] at row copy_row0, or null
+    int64_t ld_copy;
+    int copy_row0;
+    void *copyT;        // transposed copy [cols_pad][ld_copyT], or null
+    int64_t ld_copyT;
+    int tiles_c, tile0;
+};
+constexpr int MAX_ASEGS = 13;
+struct AdamBatch {
+    AdamSeg s[MAX_ASEGS];
+    int ns;
+    float *params, *m, *v;
+    const float *grad;
+    float lr, b1, b2, eps, bc1, bc2;
+    int do_adam;
+};
+
+__device__ __forceinline__ float adam_one(const AdamBatch &ab, int64_t p)
+{
+    float th = ab.params[p];
+    if (!ab.do_adam) return th;
+    const float g = ab.grad[p];
+    const float m = ab.b1 * ab.m[p] + (1.0f - ab.b1) * g;
+    const float v = ab.b2 * ab.v[p] + (1.0f - ab.b2) * (g * g);
+    ab.m[p] = m;
+    ab.v[p] = v;
+    const float mh = m / ab.bc1, vh = v / ab.bc2;
+    th = th - ab.lr * (mh / (sqrtf(vh) + ab.eps));
+    ab.params[p] = th;
+    return th;
+}
+
+template <bool BF>
+__global__ __launch_bounds__(256) void adam_kernel(AdamBatch ab)
+{
+    __shared__ Elem<BF> tile[32][33];
+    int t = blockIdx.x;
+    int si = 0;
+#pragma unroll
+    for (int q = 1; q < MAX_ASEGS; ++q)
+        if (q < ab.ns && t >= ab.s[q].tile0) si = q;
+    const AdamSeg &S = ab.s[si];
+    t -= S.tile0;
+    const int tid = threadIdx.x;
+    if (!S.copy) {   // vector segment: chunk of 1024 elements
+        const int64_t n = (int64_t)S.rows * S.cols;
+        for (int64_t e = (int64_t)t * 1024 + tid; e < n && e < (int64_t)(t + 1) * 1024; e += 256)
+            adam_one(ab, S.off + e);
+        return;
+    }
+    const int r0 = (t / S.tiles_c) * 32, c0 = (t % S.tiles_c) * 32;
+    for (int q = tid; q < 32 * 32; q += 256) {
+        const int r = r0 + (q >> 5), c = c0 + (q & 31);
+        float w = 0.0f;
+        if (r < S.rows && c < S.cols) w = adam_one(ab, S.off + (int64_t)r * S.cols + c);
+        const Elem<BF> e = to_elem<BF>(w);
+        if (r < S.rows_pad && c < S.cols_pad)
+            ((Elem<BF> *)S.copy)[(size_t)(S.copy_row0 + r) * S.ld_copy + c] = e;
+        tile[q >> 5][q & 31] = e;
+    }
+    if (!S.copyT) return;
+    __syncthreads();
+    for (int q = tid; q < 32 * 32; q += 256) {
+        const int c = c0 + (q >> 5), r = r0 + (q & 31);
+        if (r < S.rows_pad && c < S.cols_pad)
+            ((Elem<BF> *)S.copyT)[(size_t)c * S.ld_copyT + r] = tile[q & 31][q >> 5];
+    }
+}
+
+int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Layout
+// ---------------------------------------------------------------------------
+bool ppo_layout(const tp_ppo *c, PpoLayout *L)
+{
+    L->dtype = c->dtype;
+    L->S = c->dims[0];
+    L->H1 = c->dims[1];
+    L->H2 = c->dims[2];
+    L->n = c->dims[3];
+    L->C1 = c->dims[4];
+    L->C2 = c->dims[5];
+    L->B = c->batch;
+    L->Kp = (L->S + 31) / 32 * 32;
+    L->n_pad = (L->n + 31) / 32 * 32;
+    L->HC1 = L->H1 + L->C1;
+    int64_t o = 0;
+    auto seg = [&](int64_t count) {
+        const int64_t at = o;
+        o += count;
+        return at;
+    };
+    L->oW1 = seg((int64_t)L->H1 * L->S);
+    L->ob1 = seg(L->H1);
+    L->oW2 = seg((int64_t)L->H2 * L->H1);
+    L->ob2 = seg(L->H2);
+    L->oW3 = seg((int64_t)L->n * L->H2);
+    L->ob3 = seg(L->n);
+    L->ols = seg(L->n);
+    L->oWc1 = seg((int64_t)L->C1 * L->S);
+    L->obc1 = seg(L->C1);
+    L->oWc2 = seg((int64_t)L->C2 * L->C1);
+    L->obc2 = seg(L->C2);
+    L->owc3 = seg(L->C2);
+    L->obc3 = seg(1);
+    L->P = o;
+
+    const size_t es = c->dtype == TP_BF16 ? 2 : 4;
+    size_t w = 0;
+    auto area = [&](size_t bytes) {
+        const size_t at = w;
+        w += (bytes + 255) / 256 * 256;
+        return at;
+    };
+    const size_t B = L->B;
+    L->wWcat1 = area(es * L->HC1 * L->Kp);
+    L->wW2 = area(es * L->H2 * L->H1);
+    L->wW2t = area(es * L->H1 * L->H2);
+    L->wWc2 = area(es * L->C2 * L->C1);
+    L->wWc2t = area(es * L->C1 * L->C2);
+    L->wW3 = area(es * L->n_pad * L->H2);
+    L->wW3t = area(es * L->H2 * L->n_pad);
+    L->wX = area(es * B * L->Kp);
+    L->wXt = area(es * L->Kp * B);
+    L->wH1 = area(es * B * L->HC1);
+    L->wH1t = area(es * L->HC1 * B);
+    L->wH2 = area(es * B * L->H2);
+    L->wH2t = area(es * L->H2 * B);
+    L->wHc2 = area(es * B * L->C2);
+    L->wHc2t = area(es * L->C2 * B);
+    L->wMU = area(4 * B * L->n);
+    L->wAg = area(4 * B * L->n);
+    L->wRowIn = area(4 * 3 * B);
+    L->wRowOut = area(4 * 5 * B);
+    L->wdMU = area(es * B * L->n_pad);
+    L->wdMUt = area(es * L->n_pad * B);
+    L->wLSt = area(4 * L->n * B);
+    L->wdZc2 = area(es * B * L->C2);
+    L->wdZc2t = area(es * L->C2 * B);
+    L->wdZ2 = area(es * B * L->H2);
+    L->wdZ2t = area(es * L->H2 * B);
+    L->wdZ1t = area(es * L->HC1 * B);
+    L->wG = area(4 * (size_t)L->P);
+    L->total = w;
+    return true;
+}
+
+// ---------------------------------------------------------------------------
+// One call: refresh the operand copies, then n_updates minibatch updates
+// ---------------------------------------------------------------------------
+namespace {
+
+GemmProb prob(const void *A, int64_t lda, const void *B, int64_t ldb, int M, int N, int K,
+              int mode)
+{
+    GemmProb p{};
+    p.A = A;
+    p.B = B;
+    p.lda = lda;
+    p.ldb = ldb;
+    p.M = M;
+    p.N = N;
+    p.K = K;
+    p.mode = mode;
+    p.bsplit = 1 << 30;
+    p.gsplit = 1 << 30;
+    p.gcols = 1 << 30;
+    return p;
+}
+
+hipError_t run_gemms(bool bf, std::initializer_list<GemmProb> ps, hipStream_t s)
+{
+    GemmBatch gb{};
+    int tiles = 0;
+    for (const GemmProb &p : ps) {
+        GemmProb q = p;
+        q.tiles_n = cdiv(q.N, GT);
+        q.tile0 = tiles;
+        tiles += q.tiles_n * cdiv(q.M, GT);
+        gb.p[gb.np++] = q;
+    }
+    if (bf) hipLaunchKernelGGL(gemm_bf16_kernel, dim3(tiles), dim3(256), 0, s, gb);
+    else hipLaunchKernelGGL(gemm_f32_kernel, dim3(tiles), dim3(256), 0, s, gb);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
+{
+    const PpoLayout &L = a.lay;
+    const bool bf = L.dtype == TP_BF16;
+    const size_t es = bf ? 2 : 4;
+    uint8_t *ws = (uint8_t *)a.workspace;
+    auto W = [&](size_t off) { return (void *)(ws + off); };
+    const int B = L.B;
+    float *prm = a.params;
+    float *grad = (float *)W(L.wG);
+
+    // Adam / refresh segments
+    AdamBatch ab{};
+    ab.params = prm;
+    ab.m = a.adam_m;
+    ab.v = a.adam_v;
+    ab.grad = grad;
+    ab.lr = a.lr;
+    ab.b1 = a.beta1;
+    ab.b2 = a.beta2;
+    ab.eps = a.eps;
+    int atiles = 0;
+    auto mseg = [&](int64_t off, int rows, int cols, int rows_pad, int cols_pad, void *copy,
+                    int64_t ldc, int row0, void *copyT, int64_t ldt) {
+        AdamSeg g{};
+        g.off = off;
+        g.rows = rows;
+        g.cols = cols;
+        g.rows_pad = rows_pad;
+        g.cols_pad = cols_pad;
+        g.copy = copy;
+        g.ld_copy = ldc;
+        g.copy_row0 = row0;
+        g.copyT = copyT;
+        g.ld_copyT = ldt;
+        g.tile0 = atiles;
+        if (copy) {
+            g.tiles_c = cdiv(cols_pad, 32);
+            atiles += g.tiles_c * cdiv(rows_pad, 32);
+        } else {
+            g.tiles_c = 1;
+            atiles += cdiv(rows * cols, 1024);
+        }
+        ab.s[ab.ns++] = g;
+    };
+    mseg(L.oW1, L.H1, L.S, L.H1, L.Kp, W(L.wWcat1), L.Kp, 0, nullptr, 0);
+    mseg(L.oWc1, L.C1, L.S, L.C1, L.Kp, W(L.wWcat1), L.Kp, L.H1, nullptr, 0);
+    mseg(L.oW2, L.H2, L.H1, L.H2, L.H1, W(L.wW2), L.H1, 0, W(L.wW2t), L.H2);
+    mseg(L.oWc2, L.C2, L.C1, L.C2, L.C1, W(L.wWc2), L.C1, 0, W(L.wWc2t), L.C2);
+    mseg(L.oW3, L.n, L.H2, L.n_pad, L.H2, W(L.wW3), L.H2, 0, W(L.wW3t), L.n_pad);
+    // vectors: b1, b2, b3 + log_std (contiguous), bc1, bc2 + wc3 + bc3 (contiguous)
+    mseg(L.ob1, 1, L.H1, 1, L.H1, nullptr, 0, 0, nullptr, 0);
+    mseg(L.ob2, 1, L.H2, 1, L.H2, nullptr, 0, 0, nullptr, 0);
+    mseg(L.ob3, 1, 2 * L.n, 1, 2 * L.n, nullptr, 0, 0, nullptr, 0);
+    mseg(L.obc1, 1, L.C1, 1, L.C1, nullptr, 0, 0, nullptr, 0);
+    mseg(L.obc2, 1, 2 * L.C2 + 1, 1, 2 * L.C2 + 1, nullptr, 0, 0, nullptr, 0);
+
+    auto adam = [&](int do_adam, int64_t step) -> hipError_t {
+        ab.do_adam = do_adam;
+        ab.bc1 = (float)(1.0 - pow((double)a.beta1, (double)step));
+        ab.bc2 = (float)(1.0 - pow((double)a.beta2, (double)step));
+        if (bf) hipLaunchKernelGGL(adam_kernel<true>, dim3(atiles), dim3(256), 0, s, ab);
+        else hipLaunchKernelGGL(adam_kernel<false>, dim3(atiles), dim3(256), 0, s, ab);
+        return hipGetLastError();
+    };
+    hipError_t e = adam(0, 1);
+    if (e != hipSuccess) return e;
+
+    void *X = W(L.wX), *Xt = W(L.wXt), *H1 = W(L.wH1), *H1t = W(L.wH1t);
+    void *H2 = W(L.wH2), *H2t = W(L.wH2t), *Hc2 = W(L.wHc2), *Hc2t = W(L.wHc2t);
+    float *MU = (float *)W(L.wMU), *Ag = (float *)W(L.wAg);
+    float *row_in = (float *)W(L.wRowIn), *row_out = (float *)W(L.wRowOut);
+    void *dMU = W(L.wdMU), *dMUt = W(L.wdMUt);
+    float *LSt = (float *)W(L.wLSt);
+    void *dZc2 = W(L.wdZc2), *dZc2t = W(L.wdZc2t), *dZ2 = W(L.wdZ2), *dZ2t = W(L.wdZ2t);
+    void *dZ1t = W(L.wdZ1t);
+    auto at = [&](void *base, size_t elems) { return (void *)((uint8_t *)base + elems * es); };
+
+    for (int u = 0; u < a.n_updates; ++u) {
+        const int64_t *idx = a.idx + (size_t)u * B;
+        // gather
+        {
+            const dim3 grid(cdiv(B, 64), cdiv(L.Kp, 64));
+            if (bf)
+                hipLaunchKernelGGL(gather_kernel<true>, grid, dim3(256), 0, s,
+                                   (const __bf16 *)a.obs, a.ld_obs, a.action, a.logp, a.adv, a.ret,
+                                   idx, a.rows, B, L.S, L.Kp, L.n, (__bf16 *)X, (__bf16 *)Xt, Ag, row_in);
+            else
+                hipLaunchKernelGGL(gather_kernel<false>, grid, dim3(256), 0, s,
+                                   (const float *)a.obs, a.ld_obs, a.action, a.logp, a.adv, a.ret,
+                                   idx, a.rows, B, L.S, L.Kp, L.n, (float *)X, (float *)Xt, Ag, row_in);
+        }
+        // forward 1: [h1 | hc1] = tanh(X [W1; Wc1]^T + [b1 | bc1])
+        {
+            GemmProb p = prob(X, L.Kp, W(L.wWcat1), L.Kp, B, L.HC1, L.Kp, EPI_TANH);
+            p.bias0 = prm + L.ob1;
+            p.bias1 = prm + L.obc1;
+            p.bsplit = L.H1;
+            p.out = H1;
+            p.ldo = L.HC1;
+            p.outT = H1t;
+            p.ldt = B;
+            if ((e = run_gemms(bf, {p}, s)) != hipSuccess) return e;
+        }
+        // forward 2: h2 and hc2
+        {
+            GemmProb pa = prob(H1, L.HC1, W(L.wW2), L.H1, B, L.H2, L.H1, EPI_TANH);
+            pa.bias0 = prm + L.ob2;
+            pa.out = H2;
+            pa.ldo = L.H2;
+            pa.outT = H2t;
+            pa.ldt = B;
+            GemmProb pc = prob(at(H1, L.H1), L.HC1, W(L.wWc2), L.C1, B, L.C2, L.C1, EPI_TANH);
+            pc.bias0 = prm + L.obc2;
+            pc.out = Hc2;
+            pc.ldo = L.C2;
+            pc.outT = Hc2t;
+            pc.ldt = B;
+            if ((e = run_gemms(bf, {pa, pc}, s)) != hipSuccess) return e;
+        }
+        // forward 3: mu = h2 W3^T + b3
+        {
+            GemmProb p = prob(H2, L.H2, W(L.wW3), L.H2, B, L.n, L.H2, EPI_BIAS);
+            p.bias0 = prm + L.ob3;
+            p.out = MU;
+            p.ldo = L.n;
+            if ((e = run_gemms(bf, {p}, s)) != hipSuccess) return e;
+        }
+        // loss rows, then gradient tiles
+        if (bf)
+            hipLaunchKernelGGL(loss_row_kernel<true>, dim3(cdiv(B, 4)), dim3(256), 0, s, MU, Ag,
+                               row_in, (const __bf16 *)Hc2, prm, L.ols, L.owc3, L.obc3, B, L.n,
+                               L.C2, a.clip, row_out);
+        else
+            hipLaunchKernelGGL(loss_row_kernel<false>, dim3(cdiv(B, 4)), dim3(256), 0, s, MU, Ag,
+                               row_in, (const float *)Hc2, prm, L.ols, L.owc3, L.obc3, B, L.n,
+                               L.C2, a.clip, row_out);
+        {
+            // actor columns [0, n_pad) in whole tiles, then the critic's C2 columns
+            const int ntA = cdiv(L.n_pad, 64);
+            const dim3 grid(cdiv(B, 64), ntA + cdiv(L.C2, 64));
+            if (bf)
+                hipLaunchKernelGGL(loss_tile_kernel<true>, grid, dim3(256), 0, s, MU, Ag, row_out,
+                                   (const __bf16 *)Hc2, prm, L.ols, L.owc3, B, L.n, L.n_pad,
+                                   ntA * 64, L.C2, (__bf16 *)dMU, (__bf16 *)dMUt, LSt,
+                                   (__bf16 *)dZc2, (__bf16 *)dZc2t);
+            else
+                hipLaunchKernelGGL(loss_tile_kernel<false>, grid, dim3(256), 0, s, MU, Ag, row_out,
+                                   (const float *)Hc2, prm, L.ols, L.owc3, B, L.n, L.n_pad,
+                                   ntA * 64, L.C2, (float *)dMU, (float *)dMUt, LSt, (float *)dZc2,
+                                   (float *)dZc2t);
+        }
+        // backward stage A: dW3, dZ2 (actor); dWc2, dZc1 (critic)
+        {
+            GemmProb g3 = prob(dMUt, B, H2t, B, L.n, L.H2, B, EPI_GRAD);
+            g3.g0 = grad + L.oW3;
+            g3.ldg = L.H2;
+            GemmProb b3 = prob(dMU, L.n_pad, W(L.wW3t), L.n_pad, B, L.H2, L.n_pad, EPI_DTANH);
+            b3.hsrc = H2;
+            b3.ldh = L.H2;
+            b3.out = dZ2;
+            b3.ldo = L.H2;
+            b3.outT = dZ2t;
+            b3.ldt = B;
+            GemmProb gc2 = prob(dZc2t, B, at(H1t, (size_t)L.H1 * B), B, L.C2, L.C1, B, EPI_GRAD);
+            gc2.g0 = grad + L.oWc2;
+            gc2.ldg = L.C1;
+            GemmProb bc2 = prob(dZc2, L.C2, W(L.wWc2t), L.C2, B, L.C1, L.C2, EPI_DTANH);
+            bc2.hsrc = at(H1, L.H1);
+            bc2.ldh = L.HC1;
+            bc2.outT = at(dZ1t, (size_t)L.H1 * B);
+            bc2.ldt = B;
+            if ((e = run_gemms(bf, {g3, b3, gc2, bc2}, s)) != hipSuccess) return e;
+        }
+        // backward stage B: dW2, dZ1 (actor)
+        {
+            GemmProb g2 = prob(dZ2t, B, H1t, B, L.H2, L.H1, B, EPI_GRAD);
+            g2.g0 = grad + L.oW2;
+            g2.ldg = L.H1;
+            GemmProb b2 = prob(dZ2, L.H2, W(L.wW2t), L.H2, B, L.H1, L.H2, EPI_DTANH);
+            b2.hsrc = H1;
+            b2.ldh = L.HC1;
+            b2.outT = dZ1t;
+            b2.ldt = B;
+            if ((e = run_gemms(bf, {g2, b2}, s)) != hipSuccess) return e;
+        }
+        // backward stage C: [dW1; dWc1] = [dZ1; dZc1]^T X
+        {
+            GemmProb g1 = prob(dZ1t, B, Xt, B, L.HC1, L.S, B, EPI_GRAD);
+            g1.g0 = grad + L.oW1;
+            g1.g1 = grad + L.oWc1;
+            g1.gsplit = L.H1;
+            g1.ldg = L.S;
+            g1.gcols = L.S;
+            if ((e = run_gemms(bf, {g1}, s)) != hipSuccess) return e;
+        }
+        // row sums: bias, log-std and critic-head gradients; statistics
+        {
+            RedBatch rb{};
+            int rows = 0;
+            auto add = [&](const void *src, int64_t ld, int nrows, int len, int isbf,
+                           const float *w, float *dst, double *dst64, double scale,
+                           double addc) {
+                RedSeg g{};
+                g.src = src;
+                g.ld = ld;
+                g.rows = nrows;
+                g.len = len;
+                g.bf = isbf;
+                g.w = w;
+                g.dst = dst;
+                g.dst64 = dst64;
+                g.scale = scale;
+                g.add = addc;
+                g.row0 = rows;
+                rows += nrows;
+                rb.s[rb.ns++] = g;
+            };
+            add(dZ1t, B, L.H1, B, bf, nullptr, grad + L.ob1, nullptr, 1.0, 0.0);
+            add(at(dZ1t, (size_t)L.H1 * B), B, L.C1, B, bf, nullptr, grad + L.obc1, nullptr, 1.0,
+                0.0);
+            add(dZ2t, B, L.H2, B, bf, nullptr, grad + L.ob2, nullptr, 1.0, 0.0);
+            add(dZc2t, B, L.C2, B, bf, nullptr, grad + L.obc2, nullptr, 1.0, 0.0);
+            add(dMUt, B, L.n, B, bf, nullptr, grad + L.ob3, nullptr, 1.0, 0.0);
+            add(LSt, B, L.n, B, 0, nullptr, grad + L.ols, nullptr, 1.0, -(double)a.ent_coef);
+            add(Hc2t, B, L.C2, B, bf, row_out + B, grad + L.owc3, nullptr, 1.0, 0.0);
+            add(row_out + B, B, 1, B, 0, nullptr, grad + L.obc3, nullptr, 1.0, 0.0);
+            if (a.stats) {
+                double *st = a.stats + (size_t)u * 4;
+                add(row_out + 2 * B, B, 1, B, 0, nullptr, nullptr, st + 0, -1.0 / B, 0.0);
+                add(prm + L.ols, L.n, 1, L.n, 0, nullptr, nullptr, st + 1, 1.0,
+                    0.5 * (1.0 + (double)LN_2PI_F) * L.n);
+                add(row_out + 3 * B, B, 1, B, 0, nullptr, nullptr, st + 2, 1.0 / B, 0.0);
+                add(row_out + 4 * B, B, 1, B, 0, nullptr, nullptr, st + 3, 1.0 / B, 0.0);
+            }
+            rb.total_rows = rows;
+            hipLaunchKernelGGL(row_reduce_kernel, dim3(cdiv(rows, 4)), dim3(256), 0, s, rb);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        if ((e = adam(1, a.step0 + u)) != hipSuccess) return e;
+    }
+    if (a.grad_out)
+        return hipMemcpyAsync(a.grad_out, grad, sizeof(float) * (size_t)L.P,
+                              hipMemcpyDeviceToDevice, s);
+    return hipSuccess;
+}
+
+}  // namespace tpk

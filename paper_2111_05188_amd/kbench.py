@@ -21,6 +21,11 @@ Times, with HIP events on the launch stream:
     reward block (L E 4 + 8 E + 8 A bytes), keep-best over 16 agents all
     improving (A P 4 in and out) and the selector keeping 4 of 16 (12 P 4
     in and out);
+  * learner: PPO updates of the 1001-512-512-100 actor and 1001-512-512-1
+    critic (bf16 operands, fp32 masters and Adam), batch 2^10, 16 updates
+    per call on a 390 x 4,096 trajectory; algorithmic FLOPs per update
+    2B (2 S H1 + 3 H1 H2 + 3 H2 n + 2 S C1 + 3 C1 C2 + 3 C2) (forward of
+    both networks, weight gradients, and input gradients except layer 1's);
   * copy: a plain device-to-device copy of 1 GiB (the reference kernel used
     to calibrate HBM byte counters: FETCH_SIZE and WRITE_SIZE of this copy
     should each read 1 GiB per launch).
@@ -64,7 +69,8 @@ def main():
     ap.add_argument("--envs", type=int, default=65536)
     ap.add_argument("--iters", type=int, default=20)
     ap.add_argument("--only", default=None,
-                    choices=["env_step", "gae", "critic", "metrics", "evolution", "copy"])
+                    choices=["env_step", "gae", "critic", "metrics", "evolution", "learner",
+                             "copy"])
     args = ap.parse_args()
     sys.path.insert(0, __file__.rsplit("/", 2)[0])
     import workloads as W
@@ -195,6 +201,40 @@ def main():
                         "hbm_frac": nb / sec / 1e9 / PEAK_HBM_GBS}
         out["evolution"] = {"P": P, **ev}
         del rew, ret, fit, params, bestp, best, stall, rank
+        torch.cuda.empty_cache()
+
+    if args.only in (None, "learner"):
+        cc = W.get_config("nasdaq100")
+        S, H1, H2, n = cc.dims
+        C1, C2 = H1, H2
+        B, NU, rows = 1024, 16, cc.L * cc.E
+        print(f"[kbench] learner B={B} updates={NU}", file=sys.stderr, flush=True)
+        c = tp.ppo_cfg((S, H1, H2, n, C1, C2), tp.TP_BF16, B)
+        P = tp.ppo_param_count(c)
+        g = torch.Generator(device=dev).manual_seed(11)
+        obs = (0.5 * torch.randn(rows, cc.K_pad, device=dev, generator=g)).to(torch.bfloat16)
+        obs[:, S:] = 0
+        act = 0.6 * torch.randn(rows, n, device=dev, generator=g)
+        logp = torch.full((rows,), -60.0, device=dev)
+        adv = torch.randn(rows, device=dev, generator=g)
+        ret = torch.randn(rows, device=dev, generator=g)
+        params = torch.from_numpy(W.make_flat_params(cc)).to(dev)
+        m = torch.zeros(P, device=dev)
+        v = torch.zeros(P, device=dev)
+        idx = torch.randint(0, rows, (NU, B), device=dev, generator=g)
+        ws = tp.ppo_workspace(c)
+        step = [1]
+
+        def upd():
+            tp.ppo_update(c, params, m, v, step[0], obs, act, logp, adv, ret, idx, ws)
+            step[0] += NU
+        sec = _time(upd, max(1, args.iters // 4), stream) / NU
+        flops = 2.0 * B * (2 * S * H1 + 3 * H1 * H2 + 3 * H2 * n + 2 * S * C1 + 3 * C1 * C2
+                           + 3 * C2)
+        out["learner"] = {"update_ms": sec * 1e3, "flops_per_update": flops,
+                          "TFLOPs": flops / sec / 1e12,
+                          "mfma_frac": flops / sec / 1e12 / PEAK_BF16_TFLOPS, "P": P}
+        del obs, act, logp, adv, ret, params, m, v, idx, ws
         torch.cuda.empty_cache()
 
     if args.only in (None, "copy"):

@@ -59,6 +59,12 @@ class Critic(C.Structure):
                 ("W", C.c_void_p * 3), ("b", C.c_void_p * 3)]
 
 
+class Ppo(C.Structure):
+    _fields_ = [("dims", C.c_int32 * 6), ("dtype", C.c_int32), ("batch", C.c_int32),
+                ("clip", C.c_float), ("ent_coef", C.c_float), ("lr", C.c_float),
+                ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float)]
+
+
 class Traj(C.Structure):
     _fields_ = [("obs", C.c_void_p), ("ld_obs", C.c_int64),
                 ("action", C.c_void_p), ("logp", C.c_void_p),
@@ -71,6 +77,7 @@ EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_actor_pack", "tp_rollout", "tp_gae", "tp_critic_packed_bytes",
            "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
            "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
+           "tp_ppo_param_count", "tp_ppo_workspace_bytes", "tp_ppo_update",
            "tp_last_error", "tp_version")
 
 _lib = None
@@ -101,11 +108,18 @@ def load(path: str = LIB_PATH):
     L.tp_fitness.argtypes = [vp, i32, i32, i32, C.c_double, vp, vp, vp]
     L.tp_keep_best.argtypes = [vp, vp, vp, vp, vp, i32, i64, vp]
     L.tp_select.argtypes = [vp, vp, i32, i64, i32, vp, vp]
+    L.tp_ppo_param_count.restype = i64
+    L.tp_ppo_param_count.argtypes = [vp]
+    L.tp_ppo_workspace_bytes.restype = C.c_size_t
+    L.tp_ppo_workspace_bytes.argtypes = [vp]
+    L.tp_ppo_update.argtypes = [vp, vp, vp, vp, i64, i32, vp, i64, vp, vp, vp, vp, i64, vp,
+                                vp, vp, vp, C.c_size_t, vp]
     L.tp_last_error.restype = C.c_char_p
     L.tp_version.restype = C.c_int
     for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae",
               "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
-              "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select"):
+              "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
+              "tp_ppo_update"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -383,3 +397,43 @@ def select(fit, params, keep: int, rank=None, stream=None):
     _check(load().tp_select(_ptr(fit), _ptr(params), N, P, keep, _ptr(rank),
                             _stream(stream)))
     return rank
+
+
+def ppo_cfg(dims, dtype: int, batch: int, clip=0.25, ent_coef=0.02, lr=2.0 ** -14,
+            beta1=0.9, beta2=0.999, eps=1e-8) -> Ppo:
+    """Learner configuration; dims = (S, H1, H2, n, C1, C2)."""
+    c = Ppo()
+    for i in range(6):
+        c.dims[i] = int(dims[i])
+    c.dtype, c.batch = dtype, batch
+    c.clip, c.ent_coef, c.lr = clip, ent_coef, lr
+    c.beta1, c.beta2, c.eps = beta1, beta2, eps
+    return c
+
+
+def ppo_param_count(cfg: Ppo) -> int:
+    p = load().tp_ppo_param_count(C.byref(cfg))
+    if p == 0:
+        raise TPError(TP_EINVAL, load().tp_last_error().decode())
+    return p
+
+
+def ppo_workspace(cfg: Ppo, device="cuda") -> torch.Tensor:
+    nb = load().tp_ppo_workspace_bytes(C.byref(cfg))
+    if nb == 0:
+        raise TPError(TP_EINVAL, load().tp_last_error().decode())
+    return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
+def ppo_update(cfg: Ppo, params, adam_m, adam_v, step0: int, obs, action, logp, adv, ret,
+               idx, workspace, grad=None, stats=None, stream=None):
+    """n_updates = idx.shape[0] minibatch updates (idx [n_updates][B] int64);
+    obs [rows][ld] (bf16 or fp32), action [rows][n], logp/adv/ret [rows]."""
+    nu, B = idx.shape
+    assert B == cfg.batch and idx.dtype == torch.int64
+    rows, ld = obs.shape
+    _check(load().tp_ppo_update(C.byref(cfg), _ptr(params), _ptr(adam_m), _ptr(adam_v),
+                                step0, nu, _ptr(obs), ld, _ptr(action), _ptr(logp),
+                                _ptr(adv), _ptr(ret), rows, _ptr(idx), _ptr(grad),
+                                _ptr(stats), _ptr(workspace), workspace.numel(),
+                                _stream(stream)))

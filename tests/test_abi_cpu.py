@@ -158,3 +158,34 @@ def test_evolution_argument_errors_without_gpu():
     assert L.tp_select(x, x, 8, 10, 0, x, None) == tp.TP_EINVAL
     assert L.tp_select(x, x, 8, 10, 9, x, None) == tp.TP_EINVAL
     assert "keep" in tp.last_error()
+
+
+def test_ppo_sizes_and_argument_errors_without_gpu():
+    from oracle import ppo
+    L = tp.load()
+    dims = (1001, 512, 512, 100, 512, 512)
+    c = tp.ppo_cfg(dims, tp.TP_BF16, 1024)
+    assert tp.ppo_param_count(c) == ppo.param_count(*dims)
+    # workspace: at least the operand copies and the fp32 gradient
+    nb = L.tp_ppo_workspace_bytes(C.byref(c))
+    assert nb > 4 * ppo.param_count(*dims) + 2 * (1024 * 1024 * 2)
+    for bad, msg in ((tp.ppo_cfg((1001, 500, 512, 100, 512, 512), tp.TP_BF16, 1024), "multiples"),
+                     (tp.ppo_cfg(dims, tp.TP_BF16, 1000), "batch"),
+                     (tp.ppo_cfg((1001, 512, 512, 129, 512, 512), tp.TP_BF16, 1024), "n <= 128"),
+                     (tp.ppo_cfg(dims, tp.TP_BF16, 1024, clip=1.5), "clip")):
+        assert L.tp_ppo_param_count(C.byref(bad)) == 0
+        assert msg in tp.last_error()
+    x = 0x100000
+    args = [C.byref(c), x, x, x, 1, 1, x, 1024, x, x, x, x, 4096, x, None, None, x, nb, None]
+    a = list(args)
+    a[1] = None
+    assert L.tp_ppo_update(*a) == tp.TP_EINVAL and "NULL" in tp.last_error()
+    a = list(args)
+    a[17] = nb - 1
+    assert L.tp_ppo_update(*a) == tp.TP_EINVAL and "workspace" in tp.last_error()
+    a = list(args)
+    a[4] = 0
+    assert L.tp_ppo_update(*a) == tp.TP_EINVAL and "step0" in tp.last_error()
+    a = list(args)
+    a[7] = 1000
+    assert L.tp_ppo_update(*a) == tp.TP_EINVAL and "ld_obs" in tp.last_error()

@@ -1,0 +1,190 @@
+"""GPU parity of tp_ppo_update (PPO, Section 5.2; Table 2) against the
+oracle's learner: the gradient of one update segment by segment, the loss
+statistics, the parameters after one and after several Adam steps, and
+determinism, for the fp32 tiny and DOW-30 shapes and the bf16
+1001-512-512-100 shape at the paper's batch of 2^10.
+
+Inputs are seeded and synthetic (workloads.make_learner_data); the stored
+log-probabilities are the oracle's log-density of the stored action under
+the starting parameters, shifted by log-ratio offsets that keep every row
+clearly inside or clearly outside the clip (so both sides take the same
+branch).  Tolerances: gradients are compared per segment by relative L2
+error, 1e-4 for fp32 (the tanh and summation order differ) and 2e-2 for
+bf16 (operands rounded to bf16 as the kernels do); parameters by the Adam
+step they moved, in units of the learning rate.
+
+Several updates in a row are compared as two independent chains.  At the
+paper's learning rate one Adam step moves every weight by about lr, which
+moves log rho by up to about 1, so after the first update some rows cross
+the clip edge; a row whose ratio lands within rounding of the edge takes
+different branches on the two sides and the chains separate (measured: 4
+such rows after one bf16 update, 16 after two).  The bf16 multi-update test
+therefore runs at lr = 2^-22, where ratios move by ~0.005 and stay clear
+of the edges; the fp32 one keeps 2^-14."""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from gpu_common import say
+from oracle import ppo
+from paper_2111_05188_amd import tp
+
+pytestmark = pytest.mark.gpu
+
+GRAD_TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def _dims(cfg):
+    S, H1, H2, n = cfg.dims
+    return (S, H1, H2, n, H1, H2)
+
+
+def _setup(cfg, rows, B, lr=2.0 ** -14):
+    dims = _dims(cfg)
+    bf = cfg.dtype == "bf16"
+    flat = W.make_flat_params(cfg)
+    obs, action, adv, ret, which = W.make_learner_data(cfg, rows)
+    # observation values as the kernels see them (bf16 rows for bf16 configs)
+    obs_t = torch.from_numpy(obs)
+    if bf:
+        obs_t = obs_t.to(torch.bfloat16)
+    obs_vals = obs_t.float().numpy()
+    p = ppo.unflatten(flat.astype(np.float64), dims)
+    f = ppo.forward(p, obs_vals[:, :dims[0]], bf16=bf)
+    lp = ppo.log_prob(action, f["mu"], p["log_std"])
+    logp = (lp - np.asarray(W.LOG_RATIO_OFFSETS)[which]).astype(np.float32)
+    host = dict(flat=flat, obs=obs_vals, action=action, logp=logp, adv=adv, ret=ret)
+    dev = dict(obs=obs_t.cuda(), action=torch.from_numpy(action).cuda(),
+               logp=torch.from_numpy(logp).cuda(), adv=torch.from_numpy(adv).cuda(),
+               ret=torch.from_numpy(ret).cuda())
+    c = tp.ppo_cfg(dims, tp.TP_BF16 if bf else tp.TP_F32, B, lr=lr)
+    return dims, bf, c, host, dev
+
+
+def _oracle_batch(host, idx, S):
+    return ppo.gather(host["obs"], host["action"], host["logp"], host["adv"], host["ret"],
+                      idx, S)
+
+
+def _rel(a, b):
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
+
+
+def _check_grad(dims, g_gpu, g_orc, tol, what):
+    seg_g, seg_o = ppo.unflatten(g_gpu.astype(np.float64), dims), ppo.unflatten(g_orc, dims)
+    worst = 0.0
+    for name, _ in ppo.layout(*dims):
+        e = _rel(seg_g[name], seg_o[name])
+        worst = max(worst, e)
+        assert e < tol, f"{what}: gradient of {name}: relative error {e:.3g} >= {tol}"
+    say(f"[ppo] {what}: worst segment relative error {worst:.3g}")
+
+
+def _run(cfg, rows, B, n_updates, seed=7, lr=2.0 ** -14):
+    dims, bf, c, host, dev = _setup(cfg, rows, B, lr)
+    P = tp.ppo_param_count(c)
+    assert P == ppo.param_count(*dims) == host["flat"].shape[0]
+    rng = np.random.default_rng(seed)
+    idx = np.stack([rng.choice(rows, B, replace=False) for _ in range(n_updates)])
+    params = torch.from_numpy(host["flat"].copy()).cuda()
+    m = torch.zeros(P, device="cuda")
+    v = torch.zeros(P, device="cuda")
+    grad = torch.empty(P, device="cuda")
+    stats = torch.empty(n_updates, 4, dtype=torch.float64, device="cuda")
+    ws = tp.ppo_workspace(c)
+    say(f"[ppo] {cfg.name} dtype={cfg.dtype} P={P} rows={rows} B={B} updates={n_updates}")
+    tp.ppo_update(c, params, m, v, 1, dev["obs"], dev["action"], dev["logp"], dev["adv"],
+                  dev["ret"], torch.from_numpy(idx).cuda(), ws, grad=grad, stats=stats)
+    torch.cuda.synchronize()
+    # the oracle, update by update from the same start
+    theta, mo, vo = host["flat"].astype(np.float64), np.zeros(P), np.zeros(P)
+    st_o, g_o = [], None
+    for u in range(n_updates):
+        batch = _oracle_batch(host, idx[u], dims[0])
+        th32, mo, vo, st, g_o = ppo.update(theta, mo, vo, u + 1, dims, batch, lr=lr, bf16=bf)
+        theta = th32.astype(np.float64)
+        st_o.append(st)
+    return dict(dims=dims, bf=bf, c=c, lr=lr, host=host, dev=dev, idx=idx, params=params, m=m, v=v,
+                grad=grad.cpu().numpy(), stats=stats.cpu().numpy(), theta_o=theta,
+                g_o=g_o, stats_o=np.array(st_o), ws=ws)
+
+
+CASES = [("tiny", 512, 64), ("dow30", 1024, 256), ("nasdaq100", 4096, 1024)]
+
+
+@pytest.mark.parametrize("name,rows,B", CASES)
+def test_gradient_and_stats_of_one_update(name, rows, B):
+    cfg = W.get_config(name)
+    r = _run(cfg, rows, B, 1)
+    _check_grad(r["dims"], r["grad"], r["g_o"], GRAD_TOL[cfg.dtype], name)
+    st, so = r["stats"][0], r["stats_o"][0]
+    rt = 1e-5 if cfg.dtype == "f32" else 2e-3
+    np.testing.assert_allclose(st[:3], so[:3], rtol=rt, atol=1e-6)
+    assert st[3] == so[3]                    # the same rows are clipped
+    assert 0.2 < st[3] < 0.6                 # both branches present
+
+
+def _check_params(r, n_updates, frac_tol):
+    lr = r["lr"]
+    got = r["params"].cpu().numpy().astype(np.float64)
+    start = r["host"]["flat"].astype(np.float64)
+    want = r["theta_o"]
+    step_g, step_o = (got - start) / lr, (want - start) / lr
+    # no weight moves further than the oracle's furthest (Adam's step is
+    # bounded by lr (1 - b1) / sqrt(1 - b2) per update, Kingma and Ba 2.1)
+    assert np.abs(step_g).max() <= np.abs(step_o).max() * 1.001 + 1e-3
+    assert np.abs(step_o).max() <= n_updates * 0.1 / np.sqrt(0.001) + 1e-6
+    off = np.abs(step_g - step_o)
+    tol = 0.05 if r["bf"] else 2e-3
+    frac = float(np.mean(off > tol))
+    say(f"[ppo] params: {frac:.4%} of weights differ by more than {tol} lr")
+    assert frac < frac_tol
+
+
+@pytest.mark.parametrize("name,rows,B", CASES)
+def test_parameters_after_one_update(name, rows, B):
+    r = _run(W.get_config(name), rows, B, 1)
+    # the first step is lr g / (|g| + eps): only weights with a near-zero
+    # gradient (sign decided by rounding) may move differently
+    _check_params(r, 1, 0.02 if r["bf"] else 0.002)
+
+
+@pytest.mark.parametrize("name,rows,B,lr", [("tiny", 512, 64, 2.0 ** -14),
+                                            ("nasdaq100", 4096, 1024, 2.0 ** -22)])
+def test_three_updates_and_determinism(name, rows, B, lr):
+    cfg = W.get_config(name)
+    r = _run(cfg, rows, B, 3, lr=lr)
+    _check_params(r, 3, 0.03 if r["bf"] else 0.003)
+    rt = 1e-5 if cfg.dtype == "f32" else 2e-3
+    np.testing.assert_allclose(r["stats"][:, :3], r["stats_o"][:, :3], rtol=rt, atol=1e-6)
+    # the same call from the same start gives the same bits
+    P = r["params"].numel()
+    p2 = torch.from_numpy(r["host"]["flat"].copy()).cuda()
+    m2, v2 = torch.zeros(P, device="cuda"), torch.zeros(P, device="cuda")
+    d = r["dev"]
+    tp.ppo_update(r["c"], p2, m2, v2, 1, d["obs"], d["action"], d["logp"], d["adv"], d["ret"],
+                  torch.from_numpy(r["idx"]).cuda(), r["ws"])
+    torch.cuda.synchronize()
+    assert torch.equal(p2, r["params"]) and torch.equal(m2, r["m"]) and torch.equal(v2, r["v"])
+
+
+def test_minimal_batch_and_rollout_rows():
+    """B = 32 (one k-step of the batch products) on rows of a real
+    trajectory layout: obs with a wider stride than K_pad."""
+    cfg = W.get_config("tiny")
+    dims, bf, c, host, dev = _setup(cfg, 100, 32)
+    wide = torch.zeros(100, cfg.K_pad + 8, device="cuda")
+    wide[:, :cfg.K_pad] = dev["obs"]
+    P = tp.ppo_param_count(c)
+    params = torch.from_numpy(host["flat"].copy()).cuda()
+    m, v = torch.zeros(P, device="cuda"), torch.zeros(P, device="cuda")
+    grad = torch.empty(P, device="cuda")
+    idx = np.random.default_rng(3).choice(100, 32, replace=False)[None]
+    tp.ppo_update(c, params, m, v, 1, wide, dev["action"], dev["logp"], dev["adv"], dev["ret"],
+                  torch.from_numpy(idx).cuda(), tp.ppo_workspace(c), grad=grad)
+    torch.cuda.synchronize()
+    _, g_o = ppo.loss_and_grad(host["flat"].astype(np.float64), dims,
+                               *_oracle_batch(host, idx[0], dims[0]))
+    _check_grad(dims, grad.cpu().numpy(), g_o, GRAD_TOL["f32"], "tiny B=32")

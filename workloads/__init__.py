@@ -30,6 +30,7 @@ import numpy as np
 __all__ = [
     "Config", "CONFIGS", "get_config", "Market", "make_market", "make_t0",
     "make_actor", "make_critic", "make_values", "make_actions", "K_PAD_MULTIPLE",
+    "make_flat_params", "make_learner_data", "LOG_RATIO_OFFSETS",
 ]
 
 # Observation rows are padded to a multiple of the bf16 MFMA k-step.
@@ -67,7 +68,7 @@ class Config:
     log_std_init: float = -0.5
     seeds: dict = field(default_factory=lambda: dict(
         market=20211109, t0=7, actor=1234, values=99, philox=0x5EED_0F_F1_2C,
-        critic=4321))
+        critic=4321, learner=2718))
 
     @property
     def T1(self) -> int:
@@ -291,3 +292,43 @@ def make_actions(seed: int, E: int, n: int, special: bool = True):
         a[(m >= 0.11) & (m < 0.115)] = np.inf
         a[(m >= 0.115) & (m < 0.12)] = -np.inf
     return a
+
+
+def make_flat_params(cfg: Config, agent: int = 0) -> np.ndarray:
+    """One agent's actor and critic (make_actor, make_critic) as one flat fp32
+    vector, segments in the order W1, b1, W2, b2, W3, b3, log_std, Wc1, bc1,
+    Wc2, bc2, wc3, bc3."""
+    W, b, ls = make_actor(cfg)
+    Wc, bc = make_critic(cfg)
+    parts = [W[0][agent], b[0][agent], W[1][agent], b[1][agent], W[2][agent], b[2][agent],
+             ls[agent], Wc[0][agent], bc[0][agent], Wc[1][agent], bc[1][agent], Wc[2][agent],
+             bc[2][agent:agent + 1]]
+    return np.concatenate([np.asarray(p, np.float32).reshape(-1) for p in parts])
+
+
+# log(rho) offsets the learner inputs draw from: two inside the ratio clip
+# (|log rho| = 0.1), two well outside (0.6), one at rho = 1; none within
+# reach of the clip edges ln(0.75) and ln(1.25).
+LOG_RATIO_OFFSETS = (-0.6, -0.1, 0.0, 0.1, 0.6)
+
+
+def make_learner_data(cfg: Config, rows: int, seed: int | None = None):
+    """Synthetic stored transitions for the learner: observation rows fp32
+    [rows][K_pad] with the observation's structure (cash scaled near 1,
+    prices and holdings scaled by 2^-7, N(0,1) indicators, zero padding),
+    raw actions N(0, 0.6^2) [rows][n], advantages and returns N(0,1) [rows],
+    and an index into LOG_RATIO_OFFSETS per row (the test turns it into the
+    stored log-probability)."""
+    seed = cfg.seeds["learner"] if seed is None else seed
+    rng = _block_rng(seed, 5, 0)
+    n, I, K = cfg.n, cfg.n_ind, cfg.K_pad
+    obs = np.zeros((rows, K), dtype=np.float32)
+    obs[:, 0] = rng.uniform(0.5, 1.5, rows)
+    obs[:, 1:1 + n] = rng.uniform(20.0, 200.0, (rows, n)) / 128.0
+    obs[:, 1 + n:1 + 2 * n] = rng.integers(0, 300, (rows, n)) / 128.0
+    obs[:, 1 + 2 * n:1 + 2 * n + n * I] = rng.standard_normal((rows, n * I))
+    action = (0.6 * rng.standard_normal((rows, n))).astype(np.float32)
+    adv = rng.standard_normal(rows).astype(np.float32)
+    ret = rng.standard_normal(rows).astype(np.float32)
+    which = rng.integers(0, len(LOG_RATIO_OFFSETS), rows)
+    return obs, action, adv, ret, which
