@@ -101,6 +101,7 @@ def lib():
         L.orc_fitness.argtypes = [vp, i32, i32, i32, C.c_double, vp]
         L.orc_keep_best.argtypes = [vp, vp, vp, vp, vp, i32, C.c_int64]
         L.orc_select.argtypes = [vp, vp, i32, C.c_int64, i32, vp]
+        L.orc_minibatch_rows.argtypes = [u64, u64, i32, i32, i32, i32, i32, i32, vp]
         L.orc_version.restype = C.c_int
         _lib = L
     return _lib
@@ -355,3 +356,11 @@ def select(fit, params, keep):
     rank = np.zeros(N, dtype=np.int32)
     lib().orc_select(_p(fit), _p(p), N, P, keep, _p(rank))
     return rank, p
+
+
+def minibatch_rows(seed, counter, n_updates, B, L, E, agent, envs_per_agent):
+    """Learner minibatch row indices [n_updates][B] (int64) of one agent."""
+    idx = np.zeros((n_updates, B), dtype=np.int64)
+    lib().orc_minibatch_rows(seed, counter, n_updates, B, L, E, agent, envs_per_agent,
+                             _p(idx))
+    return idx

@@ -740,3 +740,30 @@ void orc_select(const double *fitness, float *params, int32_t N, int64_t P,
     }
     free(order);
 }
+
+/* Minibatch rows of the learner (the learner samples stored transitions,  */
+/* Section 4.3; batch size from Table 2).  Draw i of update counter c for   */
+/* agent g: w = word i%4 of Philox4x32-10(ctr = (i/4, c, g, 0x4D42),        */
+/* key = seed); u = floor(w R / 2^32) is uniform over the agent's R = L epa */
+/* stored transitions (steps j < L of envs g epa .. (g+1) epa - 1), and the */
+/* row is j E + e with j = u / epa, e = g epa + u % epa.  With replacement.*/
+void orc_minibatch_rows(uint64_t seed, uint64_t counter, int32_t n_updates, int32_t B,
+                        int32_t L, int32_t E, int32_t agent, int32_t envs_per_agent,
+                        int64_t *idx)
+{
+    const uint32_t key[2] = { (uint32_t)seed, (uint32_t)(seed >> 32) };
+    const uint64_t R = (uint64_t)L * (uint64_t)envs_per_agent;
+    for (int32_t u = 0; u < n_updates; ++u) {
+        for (int32_t i = 0; i < B; ++i) {
+            const uint32_t ctr[4] = { (uint32_t)(i / 4), (uint32_t)(counter + (uint64_t)u),
+                                      (uint32_t)agent, 0x4D42u };
+            uint32_t w[4];
+            orc_philox4x32_10(ctr, key, w);
+            const uint64_t draw = ((uint64_t)w[i % 4] * R) >> 32;
+            const int64_t j = (int64_t)(draw / (uint64_t)envs_per_agent);
+            const int64_t e = (int64_t)agent * envs_per_agent
+                              + (int64_t)(draw % (uint64_t)envs_per_agent);
+            idx[(size_t)u * B + i] = j * E + e;
+        }
+    }
+}

@@ -177,3 +177,39 @@ def test_bf16_forward_rounds_like_the_actor_oracle():
     act = oracle.actor(W, b, p["log_std"][None].astype(np.float32), dims[:4], True, 1)
     mu = oracle.mlp(act, 0, x.astype(np.float32))
     np.testing.assert_array_equal(f["mu"].astype(np.float32), mu)
+
+
+def test_minibatch_rows_stay_in_the_agents_transitions():
+    import oracle
+    L, E, A = 13, 12, 3
+    epa = E // A
+    for agent in range(A):
+        idx = oracle.minibatch_rows(99, 5, 4, 64, L, E, agent, epa)
+        j, e = idx // E, idx % E
+        assert np.all((0 <= j) & (j < L))
+        assert np.all((agent * epa <= e) & (e < (agent + 1) * epa))
+
+
+def test_minibatch_rows_are_uniform():
+    """Chi-square over the R = L epa transitions of one agent."""
+    import oracle
+    L, E, A, agent = 10, 8, 2, 1
+    epa = E // A
+    idx = oracle.minibatch_rows(2021, 0, 200, 256, L, E, agent, epa).reshape(-1)
+    cells = (idx // E) * epa + (idx % E - agent * epa)
+    counts = np.bincount(cells, minlength=L * epa)
+    chi2 = ((counts - counts.mean()) ** 2 / counts.mean()).sum()
+    # 39 degrees of freedom: the 0.9999 quantile is about 80
+    assert chi2 < 80
+    assert scipy.stats.chi2.sf(chi2, L * epa - 1) > 1e-4
+
+
+def test_minibatch_rows_differ_across_counters_and_agents():
+    import oracle
+    a = oracle.minibatch_rows(7, 0, 2, 128, 390, 64, 0, 16)
+    b = oracle.minibatch_rows(7, 1, 1, 128, 390, 64, 0, 16)
+    # update 1 of a call at counter 0 is update 0 of a call at counter 1
+    np.testing.assert_array_equal(a[1], b[0])
+    assert np.mean(a[0] == a[1]) < 0.05
+    c = oracle.minibatch_rows(7, 0, 1, 128, 390, 64, 1, 16)
+    assert np.mean((a[0] % 64) // 16 == 0) == 1.0 and np.mean((c[0] % 64) // 16 == 1) == 1.0
