@@ -116,6 +116,11 @@ typedef struct tp_actor {
     const float *W[3];
     const float *b[3];
     const float *log_std;
+    int64_t agent_stride;  /* floats from one agent's parameters to the next
+                              in every W / b / log_std array; 0 = the stacked
+                              layouts above.  With the learner's flat vectors
+                              [A][P] (tp_ppo_update) agent_stride = P and the
+                              pointers address agent 0's segments.          */
 } tp_actor;
 
 /* Trajectory store, time-major (Section 4.4, "Replay buffer on GPU").
@@ -239,6 +244,7 @@ typedef struct tp_critic {
     int32_t dtype;         /* tp_dtype                                       */
     const float *W[3];
     const float *b[3];
+    int64_t agent_stride;  /* as tp_actor.agent_stride                       */
 } tp_critic;
 
 /*
@@ -364,6 +370,22 @@ int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v
                   const float *action, const float *logp, const float *adv,
                   const float *ret, int64_t rows, const int64_t *idx, float *grad,
                   double *stats, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * tp_minibatch_rows -- the learner's minibatch draws (the learner samples
+ * the stored transitions, Section 4.3; batch size from Table 2), with
+ * replacement, from agent `agent`'s R = L * envs_per_agent transitions:
+ * draw i of update u is word i % 4 of Philox4x32-10 with counter
+ * (i / 4, counter + u, agent, 0x4D42) and key (seed low, seed high) -- a
+ * stream of its own beside the action noise -- mapped to
+ * x = floor(w R / 2^32), step j = x / envs_per_agent, env
+ * e = agent * envs_per_agent + x % envs_per_agent, row j * E + e.
+ *   idx [n_updates][B] int64 device out (tp_ppo_update's idx).
+ * Returns TP_EINVAL for bad sizes or an agent outside 0 .. E/envs_per_agent-1.
+ */
+int tp_minibatch_rows(uint64_t seed, uint64_t counter, int32_t n_updates, int32_t B,
+                      int32_t L, int32_t E, int32_t agent, int32_t envs_per_agent,
+                      int64_t *idx, void *stream);
 
 /*
  * Evolution layer (Section 4.2): model ensemble, evaluator and selector

@@ -136,6 +136,7 @@ int check_actor(const tp_actor *a, PackedLayout *lay)
     for (int l = 0; l < 3; ++l)
         if (!a->W[l] || !a->b[l]) return fail(TP_EINVAL, "actor W[%d] or b[%d] is NULL", l, l);
     if (!a->log_std) return fail(TP_EINVAL, "actor.log_std is NULL");
+    if (a->agent_stride < 0) return fail(TP_EINVAL, "actor.agent_stride < 0");
     const int S = a->dims[0], H1 = a->dims[1], H2 = a->dims[2], n = a->dims[3];
     if (S < 1 || H1 < 1 || H2 < 1 || n < 1 || n > 128)
         return fail(TP_EINVAL, "actor dims {%d,%d,%d,%d} invalid", S, H1, H2, n);
@@ -188,6 +189,7 @@ int check_critic(const tp_critic *c, CriticLayout *lay)
         return fail(TP_EINVAL, "critic.dtype = %d", c->dtype);
     for (int l = 0; l < 3; ++l)
         if (!c->W[l] || !c->b[l]) return fail(TP_EINVAL, "critic W[%d] or b[%d] is NULL", l, l);
+    if (c->agent_stride < 0) return fail(TP_EINVAL, "critic.agent_stride < 0");
     const int S = c->dims[0], H1 = c->dims[1], H2 = c->dims[2];
     if (S < 1 || H1 < 1 || H2 < 1 || S > 65536 || H1 > 4096 || H2 > 4096)
         return fail(TP_EINVAL, "critic dims {%d,%d,%d} invalid", S, H1, H2);
@@ -595,6 +597,24 @@ int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v
     a.eps = cfg->eps;
     hipError_t e = launch_ppo_update(a, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "learner launch");
+    return ok();
+}
+
+int tp_minibatch_rows(uint64_t seed, uint64_t counter, int32_t n_updates, int32_t B, int32_t L,
+                      int32_t E, int32_t agent, int32_t envs_per_agent, int64_t *idx,
+                      void *stream)
+{
+    if (!idx || !aligned(idx, 8)) return fail(TP_EINVAL, "idx is NULL or misaligned");
+    if (n_updates < 1 || B < 1 || L < 1 || E < 1 || envs_per_agent < 1 || E % envs_per_agent)
+        return fail(TP_EINVAL, "n_updates = %d, B = %d, L = %d, E = %d, envs_per_agent = %d",
+                    n_updates, B, L, E, envs_per_agent);
+    if (agent < 0 || agent >= E / envs_per_agent)
+        return fail(TP_EINVAL, "agent = %d outside 0..%d", agent, E / envs_per_agent - 1);
+    if ((int64_t)n_updates * B > ((int64_t)1 << 40))
+        return fail(TP_EINVAL, "n_updates * B too large");
+    hipError_t e = launch_minibatch_rows(seed, counter, n_updates, B, L, E, agent,
+                                         envs_per_agent, idx, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "minibatch launch");
     return ok();
 }
 

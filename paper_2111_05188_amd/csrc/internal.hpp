@@ -165,6 +165,8 @@ struct PpoArgs {
 };
 
 hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s);
+hipError_t launch_minibatch_rows(uint64_t seed, uint64_t counter, int n_updates, int B, int L,
+                                 int E, int agent, int epa, int64_t *idx, hipStream_t s);
 
 // Maximum LDS per workgroup on gfx950.
 constexpr size_t LDS_LIMIT = 160 * 1024;

@@ -546,9 +546,41 @@ __global__ __launch_bounds__(256) void adam_kernel(AdamBatch ab)
     }
 }
 
+// Minibatch rows: draw i of update counter c for agent g is word i % 4 of
+// Philox4x32-10(ctr = (i/4, c, g, 0x4D42), key = seed), mapped to one of the
+// agent's R = L epa stored transitions by the high half of w R, then to the
+// row j E + e of the time-major arrays.  One thread per draw.
+__global__ __launch_bounds__(256) void minibatch_rows_kernel(uint32_t k0, uint32_t k1,
+                                                             uint64_t counter, int n_updates,
+                                                             int B, int E, int agent, int epa,
+                                                             uint64_t R, int64_t *idx)
+{
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= (int64_t)n_updates * B) return;
+    const int u = (int)(t / B), i = (int)(t % B);
+    const U4 w = philox4x32_10(U4{(uint32_t)(i / 4), (uint32_t)(counter + (uint64_t)u),
+                                  (uint32_t)agent, 0x4D42u},
+                               k0, k1);
+    const uint32_t word = (i & 3) == 0 ? w.x : (i & 3) == 1 ? w.y : (i & 3) == 2 ? w.z : w.w;
+    const uint64_t draw = ((uint64_t)word * R) >> 32;
+    const int64_t j = (int64_t)(draw / (uint64_t)epa);
+    const int64_t e = (int64_t)agent * epa + (int64_t)(draw % (uint64_t)epa);
+    idx[t] = j * E + e;
+}
+
 int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
+
+hipError_t launch_minibatch_rows(uint64_t seed, uint64_t counter, int n_updates, int B, int L,
+                                 int E, int agent, int epa, int64_t *idx, hipStream_t s)
+{
+    const int64_t total = (int64_t)n_updates * B;
+    hipLaunchKernelGGL(minibatch_rows_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256),
+                       0, s, (uint32_t)seed, (uint32_t)(seed >> 32), counter, n_updates, B, E,
+                       agent, epa, (uint64_t)L * (uint64_t)epa, idx);
+    return hipGetLastError();
+}
 
 // ---------------------------------------------------------------------------
 // Layout

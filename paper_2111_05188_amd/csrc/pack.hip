@@ -83,7 +83,8 @@ hipError_t launch_critic_pack(const tp_critic *c, const CriticLayout &L, void *d
     for (int ag = 0; ag < c->n_agents; ++ag) {
         uint8_t *pa = base + (size_t)ag * L.agent_stride;
         for (int l = 0; l < 2; ++l) {
-            const float *W = c->W[l] + (size_t)ag * outs[l] * ins[l];
+            const float *W = c->W[l] + (size_t)ag * (c->agent_stride ? (size_t)c->agent_stride
+                                                                     : (size_t)outs[l] * ins[l]);
             if (L.mfma) {
                 const size_t tot = (size_t)L.NT[l] * L.KS[l] * WAVE * 8;
                 hipLaunchKernelGGL(pack_bf16_kernel, dim3(grid_for(tot)), dim3(256), 0, s, W,
@@ -95,17 +96,21 @@ hipError_t launch_critic_pack(const tp_critic *c, const CriticLayout &L, void *d
                                    (float *)(pa + L.off_W[l]));
             }
             hipLaunchKernelGGL(pack_vec_kernel, dim3(grid_for(outs[l])), dim3(256), 0, s,
-                               c->b[l] + (size_t)ag * outs[l], outs[l], outs[l],
+                               c->b[l] + (size_t)ag * (c->agent_stride ? (size_t)c->agent_stride
+                                                                       : (size_t)outs[l]),
+                               outs[l], outs[l],
                                (float *)(pa + L.off_b[l]));
         }
-        const float *w3 = c->W[2] + (size_t)ag * L.H2;
+        const float *w3 = c->W[2] + (size_t)ag * (c->agent_stride ? (size_t)c->agent_stride
+                                                                  : (size_t)L.H2);
         if (L.dtype == TP_BF16)
             hipLaunchKernelGGL(pack_vec_bf16_kernel, dim3(grid_for(L.H2)), dim3(256), 0, s, w3,
                                L.H2, L.H2, (float *)(pa + L.off_W[2]));
         else
             hipLaunchKernelGGL(pack_vec_kernel, dim3(grid_for(L.H2)), dim3(256), 0, s, w3, L.H2,
                                L.H2, (float *)(pa + L.off_W[2]));
-        hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(64), 0, s, c->b[2] + ag, 1, 1,
+        hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(64), 0, s,
+                           c->b[2] + (size_t)ag * (c->agent_stride ? (size_t)c->agent_stride : 1), 1, 1,
                            (float *)(pa + L.off_b[2]));
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -122,7 +127,8 @@ hipError_t launch_pack(const tp_actor *a, const PackedLayout &L, void *dst,
     for (int ag = 0; ag < a->n_agents; ++ag) {
         uint8_t *pa = base + (size_t)ag * L.agent_stride;
         for (int l = 0; l < 3; ++l) {
-            const float *W = a->W[l] + (size_t)ag * outs[l] * ins[l];
+            const float *W = a->W[l] + (size_t)ag * (a->agent_stride ? (size_t)a->agent_stride
+                                                                     : (size_t)outs[l] * ins[l]);
             if (L.dtype == TP_BF16) {
                 const size_t tot = (size_t)L.NT[l] * L.KS[l] * WAVE * 8;
                 const int grid = (int)((tot + 255) / 256 < 4096 ? (tot + 255) / 256 : 4096);
@@ -136,12 +142,16 @@ hipError_t launch_pack(const tp_actor *a, const PackedLayout &L, void *dst,
             }
             const int padded = L.dtype == TP_BF16 ? L.NT[l] * 16 : outs[l];
             hipLaunchKernelGGL(pack_vec_kernel, dim3((padded + 255) / 256), dim3(256), 0, s,
-                               a->b[l] + (size_t)ag * outs[l], outs[l], padded,
+                               a->b[l] + (size_t)ag * (a->agent_stride ? (size_t)a->agent_stride
+                                                                       : (size_t)outs[l]),
+                               outs[l], padded,
                                (float *)(pa + L.off_b[l]));
         }
         const int lpad = L.dtype == TP_BF16 ? L.NT[2] * 16 : L.n;
         hipLaunchKernelGGL(pack_vec_kernel, dim3((lpad + 255) / 256), dim3(256), 0, s,
-                           a->log_std + (size_t)ag * L.n, L.n, lpad,
+                           a->log_std + (size_t)ag * (a->agent_stride ? (size_t)a->agent_stride
+                                                                      : (size_t)L.n),
+                           L.n, lpad,
                            (float *)(pa + L.off_ls));
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;

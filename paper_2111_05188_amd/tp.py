@@ -12,6 +12,7 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+import numpy as np
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -50,13 +51,14 @@ class Actor(C.Structure):
     _fields_ = [("n_agents", C.c_int32), ("envs_per_agent", C.c_int32),
                 ("dims", C.c_int32 * 4), ("dtype", C.c_int32),
                 ("W", C.c_void_p * 3), ("b", C.c_void_p * 3),
-                ("log_std", C.c_void_p)]
+                ("log_std", C.c_void_p), ("agent_stride", C.c_int64)]
 
 
 class Critic(C.Structure):
     _fields_ = [("n_agents", C.c_int32), ("envs_per_agent", C.c_int32),
                 ("dims", C.c_int32 * 3), ("dtype", C.c_int32),
-                ("W", C.c_void_p * 3), ("b", C.c_void_p * 3)]
+                ("W", C.c_void_p * 3), ("b", C.c_void_p * 3),
+                ("agent_stride", C.c_int64)]
 
 
 class Ppo(C.Structure):
@@ -78,6 +80,7 @@ EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
            "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
            "tp_ppo_param_count", "tp_ppo_workspace_bytes", "tp_ppo_update",
+           "tp_minibatch_rows",
            "tp_last_error", "tp_version")
 
 _lib = None
@@ -112,6 +115,8 @@ def load(path: str = LIB_PATH):
     L.tp_ppo_param_count.argtypes = [vp]
     L.tp_ppo_workspace_bytes.restype = C.c_size_t
     L.tp_ppo_workspace_bytes.argtypes = [vp]
+    L.tp_minibatch_rows.argtypes = [C.c_uint64, C.c_uint64, i32, i32, i32, i32, i32, i32, vp,
+                                    vp]
     L.tp_ppo_update.argtypes = [vp, vp, vp, vp, i64, i32, vp, i64, vp, vp, vp, vp, i64, vp,
                                 vp, vp, vp, C.c_size_t, vp]
     L.tp_last_error.restype = C.c_char_p
@@ -119,7 +124,7 @@ def load(path: str = LIB_PATH):
     for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae",
               "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
               "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
-              "tp_ppo_update"):
+              "tp_ppo_update", "tp_minibatch_rows"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -180,12 +185,15 @@ class StateT:
 
 
 class ActorT:
-    """fp32 master parameters stacked per agent (see tp_actor)."""
+    """fp32 master parameters stacked per agent (see tp_actor), or views of
+    flat per-agent vectors (agent_stride = P, n_agents given)."""
 
-    def __init__(self, W, b, log_std, dims, dtype: int, envs_per_agent: int):
+    def __init__(self, W, b, log_std, dims, dtype: int, envs_per_agent: int,
+                 agent_stride: int = 0, n_agents: int | None = None):
         self.W, self.b, self.log_std = list(W), list(b), log_std
         s = Actor()
-        s.n_agents = W[0].shape[0]
+        s.n_agents = W[0].shape[0] if n_agents is None else n_agents
+        s.agent_stride = agent_stride
         s.envs_per_agent = envs_per_agent
         for i in range(4):
             s.dims[i] = dims[i]
@@ -214,12 +222,15 @@ class ActorT:
 
 
 class CriticT:
-    """fp32 master parameters of the critic stacked per agent (see tp_critic)."""
+    """fp32 master parameters of the critic stacked per agent (see tp_critic),
+    or views of flat per-agent vectors (agent_stride = P, n_agents given)."""
 
-    def __init__(self, W, b, dims, dtype: int, envs_per_agent: int):
+    def __init__(self, W, b, dims, dtype: int, envs_per_agent: int,
+                 agent_stride: int = 0, n_agents: int | None = None):
         self.W, self.b = list(W), list(b)
         s = Critic()
-        s.n_agents = W[0].shape[0]
+        s.n_agents = W[0].shape[0] if n_agents is None else n_agents
+        s.agent_stride = agent_stride
         s.envs_per_agent = envs_per_agent
         for i in range(3):
             s.dims[i] = dims[i]
@@ -437,3 +448,43 @@ def ppo_update(cfg: Ppo, params, adam_m, adam_v, step0: int, obs, action, logp, 
                                 _ptr(adv), _ptr(ret), rows, _ptr(idx), _ptr(grad),
                                 _ptr(stats), _ptr(workspace), workspace.numel(),
                                 _stream(stream)))
+
+
+def flat_segments(dims6):
+    """(offset, shape) of each segment of one agent's flat vector, in the
+    order tp_ppo_update documents (dims6 = S, H1, H2, n, C1, C2)."""
+    S, H1, H2, n, C1, C2 = dims6
+    shapes = [("W1", (H1, S)), ("b1", (H1,)), ("W2", (H2, H1)), ("b2", (H2,)),
+              ("W3", (n, H2)), ("b3", (n,)), ("log_std", (n,)), ("Wc1", (C1, S)),
+              ("bc1", (C1,)), ("Wc2", (C2, C1)), ("bc2", (C2,)), ("wc3", (C2,)),
+              ("bc3", (1,))]
+    out, off = {}, 0
+    for name, shp in shapes:
+        out[name] = (off, shp)
+        off += int(np.prod(shp))
+    return out, off
+
+
+def flat_views(flat: torch.Tensor, dims6, dtype: int, envs_per_agent: int):
+    """ActorT and CriticT reading agent a's networks from flat[a] ([A][P])."""
+    seg, P = flat_segments(dims6)
+    assert flat.dim() == 2 and flat.shape[1] == P and flat.is_contiguous()
+    A = flat.shape[0]
+    v = {k: flat[0, o:o + int(np.prod(shp))] for k, (o, shp) in seg.items()}
+    S, H1, H2, n, C1, C2 = dims6
+    actor = ActorT([v["W1"], v["W2"], v["W3"]], [v["b1"], v["b2"], v["b3"]], v["log_std"],
+                   (S, H1, H2, n), dtype, envs_per_agent, agent_stride=P, n_agents=A)
+    critic = CriticT([v["Wc1"], v["Wc2"], v["wc3"]], [v["bc1"], v["bc2"], v["bc3"]],
+                     (S, C1, C2), dtype, envs_per_agent, agent_stride=P, n_agents=A)
+    actor.flat = critic.flat = flat
+    return actor, critic
+
+
+def minibatch_rows(seed: int, counter: int, n_updates: int, B: int, L: int, E: int, agent: int,
+                   envs_per_agent: int, out=None, device="cuda", stream=None):
+    """Learner minibatch rows [n_updates][B] int64 of one agent."""
+    if out is None:
+        out = torch.empty(n_updates, B, dtype=torch.int64, device=device)
+    _check(load().tp_minibatch_rows(seed, counter, n_updates, B, L, E, agent, envs_per_agent,
+                                    _ptr(out), _stream(stream)))
+    return out

@@ -298,8 +298,11 @@ def make_flat_params(cfg: Config, agent: int = 0) -> np.ndarray:
     """One agent's actor and critic (make_actor, make_critic) as one flat fp32
     vector, segments in the order W1, b1, W2, b2, W3, b3, log_std, Wc1, bc1,
     Wc2, bc2, wc3, bc3."""
-    W, b, ls = make_actor(cfg)
-    Wc, bc = make_critic(cfg)
+    # each agent draws from its own stream, so agent a's vector does not
+    # depend on how many agents the config has
+    A = max(cfg.n_agents, agent + 1)
+    W, b, ls = make_actor(cfg, n_agents=A)
+    Wc, bc = make_critic(cfg, n_agents=A)
     parts = [W[0][agent], b[0][agent], W[1][agent], b[1][agent], W[2][agent], b[2][agent],
              ls[agent], Wc[0][agent], bc[0][agent], Wc[1][agent], bc[1][agent], Wc[2][agent],
              bc[2][agent:agent + 1]]
