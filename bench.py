@@ -46,13 +46,17 @@ def algorithmic_bytes_gae() -> int:
     return 4 + 4 + 1 + 4 + 4
 
 
+# Sources the rollout kernels are built from: counters taken on an older
+# version of any of them no longer describe the kernel.
+ROLLOUT_SOURCES = ("rollout_rs.hip", "rollout.hip", "env.hpp", "device.hpp")
+
+
 def kernel_source_hash() -> str:
-    import glob
     import hashlib
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2111_05188_amd", "csrc", "*"))):
-        h.update(os.path.basename(f).encode())
-        h.update(open(f, "rb").read())
+    for name in ROLLOUT_SOURCES:
+        h.update(name.encode())
+        h.update(open(os.path.join(ROOT, "paper_2111_05188_amd", "csrc", name), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -81,7 +85,7 @@ def main():
     ap.add_argument("--workload", default="nasdaq100",
                     choices=["nasdaq100", "ensemble", "stress", "dow30", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-envs", type=int, default=32)
+    ap.add_argument("--cpu-envs", type=int, default=64)
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -115,6 +119,7 @@ def main():
     pb.set_values(values)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
+    kname = "rollout_rs_kernel" if tp.rollout_path(pb.mkt, pb.actor) == 1 else "rollout_kernel"
 
     for k in range(args.warmup):
         pb.step(SEED + k)
@@ -181,12 +186,12 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "rollout_kernel (fused actor + sampling + env step + store)",
+            "kernel": f"{kname} (fused actor + sampling + env step + store)",
             "achieved": achieved_tflops,
             "peak": peak_flops,
             "unit": "TFLOP/s",
             "frac": achieved_tflops / peak_flops,
-            "traffic": counter_traffic(f"rollout_kernel {cfg.name}"),
+            "traffic": counter_traffic(f"{kname} {cfg.name}"),
             "launch_ms": t_roll * 1e3,
             "flops_per_launch": flops,
             "hbm_achieved_GBs": roll_bytes / t_roll / 1e9,

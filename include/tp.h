@@ -218,6 +218,15 @@ int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg,
                uint64_t step0, int32_t L, const tp_traj *traj, void *stream);
 
 /*
+ * tp_rollout_path -- which rollout kernel tp_rollout launches for this
+ * market and actor shape: 1 = the role-split kernel (bf16, 100 stocks x 8
+ * indicators, 1001-512-512-100 or 1001-1024-1024-100, given 16-byte
+ * aligned market, action and holdings-tap buffers), 0 = the generic kernel,
+ * or a negative tp_status for an invalid market or actor.  Host only.
+ */
+int tp_rollout_path(const tp_market *market, const tp_actor *actor);
+
+/*
  * tp_gae -- generalized advantage estimation over a rollout (PPO's
  * estimator; discounting as in eq. (1), gamma from Table 2).
  *   reward, done, adv, ret [L][E]; value [L+1][E] (row L = bootstrap).

@@ -359,6 +359,16 @@ int tp_actor_pack(const tp_actor *actor, void *packed, size_t packed_bytes, void
     return ok();
 }
 
+int tp_rollout_path(const tp_market *mkt, const tp_actor *actor)
+{
+    PackedLayout lay;
+    int rc = check_market(mkt);
+    if (rc != TP_OK) return rc;
+    if ((rc = check_actor(actor, &lay)) != TP_OK) return rc;
+    ok();
+    return rollout_rs_shape(lay, mkt->n * mkt->n_ind) ? 1 : 0;
+}
+
 int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *st,
                const tp_actor *actor, const void *packed, size_t packed_bytes, uint64_t seed,
                uint64_t step0, int32_t L, const tp_traj *traj, void *stream)

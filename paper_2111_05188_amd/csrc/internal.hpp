@@ -74,6 +74,9 @@ struct RolloutArgs {
 
 hipError_t launch_rollout(RolloutArgs &a, hipStream_t s);
 hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s);
+// the role-split kernel's shapes (it also needs 16-byte aligned market,
+// action and holdings-tap buffers)
+bool rollout_rs_shape(const PackedLayout &P, int nI);
 hipError_t launch_env_reset(const EnvConst &c, double *cash, int32_t *shares,
                             int64_t *t, const int64_t *t0, int E, void *obs,
                             int64_t ld_obs, int obs_bf16, hipStream_t s);

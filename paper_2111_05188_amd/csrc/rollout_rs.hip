@@ -600,12 +600,16 @@ hipError_t launch(RolloutArgs &a, hipStream_t st)
 // (1001 inputs: KS1 = 32, the balance/prices/holdings in the first 7
 // k-steps) and hidden widths 512 or 1024; returns hipErrorNotSupported for
 // other shapes.
+bool rollout_rs_shape(const PackedLayout &P, int nI)
+{
+    return P.dtype == TP_BF16 && P.n == 100 && P.S == 1001 && nI == 800 && P.KS[0] == 32 &&
+           P.NT[2] == 8 && ((P.H1 == 512 && P.H2 == 512) || (P.H1 == 1024 && P.H2 == 1024));
+}
+
 hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
 {
     const PackedLayout &P = a.lay;
-    if (P.dtype != TP_BF16 || P.n != 100 || P.S != 1001 || a.env.nI != 800 || P.KS[0] != 32 ||
-        P.NT[2] != 8)
-        return hipErrorNotSupported;
+    if (!rollout_rs_shape(P, a.env.nI)) return hipErrorNotSupported;
     // the env waves move prices, indicators, actions and holdings in
     // 16-byte accesses
     if ((uintptr_t)a.env.price % 16 || (uintptr_t)a.env.ind % 16 || (uintptr_t)a.action % 16 ||

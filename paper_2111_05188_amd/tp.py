@@ -80,7 +80,7 @@ EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
            "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
            "tp_ppo_param_count", "tp_ppo_workspace_bytes", "tp_ppo_update",
-           "tp_minibatch_rows",
+           "tp_minibatch_rows", "tp_rollout_path",
            "tp_last_error", "tp_version")
 
 _lib = None
@@ -115,6 +115,7 @@ def load(path: str = LIB_PATH):
     L.tp_ppo_param_count.argtypes = [vp]
     L.tp_ppo_workspace_bytes.restype = C.c_size_t
     L.tp_ppo_workspace_bytes.argtypes = [vp]
+    L.tp_rollout_path.argtypes = [vp, vp]
     L.tp_minibatch_rows.argtypes = [C.c_uint64, C.c_uint64, i32, i32, i32, i32, i32, i32, vp,
                                     vp]
     L.tp_ppo_update.argtypes = [vp, vp, vp, vp, i64, i32, vp, i64, vp, vp, vp, vp, i64, vp,
@@ -488,3 +489,11 @@ def minibatch_rows(seed: int, counter: int, n_updates: int, B: int, L: int, E: i
     _check(load().tp_minibatch_rows(seed, counter, n_updates, B, L, E, agent, envs_per_agent,
                                     _ptr(out), _stream(stream)))
     return out
+
+
+def rollout_path(mkt: MarketT, actor: ActorT) -> int:
+    """1 if tp_rollout runs the role-split kernel for this shape, else 0."""
+    r = load().tp_rollout_path(C.byref(mkt.s), C.byref(actor.s))
+    if r < 0:
+        _check(r)
+    return r
