@@ -52,11 +52,13 @@ def _backtest(cfg, E, L, rows, ppy, held_out_from):
     out = oracle_replay(c, mk, params, t0, ids, SEED, L, teacher, E)
     g_asset = pb.traj.asset_tap[:L].cpu().numpy()
     assert np.array_equal(g_asset, out["asset"])
-    # metrics on the GPU against the oracle's on the same series
+    # metrics on the GPU (of its own tap) against the oracle's metrics of the
+    # oracle's own series (equal to the tap, as just checked)
     met = tp.backtest_metrics(v0, pb.traj.asset_tap[:L], ppy, 0.02)
     torch.cuda.synchronize()
-    want = oracle.backtest_metrics(v0.cpu().numpy(), g_asset, ppy, 0.02)
-    check_metrics(met.cpu().numpy(), want, v0.cpu().numpy(), g_asset, ppy, 0.02)
+    o_v0 = np.full(E, c.cash0)
+    want = oracle.backtest_metrics(o_v0, out["asset"], ppy, 0.02)
+    check_metrics(met.cpu().numpy(), want, o_v0, out["asset"], ppy, 0.02)
     return met.cpu().numpy()
 
 

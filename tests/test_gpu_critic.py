@@ -1,9 +1,13 @@
 """GPU parity of tp_critic_value (the PPO critic's forward pass over a
-trajectory's observations) against the oracle's MLP, on observation rows a
-rollout writes: the bf16 MFMA kernel at 512- and 1024-wide layers (one agent
-and several agents, ragged row blocks), the generic kernel (fp32 and another
-bf16 shape), the full 100-stock minute trajectory on sampled rows, and
-determinism."""
+trajectory's observations) against the oracle's MLP: the bf16 MFMA kernel at
+512- and 1024-wide layers (one agent and several agents, ragged row blocks),
+the generic kernel (fp32 and another bf16 shape), the full 100-stock minute
+trajectory shape on sampled rows, and determinism.
+
+Observation blocks [T][E][K_pad] come from the seeded generator
+(workloads.make_learner_data: the observation's structure and scales, zero
+padding), rounded to bf16 on the CPU for bf16 critics; both sides read the
+same values."""
 
 import numpy as np
 import pytest
@@ -11,11 +15,10 @@ import torch
 
 import oracle
 import workloads as W
-from gpu_common import TOL_MLP, build_problem, rel_check, say
+from gpu_common import TOL_MLP, rel_check, say
+from paper_2111_05188_amd import tp
 
 pytestmark = pytest.mark.gpu
-
-SEED = 0x5EED0FF12C
 
 
 def _oracle_critic(cfg, params, A):
@@ -28,28 +31,41 @@ def _oracle_critic(cfg, params, A):
                         cfg.dtype == "bf16", cfg.E // A)
 
 
-def _obs_f32(obs):
-    return obs.float().cpu().numpy()
+POOL = 65536
 
 
-def _run(cfg, E, L, rows, n_agents=1, sample=None):
-    # episode length L, so that the bootstrap row obs_L is row L of the block
-    c = cfg.with_(N=rows - 1, E=E, n_agents=n_agents, L=L)
-    mk = W.make_market(c)
-    t0 = W.make_t0(c)
-    pb, _ = build_problem(c, mk, t0, taps=False)
-    pb.reset()
-    pb.rollout(SEED, 0, L)
+def _obs_block(c, T, E, seed):
+    """[T][E][K_pad] observation rows of the critic's dtype on the device,
+    row r = t E + e holding generated row r mod POOL, and the host values
+    of the generated rows (what the oracle reads)."""
+    n = min(T * E, POOL)
+    obs, *_ = W.make_learner_data(c, n, seed=seed)
+    base = torch.from_numpy(obs)
+    if c.dtype == "bf16":
+        base = base.to(torch.bfloat16)
+    host = base.float().numpy()
+    dev = base.cuda()
+    sel = torch.arange(T * E, device="cuda") % n
+    return dev.index_select(0, sel).reshape(T, E, c.K_pad), host
+
+
+def _run(cfg, E, L, n_agents=1, sample=None):
+    c = cfg.with_(E=E, n_agents=n_agents, L=L)
+    T1 = L + 1
+    obs_all, host = _obs_block(c, T1, E, seed=E * 7 + L)
     cp = W.make_critic(c)
-    pb.set_critic(cp)
-    say(f"[critic] {cfg.name} E={E} L={L} agents={n_agents} mfma={pb.critic.s.dims[:]}")
-    pb.critic_values()
+    dt = tp.TP_BF16 if c.dtype == "bf16" else tp.TP_F32
+    crit = tp.CriticT([torch.from_numpy(w).cuda() for w in cp[0]],
+                      [torch.from_numpy(x).cuda() for x in cp[1]], c.dims[:3], dt,
+                      E // n_agents)
+    crit.pack()
+    values = torch.empty(T1, E, dtype=torch.float32, device="cuda")
+    say(f"[critic] {cfg.name} E={E} T={T1} agents={n_agents}")
+    tp.critic_value(crit, obs_all, values)
     torch.cuda.synchronize()
-    v = pb.values.cpu().numpy()                       # [L+1][E]
-    obs = pb.traj.obs_all[:, :, :c.S]                 # [L+1][E][S]
+    v = values.cpu().numpy()                          # [L+1][E]
     act = _oracle_critic(c, cp, n_agents)
     epa = E // n_agents
-    T1 = L + 1
     if sample is None:
         rows_ = [(t, e) for t in range(T1) for e in range(E)]
     else:
@@ -60,46 +76,42 @@ def _run(cfg, E, L, rows, n_agents=1, sample=None):
         sel = [(t, e) for (t, e) in rows_ if e // epa == a]
         if not sel:
             continue
-        ts = torch.as_tensor([t for t, _ in sel], device="cuda")
-        es = torch.as_tensor([e for _, e in sel], device="cuda")
-        x = _obs_f32(obs[ts, es])
+        x = host[[(t * E + e) % host.shape[0] for t, e in sel], :c.S]
         want.append(oracle.mlp(act, a, x)[:, 0])
         got.append(np.array([v[t, e] for t, e in sel]))
     got, want = np.concatenate(got), np.concatenate(want)
-    # rows of envs that were not stepped hold no observation: skip them
-    ok = np.isfinite(want)
-    rel_check(f"critic {cfg.name}", got[ok], want[ok], TOL_MLP[c.dtype])
-    return pb
+    rel_check(f"critic {cfg.name}", got, want, TOL_MLP[c.dtype])
+    return crit, obs_all, values
 
 
 def test_critic_mfma_512_ragged():
     # 1001-512-512-1 bf16: 300 envs = two 128-row blocks and a ragged 44
-    _run(W.get_config("nasdaq100"), 300, 6, 20 * 390 + 1)
+    _run(W.get_config("nasdaq100"), 300, 6)
 
 
 def test_critic_mfma_1024():
-    _run(W.get_config("stress"), 70, 4, 20 * 390 + 1)
+    _run(W.get_config("stress"), 70, 4)
 
 
 def test_critic_mfma_three_agents():
     # agent blocks of 45 envs: every block of rows stays inside one agent
-    _run(W.get_config("ensemble"), 135, 5, 20 * 390 + 1, n_agents=3)
+    _run(W.get_config("ensemble"), 135, 5, n_agents=3)
 
 
 def test_critic_generic_fp32():
-    _run(W.get_config("tiny"), 40, 30, 257)
-    _run(W.get_config("dow30"), 33, 20, 2521)
+    _run(W.get_config("tiny"), 40, 30)
+    _run(W.get_config("dow30"), 33, 20)
 
 
 def test_critic_generic_bf16_other_shape():
-    _run(W.get_config("dow30").with_(dtype="bf16"), 33, 20, 2521)
+    _run(W.get_config("dow30").with_(dtype="bf16"), 33, 20)
 
 
 def test_critic_full_nasdaq_trajectory_sampled():
     cfg = W.get_config("nasdaq100")
-    pb = _run(cfg, cfg.E, cfg.L, cfg.T1, sample=256)
+    crit, obs_all, values = _run(cfg, cfg.E, cfg.L, sample=256)
     # determinism: a second call gives the same bits
-    v0 = pb.values.clone()
-    pb.critic_values()
+    v0 = values.clone()
+    tp.critic_value(crit, obs_all, values)
     torch.cuda.synchronize()
-    assert torch.equal(v0, pb.values)
+    assert torch.equal(v0, values)
