@@ -21,6 +21,8 @@
 // row, fixed order).  Adam runs over 32x32 tiles of each weight matrix and
 // rewrites the operand copies (and their transposes, through LDS) in the
 // same pass.
+#include <type_traits>
+
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -156,9 +158,101 @@ __device__ __forceinline__ int find_prob(const GemmBatch &g, int t)
 
 // bf16: four waves, each a 32x32 block of the 64x64 tile (2x2 MFMA tiles of
 // 16x16, v_mfma_f32_16x16x32_bf16), fragments loaded straight from global
-// memory (operands are small and L2-resident), one k-step ahead.
+// memory (operands are small and L2-resident) through a ring of GEMM_PF
+// k-steps of registers: consuming k-step k issues the loads of k + GEMM_PF,
+// so that many k-steps are in flight to cover the L2 latency.
+#ifndef GEMM_PF
+#define GEMM_PF 8
+#endif
+
+template <int I>
+using ic = std::integral_constant<int, I>;
+
+template <int B, int E, typename Fn>
+__device__ __forceinline__ void static_for(Fn &&fn)
+{
+    if constexpr (B < E) {
+        fn(ic<B>{});
+        static_for<B + 1, E>(fn);
+    }
+}
+
+__device__ __forceinline__ void mma_2x2(const bf16x8 a[2], const bf16x8 b[2], floatx4 acc[2][2])
+{
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+}
+
+// NK k-steps fully unrolled: every ring slot is a compile-time register
+// set, so each wait is for exactly the k-step about to be used.
+template <int NK, int PF>
+__device__ __forceinline__ void kloop_fixed(const __bf16 *const pa[2], const __bf16 *const pb[2],
+                                            floatx4 acc[2][2])
+{
+    constexpr int D = NK < PF ? NK : PF;
+    bf16x8 ra[D][2], rb[D][2];
+    static_for<0, D>([&](auto q) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            ra[q][i] = *(const bf16x8 *)(pa[i] + q * 32);
+            rb[q][i] = *(const bf16x8 *)(pb[i] + q * 32);
+        }
+    });
+    // the scheduling barriers keep each refill where it is issued (the
+    // scheduler would otherwise sink the loads next to their use and
+    // shrink the ring to a step or two)
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, NK>([&](auto k) {
+        constexpr int slot = k % D;
+        mma_2x2(ra[slot], rb[slot], acc);
+        if constexpr (k + D < NK) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                ra[slot][i] = *(const bf16x8 *)(pa[i] + (k + D) * 32);
+                rb[slot][i] = *(const bf16x8 *)(pb[i] + (k + D) * 32);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    });
+}
+
+// Any k-step count: the same ring under a runtime bound.
+template <int PF>
+__device__ __forceinline__ void kloop_any(const __bf16 *const pa[2], const __bf16 *const pb[2],
+                                          floatx4 acc[2][2], int nk)
+{
+    bf16x8 ra[PF][2], rb[PF][2];
+    static_for<0, PF>([&](auto q) {
+        if (q < nk) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                ra[q][i] = *(const bf16x8 *)(pa[i] + q * 32);
+                rb[q][i] = *(const bf16x8 *)(pb[i] + q * 32);
+            }
+        }
+    });
+    for (int kb = 0; kb < nk; kb += PF) {
+        static_for<0, PF>([&](auto q) {
+            const int k = kb + q;
+            if (k < nk) {
+                mma_2x2(ra[q], rb[q], acc);
+                if (k + PF < nk) {
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) {
+                        ra[q][i] = *(const bf16x8 *)(pa[i] + (k + PF) * 32);
+                        rb[q][i] = *(const bf16x8 *)(pb[i] + (k + PF) * 32);
+                    }
+                }
+            }
+        });
+    }
+}
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
 {
+    constexpr int PF = GEMM_PF;
     int t = blockIdx.x;
     const int pi = find_prob(gb, t);
     const GemmProb &P = gb.p[pi];
@@ -179,34 +273,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    bf16x8 fa[2], fb[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        fa[i] = *(const bf16x8 *)pa[i];
-        fb[i] = *(const bf16x8 *)pb[i];
-    }
-    for (int k = 32; k <= P.K; k += 32) {
-        bf16x8 na[2], nb[2];
-        const bool more = k < P.K;
-        if (more) {
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                na[i] = *(const bf16x8 *)(pa[i] + k);
-                nb[i] = *(const bf16x8 *)(pb[i] + k);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-        if (more) {
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                fa[i] = na[i];
-                fb[i] = nb[i];
-            }
-        }
+    const int nk = P.K / 32;
+    switch (nk) {   // the products in use have 4, 16 or 32 k-steps
+    case 4: kloop_fixed<4, PF>(pa, pb, acc); break;
+    case 16: kloop_fixed<16, PF>(pa, pb, acc); break;
+    case 32: kloop_fixed<32, PF>(pa, pb, acc); break;
+    default: kloop_any<PF>(pa, pb, acc, nk); break;
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -214,6 +286,113 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
         for (int j = 0; j < 2; ++j) {
             const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
             epi4<true>(P, m0 + i * 16 + kq * 4, n0 + j * 16 + r16, v);
+        }
+}
+
+// bf16 through LDS, for products whose K is a multiple of 128 (all of the
+// bf16 learner's): chunks of 64 rows x 128 k of A and of B are staged in
+// LDS (rows padded by 16 bytes so the fragment reads of 16 rows fall in
+// different banks), loaded with whole-line accesses (each wave instruction
+// reads 4 rows x 256 contiguous bytes), two chunks ahead in registers; the
+// four waves read their 32x32 blocks' fragments from LDS.
+constexpr int LBK = 128;              // k per chunk
+constexpr int LROW = LBK + 8;         // padded LDS row (bf16)
+constexpr int LTILE = GT * LROW;      // one operand's chunk (bf16)
+
+typedef uint32_t v4u_t __attribute__((ext_vector_type(4)));
+
+template <int NC>
+__device__ __forceinline__ void lds_kloop(const __bf16 *const ga, const __bf16 *const gb,
+                                          int64_t lda, int64_t ldb, int Mr, int Nr,
+                                          __bf16 *smem, floatx4 acc[2][2])
+{
+    const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
+    const int r16 = lane & 15, kq = lane >> 4;
+    // loader: thread t moves 16 bytes of rows (t / 16) + 16 j, piece t % 16
+    const int lrow = tid >> 4, lpiece = tid & 15;
+    const __bf16 *la[4], *lb[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        la[j] = ga + (size_t)min(lrow + 16 * j, Mr - 1) * lda + lpiece * 8;
+        lb[j] = gb + (size_t)min(lrow + 16 * j, Nr - 1) * ldb + lpiece * 8;
+    }
+    constexpr int D = NC < 2 ? NC : 2;     // chunks in flight in registers
+    v4u_t ra[D][4], rb[D][4];
+    auto load = [&](v4u_t (&xa)[4], v4u_t (&xb)[4], int c) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            xa[j] = *(const v4u_t *)(la[j] + c * LBK);
+            xb[j] = *(const v4u_t *)(lb[j] + c * LBK);
+        }
+    };
+    auto store = [&](const v4u_t (&xa)[4], const v4u_t (&xb)[4], int buf) {
+        __bf16 *As = smem + buf * 2 * LTILE, *Bs = As + LTILE;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            *(v4u_t *)(As + (lrow + 16 * j) * LROW + lpiece * 8) = xa[j];
+            *(v4u_t *)(Bs + (lrow + 16 * j) * LROW + lpiece * 8) = xb[j];
+        }
+    };
+    static_for<0, D>([&](auto c) { load(ra[c], rb[c], c); });
+    store(ra[0], rb[0], 0);
+    if constexpr (D < NC) load(ra[0], rb[0], D);
+    __syncthreads();
+    const int am = (wave >> 1) * 32, bn = (wave & 1) * 32;
+    static_for<0, NC>([&](auto c) {
+        constexpr int buf = c & 1;
+        const __bf16 *As = smem + buf * 2 * LTILE, *Bs = As + LTILE;
+#pragma unroll
+        for (int q = 0; q < LBK / 32; ++q) {
+            bf16x8 fa[2], fb[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                fa[i] = *(const bf16x8 *)(As + (am + i * 16 + r16) * LROW + q * 32 + kq * 8);
+                fb[i] = *(const bf16x8 *)(Bs + (bn + i * 16 + r16) * LROW + q * 32 + kq * 8);
+            }
+            mma_2x2(fa, fb, acc);
+        }
+        if constexpr (c + 1 < NC) {
+            // chunk c + 1 sits in register set (c + 1) % D; refill it with c + 1 + D
+            constexpr int slot = (c + 1) % D;
+            store(ra[slot], rb[slot], (c + 1) & 1);
+            if constexpr (c + 1 + D < NC) load(ra[slot], rb[slot], c + 1 + D);
+            __syncthreads();
+        }
+    });
+}
+
+__global__ __launch_bounds__(256, 2) void gemm_lds_kernel(GemmBatch gb)
+{
+    __shared__ __attribute__((aligned(16))) __bf16 smem[2 * 2 * LTILE];
+    int t = blockIdx.x;
+    const int pi = find_prob(gb, t);
+    const GemmProb &P = gb.p[pi];
+    t -= P.tile0;
+    const int tn = t % P.tiles_n, tm = t / P.tiles_n;
+    const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
+    const int m0 = tm * GT, n0 = tn * GT;
+    const int r16 = lane & 15, kq = lane >> 4;
+    const __bf16 *ga = (const __bf16 *)P.A + (size_t)m0 * P.lda;
+    const __bf16 *gbp = (const __bf16 *)P.B + (size_t)n0 * P.ldb;
+    floatx4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int Mr = P.M - m0, Nr = P.N - n0;     // rows left in this tile (>= 1)
+    switch (P.K / LBK) {
+    case 1: lds_kloop<1>(ga, gbp, P.lda, P.ldb, Mr, Nr, smem, acc); break;
+    case 4: lds_kloop<4>(ga, gbp, P.lda, P.ldb, Mr, Nr, smem, acc); break;
+    case 8: lds_kloop<8>(ga, gbp, P.lda, P.ldb, Mr, Nr, smem, acc); break;
+    default: break;   // the launcher routes other K to gemm_bf16_kernel
+    }
+    const int wm = m0 + (wave >> 1) * 32, wn = n0 + (wave & 1) * 32;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+            epi4<true>(P, wm + i * 16 + kq * 4, wn + j * 16 + r16, v);
         }
 }
 
@@ -276,42 +455,73 @@ __device__ __forceinline__ int64_t clamp_row(int64_t r, int64_t rows)
 // ---------------------------------------------------------------------------
 template <bool BF>
 __global__ __launch_bounds__(256) void gather_kernel(
-    const Elem<BF> *__restrict__ obs, int64_t ld_obs, const float *__restrict__ action,
+    const Elem<BF> *__restrict__ obs, int64_t ld_obs, int vec_obs, const float *__restrict__ action,
     const float *__restrict__ logp, const float *__restrict__ adv, const float *__restrict__ ret,
     const int64_t *__restrict__ idx, int64_t rows, int B, int S, int Kp, int n,
-    Elem<BF> *__restrict__ X,
-    Elem<BF> *__restrict__ Xt, float *__restrict__ Ag, float *__restrict__ row_in)
+    Elem<BF> *__restrict__ X, Elem<BF> *__restrict__ Xt, float *__restrict__ Ag,
+    float *__restrict__ row_in)
 {
-    __shared__ Elem<BF> tile[64][65];
+    typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+    constexpr int VE = 16 / sizeof(Elem<BF>);   // elements per 16-byte vector
+    constexpr int VPR = 64 / VE;                 // vectors per tile row
+    __shared__ int64_t s_idx[64];
+    __shared__ Elem<BF> tile[64][64 + VE];
     const int i0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
     const int tid = threadIdx.x;
-    for (int q = tid; q < 64 * 64; q += 256) {
-        const int r = q >> 6, c = q & 63;
-        const int i = i0 + r, col = c0 + c;
-        Elem<BF> v = to_elem<BF>(0.0f);
-        if (i < B && col < S) v = obs[(size_t)clamp_row(idx[i], rows) * ld_obs + col];
-        if (i < B && col < Kp) X[(size_t)i * Kp + col] = v;
-        tile[r][c] = v;
+    if (tid < 64) s_idx[tid] = i0 + tid < B ? clamp_row(idx[i0 + tid], rows) : 0;
+    __syncthreads();
+    // rows of X (16-byte loads and stores), staged in LDS
+#pragma unroll
+    for (int q = tid; q < 64 * VPR; q += 256) {
+        const int r = q / VPR, cv = q % VPR;
+        const int i = i0 + r, col = c0 + cv * VE;
+        union {
+            v4u v;
+            Elem<BF> e[VE];
+        } u;
+        u.v = v4u{0u, 0u, 0u, 0u};
+        if (i < B && col < S) {
+            const Elem<BF> *src = obs + (size_t)s_idx[r] * ld_obs + col;
+            if (vec_obs && col + VE <= S) {
+                u.v = *(const v4u *)src;
+            } else {
+#pragma unroll
+                for (int e = 0; e < VE; ++e)
+                    if (col + e < S) u.e[e] = src[e];
+            }
+        }
+        if (i < B && col < Kp) *(v4u *)(X + (size_t)i * Kp + col) = u.v;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) tile[r][cv * VE + e] = u.e[e];
     }
     __syncthreads();
-    for (int q = tid; q < 64 * 64; q += 256) {
-        const int c = q >> 6, r = q & 63;
-        const int i = i0 + r, col = c0 + c;
-        if (i < B && col < Kp) Xt[(size_t)col * B + i] = tile[r][c];
+    // columns of X^T: VE consecutive rows of one column per 16-byte store
+#pragma unroll
+    for (int q = tid; q < 64 * VPR; q += 256) {
+        const int c = q / VPR, rv = q % VPR;
+        const int col = c0 + c, i = i0 + rv * VE;
+        if (col >= Kp || i >= B) continue;
+        union {
+            v4u v;
+            Elem<BF> e[VE];
+        } u;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) u.e[e] = tile[rv * VE + e][c];
+        *(v4u *)(Xt + (size_t)col * B + i) = u.v;
     }
-    if (blockIdx.y == 0) {
-        for (int q = tid; q < 64 * n; q += 256) {
-            const int r = q / n, k = q % n;
-            const int i = i0 + r;
-            if (i < B) Ag[(size_t)i * n + k] = action[(size_t)clamp_row(idx[i], rows) * n + k];
-        }
-        if (tid < 64 && i0 + tid < B) {
-            const int i = i0 + tid;
-            const int64_t g = clamp_row(idx[i], rows);
-            row_in[i] = logp[g];
-            row_in[B + i] = adv[g];
-            row_in[2 * B + i] = ret[g];
-        }
+    // actions, spread over the column blocks; per-row scalars in the first
+    const int per = (n + gridDim.y - 1) / gridDim.y;
+    const int k0 = blockIdx.y * per, k1 = min(n, k0 + per);
+    for (int q = tid; q < 64 * (k1 - k0); q += 256) {
+        const int r = q / (k1 - k0), k = k0 + q % (k1 - k0);
+        if (i0 + r < B) Ag[(size_t)(i0 + r) * n + k] = action[(size_t)s_idx[r] * n + k];
+    }
+    if (blockIdx.y == 0 && tid < 64 && i0 + tid < B) {
+        const int i = i0 + tid;
+        const int64_t g = s_idx[tid];
+        row_in[i] = logp[g];
+        row_in[B + i] = adv[g];
+        row_in[2 * B + i] = ret[g];
     }
 }
 
@@ -373,11 +583,29 @@ __global__ __launch_bounds__(256) void loss_tile_kernel(
 {
     __shared__ float t1[64][65];
     __shared__ float t2[64][65];
+    __shared__ float s_row[64];   // dL/dlogp (actor tiles) or dL/dV (critic tiles)
+    __shared__ float s_col[64];   // 1/sigma^2 (actor) or the critic head's weight
     const int i0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
     const bool actor = c0 < vsplit;
     const int tid = threadIdx.x;
     const float *ls = params + ols, *wc3 = params + owc3;
-    for (int q = tid; q < 64 * 64; q += 256) {
+    if (tid < 64) {
+        const int i = i0 + tid;
+        s_row[tid] = i < B ? (actor ? row_out[i] : row_out[B + i]) : 0.f;
+    } else if (tid < 128) {
+        const int col = c0 + tid - 64;
+        float v = 0.f;
+        if (actor) {
+            if (col < n) v = expf(-2.0f * ls[col]);
+        } else if (col - vsplit < C2) {
+            v = (float)to_elem<BF>(wc3[col - vsplit]);
+        }
+        s_col[tid - 64] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const int q = tid + 256 * j;
         const int r = q >> 6, c = q & 63;
         const int i = i0 + r, col = c0 + c;
         float a = 0.f, b = 0.f;
@@ -385,8 +613,8 @@ __global__ __launch_bounds__(256) void loss_tile_kernel(
             if (actor) {
                 if (col < n) {
                     const float d = Ag[(size_t)i * n + col] - mu[(size_t)i * n + col];
-                    const float inv = expf(-2.0f * ls[col]);
-                    const float g = row_out[i];
+                    const float inv = s_col[c];
+                    const float g = s_row[r];
                     a = g * (d * inv);
                     b = g * (d * d * inv - 1.0f);
                 }
@@ -395,7 +623,7 @@ __global__ __launch_bounds__(256) void loss_tile_kernel(
                 const int k = col - vsplit;
                 if (k < C2) {
                     const float h = (float)Hc2[(size_t)i * C2 + k];
-                    a = row_out[B + i] * (float)to_elem<BF>(wc3[k]) * (1.0f - h * h);
+                    a = s_row[r] * s_col[c] * (1.0f - h * h);
                     dZc2[(size_t)i * C2 + k] = to_elem<BF>(a);
                 }
             }
@@ -404,7 +632,9 @@ __global__ __launch_bounds__(256) void loss_tile_kernel(
         t2[r][c] = b;
     }
     __syncthreads();
-    for (int q = tid; q < 64 * 64; q += 256) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const int q = tid + 256 * j;
         const int c = q >> 6, r = q & 63;
         const int i = i0 + r, col = c0 + c;
         if (i >= B) continue;
@@ -431,6 +661,7 @@ struct RedSeg {
     double *dst64;      // fp64 destination (stats)
     double scale, add;
     int row0;           // first global row of this segment
+    int vec;            // rows 16-byte aligned and len a multiple of 16 bytes
 };
 constexpr int MAX_SEGS = 12;
 struct RedBatch {
@@ -450,7 +681,25 @@ __global__ __launch_bounds__(256) void row_reduce_kernel(RedBatch rb)
     const RedSeg &S = rb.s[si];
     const int r = g - S.row0;
     double acc = 0.0;
-    if (S.bf) {
+    if (S.vec && S.bf) {   // 8 bf16 per lane per step
+        const __bf16 *p = (const __bf16 *)S.src + (size_t)r * S.ld;
+        for (int b = lane * 8; b < S.len; b += WAVE * 8) {
+            const bf16x8 x = *(const bf16x8 *)(p + b);
+            float part = 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) part += (float)x[e] * (S.w ? S.w[b + e] : 1.0f);
+            acc += (double)part;
+        }
+    } else if (S.vec) {    // 4 floats per lane per step
+        const float *p = (const float *)S.src + (size_t)r * S.ld;
+        for (int b = lane * 4; b < S.len; b += WAVE * 4) {
+            const floatx4 x = *(const floatx4 *)(p + b);
+            float part = 0.f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) part += x[e] * (S.w ? S.w[b + e] : 1.0f);
+            acc += (double)part;
+        }
+    } else if (S.bf) {
         const __bf16 *p = (const __bf16 *)S.src + (size_t)r * S.ld;
         for (int b = lane; b < S.len; b += WAVE)
             acc += (double)((float)p[b] * (S.w ? S.w[b] : 1.0f));
@@ -509,6 +758,18 @@ __device__ __forceinline__ float adam_one(const AdamBatch &ab, int64_t p)
     return th;
 }
 
+// Adam over the flat vector: 4 elements per thread, each access coalesced
+// across the wave.
+__global__ __launch_bounds__(256) void adam_flat_kernel(AdamBatch ab, int64_t P)
+{
+    const int64_t base = (int64_t)blockIdx.x * 1024 + threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int64_t p = base + j * 256;
+        if (p < P) adam_one(ab, p);
+    }
+}
+
 template <bool BF>
 __global__ __launch_bounds__(256) void adam_kernel(AdamBatch ab)
 {
@@ -528,7 +789,9 @@ __global__ __launch_bounds__(256) void adam_kernel(AdamBatch ab)
         return;
     }
     const int r0 = (t / S.tiles_c) * 32, c0 = (t % S.tiles_c) * 32;
-    for (int q = tid; q < 32 * 32; q += 256) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int q = tid + 256 * j;
         const int r = r0 + (q >> 5), c = c0 + (q & 31);
         float w = 0.0f;
         if (r < S.rows && c < S.cols) w = adam_one(ab, S.off + (int64_t)r * S.cols + c);
@@ -539,7 +802,9 @@ __global__ __launch_bounds__(256) void adam_kernel(AdamBatch ab)
     }
     if (!S.copyT) return;
     __syncthreads();
-    for (int q = tid; q < 32 * 32; q += 256) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int q = tid + 256 * j;
         const int c = c0 + (q >> 5), r = r0 + (q & 31);
         if (r < S.rows_pad && c < S.cols_pad)
             ((Elem<BF> *)S.copyT)[(size_t)c * S.ld_copyT + r] = tile[q & 31][q >> 5];
@@ -693,7 +958,14 @@ hipError_t run_gemms(bool bf, std::initializer_list<GemmProb> ps, hipStream_t s)
         tiles += q.tiles_n * cdiv(q.M, GT);
         gb.p[gb.np++] = q;
     }
-    if (bf) hipLaunchKernelGGL(gemm_bf16_kernel, dim3(tiles), dim3(256), 0, s, gb);
+    bool staged = bf;   // K in {128, 512, 1024}: the LDS-staged kernel
+    for (int q = 0; q < gb.np; ++q) {
+        const int nc = gb.p[q].K / LBK;
+        staged = staged && gb.p[q].K % LBK == 0 && (nc == 1 || nc == 4 || nc == 8) &&
+                 gb.p[q].lda % 8 == 0 && gb.p[q].ldb % 8 == 0;
+    }
+    if (staged) hipLaunchKernelGGL(gemm_lds_kernel, dim3(tiles), dim3(256), 0, s, gb);
+    else if (bf) hipLaunchKernelGGL(gemm_bf16_kernel, dim3(tiles), dim3(256), 0, s, gb);
     else hipLaunchKernelGGL(gemm_f32_kernel, dim3(tiles), dim3(256), 0, s, gb);
     return hipGetLastError();
 }
@@ -757,12 +1029,21 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
     mseg(L.obc1, 1, L.C1, 1, L.C1, nullptr, 0, 0, nullptr, 0);
     mseg(L.obc2, 1, 2 * L.C2 + 1, 1, 2 * L.C2 + 1, nullptr, 0, 0, nullptr, 0);
 
+    // the operand copies are refreshed by the matrix segments alone
+    AdamBatch refresh = ab;
+    refresh.ns = 5;
+    const int rtiles = ab.s[5].tile0;
     auto adam = [&](int do_adam, int64_t step) -> hipError_t {
-        ab.do_adam = do_adam;
-        ab.bc1 = (float)(1.0 - pow((double)a.beta1, (double)step));
-        ab.bc2 = (float)(1.0 - pow((double)a.beta2, (double)step));
-        if (bf) hipLaunchKernelGGL(adam_kernel<true>, dim3(atiles), dim3(256), 0, s, ab);
-        else hipLaunchKernelGGL(adam_kernel<false>, dim3(atiles), dim3(256), 0, s, ab);
+        if (do_adam) {
+            ab.do_adam = 1;
+            ab.bc1 = (float)(1.0 - pow((double)a.beta1, (double)step));
+            ab.bc2 = (float)(1.0 - pow((double)a.beta2, (double)step));
+            hipLaunchKernelGGL(adam_flat_kernel, dim3((unsigned)((L.P + 1023) / 1024)), dim3(256),
+                               0, s, ab, L.P);
+        }
+        refresh.do_adam = 0;
+        if (bf) hipLaunchKernelGGL(adam_kernel<true>, dim3(rtiles), dim3(256), 0, s, refresh);
+        else hipLaunchKernelGGL(adam_kernel<false>, dim3(rtiles), dim3(256), 0, s, refresh);
         return hipGetLastError();
     };
     hipError_t e = adam(0, 1);
@@ -778,6 +1059,8 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
     void *dZ1t = W(L.wdZ1t);
     auto at = [&](void *base, size_t elems) { return (void *)((uint8_t *)base + elems * es); };
 
+    // observation rows take 16-byte loads when every row starts 16-byte aligned
+    const int vec_obs = ((uintptr_t)a.obs % 16 == 0 && (a.ld_obs * (int64_t)es) % 16 == 0) ? 1 : 0;
     for (int u = 0; u < a.n_updates; ++u) {
         const int64_t *idx = a.idx + (size_t)u * B;
         // gather
@@ -785,12 +1068,14 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             const dim3 grid(cdiv(B, 64), cdiv(L.Kp, 64));
             if (bf)
                 hipLaunchKernelGGL(gather_kernel<true>, grid, dim3(256), 0, s,
-                                   (const __bf16 *)a.obs, a.ld_obs, a.action, a.logp, a.adv, a.ret,
-                                   idx, a.rows, B, L.S, L.Kp, L.n, (__bf16 *)X, (__bf16 *)Xt, Ag, row_in);
+                                   (const __bf16 *)a.obs, a.ld_obs, vec_obs, a.action, a.logp,
+                                   a.adv, a.ret, idx, a.rows, B, L.S, L.Kp, L.n, (__bf16 *)X,
+                                   (__bf16 *)Xt, Ag, row_in);
             else
                 hipLaunchKernelGGL(gather_kernel<false>, grid, dim3(256), 0, s,
-                                   (const float *)a.obs, a.ld_obs, a.action, a.logp, a.adv, a.ret,
-                                   idx, a.rows, B, L.S, L.Kp, L.n, (float *)X, (float *)Xt, Ag, row_in);
+                                   (const float *)a.obs, a.ld_obs, vec_obs, a.action, a.logp,
+                                   a.adv, a.ret, idx, a.rows, B, L.S, L.Kp, L.n, (float *)X,
+                                   (float *)Xt, Ag, row_in);
         }
         // forward 1: [h1 | hc1] = tanh(X [W1; Wc1]^T + [b1 | bc1])
         {
@@ -915,6 +1200,9 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
                 g.scale = scale;
                 g.add = addc;
                 g.row0 = rows;
+                const size_t esz = isbf ? 2 : 4;
+                g.vec = (uintptr_t)src % 16 == 0 && (ld * (int64_t)esz) % 16 == 0 &&
+                        ((int64_t)len * (int64_t)esz) % 16 == 0 && (!w || (uintptr_t)w % 16 == 0);
                 rows += nrows;
                 rb.s[rb.ns++] = g;
             };
