@@ -295,11 +295,20 @@ int tp_critic_value(const tp_critic *critic, const void *packed,
  *                                max_{u <= t} V_u
  *   with P = periods_per_year (252 for daily bars, 252 * 390 for minute
  *   bars) and risk_free the annual rate.  v0 [E], v [T][E], out [E][5] fp64
- *   device arrays; T, E >= 1, periods_per_year > 0.
+ *   device arrays; T, E >= 1, periods_per_year > 0; work: a device buffer of
+ *   at least tp_backtest_metrics_work_bytes(T, E) bytes (contents are
+ *   scratch; calls that share one workspace must not overlap).
+ * The sums behind the volatility and the Sharpe ratio are taken over time
+ * segments in a fixed order (deterministic); the drawdown is exact.
  */
 int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
                         double periods_per_year, double risk_free, double *out,
-                        void *stream);
+                        void *work, size_t work_bytes, void *stream);
+
+/* Bytes of the caller-owned device workspace tp_backtest_metrics needs for
+ * T steps of E series (8-byte aligned; segment partial sums and maxima), or
+ * 0 for T < 1 or E outside 1 .. 64 * 65535.  Host only. */
+size_t tp_backtest_metrics_work_bytes(int32_t T, int32_t E);
 
 /*
  * PPO learner (PPO, Section 5.2; hyper-parameters of Table 2: Adam,

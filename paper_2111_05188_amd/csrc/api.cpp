@@ -526,17 +526,32 @@ int tp_critic_value(const tp_critic *critic, const void *packed, size_t packed_b
     return ok();
 }
 
-int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
-                        double periods_per_year, double risk_free, double *out, void *stream)
+size_t tp_backtest_metrics_work_bytes(int32_t T, int32_t E)
 {
-    if (!v0 || !v || !out) return fail(TP_EINVAL, "a metrics array is NULL");
-    if (!aligned(v0, 8) || !aligned(v, 8) || !aligned(out, 8))
+    if (T < 1 || E < 1 || E > 64 * 65535) {
+        fail(TP_EINVAL, "T = %d, E = %d (1 <= E <= %d)", T, E, 64 * 65535);
+        return 0;
+    }
+    ok();
+    return backtest_metrics_work_bytes(T, E);
+}
+
+int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
+                        double periods_per_year, double risk_free, double *out, void *work,
+                        size_t work_bytes, void *stream)
+{
+    if (!v0 || !v || !out || !work) return fail(TP_EINVAL, "a metrics array is NULL");
+    if (!aligned(v0, 8) || !aligned(v, 8) || !aligned(out, 8) || !aligned(work, 8))
         return fail(TP_EINVAL, "metrics arrays are not 8-byte aligned");
-    if (T < 1 || E < 1) return fail(TP_EINVAL, "T = %d, E = %d must be >= 1", T, E);
+    if (T < 1 || E < 1 || E > 64 * 65535)
+        return fail(TP_EINVAL, "T = %d, E = %d (1 <= E <= %d)", T, E, 64 * 65535);
+    if (work_bytes < backtest_metrics_work_bytes(T, E))
+        return fail(TP_EINVAL, "metrics workspace of %zu bytes, %zu needed", work_bytes,
+                    backtest_metrics_work_bytes(T, E));
     if (!(periods_per_year > 0.0))
         return fail(TP_EINVAL, "periods_per_year = %g must be > 0", periods_per_year);
     if (!std::isfinite(risk_free)) return fail(TP_EINVAL, "risk_free = %g", risk_free);
-    hipError_t e = launch_backtest_metrics(v0, v, T, E, periods_per_year, risk_free, out,
+    hipError_t e = launch_backtest_metrics(v0, v, T, E, periods_per_year, risk_free, out, work,
                                            (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "metrics launch");
     return ok();

@@ -43,7 +43,21 @@ __global__ __launch_bounds__(EV_THREADS) void env_return_kernel(const float *__r
     if (e >= E) return;
     double acc = 0.0, disc = 1.0;
     bool ok = true;
-    for (int j = 0; j < L; ++j) {
+    // loads of a block of steps are issued together; the sum keeps step order
+    constexpr int U = 16;
+    int j = 0;
+    for (; j + U <= L; j += U) {
+        float x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[u] = r[(size_t)(j + u) * E + e];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            ok &= !isnan(x[u]);
+            acc += disc * (double)x[u];
+            disc *= gamma;
+        }
+    }
+    for (; j < L; ++j) {
         const float x = r[(size_t)j * E + e];
         ok &= !isnan(x);
         acc += disc * (double)x;
@@ -61,8 +75,22 @@ __global__ __launch_bounds__(64) void agent_mean_kernel(const double *__restrict
     const int g = blockIdx.x;
     double s = 0.0;
     int cnt = 0;
-    for (int e = g * epa; e < (g + 1) * epa; ++e) {
-        const double x = ret[e];
+    const double *p = ret + (size_t)g * epa;
+    constexpr int U = 16;
+    int e = 0;
+    for (; e + U <= epa; e += U) {
+        double x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[u] = p[e + u];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (!isnan(x[u])) {
+                s += x[u];
+                ++cnt;
+            }
+    }
+    for (; e < epa; ++e) {
+        const double x = p[e];
         if (!isnan(x)) {
             s += x;
             ++cnt;

@@ -84,9 +84,10 @@ hipError_t launch_env_step(const EnvConst &c, double *cash, int32_t *shares,
                            int64_t *t, const float *action, float *reward,
                            int E, void *obs, int64_t ld_obs, int obs_bf16,
                            hipStream_t s);
+size_t backtest_metrics_work_bytes(int T, int E);
 hipError_t launch_backtest_metrics(const double *v0, const double *v, int T, int E,
                                    double periods_per_year, double risk_free, double *out,
-                                   hipStream_t s);
+                                   void *work, hipStream_t s);
 hipError_t launch_ensemble_fuse(float *params, int N, int K, int64_t P, hipStream_t s);
 hipError_t launch_fitness(const float *r, int L, int E, int A, double gamma, double *fit,
                           double *env_return, hipStream_t s);

@@ -1,19 +1,28 @@
 // Backtest metrics of total-asset series (Section 5.2, "Evaluation
-// metrics"), time-parallel.  A workgroup of 1024 threads takes EB
-// consecutive envs and splits each env's series V_1 .. V_T into TC = 1024/EB
-// contiguous time chunks, one per thread; lanes with the same chunk read
-// consecutive envs of a time row.  EB is chosen per launch: wide groups
-// (whole cache lines of a row) when there are many envs, one env per
-// workgroup with 1024 time lanes when a few envs have long series.
+// metrics").  Many envs: one launch, a workgroup per group of envs (see
+// metrics_onepass_kernel).  Few envs with long series: split over time so
+// that they still fill the GPU, as follows.
 //
-// Pass 1: per chunk, the sum of its returns r_t = V_t / V_{t-1} - 1 and its
-// largest value; an LDS tree sums the returns per env (the mean) and an
-// LDS scan gives each chunk the running peak of everything before it.
-// Pass 2: per chunk, the squared deviations from the mean and the drawdown
-// (peak_t - V_t) / peak_t with the running peak seeded from the scan, so
-// every drawdown term is computed from the operands a serial walk uses and
-// the maximum is exact; only the two sums are reassociated (a fixed tree,
-// deterministic).
+// Geometry: a workgroup of 256 threads takes EB consecutive envs (a power of
+// two, at most 64: 16 or more envs make every row access whole 128-byte
+// lines) and one segment of SL = TC x CL consecutive steps, TC = 256 / EB
+// time lanes each walking a chunk of CL steps.  Segments are sized so that
+// the grid has about 1024 workgroups.
+//
+// Three launches over a caller-provided workspace:
+//   1. per segment: the sum of its returns r_t = V_t / V_{t-1} - 1, its
+//      largest value, and each chunk's largest value;
+//   2. per segment: every workgroup of an env group computes the envs' mean
+//      return from the segment sums (lanes stride over the segments, then a
+//      fixed LDS tree, so all workgroups agree) and the running peak before
+//      its segment (earlier segments' maxima, then earlier chunks'); each
+//      lane then walks its chunk once for the squared deviations and the
+//      drawdowns (peak_t - V_t) / peak_t, seeded with that peak, so every
+//      drawdown term has the operands of a serial walk and their maximum is
+//      exact;
+//   3. per env: the segments' squared deviations summed in segment order,
+//      their largest drawdown, and the five metrics.
+// Only the sums are reassociated (fixed order, deterministic).
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -21,9 +30,247 @@ namespace tpk {
 
 namespace {
 
+constexpr int MT = 256;
+
+struct MetGeo {
+    int eb_log2, EB, TC, CL, SL, nseg, ngroups;
+};
+
+int pow2_ceil(int x)
+{
+    int p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+MetGeo metrics_geometry(int T, int E)
+{
+    MetGeo g;
+    g.EB = pow2_ceil(E < 64 ? E : 64);
+    g.eb_log2 = 0;
+    while ((1 << g.eb_log2) < g.EB) ++g.eb_log2;
+    g.TC = MT / g.EB;
+    g.ngroups = (E + g.EB - 1) / g.EB;
+    int target = 1024 / g.ngroups;
+    if (target < 1) target = 1;
+    const int sl = (T + target - 1) / target;
+    g.CL = (sl + g.TC - 1) / g.TC;
+    if (g.CL < 1) g.CL = 1;
+    g.SL = g.CL * g.TC;
+    g.nseg = (T + g.SL - 1) / g.SL;
+    return g;
+}
+
+// workspace arrays, each [nseg][E] doubles except cmax [nseg * TC][E] and
+// mean [E]
+struct MetWork {
+    double *psum, *pmax, *pss, *pmdd, *cmax, *mean;
+};
+
+MetWork carve(void *work, const MetGeo &g, int E)
+{
+    double *w = (double *)work;
+    const size_t se = (size_t)g.nseg * E;
+    MetWork m;
+    m.psum = w;
+    m.pmax = w + se;
+    m.pss = w + 2 * se;
+    m.pmdd = w + 3 * se;
+    m.cmax = w + 4 * se;
+    m.mean = w + 4 * se + se * g.TC;
+    return m;
+}
+
+struct Lane {
+    int eb, tc, e, t0, t1;
+    bool act;
+};
+
+__device__ __forceinline__ Lane lane_of(const MetGeo &g, int T, int E)
+{
+    Lane l;
+    const int tid = threadIdx.x;
+    l.eb = tid & (g.EB - 1);
+    l.tc = tid >> g.eb_log2;
+    l.e = blockIdx.y * g.EB + l.eb;
+    l.act = l.e < E;
+    const int s0 = blockIdx.x * g.SL;
+    l.t0 = min(T, s0 + l.tc * g.CL);
+    l.t1 = min(T, l.t0 + g.CL);
+    return l;
+}
+
+__global__ __launch_bounds__(MT) void metrics_pass1_kernel(const double *__restrict__ v0,
+                                                           const double *__restrict__ v, int T,
+                                                           int E, MetGeo g, MetWork w)
+{
+    __shared__ double s_a[MT];
+    __shared__ double s_b[MT];
+    const Lane l = lane_of(g, T, E);
+    const int tid = threadIdx.x;
+    const size_t ld = (size_t)E;
+    double sum = 0.0, cmax = -__builtin_inf();
+    if (l.act && l.t0 < l.t1) {
+        const double *col = v + l.e;
+        double prev = l.t0 > 0 ? col[(size_t)(l.t0 - 1) * ld] : v0[l.e];
+#pragma unroll 4
+        for (int t = l.t0; t < l.t1; ++t) {
+            const double cur = col[(size_t)t * ld];
+            sum += cur / prev - 1.0;
+            if (cur > cmax) cmax = cur;
+            prev = cur;
+        }
+    }
+    if (l.act) w.cmax[((size_t)blockIdx.x * g.TC + l.tc) * ld + l.e] = cmax;
+    s_a[tid] = sum;
+    s_b[tid] = cmax;
+    __syncthreads();
+    for (int o = g.TC >> 1; o >= 1; o >>= 1) {
+        if (l.tc < o) {
+            s_a[tid] += s_a[tid + o * g.EB];
+            if (s_b[tid + o * g.EB] > s_b[tid]) s_b[tid] = s_b[tid + o * g.EB];
+        }
+        __syncthreads();
+    }
+    if (l.tc == 0 && l.act) {
+        w.psum[(size_t)blockIdx.x * ld + l.e] = s_a[tid];
+        w.pmax[(size_t)blockIdx.x * ld + l.e] = s_b[tid];
+    }
+}
+
+__global__ __launch_bounds__(MT) void metrics_pass2_kernel(const double *__restrict__ v0,
+                                                           const double *__restrict__ v, int T,
+                                                           int E, MetGeo g, MetWork w)
+{
+    __shared__ double s_a[MT];
+    __shared__ double s_b[MT];
+    const Lane l = lane_of(g, T, E);
+    const int tid = threadIdx.x;
+    const size_t ld = (size_t)E;
+    const int seg = blockIdx.x;
+    // mean over all segments and peak over earlier ones, lanes striding
+    double sum = 0.0, peak = -__builtin_inf();
+    if (l.act) {
+        for (int s = l.tc; s < g.nseg; s += g.TC) {
+            sum += w.psum[(size_t)s * ld + l.e];
+            if (s < seg) {
+                const double m = w.pmax[(size_t)s * ld + l.e];
+                if (m > peak) peak = m;
+            }
+        }
+    }
+    s_a[tid] = sum;
+    s_b[tid] = peak;
+    __syncthreads();
+    for (int o = g.TC >> 1; o >= 1; o >>= 1) {
+        if (l.tc < o) {
+            s_a[tid] += s_a[tid + o * g.EB];
+            if (s_b[tid + o * g.EB] > s_b[tid]) s_b[tid] = s_b[tid + o * g.EB];
+        }
+        __syncthreads();
+    }
+    const double mean = s_a[l.eb] / (double)T;
+    const double first = l.act ? v0[l.e] : 1.0;
+    double pk = first;
+    if (s_b[l.eb] > pk) pk = s_b[l.eb];
+    __syncthreads();
+    // exclusive max-scan of this segment's chunk maxima (Hillis-Steele)
+    s_b[tid] = l.act ? w.cmax[((size_t)seg * g.TC + l.tc) * ld + l.e] : -__builtin_inf();
+    __syncthreads();
+    for (int o = 1; o < g.TC; o <<= 1) {
+        const double other = l.tc >= o ? s_b[tid - o * g.EB] : -__builtin_inf();
+        __syncthreads();
+        if (other > s_b[tid]) s_b[tid] = other;
+        __syncthreads();
+    }
+    if (l.tc > 0 && s_b[tid - g.EB] > pk) pk = s_b[tid - g.EB];
+    if (seg == 0 && l.tc == 0 && l.act) w.mean[l.e] = mean;
+    // the chunk: squared deviations and drawdowns
+    double ss = 0.0, mdd = 0.0;
+    if (l.act && l.t0 < l.t1) {
+        const double *col = v + l.e;
+        double prev = l.t0 > 0 ? col[(size_t)(l.t0 - 1) * ld] : first;
+#pragma unroll 4
+        for (int t = l.t0; t < l.t1; ++t) {
+            const double cur = col[(size_t)t * ld];
+            const double d = (cur / prev - 1.0) - mean;
+            ss += d * d;
+            if (cur > pk) pk = cur;
+            const double dd = (pk - cur) / pk;
+            if (dd > mdd) mdd = dd;
+            prev = cur;
+        }
+    }
+    __syncthreads();
+    s_a[tid] = ss;
+    s_b[tid] = mdd;
+    __syncthreads();
+    for (int o = g.TC >> 1; o >= 1; o >>= 1) {
+        if (l.tc < o) {
+            s_a[tid] += s_a[tid + o * g.EB];
+            if (s_b[tid + o * g.EB] > s_b[tid]) s_b[tid] = s_b[tid + o * g.EB];
+        }
+        __syncthreads();
+    }
+    if (l.tc == 0 && l.act) {
+        w.pss[(size_t)seg * ld + l.e] = s_a[tid];
+        w.pmdd[(size_t)seg * ld + l.e] = s_b[tid];
+    }
+}
+
+// one workgroup per env group: lanes stride over the segments
+__global__ __launch_bounds__(MT) void metrics_final_kernel(const double *__restrict__ v0,
+                                                           const double *__restrict__ v, int T,
+                                                           int E, double P, double rf, MetGeo g,
+                                                           MetWork w, double *__restrict__ out)
+{
+    __shared__ double s_a[MT];
+    __shared__ double s_b[MT];
+    const int tid = threadIdx.x;
+    const int eb = tid & (g.EB - 1), tc = tid >> g.eb_log2;
+    const int e = blockIdx.x * g.EB + eb;
+    const bool act = e < E;
+    const size_t ld = (size_t)E;
+    double ss = 0.0, mdd = 0.0;
+    if (act) {
+        for (int s = tc; s < g.nseg; s += g.TC) {
+            ss += w.pss[(size_t)s * ld + e];
+            const double m = w.pmdd[(size_t)s * ld + e];
+            if (m > mdd) mdd = m;
+        }
+    }
+    s_a[tid] = ss;
+    s_b[tid] = mdd;
+    __syncthreads();
+    for (int o = g.TC >> 1; o >= 1; o >>= 1) {
+        if (tc < o) {
+            s_a[tid] += s_a[tid + o * g.EB];
+            if (s_b[tid + o * g.EB] > s_b[tid]) s_b[tid] = s_b[tid + o * g.EB];
+        }
+        __syncthreads();
+    }
+    if (tc != 0 || !act) return;
+    const double first = v0[e], last = v[(size_t)(T - 1) * ld + e];
+    const double mean = w.mean[e];
+    const double sd = T > 1 ? sqrt(s_a[tid] / (double)(T - 1)) : 0.0;
+    double *o = out + (size_t)e * 5;
+    o[0] = last / first - 1.0;
+    o[1] = pow(last / first, P / (double)T) - 1.0;
+    o[2] = sd * sqrt(P);
+    o[3] = sd > 0.0 ? (mean - rf / P) / sd * sqrt(P) : 0.0;
+    o[4] = s_b[tid];
+}
+
+// ---------------------------------------------------------------------------
+// One launch, when the envs alone give the GPU enough workgroups: a
+// workgroup of 1024 threads takes EB envs and splits each series into
+// 1024 / EB contiguous chunks; pass 1 (chunk return sums and maxima), an LDS
+// tree (the mean) and an LDS max-scan (the peak before each chunk), then
+// pass 2 over the same chunks (squared deviations, exact drawdowns).
+// ---------------------------------------------------------------------------
 constexpr int MET_THREADS = 1024;
 
-__global__ __launch_bounds__(MET_THREADS) void backtest_metrics_kernel(
+__global__ __launch_bounds__(MET_THREADS) void metrics_onepass_kernel(
     const double *__restrict__ v0, const double *__restrict__ v, int T, int E, double P,
     double rf, double *__restrict__ out, int eb_log2)
 {
@@ -123,14 +370,33 @@ int metrics_eb_log2(int T, int E)
 
 }  // namespace
 
+size_t backtest_metrics_work_bytes(int T, int E)
+{
+    const MetGeo g = metrics_geometry(T, E);
+    const size_t se = (size_t)g.nseg * E;
+    return sizeof(double) * (4 * se + se * g.TC + (size_t)E);
+}
+
 hipError_t launch_backtest_metrics(const double *v0, const double *v, int T, int E,
                                    double periods_per_year, double risk_free, double *out,
-                                   hipStream_t s)
+                                   void *work, hipStream_t s)
 {
-    const int lg = metrics_eb_log2(T, E);
-    const int eb = 1 << lg;
-    hipLaunchKernelGGL(backtest_metrics_kernel, dim3((E + eb - 1) / eb), dim3(MET_THREADS), 0, s,
-                       v0, v, T, E, periods_per_year, risk_free, out, lg);
+    {
+        const int lg = metrics_eb_log2(T, E);
+        const int blocks = (E + (1 << lg) - 1) >> lg;
+        if (blocks >= 256) {
+            hipLaunchKernelGGL(metrics_onepass_kernel, dim3(blocks), dim3(MET_THREADS), 0, s, v0, v,
+                               T, E, periods_per_year, risk_free, out, lg);
+            return hipGetLastError();
+        }
+    }
+    const MetGeo g = metrics_geometry(T, E);
+    const MetWork w = carve(work, g, E);
+    const dim3 grid(g.nseg, g.ngroups);
+    hipLaunchKernelGGL(metrics_pass1_kernel, grid, dim3(MT), 0, s, v0, v, T, E, g, w);
+    hipLaunchKernelGGL(metrics_pass2_kernel, grid, dim3(MT), 0, s, v0, v, T, E, g, w);
+    hipLaunchKernelGGL(metrics_final_kernel, dim3(g.ngroups), dim3(MT), 0, s, v0, v, T, E,
+                       periods_per_year, risk_free, g, w, out);
     return hipGetLastError();
 }
 

@@ -149,13 +149,14 @@ def main():
             steps = 1.0 + 1e-3 * torch.randn(T, Em, dtype=torch.float64, device=dev, generator=g)
             v = v0 * torch.cumprod(steps, dim=0)
             met = torch.empty(Em, 5, dtype=torch.float64, device=dev)
-            sec = _time(lambda: tp.backtest_metrics(v0, v, 252.0 * 390, 0.02, out=met),
+            wk = tp.backtest_metrics_workspace(T, Em, dev)
+            sec = _time(lambda: tp.backtest_metrics(v0, v, 252.0 * 390, 0.02, out=met, work=wk),
                         args.iters, stream)
             nbytes = 8 * T * Em + 8 * Em + 40 * Em
             out["metrics"][f"T{T}_E{Em}"] = {
                 "launch_ms": sec * 1e3, "bytes_per_launch": nbytes, "GBs": nbytes / sec / 1e9,
                 "hbm_frac": nbytes / sec / 1e9 / PEAK_HBM_GBS}
-            del v0, steps, v, met
+            del v0, steps, v, met, wk
         torch.cuda.empty_cache()
 
     if args.only in (None, "evolution"):

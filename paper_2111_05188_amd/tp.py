@@ -78,7 +78,8 @@ class Traj(C.Structure):
 EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_actor_pack", "tp_rollout", "tp_gae", "tp_critic_packed_bytes",
            "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
-           "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
+           "tp_backtest_metrics_work_bytes", "tp_ensemble_fuse", "tp_fitness",
+           "tp_keep_best", "tp_select",
            "tp_ppo_param_count", "tp_ppo_workspace_bytes", "tp_ppo_update",
            "tp_minibatch_rows", "tp_rollout_path",
            "tp_last_error", "tp_version")
@@ -106,7 +107,10 @@ def load(path: str = LIB_PATH):
     L.tp_critic_packed_bytes.restype = sz
     L.tp_critic_pack.argtypes = [vp, vp, sz, vp]
     L.tp_critic_value.argtypes = [vp, vp, sz, vp, i64, i64, i32, vp, vp]
-    L.tp_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp, vp]
+    L.tp_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp, vp,
+                                      C.c_size_t, vp]
+    L.tp_backtest_metrics_work_bytes.restype = C.c_size_t
+    L.tp_backtest_metrics_work_bytes.argtypes = [i32, i32]
     L.tp_ensemble_fuse.argtypes = [vp, i32, i32, i64, vp]
     L.tp_fitness.argtypes = [vp, i32, i32, i32, C.c_double, vp, vp, vp]
     L.tp_keep_best.argtypes = [vp, vp, vp, vp, vp, i32, i64, vp]
@@ -365,15 +369,26 @@ def critic_value(critic: CriticT, obs: torch.Tensor, value: torch.Tensor, stream
                                   _ptr(value), _stream(stream)))
 
 
+def backtest_metrics_workspace(T: int, E: int, device="cuda") -> torch.Tensor:
+    nb = load().tp_backtest_metrics_work_bytes(T, E)
+    if nb == 0:
+        raise TPError(TP_EINVAL, load().tp_last_error().decode())
+    return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
 def backtest_metrics(v0: torch.Tensor, v: torch.Tensor, periods_per_year: float,
-                     risk_free: float = 0.0, out: torch.Tensor | None = None, stream=None):
+                     risk_free: float = 0.0, out: torch.Tensor | None = None, work=None,
+                     stream=None):
     """Per-env [cumulative, annual return, annual volatility, Sharpe, max
     drawdown] of V_0 = v0 [E], V_1..V_T = v [T][E] (fp64)."""
     T, E = v.shape
     if out is None:
         out = torch.empty(E, 5, dtype=torch.float64, device=v.device)
+    if work is None:
+        work = backtest_metrics_workspace(T, E, v.device)
     _check(load().tp_backtest_metrics(_ptr(v0), _ptr(v), T, E, periods_per_year,
-                                      risk_free, _ptr(out), _stream(stream)))
+                                      risk_free, _ptr(out), _ptr(work), work.numel(),
+                                      _stream(stream)))
     return out
 
 
