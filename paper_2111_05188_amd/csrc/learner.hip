@@ -293,8 +293,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
 // bf16 learner's): chunks of 64 rows x 128 k of A and of B are staged in
 // LDS (rows padded by 16 bytes so the fragment reads of 16 rows fall in
 // different banks), loaded with whole-line accesses (each wave instruction
-// reads 4 rows x 256 contiguous bytes), two chunks ahead in registers; the
-// four waves read their 32x32 blocks' fragments from LDS.
+// reads 4 rows x 256 contiguous bytes), GEMM_LD chunks ahead in registers
+// (deeper prefetch measured slower); the four waves read their 32x32
+// blocks' fragments from LDS.
+#ifndef GEMM_LD
+#define GEMM_LD 2                     // chunks in flight in registers
+#endif
 constexpr int LBK = 128;              // k per chunk
 constexpr int LROW = LBK + 8;         // padded LDS row (bf16)
 constexpr int LTILE = GT * LROW;      // one operand's chunk (bf16)
@@ -316,7 +320,7 @@ __device__ __forceinline__ void lds_kloop(const __bf16 *const ga, const __bf16 *
         la[j] = ga + (size_t)min(lrow + 16 * j, Mr - 1) * lda + lpiece * 8;
         lb[j] = gb + (size_t)min(lrow + 16 * j, Nr - 1) * ldb + lpiece * 8;
     }
-    constexpr int D = NC < 2 ? NC : 2;     // chunks in flight in registers
+    constexpr int D = NC < GEMM_LD ? NC : GEMM_LD;   // chunks in flight in registers
     v4u_t ra[D][4], rb[D][4];
     auto load = [&](v4u_t (&xa)[4], v4u_t (&xb)[4], int c) {
 #pragma unroll
