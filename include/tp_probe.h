@@ -1,0 +1,37 @@
+/*
+ * tp_probe.h -- hardware probes behind the roofline ceilings quoted for the
+ * kernels (measurement tooling; libtpprobe.so, separate from libtp.so).
+ * Device pointers, asynchronous on `stream` (a hipStream_t); 0 = launched,
+ * -1 = bad arguments, -4 = launch error.  The caller times the launches.
+ */
+#pragma once
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* `blocks` workgroups of four waves, each issuing iters x 8 independent
+ * v_mfma_f32_16x16x32_bf16 on register operands.  out: blocks * 256 floats
+ * (written only under a condition the data never meets). */
+int tpp_mfma_issue(int blocks, int iters, float *out, void *stream);
+
+/* Algorithmic FLOPs of one tpp_mfma_issue launch. */
+double tpp_mfma_issue_flops(int blocks, int iters);
+
+/* The same with v_mfma_f32_32x32x16_bf16, four independent accumulators. */
+int tpp_mfma32_issue(int blocks, int iters, float *out, void *stream);
+double tpp_mfma32_issue_flops(int blocks, int iters);
+
+/* `blocks` workgroups of eight waves; wave w streams 1-KiB fragments
+ * f = 0 .. frags_per_wave-1 of buf + w * frags_per_wave KiB, reps times,
+ * 16 loads in flight.  buf >= 8 * frags_per_wave KiB (every workgroup reads
+ * the same bytes, so they come from L2 after the first pass); out:
+ * blocks * 512 * 16 bytes.  Bytes pulled per workgroup:
+ * 8 * frags_per_wave * 1024 * reps. */
+int tpp_l2_stream(const void *buf, size_t buf_bytes, int frags_per_wave, int reps, int blocks,
+                  void *out, void *stream);
+
+#ifdef __cplusplus
+}
+#endif

@@ -31,15 +31,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build() -> str:
-    """Compile every source and link libtp.so (always rebuilds)."""
-    os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(len(SOURCES)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+PROBE_LIB = os.path.join(HERE, "libtpprobe.so")
+
+
+def _link(objs, lib):
+    tmp = lib + ".tmp"
     subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC",
                            "-o", tmp, *objs])
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build() -> str:
+    """Compile every source and link libtp.so and the probe library
+    libtpprobe.so (always rebuilds)."""
+    os.makedirs(BUILD, exist_ok=True)
+    with ThreadPoolExecutor(len(SOURCES) + 1) as ex:
+        objs = list(ex.map(_compile, SOURCES + ["probe.hip"]))
+    _link(objs[:-1], LIB)
+    _link(objs[-1:], PROBE_LIB)
     return LIB
 
 

@@ -1,0 +1,148 @@
+// Hardware probes for the roofline ceilings the design notes quote
+// (measurement tooling, built as libtpprobe.so; not part of the method):
+//   * tpp_mfma_issue / tpp_mfma32_issue: waves issuing
+//     v_mfma_f32_16x16x32_bf16 (eight independent accumulators per wave) or
+//     v_mfma_f32_32x32x16_bf16 (four) back to back on register operands:
+//     the achievable dense bf16 MFMA rate of each instruction;
+//   * tpp_l2_stream: every workgroup streams the same L2-resident buffer in
+//     the pattern of the rollout's weight stream (a wave instruction reads
+//     1 KiB: lane l the 16 bytes at 16 l), 16 loads in flight per wave: the
+//     L2 -> CU bandwidth one CU can pull.
+// Both write to `out` only under a condition the data never meets, so the
+// results stay live without memory traffic.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tp_probe.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int NACC = 8;
+
+__global__ __launch_bounds__(256) void mfma_issue_kernel(int iters, float *out)
+{
+    const int lane = threadIdx.x % 64;
+    bf16x8 a, b;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        a[e] = (__bf16)(0.001f * (float)(lane + e));
+        b[e] = (__bf16)(0.002f * (float)(lane - e));
+    }
+    floatx4 acc[NACC];
+#pragma unroll
+    for (int j = 0; j < NACC; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int j = 0; j < NACC; ++j)
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[j], 0, 0, 0);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < NACC; ++j) s += acc[j][0] + acc[j][1] + acc[j][2] + acc[j][3];
+    if (s == 1234567.0f) out[blockIdx.x * 256 + threadIdx.x] = s;
+}
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+// the same with v_mfma_f32_32x32x16_bf16 (four independent accumulators)
+__global__ __launch_bounds__(256) void mfma32_issue_kernel(int iters, float *out)
+{
+    const int lane = threadIdx.x % 64;
+    bf16x8 a, b;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        a[e] = (__bf16)(0.001f * (float)(lane + e));
+        b[e] = (__bf16)(0.002f * (float)(lane - e));
+    }
+    floatx16 acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[j][q] = 0.f;
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) s += acc[j][q];
+    if (s == 1234567.0f) out[blockIdx.x * 256 + threadIdx.x] = s;
+}
+
+constexpr int SD = 16;   // loads in flight per wave
+
+__global__ __launch_bounds__(512) void l2_stream_kernel(const u32x4 *__restrict__ buf,
+                                                        int frags_per_wave, int reps,
+                                                        u32x4 *out)
+{
+    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+    const u32x4 *p = buf + (size_t)wave * frags_per_wave * 64 + lane;
+    u32x4 acc = {0u, 0u, 0u, 0u};
+    for (int r = 0; r < reps; ++r) {
+        u32x4 b[SD];
+#pragma unroll
+        for (int d = 0; d < SD; ++d) b[d] = p[(size_t)(d % frags_per_wave) * 64];
+        for (int f0 = 0; f0 < frags_per_wave; f0 += SD) {
+#pragma unroll
+            for (int d = 0; d < SD; ++d) {
+                acc ^= b[d];
+                int nf = f0 + d + SD;
+                while (nf >= frags_per_wave) nf -= frags_per_wave;
+                b[d] = p[(size_t)nf * 64];
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < SD; ++d) acc ^= b[d];
+    }
+    if (acc.x == 0x12345678u && acc.y == 0x9abcdef0u) out[blockIdx.x * 512 + threadIdx.x] = acc;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tpp_mfma_issue(int blocks, int iters, float *out, void *stream)
+{
+    if (blocks < 1 || iters < 1 || !out) return -1;
+    hipLaunchKernelGGL(mfma_issue_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, iters,
+                       out);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+double tpp_mfma_issue_flops(int blocks, int iters)
+{
+    return (double)blocks * 4.0 * iters * NACC * (2.0 * 16 * 16 * 32);
+}
+
+int tpp_mfma32_issue(int blocks, int iters, float *out, void *stream)
+{
+    if (blocks < 1 || iters < 1 || !out) return -1;
+    hipLaunchKernelGGL(mfma32_issue_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream,
+                       iters, out);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+double tpp_mfma32_issue_flops(int blocks, int iters)
+{
+    return (double)blocks * 4.0 * iters * 4 * (2.0 * 32 * 32 * 16);
+}
+
+int tpp_l2_stream(const void *buf, size_t buf_bytes, int frags_per_wave, int reps, int blocks,
+                  void *out, void *stream)
+{
+    if (!buf || !out || frags_per_wave < 1 || reps < 1 || blocks < 1) return -1;
+    if ((size_t)8 * frags_per_wave * 1024 > buf_bytes) return -1;
+    hipLaunchKernelGGL(l2_stream_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream,
+                       (const u32x4 *)buf, frags_per_wave, reps, (u32x4 *)out);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+}  // extern "C"

@@ -26,6 +26,11 @@ Times, with HIP events on the launch stream:
     per call on a 390 x 4,096 trajectory; algorithmic FLOPs per update
     2B (2 S H1 + 3 H1 H2 + 3 H2 n + 2 S C1 + 3 C1 C2 + 3 C2) (forward of
     both networks, weight gradients, and input gradients except layer 1's);
+  * probes: the device ceilings the roofline figures are read against,
+    from libtpprobe.so: the dense bf16 MFMA issue rate (back-to-back
+    v_mfma_f32_16x16x32_bf16 or v_mfma_f32_32x32x16_bf16 on register
+    operands, 4 workgroups of four waves per CU) and the L2 -> CU stream one CU can pull in the rollout's
+    weight-stream pattern (256 workgroups, one per CU, and 8 workgroups);
   * copy: a plain device-to-device copy of 1 GiB (the reference kernel used
     to calibrate HBM byte counters: FETCH_SIZE and WRITE_SIZE of this copy
     should each read 1 GiB per launch).
@@ -70,7 +75,7 @@ def main():
     ap.add_argument("--iters", type=int, default=20)
     ap.add_argument("--only", default=None,
                     choices=["env_step", "gae", "critic", "metrics", "evolution", "learner",
-                             "copy"])
+                             "probes", "copy"])
     args = ap.parse_args()
     sys.path.insert(0, __file__.rsplit("/", 2)[0])
     import workloads as W
@@ -237,6 +242,40 @@ def main():
                           "mfma_frac": flops / sec / 1e12 / PEAK_BF16_TFLOPS, "P": P}
         del obs, act, logp, adv, ret, params, m, v, idx, ws
         torch.cuda.empty_cache()
+
+    if args.only in (None, "probes"):
+        import ctypes as C
+        import os
+        pl = C.CDLL(os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpprobe.so"))
+        pl.tpp_mfma_issue.argtypes = [C.c_int, C.c_int, C.c_void_p, C.c_void_p]
+        pl.tpp_mfma_issue_flops.restype = C.c_double
+        pl.tpp_mfma_issue_flops.argtypes = [C.c_int, C.c_int]
+        pl.tpp_l2_stream.argtypes = [C.c_void_p, C.c_size_t, C.c_int, C.c_int, C.c_int,
+                                     C.c_void_p, C.c_void_p]
+        sp = stream.cuda_stream
+        blocks, iters = 1024, 4096
+        sink = torch.empty(blocks * 256, device=dev)
+        sec = _time(lambda: pl.tpp_mfma_issue(blocks, iters, sink.data_ptr(), sp), 5, stream)
+        fl = pl.tpp_mfma_issue_flops(blocks, iters)
+        probes = {"mfma_16x16x32_bf16_TFLOPs": fl / sec / 1e12,
+                  "mfma_16x16x32_frac_of_2500": fl / sec / 1e12 / PEAK_BF16_TFLOPS}
+        pl.tpp_mfma32_issue.argtypes = [C.c_int, C.c_int, C.c_void_p, C.c_void_p]
+        pl.tpp_mfma32_issue_flops.restype = C.c_double
+        pl.tpp_mfma32_issue_flops.argtypes = [C.c_int, C.c_int]
+        sec = _time(lambda: pl.tpp_mfma32_issue(blocks, iters // 2, sink.data_ptr(), sp), 5,
+                    stream)
+        fl = pl.tpp_mfma32_issue_flops(blocks, iters // 2)
+        probes["mfma_32x32x16_bf16_TFLOPs"] = fl / sec / 1e12
+        probes["mfma_32x32x16_frac_of_2500"] = fl / sec / 1e12 / PEAK_BF16_TFLOPS
+        fpw, reps = 200, 20
+        buf = torch.ones(8 * fpw * 1024 // 4 + 16384, dtype=torch.int32, device=dev)
+        for nb in (256, 8):
+            so = torch.empty(nb * 512 * 4, dtype=torch.int32, device=dev)
+            sec = _time(lambda: pl.tpp_l2_stream(buf.data_ptr(), buf.numel() * 4, fpw, reps, nb,
+                                                 so.data_ptr(), sp), 5, stream)
+            per_cu = 8 * fpw * 1024 * reps / sec / 1e9
+            probes[f"l2_stream_GBs_per_CU_{nb}wg"] = per_cu
+        out["probes"] = probes
 
     if args.only in (None, "copy"):
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
