@@ -294,8 +294,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
 // LDS (rows padded by 16 bytes so the fragment reads of 16 rows fall in
 // different banks), loaded with whole-line accesses (each wave instruction
 // reads 4 rows x 256 contiguous bytes), GEMM_LD chunks ahead in registers
-// (deeper prefetch measured slower); the four waves read their 32x32
-// blocks' fragments from LDS.
+// (deeper prefetch measured slower); eight waves (a 2 x 4 grid of 32x16
+// blocks: twice the waves of a 2 x 2 grid of 32x32 blocks, for latency
+// hiding, at 1.5x the LDS fragment reads) read their fragments from LDS.
 #ifndef GEMM_LD
 #define GEMM_LD 2                     // chunks in flight in registers
 #endif
@@ -305,55 +306,61 @@ constexpr int LTILE = GT * LROW;      // one operand's chunk (bf16)
 
 typedef uint32_t v4u_t __attribute__((ext_vector_type(4)));
 
+constexpr int LWAVES = 8;              // waves per workgroup: 2 (rows) x 4 (columns)
+constexpr int LTHREADS = LWAVES * WAVE;
+
+// Chunk loop: LTHREADS threads move a 64 x 128 chunk of A and one of B
+// (thread t: rows (t / 16) + 32 j, 16-byte piece t % 16); wave (wm, wn)
+// multiplies rows 32 wm .. +31 by columns 16 wn .. +15 (two 16x16 tiles).
 template <int NC>
 __device__ __forceinline__ void lds_kloop(const __bf16 *const ga, const __bf16 *const gb,
                                           int64_t lda, int64_t ldb, int Mr, int Nr,
-                                          __bf16 *smem, floatx4 acc[2][2])
+                                          __bf16 *smem, floatx4 acc[2])
 {
     const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
     const int r16 = lane & 15, kq = lane >> 4;
-    // loader: thread t moves 16 bytes of rows (t / 16) + 16 j, piece t % 16
     const int lrow = tid >> 4, lpiece = tid & 15;
-    const __bf16 *la[4], *lb[4];
+    const __bf16 *la[2], *lb[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        la[j] = ga + (size_t)min(lrow + 16 * j, Mr - 1) * lda + lpiece * 8;
-        lb[j] = gb + (size_t)min(lrow + 16 * j, Nr - 1) * ldb + lpiece * 8;
+    for (int j = 0; j < 2; ++j) {
+        la[j] = ga + (size_t)min(lrow + 32 * j, Mr - 1) * lda + lpiece * 8;
+        lb[j] = gb + (size_t)min(lrow + 32 * j, Nr - 1) * ldb + lpiece * 8;
     }
     constexpr int D = NC < GEMM_LD ? NC : GEMM_LD;   // chunks in flight in registers
-    v4u_t ra[D][4], rb[D][4];
-    auto load = [&](v4u_t (&xa)[4], v4u_t (&xb)[4], int c) {
+    v4u_t ra[D][2], rb[D][2];
+    auto load = [&](v4u_t (&xa)[2], v4u_t (&xb)[2], int c) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < 2; ++j) {
             xa[j] = *(const v4u_t *)(la[j] + c * LBK);
             xb[j] = *(const v4u_t *)(lb[j] + c * LBK);
         }
     };
-    auto store = [&](const v4u_t (&xa)[4], const v4u_t (&xb)[4], int buf) {
+    auto store = [&](const v4u_t (&xa)[2], const v4u_t (&xb)[2], int buf) {
         __bf16 *As = smem + buf * 2 * LTILE, *Bs = As + LTILE;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            *(v4u_t *)(As + (lrow + 16 * j) * LROW + lpiece * 8) = xa[j];
-            *(v4u_t *)(Bs + (lrow + 16 * j) * LROW + lpiece * 8) = xb[j];
+        for (int j = 0; j < 2; ++j) {
+            *(v4u_t *)(As + (lrow + 32 * j) * LROW + lpiece * 8) = xa[j];
+            *(v4u_t *)(Bs + (lrow + 32 * j) * LROW + lpiece * 8) = xb[j];
         }
     };
     static_for<0, D>([&](auto c) { load(ra[c], rb[c], c); });
     store(ra[0], rb[0], 0);
     if constexpr (D < NC) load(ra[0], rb[0], D);
     __syncthreads();
-    const int am = (wave >> 1) * 32, bn = (wave & 1) * 32;
+    const int am = (wave >> 2) * 32, bn = (wave & 3) * 16;
     static_for<0, NC>([&](auto c) {
         constexpr int buf = c & 1;
         const __bf16 *As = smem + buf * 2 * LTILE, *Bs = As + LTILE;
 #pragma unroll
         for (int q = 0; q < LBK / 32; ++q) {
-            bf16x8 fa[2], fb[2];
+            bf16x8 fa[2];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
+            for (int i = 0; i < 2; ++i)
                 fa[i] = *(const bf16x8 *)(As + (am + i * 16 + r16) * LROW + q * 32 + kq * 8);
-                fb[i] = *(const bf16x8 *)(Bs + (bn + i * 16 + r16) * LROW + q * 32 + kq * 8);
-            }
-            mma_2x2(fa, fb, acc);
+            const bf16x8 fb = *(const bf16x8 *)(Bs + (bn + r16) * LROW + q * 32 + kq * 8);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb, acc[i], 0, 0, 0);
         }
         if constexpr (c + 1 < NC) {
             // chunk c + 1 sits in register set (c + 1) % D; refill it with c + 1 + D
@@ -365,7 +372,7 @@ __device__ __forceinline__ void lds_kloop(const __bf16 *const ga, const __bf16 *
     });
 }
 
-__global__ __launch_bounds__(256, 2) void gemm_lds_kernel(GemmBatch gb)
+__global__ __launch_bounds__(LTHREADS, 2) void gemm_lds_kernel(GemmBatch gb)
 {
     __shared__ __attribute__((aligned(16))) __bf16 smem[2 * 2 * LTILE];
     int t = blockIdx.x;
@@ -378,11 +385,9 @@ __global__ __launch_bounds__(256, 2) void gemm_lds_kernel(GemmBatch gb)
     const int r16 = lane & 15, kq = lane >> 4;
     const __bf16 *ga = (const __bf16 *)P.A + (size_t)m0 * P.lda;
     const __bf16 *gbp = (const __bf16 *)P.B + (size_t)n0 * P.ldb;
-    floatx4 acc[2][2];
+    floatx4 acc[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < 2; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
     const int Mr = P.M - m0, Nr = P.N - n0;     // rows left in this tile (>= 1)
     switch (P.K / LBK) {
     case 1: lds_kloop<1>(ga, gbp, P.lda, P.ldb, Mr, Nr, smem, acc); break;
@@ -390,14 +395,12 @@ __global__ __launch_bounds__(256, 2) void gemm_lds_kernel(GemmBatch gb)
     case 8: lds_kloop<8>(ga, gbp, P.lda, P.ldb, Mr, Nr, smem, acc); break;
     default: break;   // the launcher routes other K to gemm_bf16_kernel
     }
-    const int wm = m0 + (wave >> 1) * 32, wn = n0 + (wave & 1) * 32;
+    const int wm = m0 + (wave >> 2) * 32, wn = n0 + (wave & 3) * 16;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-            epi4<true>(P, wm + i * 16 + kq * 4, wn + j * 16 + r16, v);
-        }
+    for (int i = 0; i < 2; ++i) {
+        const float v[4] = {acc[i][0], acc[i][1], acc[i][2], acc[i][3]};
+        epi4<true>(P, wm + i * 16 + kq * 4, wn + r16, v);
+    }
 }
 
 // fp32: 16x16 threads, each a 4x4 block of the 64x64 tile; k-slices of 16
@@ -968,7 +971,7 @@ hipError_t run_gemms(bool bf, std::initializer_list<GemmProb> ps, hipStream_t s)
         staged = staged && gb.p[q].K % LBK == 0 && (nc == 1 || nc == 4 || nc == 8) &&
                  gb.p[q].lda % 8 == 0 && gb.p[q].ldb % 8 == 0;
     }
-    if (staged) hipLaunchKernelGGL(gemm_lds_kernel, dim3(tiles), dim3(256), 0, s, gb);
+    if (staged) hipLaunchKernelGGL(gemm_lds_kernel, dim3(tiles), dim3(LTHREADS), 0, s, gb);
     else if (bf) hipLaunchKernelGGL(gemm_bf16_kernel, dim3(tiles), dim3(256), 0, s, gb);
     else hipLaunchKernelGGL(gemm_f32_kernel, dim3(tiles), dim3(256), 0, s, gb);
     return hipGetLastError();
