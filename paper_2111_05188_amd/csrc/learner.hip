@@ -533,110 +533,189 @@ __global__ __launch_bounds__(256) void gather_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Loss, per row (one wave per row): log-probability, ratio, clip decision,
-// the critic's value, and the per-row factors the gradient tiles use.
-//   row_out[0][i] = dL/dlogp_i (zero on the clipped branch)
-//   row_out[1][i] = dL/dV_i = 2 (V_i - R_i) / B
-//   row_out[2..4][i] = surrogate, squared error, |rho - 1| > clip
+// Loss and its gradient, one launch over [B] x [vsplit + C2] virtual
+// columns in 64 x 64 tiles (vsplit = n_pad rounded up to a whole tile).
+// Each workgroup first takes its 64 rows' terms: four threads per row,
+// partial sums in fp64 combined in a fixed order, so every column tile of
+// the same rows gets the same values:
+//   actor tiles: log-probability, ratio, clip decision, g_i = dL/dlogp_i
+//     (zero on the clipped branch);
+//   critic tiles: V_i and dL/dV_i = 2 (V_i - R_i) / B.
+// The first actor tile of a row block writes row_out[0], [2], [4]
+// (g, surrogate, |rho - 1| > clip), the first critic tile row_out[1], [3]
+// (dL/dV, squared error).  Then the tile: columns < vsplit give dmu
+// (row-major and transposed, zero for n <= col < n_pad) and the log-std
+// terms (transposed), the rest the critic's second pre-activation gradient
+// dV wc3 (1 - hc2^2) (row-major and transposed).  Every global load of a
+// phase is issued before the first use, with clamped addresses.
 // ---------------------------------------------------------------------------
 template <bool BF>
-__global__ __launch_bounds__(256) void loss_row_kernel(
+__global__ __launch_bounds__(256) void loss_kernel(
     const float *__restrict__ mu, const float *__restrict__ Ag, const float *__restrict__ row_in,
     const Elem<BF> *__restrict__ Hc2, const float *__restrict__ params, int64_t ols,
-    int64_t owc3, int64_t obc3, int B, int n, int C2, float clip, float *__restrict__ row_out)
-{
-    const int lane = threadIdx.x % WAVE;
-    const int i = blockIdx.x * 4 + threadIdx.x / WAVE;
-    if (i >= B) return;
-    const float *ls = params + ols;
-    double lp = 0.0;
-    for (int k = lane; k < n; k += WAVE) {
-        const float d = Ag[(size_t)i * n + k] - mu[(size_t)i * n + k];
-        const float inv = expf(-2.0f * ls[k]);
-        lp += (double)(-0.5f * (d * d * inv) - ls[k]);
-    }
-    lp = wave_sum(lp) - 0.5 * (double)n * (double)LN_2PI_F;
-    const float *wc3 = params + owc3;
-    double v = 0.0;
-    for (int k = lane; k < C2; k += WAVE)
-        v += (double)((float)to_elem<BF>(wc3[k]) * (float)Hc2[(size_t)i * C2 + k]);
-    v = wave_sum(v);
-    if (lane != 0) return;
-    const float V = (float)(v + (double)params[obc3]);
-    const double lp_old = row_in[i], A = row_in[B + i], R = row_in[2 * B + i];
-    const double rho = exp(lp - lp_old);
-    const double rc = fmin(fmax(rho, 1.0 - clip), 1.0 + clip);
-    const bool unclipped = rho * A <= rc * A;
-    row_out[i] = unclipped ? (float)(-A * rho / (double)B) : 0.0f;
-    const double e = (double)V - R;
-    row_out[B + i] = (float)(2.0 * e / (double)B);
-    row_out[2 * B + i] = (float)(unclipped ? rho * A : rc * A);
-    row_out[3 * B + i] = (float)(e * e);
-    row_out[4 * B + i] = fabs(rho - 1.0) > (double)clip ? 1.0f : 0.0f;
-}
-
-// Gradient tiles over [B] x [vsplit + C2] virtual columns (64 x 64 through
-// LDS; vsplit = n_pad rounded up to a whole tile): columns < vsplit give
-// dmu (row-major and transposed, zero for n <= col < n_pad) and the
-// log-std terms (transposed), the rest the critic's second pre-activation
-// gradient dV wc3 (1 - hc2^2) (row-major and transposed).
-template <bool BF>
-__global__ __launch_bounds__(256) void loss_tile_kernel(
-    const float *__restrict__ mu, const float *__restrict__ Ag, const float *__restrict__ row_out,
-    const Elem<BF> *__restrict__ Hc2, const float *__restrict__ params, int64_t ols,
-    int64_t owc3, int B, int n, int n_pad, int vsplit, int C2, Elem<BF> *__restrict__ dMU,
-    Elem<BF> *__restrict__ dMUt, float *__restrict__ LSt, Elem<BF> *__restrict__ dZc2,
-    Elem<BF> *__restrict__ dZc2t)
+    int64_t owc3, int64_t obc3, int B, int n, int n_pad, int vsplit, int C2, float clip,
+    float *__restrict__ row_out, Elem<BF> *__restrict__ dMU, Elem<BF> *__restrict__ dMUt,
+    float *__restrict__ LSt, Elem<BF> *__restrict__ dZc2, Elem<BF> *__restrict__ dZc2t)
 {
     __shared__ float t1[64][65];
     __shared__ float t2[64][65];
-    __shared__ float s_row[64];   // dL/dlogp (actor tiles) or dL/dV (critic tiles)
-    __shared__ float s_col[64];   // 1/sigma^2 (actor) or the critic head's weight
+    __shared__ float s_row[64];    // g (actor tiles) or dL/dV (critic tiles)
+    __shared__ float s_col[64];    // 1/sigma^2 (actor) or the critic head's weight
+    __shared__ float s_inv[128];   // 1/sigma_k^2, k < n (actor tiles)
+    __shared__ float s_ls[128];    // log sigma_k, k < n
     const int i0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
     const bool actor = c0 < vsplit;
     const int tid = threadIdx.x;
     const float *ls = params + ols, *wc3 = params + owc3;
-    if (tid < 64) {
-        const int i = i0 + tid;
-        s_row[tid] = i < B ? (actor ? row_out[i] : row_out[B + i]) : 0.f;
-    } else if (tid < 128) {
-        const int col = c0 + tid - 64;
-        float v = 0.f;
+    {
+        // every load of the set-up at once (clamped), then the role's values
+        const int col = c0 + (tid & 63);
+        const float l_k = ls[min(tid & 127, n - 1)];
+        const float l_c = ls[min(col, n - 1)];
+        const float w_c = wc3[min(max(col - vsplit, 0), C2 - 1)];
         if (actor) {
-            if (col < n) v = expf(-2.0f * ls[col]);
-        } else if (col - vsplit < C2) {
-            v = (float)to_elem<BF>(wc3[col - vsplit]);
+            if (tid < 128) {
+                if (tid < n) s_inv[tid] = expf(-2.0f * l_k);
+            } else if (tid - 128 < n) {
+                s_ls[tid - 128] = l_k;
+            }
         }
-        s_col[tid - 64] = v;
+        if (tid < 64)
+            s_col[tid] = actor ? (col < n ? expf(-2.0f * l_c) : 0.f)
+                               : (col - vsplit < C2 ? (float)to_elem<BF>(w_c) : 0.f);
     }
     __syncthreads();
+
+    // row terms: thread (r = tid / 4, sub = tid % 4)
+    {
+        const int r = tid >> 2, sub = tid & 3;
+        const int i = min(i0 + r, B - 1);
+        const float lp_old = row_in[i], A_i = row_in[B + i], R_i = row_in[2 * B + i];
+        double part = 0.0;
+        if (actor) {
+            // log N(a; mu, sigma) over k = sub + 4 j (n <= 128)
+            float x[32], y[32];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        const int q = tid + 256 * j;
-        const int r = q >> 6, c = q & 63;
-        const int i = i0 + r, col = c0 + c;
-        float a = 0.f, b = 0.f;
-        if (i < B) {
-            if (actor) {
-                if (col < n) {
-                    const float d = Ag[(size_t)i * n + col] - mu[(size_t)i * n + col];
-                    const float inv = s_col[c];
-                    const float g = s_row[r];
-                    a = g * (d * inv);
-                    b = g * (d * d * inv - 1.0f);
+            for (int j = 0; j < 32; ++j) {
+                const int k = min(sub + 4 * j, n - 1);
+                x[j] = Ag[(size_t)i * n + k];
+                y[j] = mu[(size_t)i * n + k];
+            }
+#pragma unroll
+            for (int j = 0; j < 32; ++j) {
+                const int k = sub + 4 * j;
+                if (k < n) {
+                    const float d = x[j] - y[j];
+                    part += (double)(-0.5f * (d * d * s_inv[k]) - s_ls[k]);
                 }
-                if (col < n_pad) dMU[(size_t)i * n_pad + col] = to_elem<BF>(a);
+            }
+        } else {
+            // V = wc3 . hc2 over 8-element pieces q = sub + 4 j (C2 % 32 == 0)
+            const Elem<BF> *h = Hc2 + (size_t)i * C2;
+            const int nq = C2 / 32;
+#pragma unroll 4
+            for (int j = 0; j < nq; ++j) {
+                const int k0 = (sub + 4 * j) * 8;
+                float hv[8];
+                if constexpr (BF) {
+                    const bf16x8 v = *(const bf16x8 *)(h + k0);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) hv[e] = (float)v[e];
+                } else {
+                    const floatx4 v0 = *(const floatx4 *)(h + k0);
+                    const floatx4 v1 = *(const floatx4 *)(h + k0 + 4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        hv[e] = v0[e];
+                        hv[4 + e] = v1[e];
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    part += (double)((float)to_elem<BF>(wc3[k0 + e]) * hv[e]);
+            }
+        }
+        // ((s0 + s1) + (s2 + s3)): the same sum in all four lanes
+        part += __shfl_xor(part, 1);
+        part += __shfl_xor(part, 2);
+        if (sub == 0) {
+            const bool live = i0 + r < B;
+            const int ii = i0 + r;
+            if (actor) {
+                const double lp = part - 0.5 * (double)n * (double)LN_2PI_F;
+                const double A = A_i;
+                const double rho = exp(lp - (double)lp_old);
+                const double rc = fmin(fmax(rho, 1.0 - clip), 1.0 + clip);
+                const bool unclipped = rho * A <= rc * A;
+                const float g = unclipped ? (float)(-A * rho / (double)B) : 0.0f;
+                s_row[r] = live ? g : 0.f;
+                if (live && blockIdx.y == 0) {
+                    row_out[ii] = g;
+                    row_out[2 * B + ii] = (float)(unclipped ? rho * A : rc * A);
+                    row_out[4 * B + ii] = fabs(rho - 1.0) > (double)clip ? 1.0f : 0.0f;
+                }
             } else {
-                const int k = col - vsplit;
-                if (k < C2) {
-                    const float h = (float)Hc2[(size_t)i * C2 + k];
-                    a = s_row[r] * s_col[c] * (1.0f - h * h);
-                    dZc2[(size_t)i * C2 + k] = to_elem<BF>(a);
+                const float V = (float)(part + (double)params[obc3]);
+                const double e = (double)V - (double)R_i;
+                const float dV = (float)(2.0 * e / (double)B);
+                s_row[r] = live ? dV : 0.f;
+                if (live && c0 == vsplit) {
+                    row_out[B + ii] = dV;
+                    row_out[3 * B + ii] = (float)(e * e);
                 }
             }
         }
-        t1[r][c] = a;
-        t2[r][c] = b;
+    }
+    __syncthreads();
+
+    // the tile, row-major: loads first, then values and stores
+    if (actor) {
+        float va[16], vb[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int q = tid + 256 * j;
+            const int i = min(i0 + (q >> 6), B - 1), k = min(c0 + (q & 63), n - 1);
+            va[j] = Ag[(size_t)i * n + k];
+            vb[j] = mu[(size_t)i * n + k];
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int q = tid + 256 * j;
+            const int r = q >> 6, c = q & 63;
+            const int i = i0 + r, col = c0 + c;
+            float a = 0.f, b = 0.f;
+            if (col < n) {
+                const float d = va[j] - vb[j];
+                const float inv = s_col[c];
+                const float g = s_row[r];
+                a = g * (d * inv);
+                b = g * (d * d * inv - 1.0f);
+            }
+            if (i < B && col < n_pad) dMU[(size_t)i * n_pad + col] = to_elem<BF>(a);
+            t1[r][c] = a;
+            t2[r][c] = b;
+        }
+    } else {
+        Elem<BF> vh[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int q = tid + 256 * j;
+            const int i = min(i0 + (q >> 6), B - 1), k = min(c0 - vsplit + (q & 63), C2 - 1);
+            vh[j] = Hc2[(size_t)i * C2 + k];
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int q = tid + 256 * j;
+            const int r = q >> 6, c = q & 63;
+            const int i = i0 + r, k = c0 - vsplit + c;
+            float a = 0.f;
+            if (k < C2) {
+                const float h = (float)vh[j];
+                a = s_row[r] * s_col[c] * (1.0f - h * h);
+                if (i < B) dZc2[(size_t)i * C2 + k] = to_elem<BF>(a);
+            }
+            t1[r][c] = a;
+        }
     }
     __syncthreads();
 #pragma unroll
@@ -1120,29 +1199,21 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             p.ldo = L.n;
             if ((e = run_gemms(bf, {p}, s)) != hipSuccess) return e;
         }
-        // loss rows, then gradient tiles
-        if (bf)
-            hipLaunchKernelGGL(loss_row_kernel<true>, dim3(cdiv(B, 4)), dim3(256), 0, s, MU, Ag,
-                               row_in, (const __bf16 *)Hc2, prm, L.ols, L.owc3, L.obc3, B, L.n,
-                               L.C2, a.clip, row_out);
-        else
-            hipLaunchKernelGGL(loss_row_kernel<false>, dim3(cdiv(B, 4)), dim3(256), 0, s, MU, Ag,
-                               row_in, (const float *)Hc2, prm, L.ols, L.owc3, L.obc3, B, L.n,
-                               L.C2, a.clip, row_out);
+        // loss and its gradient tiles: actor columns [0, n_pad) in whole
+        // tiles, then the critic's C2 columns
         {
-            // actor columns [0, n_pad) in whole tiles, then the critic's C2 columns
             const int ntA = cdiv(L.n_pad, 64);
             const dim3 grid(cdiv(B, 64), ntA + cdiv(L.C2, 64));
             if (bf)
-                hipLaunchKernelGGL(loss_tile_kernel<true>, grid, dim3(256), 0, s, MU, Ag, row_out,
-                                   (const __bf16 *)Hc2, prm, L.ols, L.owc3, B, L.n, L.n_pad,
-                                   ntA * 64, L.C2, (__bf16 *)dMU, (__bf16 *)dMUt, LSt,
-                                   (__bf16 *)dZc2, (__bf16 *)dZc2t);
+                hipLaunchKernelGGL(loss_kernel<true>, grid, dim3(256), 0, s, MU, Ag, row_in,
+                                   (const __bf16 *)Hc2, prm, L.ols, L.owc3, L.obc3, B, L.n,
+                                   L.n_pad, ntA * 64, L.C2, a.clip, row_out, (__bf16 *)dMU,
+                                   (__bf16 *)dMUt, LSt, (__bf16 *)dZc2, (__bf16 *)dZc2t);
             else
-                hipLaunchKernelGGL(loss_tile_kernel<false>, grid, dim3(256), 0, s, MU, Ag, row_out,
-                                   (const float *)Hc2, prm, L.ols, L.owc3, B, L.n, L.n_pad,
-                                   ntA * 64, L.C2, (float *)dMU, (float *)dMUt, LSt, (float *)dZc2,
-                                   (float *)dZc2t);
+                hipLaunchKernelGGL(loss_kernel<false>, grid, dim3(256), 0, s, MU, Ag, row_in,
+                                   (const float *)Hc2, prm, L.ols, L.owc3, L.obc3, B, L.n,
+                                   L.n_pad, ntA * 64, L.C2, a.clip, row_out, (float *)dMU,
+                                   (float *)dMUt, LSt, (float *)dZc2, (float *)dZc2t);
         }
         // backward stage A: dW3, dZ2 (actor); dWc2, dZc1 (critic)
         {
