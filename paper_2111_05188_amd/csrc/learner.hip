@@ -543,7 +543,8 @@ __global__ __launch_bounds__(256) void gather_kernel(
 //   critic tiles: V_i and dL/dV_i = 2 (V_i - R_i) / B.
 // The first actor tile of a row block writes row_out[0], [2], [4]
 // (g, surrogate, |rho - 1| > clip), the first critic tile row_out[1], [3]
-// (dL/dV, squared error).  Then the tile: columns < vsplit give dmu
+// (dL/dV, squared error); the first actor tile of all writes
+// row_out[5 B] = sum_k log sigma_k.  Then the tile: columns < vsplit give dmu
 // (row-major and transposed, zero for n <= col < n_pad) and the log-std
 // terms (transposed), the rest the critic's second pre-activation gradient
 // dV wc3 (1 - hc2^2) (row-major and transposed).  Every global load of a
@@ -585,6 +586,12 @@ __global__ __launch_bounds__(256) void loss_kernel(
                                : (col - vsplit < C2 ? (float)to_elem<BF>(w_c) : 0.f);
     }
     __syncthreads();
+    if (actor && blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) {
+        // sum_k log sigma_k before this update's Adam step (the entropy)
+        double sl = 0.0;
+        for (int k = 0; k < n; ++k) sl += (double)s_ls[k];
+        row_out[5 * B] = (float)sl;
+    }
 
     // row terms: thread (r = tid / 4, sub = tid % 4)
     {
@@ -734,8 +741,15 @@ __global__ __launch_bounds__(256) void loss_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Row sums (one wave per row, fp64 partials, fixed order):
-// dst[r] = scale * sum_b src[r][b] (* w[b]) + add
+// The tail of an update, one launch of two kinds of workgroups:
+//  - blocks [0, mtiles): Adam over 64 x 64 tiles of the weight matrices
+//    (when do_adam), each updated weight written back and rounded into its
+//    row-major operand copy and, through LDS, its transposed copy;
+//  - the rest: row sums, one wave per row (fp64 partials, fixed order),
+//    dst[r] = scale * sum_b src[r][b] (* w[b]) + add; a row that is the
+//    gradient of a bias, log-std or critic-head element (pidx >= 0) also
+//    takes that element's Adam step.  The statistics are rows too.
+// The two kinds touch disjoint memory.
 // ---------------------------------------------------------------------------
 struct RedSeg {
     const void *src;
@@ -748,6 +762,7 @@ struct RedSeg {
     double scale, add;
     int row0;           // first global row of this segment
     int vec;            // rows 16-byte aligned and len a multiple of 16 bytes
+    int64_t pidx;       // flat index of row 0's parameter, or -1
 };
 constexpr int MAX_SEGS = 12;
 struct RedBatch {
@@ -755,11 +770,97 @@ struct RedBatch {
     int ns, total_rows;
 };
 
-__global__ __launch_bounds__(256) void row_reduce_kernel(RedBatch rb)
+struct AdamSeg {
+    int64_t off;        // flat offset of the master
+    int rows, cols;     // master shape
+    int rows_pad, cols_pad;   // copy shape (zero outside the master)
+    void *copy;         // row-major copy [.][ld_copy] at row copy_row0
+    int64_t ld_copy;
+    int copy_row0;
+    void *copyT;        // transposed copy [cols_pad][ld_copyT], or null
+    int64_t ld_copyT;
+    int tiles_c, tile0;
+};
+constexpr int MAX_ASEGS = 5;
+constexpr int AT = 64;              // Adam tile edge
+struct AdamBatch {
+    AdamSeg s[MAX_ASEGS];
+    int ns;
+    float *params, *m, *v;
+    const float *grad;
+    float lr, b1, b2, eps, bc1, bc2;
+    int do_adam;
+};
+
+// One Adam step of one element (the moments and the master written back).
+__device__ __forceinline__ float adam_step(const AdamBatch &ab, int64_t p, float th, float g,
+                                           float m0, float v0)
+{
+    const float m = ab.b1 * m0 + (1.0f - ab.b1) * g;
+    const float v = ab.b2 * v0 + (1.0f - ab.b2) * (g * g);
+    ab.m[p] = m;
+    ab.v[p] = v;
+    const float mh = m / ab.bc1, vh = v / ab.bc2;
+    th = th - ab.lr * (mh / (sqrtf(vh) + ab.eps));
+    ab.params[p] = th;
+    return th;
+}
+
+template <bool BF>
+__device__ __forceinline__ void adam_tile(const AdamBatch &ab, int t, Elem<BF> (*tile)[AT + 1])
+{
+    int si = 0;
+#pragma unroll
+    for (int q = 1; q < MAX_ASEGS; ++q)
+        if (q < ab.ns && t >= ab.s[q].tile0) si = q;
+    const AdamSeg &S = ab.s[si];
+    t -= S.tile0;
+    const int tid = threadIdx.x;
+    const int r0 = (t / S.tiles_c) * AT, c0 = (t % S.tiles_c) * AT;
+    // element j of a thread: row r0 + q / 64, column c0 + q % 64, q = tid + 256 j
+    constexpr int NJ = AT * AT / 256;
+    float th[NJ], gg[NJ], mm[NJ], vv[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int q = tid + 256 * j;
+        const int r = min(r0 + q / AT, S.rows - 1), c = min(c0 + q % AT, S.cols - 1);
+        const int64_t p = S.off + (int64_t)r * S.cols + c;
+        th[j] = ab.params[p];
+        if (ab.do_adam) {
+            gg[j] = ab.grad[p];
+            mm[j] = ab.m[p];
+            vv[j] = ab.v[p];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int q = tid + 256 * j;
+        const int r = r0 + q / AT, c = c0 + q % AT;
+        float w = 0.0f;
+        if (r < S.rows && c < S.cols) {
+            w = th[j];
+            if (ab.do_adam)
+                w = adam_step(ab, S.off + (int64_t)r * S.cols + c, w, gg[j], mm[j], vv[j]);
+        }
+        const Elem<BF> e = to_elem<BF>(w);
+        if (r < S.rows_pad && c < S.cols_pad)
+            ((Elem<BF> *)S.copy)[(size_t)(S.copy_row0 + r) * S.ld_copy + c] = e;
+        tile[q / AT][q % AT] = e;
+    }
+    if (!S.copyT) return;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int q = tid + 256 * j;
+        const int c = c0 + q / AT, r = r0 + q % AT;
+        if (r < S.rows_pad && c < S.cols_pad)
+            ((Elem<BF> *)S.copyT)[(size_t)c * S.ld_copyT + r] = tile[q % AT][q / AT];
+    }
+}
+
+__device__ __forceinline__ void reduce_row(const RedBatch &rb, const AdamBatch &ab, int g)
 {
     const int lane = threadIdx.x % WAVE;
-    const int g = blockIdx.x * 4 + threadIdx.x / WAVE;
-    if (g >= rb.total_rows) return;
     int si = 0;
 #pragma unroll
     for (int q = 1; q < MAX_SEGS; ++q)
@@ -797,104 +898,35 @@ __global__ __launch_bounds__(256) void row_reduce_kernel(RedBatch rb)
     acc = wave_sum(acc);
     if (lane == 0) {
         const double v = S.scale * acc + S.add;
-        if (S.dst64) S.dst64[r] = v;
-        else S.dst[r] = (float)v;
+        if (S.dst64) {
+            S.dst64[r] = v;
+        } else {
+            S.dst[r] = (float)v;
+            if (S.pidx >= 0 && ab.do_adam) {
+                const int64_t p = S.pidx + r;
+                adam_step(ab, p, ab.params[p], (float)v, ab.m[p], ab.v[p]);
+            }
+        }
     }
 }
 
-// ---------------------------------------------------------------------------
-// Adam over the flat vector and the operand copies of the weights.
-// Matrix segments run in 32x32 tiles of the (padded) copy: each element is
-// updated (when do_adam), its master written back, its copy written
-// row-major and, through LDS, transposed.  Vector segments run in chunks.
-// ---------------------------------------------------------------------------
-struct AdamSeg {
-    int64_t off;        // flat offset of the master
-    int rows, cols;     // master shape (vectors: rows = 1)
-    int rows_pad, cols_pad;   // copy shape (zero outside the master)
-    void *copy;         // row-major copy [.][ld_copy] at row copy_row0, or null
-    int64_t ld_copy;
-    int copy_row0;
-    void *copyT;        // transposed copy [cols_pad][ld_copyT], or null
-    int64_t ld_copyT;
-    int tiles_c, tile0;
-};
-constexpr int MAX_ASEGS = 13;
-struct AdamBatch {
-    AdamSeg s[MAX_ASEGS];
-    int ns;
-    float *params, *m, *v;
-    const float *grad;
-    float lr, b1, b2, eps, bc1, bc2;
-    int do_adam;
-};
-
-__device__ __forceinline__ float adam_one(const AdamBatch &ab, int64_t p)
-{
-    float th = ab.params[p];
-    if (!ab.do_adam) return th;
-    const float g = ab.grad[p];
-    const float m = ab.b1 * ab.m[p] + (1.0f - ab.b1) * g;
-    const float v = ab.b2 * ab.v[p] + (1.0f - ab.b2) * (g * g);
-    ab.m[p] = m;
-    ab.v[p] = v;
-    const float mh = m / ab.bc1, vh = v / ab.bc2;
-    th = th - ab.lr * (mh / (sqrtf(vh) + ab.eps));
-    ab.params[p] = th;
-    return th;
-}
-
-// Adam over the flat vector: 4 elements per thread, each access coalesced
-// across the wave.
-__global__ __launch_bounds__(256) void adam_flat_kernel(AdamBatch ab, int64_t P)
-{
-    const int64_t base = (int64_t)blockIdx.x * 1024 + threadIdx.x;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int64_t p = base + j * 256;
-        if (p < P) adam_one(ab, p);
-    }
-}
-
+// Blocks [0, 8 per) take the matrix tiles, XCD-aware: workgroups are
+// dealt round-robin over the 8 XCDs, so block b takes tile (b % 8) per +
+// b / 8 and each XCD walks a contiguous run of tiles (rows of W1 and Wc1
+// are not line-aligned: neighbouring tiles share lines, now in one L2).
 template <bool BF>
-__global__ __launch_bounds__(256) void adam_kernel(AdamBatch ab)
+__global__ __launch_bounds__(256) void adam_tail_kernel(AdamBatch ab, RedBatch rb, int mtiles)
 {
-    __shared__ Elem<BF> tile[32][33];
-    int t = blockIdx.x;
-    int si = 0;
-#pragma unroll
-    for (int q = 1; q < MAX_ASEGS; ++q)
-        if (q < ab.ns && t >= ab.s[q].tile0) si = q;
-    const AdamSeg &S = ab.s[si];
-    t -= S.tile0;
-    const int tid = threadIdx.x;
-    if (!S.copy) {   // vector segment: chunk of 1024 elements
-        const int64_t n = (int64_t)S.rows * S.cols;
-        for (int64_t e = (int64_t)t * 1024 + tid; e < n && e < (int64_t)(t + 1) * 1024; e += 256)
-            adam_one(ab, S.off + e);
+    __shared__ Elem<BF> tile[AT][AT + 1];
+    const int per = (mtiles + 7) / 8;
+    const int b = blockIdx.x;
+    if (b < 8 * per) {
+        const int t = (b % 8) * per + b / 8;
+        if (t < mtiles) adam_tile<BF>(ab, t, tile);
         return;
     }
-    const int r0 = (t / S.tiles_c) * 32, c0 = (t % S.tiles_c) * 32;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int q = tid + 256 * j;
-        const int r = r0 + (q >> 5), c = c0 + (q & 31);
-        float w = 0.0f;
-        if (r < S.rows && c < S.cols) w = adam_one(ab, S.off + (int64_t)r * S.cols + c);
-        const Elem<BF> e = to_elem<BF>(w);
-        if (r < S.rows_pad && c < S.cols_pad)
-            ((Elem<BF> *)S.copy)[(size_t)(S.copy_row0 + r) * S.ld_copy + c] = e;
-        tile[q >> 5][q & 31] = e;
-    }
-    if (!S.copyT) return;
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int q = tid + 256 * j;
-        const int c = c0 + (q >> 5), r = r0 + (q & 31);
-        if (r < S.rows_pad && c < S.cols_pad)
-            ((Elem<BF> *)S.copyT)[(size_t)c * S.ld_copyT + r] = tile[q & 31][q >> 5];
-    }
+    const int g = (b - 8 * per) * 4 + threadIdx.x / WAVE;
+    if (g < rb.total_rows) reduce_row(rb, ab, g);
 }
 
 // Minibatch rows: draw i of update counter c for agent g is word i % 4 of
@@ -996,7 +1028,7 @@ bool ppo_layout(const tp_ppo *c, PpoLayout *L)
     L->wMU = area(4 * B * L->n);
     L->wAg = area(4 * B * L->n);
     L->wRowIn = area(4 * 3 * B);
-    L->wRowOut = area(4 * 5 * B);
+    L->wRowOut = area(4 * (5 * B + 1));
     L->wdMU = area(es * B * L->n_pad);
     L->wdMUt = area(es * L->n_pad * B);
     L->wLSt = area(4 * L->n * B);
@@ -1094,13 +1126,8 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
         g.copyT = copyT;
         g.ld_copyT = ldt;
         g.tile0 = atiles;
-        if (copy) {
-            g.tiles_c = cdiv(cols_pad, 32);
-            atiles += g.tiles_c * cdiv(rows_pad, 32);
-        } else {
-            g.tiles_c = 1;
-            atiles += cdiv(rows * cols, 1024);
-        }
+        g.tiles_c = cdiv(cols_pad, AT);
+        atiles += g.tiles_c * cdiv(rows_pad, AT);
         ab.s[ab.ns++] = g;
     };
     mseg(L.oW1, L.H1, L.S, L.H1, L.Kp, W(L.wWcat1), L.Kp, 0, nullptr, 0);
@@ -1108,31 +1135,22 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
     mseg(L.oW2, L.H2, L.H1, L.H2, L.H1, W(L.wW2), L.H1, 0, W(L.wW2t), L.H2);
     mseg(L.oWc2, L.C2, L.C1, L.C2, L.C1, W(L.wWc2), L.C1, 0, W(L.wWc2t), L.C2);
     mseg(L.oW3, L.n, L.H2, L.n_pad, L.H2, W(L.wW3), L.H2, 0, W(L.wW3t), L.n_pad);
-    // vectors: b1, b2, b3 + log_std (contiguous), bc1, bc2 + wc3 + bc3 (contiguous)
-    mseg(L.ob1, 1, L.H1, 1, L.H1, nullptr, 0, 0, nullptr, 0);
-    mseg(L.ob2, 1, L.H2, 1, L.H2, nullptr, 0, 0, nullptr, 0);
-    mseg(L.ob3, 1, 2 * L.n, 1, 2 * L.n, nullptr, 0, 0, nullptr, 0);
-    mseg(L.obc1, 1, L.C1, 1, L.C1, nullptr, 0, 0, nullptr, 0);
-    mseg(L.obc2, 1, 2 * L.C2 + 1, 1, 2 * L.C2 + 1, nullptr, 0, 0, nullptr, 0);
+    // The vectors (b1, b2, b3, log-std, bc1, bc2, wc3, bc3) take their Adam
+    // steps in the row sums that produce their gradients.
+    const int mtiles = atiles;
 
-    // the operand copies are refreshed by the matrix segments alone
-    AdamBatch refresh = ab;
-    refresh.ns = 5;
-    const int rtiles = ab.s[5].tile0;
-    auto adam = [&](int do_adam, int64_t step) -> hipError_t {
-        if (do_adam) {
-            ab.do_adam = 1;
-            ab.bc1 = (float)(1.0 - pow((double)a.beta1, (double)step));
-            ab.bc2 = (float)(1.0 - pow((double)a.beta2, (double)step));
-            hipLaunchKernelGGL(adam_flat_kernel, dim3((unsigned)((L.P + 1023) / 1024)), dim3(256),
-                               0, s, ab, L.P);
-        }
-        refresh.do_adam = 0;
-        if (bf) hipLaunchKernelGGL(adam_kernel<true>, dim3(rtiles), dim3(256), 0, s, refresh);
-        else hipLaunchKernelGGL(adam_kernel<false>, dim3(rtiles), dim3(256), 0, s, refresh);
+    // Adam (or, with do_adam = 0, only the operand-copy refresh) and the
+    // row sums, one launch
+    auto tail = [&](int do_adam, int64_t step, const RedBatch &rb) -> hipError_t {
+        ab.do_adam = do_adam;
+        ab.bc1 = (float)(1.0 - pow((double)a.beta1, (double)step));
+        ab.bc2 = (float)(1.0 - pow((double)a.beta2, (double)step));
+        const dim3 grid(8 * cdiv(mtiles, 8) + cdiv(rb.total_rows, 4));
+        if (bf) hipLaunchKernelGGL(adam_tail_kernel<true>, grid, dim3(256), 0, s, ab, rb, mtiles);
+        else hipLaunchKernelGGL(adam_tail_kernel<false>, grid, dim3(256), 0, s, ab, rb, mtiles);
         return hipGetLastError();
     };
-    hipError_t e = adam(0, 1);
+    hipError_t e = tail(0, 1, RedBatch{});
     if (e != hipSuccess) return e;
 
     void *X = W(L.wX), *Xt = W(L.wXt), *H1 = W(L.wH1), *H1t = W(L.wH1t);
@@ -1259,14 +1277,18 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             g1.gcols = L.S;
             if ((e = run_gemms(bf, {g1}, s)) != hipSuccess) return e;
         }
-        // row sums: bias, log-std and critic-head gradients; statistics
+        // the tail: Adam over the matrices; row sums of the bias, log-std
+        // and critic-head gradients (each with its element's Adam step) and
+        // of the statistics
         {
             RedBatch rb{};
             int rows = 0;
             auto add = [&](const void *src, int64_t ld, int nrows, int len, int isbf,
-                           const float *w, float *dst, double *dst64, double scale,
+                           const float *w, int64_t pidx, double *dst64, double scale,
                            double addc) {
                 RedSeg g{};
+                g.pidx = pidx;
+                float *dst = pidx >= 0 ? grad + pidx : nullptr;
                 g.src = src;
                 g.ld = ld;
                 g.rows = nrows;
@@ -1284,28 +1306,26 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
                 rows += nrows;
                 rb.s[rb.ns++] = g;
             };
-            add(dZ1t, B, L.H1, B, bf, nullptr, grad + L.ob1, nullptr, 1.0, 0.0);
-            add(at(dZ1t, (size_t)L.H1 * B), B, L.C1, B, bf, nullptr, grad + L.obc1, nullptr, 1.0,
-                0.0);
-            add(dZ2t, B, L.H2, B, bf, nullptr, grad + L.ob2, nullptr, 1.0, 0.0);
-            add(dZc2t, B, L.C2, B, bf, nullptr, grad + L.obc2, nullptr, 1.0, 0.0);
-            add(dMUt, B, L.n, B, bf, nullptr, grad + L.ob3, nullptr, 1.0, 0.0);
-            add(LSt, B, L.n, B, 0, nullptr, grad + L.ols, nullptr, 1.0, -(double)a.ent_coef);
-            add(Hc2t, B, L.C2, B, bf, row_out + B, grad + L.owc3, nullptr, 1.0, 0.0);
-            add(row_out + B, B, 1, B, 0, nullptr, grad + L.obc3, nullptr, 1.0, 0.0);
+            add(dZ1t, B, L.H1, B, bf, nullptr, L.ob1, nullptr, 1.0, 0.0);
+            add(at(dZ1t, (size_t)L.H1 * B), B, L.C1, B, bf, nullptr, L.obc1, nullptr, 1.0, 0.0);
+            add(dZ2t, B, L.H2, B, bf, nullptr, L.ob2, nullptr, 1.0, 0.0);
+            add(dZc2t, B, L.C2, B, bf, nullptr, L.obc2, nullptr, 1.0, 0.0);
+            add(dMUt, B, L.n, B, bf, nullptr, L.ob3, nullptr, 1.0, 0.0);
+            add(LSt, B, L.n, B, 0, nullptr, L.ols, nullptr, 1.0, -(double)a.ent_coef);
+            add(Hc2t, B, L.C2, B, bf, row_out + B, L.owc3, nullptr, 1.0, 0.0);
+            add(row_out + B, B, 1, B, 0, nullptr, L.obc3, nullptr, 1.0, 0.0);
             if (a.stats) {
                 double *st = a.stats + (size_t)u * 4;
-                add(row_out + 2 * B, B, 1, B, 0, nullptr, nullptr, st + 0, -1.0 / B, 0.0);
-                add(prm + L.ols, L.n, 1, L.n, 0, nullptr, nullptr, st + 1, 1.0,
+                add(row_out + 2 * B, B, 1, B, 0, nullptr, -1, st + 0, -1.0 / B, 0.0);
+                // the entropy from the log-std before this update's step
+                add(row_out + 5 * B, 1, 1, 1, 0, nullptr, -1, st + 1, 1.0,
                     0.5 * (1.0 + (double)LN_2PI_F) * L.n);
-                add(row_out + 3 * B, B, 1, B, 0, nullptr, nullptr, st + 2, 1.0 / B, 0.0);
-                add(row_out + 4 * B, B, 1, B, 0, nullptr, nullptr, st + 3, 1.0 / B, 0.0);
+                add(row_out + 3 * B, B, 1, B, 0, nullptr, -1, st + 2, 1.0 / B, 0.0);
+                add(row_out + 4 * B, B, 1, B, 0, nullptr, -1, st + 3, 1.0 / B, 0.0);
             }
             rb.total_rows = rows;
-            hipLaunchKernelGGL(row_reduce_kernel, dim3(cdiv(rows, 4)), dim3(256), 0, s, rb);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
+            if ((e = tail(1, a.step0 + u, rb)) != hipSuccess) return e;
         }
-        if ((e = adam(1, a.step0 + u)) != hipSuccess) return e;
     }
     if (a.grad_out)
         return hipMemcpyAsync(a.grad_out, grad, sizeof(float) * (size_t)L.P,
