@@ -26,12 +26,10 @@
  *     the readings used are listed beside each function.
  *
  * Parity pins (tests that tie this file to the paper and to mathematics
- * rather than to itself) live in tests/test_oracle_*.py.  Two functions have
- * no external value to be pinned against:
- *   - orc_obs: the observation scales are a reading (parity unpinned);
- *   - orc_philox4x32_10: no published known-answer vectors are available
- *     here; it is pinned by an independently written inverse and by
- *     statistics only (conformance to the published KAT: parity unpinned).
+ * rather than to itself) live in tests/test_oracle_*.py.  orc_philox4x32_10
+ * is pinned against ROCm's rocRAND host implementation of the same
+ * generator.  One function has no external value to be pinned against:
+ *   - orc_obs: the observation scales are a reading (parity unpinned).
  */
 #include <math.h>
 #include <stddef.h>

@@ -3,11 +3,13 @@ sampling and log-probability.
 
 * MLP: against numpy fp64 matmul + tanh (a library routine).
 * bf16 round-to-nearest-even: against torch's CPU float32 -> bfloat16 cast.
-* Philox4x32-10 (Salmon et al., SC'11): no published known-answer vectors are
-  available in this environment, so conformance is pinned by (a) an inverse
-  written independently from the round's definition that recovers the
-  counter, and (b) statistics (uniformity, avalanche).  Conformance to the
-  published KAT itself: parity unpinned.
+* Philox4x32-10 (Salmon et al., SC'11): against ROCm's rocRAND host
+  implementation of the same generator (its header-only engine, compiled
+  here with g++ from `tests/philox_rocrand.cpp`), on random and edge-case
+  counters and keys and on the counter patterns the sampling and the
+  minibatch draws use; further, an inverse written independently from the
+  round's definition recovers the counter, and statistics (uniformity,
+  avalanche).
 * Box-Muller normals: moments and a KS test against N(0,1); independence
   across counters.
 * Sampling: sigma -> 0 gives a = mu exactly; logp equals the analytic
@@ -120,6 +122,56 @@ def _philox_inverse(y, key):
         x3 = y2 ^ ((M0 * x0) >> 32) ^ k1
         y0, y1, y2, y3 = x0, x1, x2, x3
     return [y0, y1, y2, y3]
+
+
+ROCRAND_HEADER = "/opt/rocm/include/rocrand/rocrand_philox4x32_10.h"
+
+
+@pytest.fixture(scope="module")
+def rocrand_philox(tmp_path_factory):
+    """Philox4x32-10 words from rocRAND's host engine, for lists of
+    (ctr, key) pairs (four and two 32-bit words)."""
+    import os
+    import shutil
+    import subprocess
+    if not os.path.exists(ROCRAND_HEADER) or shutil.which("g++") is None:
+        pytest.skip("rocRAND headers or g++ not available")
+    src = os.path.join(os.path.dirname(__file__), "philox_rocrand.cpp")
+    exe = str(tmp_path_factory.mktemp("philox") / "philox_rocrand")
+    subprocess.run(["g++", "-O1", "-std=c++17", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                    src, "-o", exe], check=True, capture_output=True)
+
+    def run(cases):
+        lines = "".join(f"{k[0] | k[1] << 32} {c[0] | c[1] << 32} {c[2] | c[3] << 32}\n"
+                        for c, k in cases)
+        out = subprocess.run([exe], input=lines, check=True, capture_output=True, text=True)
+        return [[int(w) for w in ln.split()] for ln in out.stdout.splitlines()]
+    return run
+
+
+def test_philox_matches_rocrand(rocrand_philox):
+    rng = np.random.default_rng(11)
+    edge = [0, 1, 0x7FFFFFFF, 0x80000000, 0xFFFFFFFE, MASK]
+    cases = []
+    for _ in range(1500):
+        ctr = [int(v) for v in rng.integers(0, 2 ** 32, 4, dtype=np.uint64)]
+        key = [int(v) for v in rng.integers(0, 2 ** 32, 2, dtype=np.uint64)]
+        cases.append((ctr, key))
+    for _ in range(300):
+        cases.append(([int(rng.choice(edge)) for _ in range(4)],
+                      [int(rng.choice(edge)) for _ in range(2)]))
+    # the counter patterns of the action noise (i/4, env, step, agent) and of
+    # the minibatch draws (i/4, counter, agent, 0x4D42), key = the seed's halves
+    seed = 0x0123456789ABCDEF
+    key = [seed & MASK, seed >> 32]
+    for q in range(0, 25, 6):
+        for env in (0, 4095, 65535):
+            cases.append(([q, env, 389, 15], key))
+    for q in (0, 255):
+        cases.append(([q, 12479, 3, 0x4D42], key))
+    want = rocrand_philox(cases)
+    got = [[int(w) for w in oracle.philox(c, k)] for c, k in cases]
+    assert got == want
 
 
 def test_philox_inverse_recovers_counter():
