@@ -28,8 +28,8 @@
  * Parity pins (tests that tie this file to the paper and to mathematics
  * rather than to itself) live in tests/test_oracle_*.py.  orc_philox4x32_10
  * is pinned against ROCm's rocRAND host implementation of the same
- * generator.  One function has no external value to be pinned against:
- *   - orc_obs: the observation scales are a reading (parity unpinned).
+ * generator.  orc_obs has its layout and its power-of-two block scaling
+ * pinned; the two scale constants are a reading (parity unpinned).
  */
 #include <math.h>
 #include <stddef.h>
@@ -176,7 +176,8 @@ void orc_normals(uint64_t seed, uint32_t step, uint32_t env, uint32_t agent,
 /* Observation (Section 3, "State space"): [b, p_t, h_t, indicators_t].     */
 /* Scales are a reading (power-of-two, exact): b*cash_scale, p*price_scale,  */
 /* h*share_scale, indicators raw.  Pad positions S..K_pad-1 are zero.        */
-/* parity unpinned (no value in the paper fixes the scales).                 */
+/* Layout and power-of-two scaling pinned; the two constants: parity        */
+/* unpinned (no value in the paper fixes them).                              */
 /* ------------------------------------------------------------------------ */
 
 static const float *price_row(const orc_market *m, int64_t t)

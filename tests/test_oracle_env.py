@@ -307,3 +307,74 @@ def test_env_without_next_row_is_not_stepped():
         r, nb, h1, t1, _ = oracle.env_step_one(m, c, 100.0, [3, 4], t,
                                                actions_for([5, -5], 64))
         assert np.isnan(r) and nb == 100.0 and list(h1) == [3, 4] and t1 == t
+
+
+# ----------------------------------------------------------- observation
+
+def test_observation_layout_and_power_of_two_scales():
+    """The state of Section 3 ("State space") is the balance, the prices,
+    the holdings and the indicators.  Pinned without the scale constants:
+    perturbing one state component moves exactly one observation entry, at
+    [balance | n prices | n holdings | n*I indicators, stock-major | zero
+    padding]; each block scales its inputs by one power of two, the same for
+    every stock (so the observation is exact); indicators enter unscaled;
+    the bf16 observation is torch's RNE rounding of the fp32 one.  Which
+    powers of two is a reading (the paper gives none)."""
+    import torch
+    rng = np.random.default_rng(5)
+    n, nI, rows = 5, 3, 4
+    S = 1 + 2 * n + n * nI
+    K_pad = 32
+    prices = np.ldexp(rng.integers(1 << 10, 1 << 20, (rows, n)), rng.integers(-10, 4, (rows, n)))
+    prices = np.clip(prices, 0.25, 8191.0).astype(np.float32)
+    ind = rng.normal(0, 3, (rows, n, nI)).astype(np.float32)
+    c = ecfg()
+    cash = 765432.0                                  # exact in fp32
+    shares = rng.integers(0, 5000, n).astype(np.int32)
+
+    def obs(p=prices, x=ind, b=cash, h=shares, t=2, bf16=False):
+        return oracle.obs(oracle.market(p, x), c, t, b, h, K_pad, bf16)
+
+    base = obs()
+    assert base.shape == (K_pad,) and (base[S:] == 0).all()
+    # one component -> one entry
+    moved = []
+    moved.append(np.flatnonzero(obs(b=cash + 4096.0) != base))
+    for i in range(n):
+        p2 = prices.copy()
+        p2[2, i] *= 2
+        moved.append(np.flatnonzero(obs(p=p2) != base))
+    for i in range(n):
+        h2 = shares.copy()
+        h2[i] += 7
+        moved.append(np.flatnonzero(obs(h=h2) != base))
+    for i in range(n):
+        for k in range(nI):
+            x2 = ind.copy()
+            x2[2, i, k] += 1.0
+            moved.append(np.flatnonzero(obs(x=x2) != base))
+    assert [list(m) for m in moved] == [[j] for j in range(S)]
+    # other market rows do not enter the observation of row t
+    p3, x3 = prices.copy(), ind.copy()
+    p3[[0, 1, 3]] *= 2
+    x3[[0, 1, 3]] += 1
+    assert np.array_equal(obs(p=p3, x=x3), base)
+
+    def pow2_ratio(num, den):
+        r = np.asarray(num, np.float64) / np.asarray(den, np.float64)
+        e = np.log2(r)
+        assert np.all(r > 0) and np.all(e == np.round(e)), r
+        return set(np.round(e).astype(int).tolist())
+
+    # one power of two per block, shared by every stock, row and value
+    e_cash = pow2_ratio([obs(b=b)[0] for b in (cash, 1.0, 3.0 * 2 ** 20, 123456.0)],
+                        [cash, 1.0, 3.0 * 2 ** 20, 123456.0])
+    e_p = pow2_ratio(np.concatenate([obs(t=t)[1:1 + n] for t in range(rows)]), prices.ravel())
+    nz = shares != 0
+    e_h = pow2_ratio(base[1 + n:1 + 2 * n][nz], shares[nz])
+    assert len(e_cash) == 1 and len(e_p) == 1 and len(e_h) == 1
+    assert np.array_equal(np.concatenate([obs(t=t)[1 + 2 * n:S] for t in range(rows)]),
+                          ind.reshape(rows, -1).ravel())
+    # bf16 = RNE of the fp32 observation
+    want = torch.from_numpy(base).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(obs(bf16=True), want)
