@@ -390,6 +390,34 @@ int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v
                   double *stats, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * tp_ppo_update_agents -- tp_ppo_update for n_agents independent learners
+ * in one call (the population's agents, and the pods of an agent, train
+ * separately between fusions: Section 4.4).  Every launch of an update
+ * covers all agents, so small minibatches still fill the device.
+ *   n_agents       1 .. 1024;
+ *   agent_stride   floats from one agent's params / adam_m / adam_v to the
+ *                  next (>= P; ignored for one agent): the flat [A][P]
+ *                  layout has agent_stride = P;
+ *   idx            [n_agents][n_updates][B] int64 device row indices into
+ *                  the shared trajectory arrays (each agent draws its own
+ *                  rows, e.g. from its envs with tp_minibatch_rows);
+ *   grad           optional [n_agents][P]; stats optional
+ *                  [n_agents][n_updates][4];
+ *   workspace      >= n_agents * tp_ppo_workspace_bytes(cfg), 256-byte
+ *                  aligned; agent a uses the a-th slice.
+ * Agent a's results equal those of tp_ppo_update on its own arrays, bit
+ * for bit.  Returns TP_EINVAL as tp_ppo_update does, and for n_agents out
+ * of range or agent_stride < P.
+ */
+int tp_ppo_update_agents(const tp_ppo *cfg, int32_t n_agents, int64_t agent_stride,
+                         float *params, float *adam_m, float *adam_v, int64_t step0,
+                         int32_t n_updates, const void *obs, int64_t ld_obs,
+                         const float *action, const float *logp, const float *adv,
+                         const float *ret, int64_t rows, const int64_t *idx, float *grad,
+                         double *stats, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/*
  * tp_minibatch_rows -- the learner's minibatch draws (the learner samples
  * the stored transitions, Section 4.3; batch size from Table 2), with
  * replacement, from agent `agent`'s R = L * envs_per_agent transitions:

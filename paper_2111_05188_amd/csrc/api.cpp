@@ -573,15 +573,21 @@ size_t tp_ppo_workspace_bytes(const tp_ppo *cfg)
     return L.total;
 }
 
-int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v, int64_t step0,
-                  int32_t n_updates, const void *obs, int64_t ld_obs, const float *action,
-                  const float *logp, const float *adv, const float *ret, int64_t rows,
-                  const int64_t *idx, float *grad, double *stats, void *workspace,
-                  size_t workspace_bytes, void *stream)
+int tp_ppo_update_agents(const tp_ppo *cfg, int32_t n_agents, int64_t agent_stride,
+                         float *params, float *adam_m, float *adam_v, int64_t step0,
+                         int32_t n_updates, const void *obs, int64_t ld_obs, const float *action,
+                         const float *logp, const float *adv, const float *ret, int64_t rows,
+                         const int64_t *idx, float *grad, double *stats, void *workspace,
+                         size_t workspace_bytes, void *stream)
 {
     PpoArgs a{};
     int rc = check_ppo(cfg, &a.lay);
     if (rc != TP_OK) return rc;
+    if (n_agents < 1 || n_agents > 1024)
+        return fail(TP_EINVAL, "n_agents = %d outside [1, 1024]", n_agents);
+    if (n_agents > 1 && agent_stride < a.lay.P)
+        return fail(TP_EINVAL, "agent_stride = %lld < P = %lld: agents would overlap",
+                    (long long)agent_stride, (long long)a.lay.P);
     if (!params || !adam_m || !adam_v || !obs || !action || !logp || !adv || !ret || !idx ||
         !workspace)
         return fail(TP_EINVAL, "a learner array is NULL");
@@ -591,13 +597,17 @@ int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v
         (grad && !aligned(grad, 4)) || (stats && !aligned(stats, 8)))
         return fail(TP_EINVAL, "learner arrays are misaligned");
     if (!aligned(workspace, 256)) return fail(TP_EINVAL, "workspace must be 256-byte aligned");
-    if (workspace_bytes < a.lay.total)
-        return fail(TP_EINVAL, "workspace of %zu bytes, %zu needed", workspace_bytes, a.lay.total);
+    if (workspace_bytes / (size_t)n_agents < a.lay.total)
+        return fail(TP_EINVAL, "workspace of %zu bytes, %zu needed", workspace_bytes,
+                    a.lay.total * (size_t)n_agents);
     if (step0 < 1) return fail(TP_EINVAL, "step0 = %lld must be >= 1", (long long)step0);
     if (n_updates < 1) return fail(TP_EINVAL, "n_updates = %d must be >= 1", n_updates);
     if (rows < 1) return fail(TP_EINVAL, "rows = %lld must be >= 1", (long long)rows);
     if (ld_obs < cfg->dims[0])
         return fail(TP_EINVAL, "ld_obs = %lld < S = %d", (long long)ld_obs, cfg->dims[0]);
+    a.n_agents = n_agents;
+    a.agent_stride = n_agents > 1 ? agent_stride : a.lay.P;
+    a.ws_stride = (int64_t)a.lay.total;
     a.params = params;
     a.adam_m = adam_m;
     a.adam_v = adam_v;
@@ -623,6 +633,17 @@ int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v
     hipError_t e = launch_ppo_update(a, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "learner launch");
     return ok();
+}
+
+int tp_ppo_update(const tp_ppo *cfg, float *params, float *adam_m, float *adam_v, int64_t step0,
+                  int32_t n_updates, const void *obs, int64_t ld_obs, const float *action,
+                  const float *logp, const float *adv, const float *ret, int64_t rows,
+                  const int64_t *idx, float *grad, double *stats, void *workspace,
+                  size_t workspace_bytes, void *stream)
+{
+    return tp_ppo_update_agents(cfg, 1, 0, params, adam_m, adam_v, step0, n_updates, obs, ld_obs,
+                                action, logp, adv, ret, rows, idx, grad, stats, workspace,
+                                workspace_bytes, stream);
 }
 
 int tp_minibatch_rows(uint64_t seed, uint64_t counter, int32_t n_updates, int32_t B, int32_t L,

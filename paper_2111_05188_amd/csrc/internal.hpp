@@ -154,6 +154,9 @@ bool ppo_layout(const tp_ppo *c, PpoLayout *out);
 
 struct PpoArgs {
     PpoLayout lay;
+    int n_agents;              // independent learners in one call
+    int64_t agent_stride;      // floats between agents' parameters (and moments)
+    int64_t ws_stride;         // bytes between agents' workspaces
     float *params, *adam_m, *adam_v;
     int64_t step0;
     int n_updates;

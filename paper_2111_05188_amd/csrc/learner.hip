@@ -79,7 +79,57 @@ constexpr int MAX_PROBS = 4;
 struct GemmBatch {
     GemmProb p[MAX_PROBS];
     int np;
+    int tiles, na;       // tiles per agent, agents
+    int64_t aws, aprm;   // bytes between agents: workspace, parameters
 };
+
+// The (agent, tile) slot of this workgroup.  With several agents it is
+// XCD-aware: workgroups are dealt round-robin over the 8 XCDs; the grid
+// holds 8 per of them (per = gridDim.x / 8), and workgroup b takes slot
+// (b % 8) per + b / 8, so each XCD walks a contiguous run of slots, whole
+// agents whose operands stay in that XCD's L2.  One agent keeps slot b
+// (measured faster there).  False for the padding slots past the last.
+__device__ __forceinline__ bool gemm_slot(const GemmBatch &gb, int &agent, int &t)
+{
+    const int b = blockIdx.x, per = gridDim.x / 8;
+    const int v = gb.na == 1 ? b : (b % 8) * per + b / 8;
+    if (v >= gb.tiles * gb.na) return false;
+    agent = v / gb.tiles;
+    t = v % gb.tiles;
+    return true;
+}
+
+// p + by bytes (null stays null), computed on the global address space.
+// Pointers that reach a kernel inside a struct are generic to the compiler,
+// so accesses through them become flat instructions; a flat load counts
+// against the LDS counter too, and every wait for an LDS read would then
+// also wait for the operand prefetches in flight.  Derived from a global
+// pointer, they compile to global loads and stores.
+template <class T>
+__device__ __forceinline__ T *shifted(T *p, size_t by)
+{
+    typedef __attribute__((address_space(1))) char gchar;
+    return (T *)((gchar *)p + (p ? by : 0));
+}
+
+// Problem pi for agent `agent`: the operands, outputs, gradient blocks and
+// activation sources live in the agent's workspace, the biases in its
+// parameters.
+__device__ __forceinline__ GemmProb agent_prob(const GemmBatch &gb, int pi, int agent)
+{
+    GemmProb P = gb.p[pi];
+    const size_t w = (size_t)agent * (size_t)gb.aws, q = (size_t)agent * (size_t)gb.aprm;
+    P.A = shifted(P.A, w);
+    P.B = shifted(P.B, w);
+    P.out = shifted(P.out, w);
+    P.outT = shifted(P.outT, w);
+    P.g0 = shifted(P.g0, w);
+    P.g1 = shifted(P.g1, w);
+    P.hsrc = shifted(P.hsrc, w);
+    P.bias0 = shifted(P.bias0, q);
+    P.bias1 = shifted(P.bias1, q);
+    return P;
+}
 
 constexpr int GT = 64;   // workgroup tile (rows and columns)
 
@@ -253,9 +303,10 @@ __device__ __forceinline__ void kloop_any(const __bf16 *const pa[2], const __bf1
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
 {
     constexpr int PF = GEMM_PF;
-    int t = blockIdx.x;
+    int agent, t;
+    if (!gemm_slot(gb, agent, t)) return;
     const int pi = find_prob(gb, t);
-    const GemmProb &P = gb.p[pi];
+    const GemmProb P = agent_prob(gb, pi, agent);
     t -= P.tile0;
     const int tn = t % P.tiles_n, tm = t / P.tiles_n;
     const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
@@ -291,8 +342,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
 
 // bf16 through LDS, for products whose K is a multiple of 128 (all of the
 // bf16 learner's): chunks of 64 rows x 128 k of A and of B are staged in
-// LDS (rows padded by 16 bytes so the fragment reads of 16 rows fall in
-// different banks), loaded with whole-line accesses (each wave instruction
+// LDS (rows padded by 32 bytes, measured faster than 16 or 48), loaded
+// with whole-line accesses (each wave instruction
 // reads 4 rows x 256 contiguous bytes), GEMM_LD chunks ahead in registers
 // (deeper prefetch measured slower); eight waves (a 2 x 4 grid of 32x16
 // blocks: twice the waves of a 2 x 2 grid of 32x32 blocks, for latency
@@ -300,8 +351,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
 #ifndef GEMM_LD
 #define GEMM_LD 2                     // chunks in flight in registers
 #endif
+#ifndef GEMM_LPAD
+#define GEMM_LPAD 16                  // LDS row padding (bf16 elements)
+#endif
 constexpr int LBK = 128;              // k per chunk
-constexpr int LROW = LBK + 8;         // padded LDS row (bf16)
+constexpr int LROW = LBK + GEMM_LPAD; // padded LDS row (bf16)
 constexpr int LTILE = GT * LROW;      // one operand's chunk (bf16)
 
 typedef uint32_t v4u_t __attribute__((ext_vector_type(4)));
@@ -348,36 +402,45 @@ __device__ __forceinline__ void lds_kloop(const __bf16 *const ga, const __bf16 *
     if constexpr (D < NC) load(ra[0], rb[0], D);
     __syncthreads();
     const int am = (wave >> 2) * 32, bn = (wave & 3) * 16;
+    // Per chunk c: read its fragments (all four k-steps); store chunk c + 1
+    // into the other LDS buffer (free since the last barrier) and issue the
+    // load of chunk c + 1 + D; then the MFMAs; one barrier.
     static_for<0, NC>([&](auto c) {
         constexpr int buf = c & 1;
         const __bf16 *As = smem + buf * 2 * LTILE, *Bs = As + LTILE;
+        bf16x8 fa[LBK / 32][2], fb[LBK / 32];
 #pragma unroll
         for (int q = 0; q < LBK / 32; ++q) {
-            bf16x8 fa[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i)
-                fa[i] = *(const bf16x8 *)(As + (am + i * 16 + r16) * LROW + q * 32 + kq * 8);
-            const bf16x8 fb = *(const bf16x8 *)(Bs + (bn + r16) * LROW + q * 32 + kq * 8);
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-                acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb, acc[i], 0, 0, 0);
+                fa[q][i] = *(const bf16x8 *)(As + (am + i * 16 + r16) * LROW + q * 32 + kq * 8);
+            fb[q] = *(const bf16x8 *)(Bs + (bn + r16) * LROW + q * 32 + kq * 8);
         }
         if constexpr (c + 1 < NC) {
             // chunk c + 1 sits in register set (c + 1) % D; refill it with c + 1 + D
             constexpr int slot = (c + 1) % D;
             store(ra[slot], rb[slot], (c + 1) & 1);
             if constexpr (c + 1 + D < NC) load(ra[slot], rb[slot], c + 1 + D);
-            __syncthreads();
         }
+#pragma unroll
+        for (int q = 0; q < LBK / 32; ++q) {
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[q][i], fb[q], acc[i], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (c + 1 < NC) __syncthreads();
     });
 }
 
 __global__ __launch_bounds__(LTHREADS, 2) void gemm_lds_kernel(GemmBatch gb)
 {
     __shared__ __attribute__((aligned(16))) __bf16 smem[2 * 2 * LTILE];
-    int t = blockIdx.x;
+    int agent, t;
+    if (!gemm_slot(gb, agent, t)) return;
     const int pi = find_prob(gb, t);
-    const GemmProb &P = gb.p[pi];
+    const GemmProb P = agent_prob(gb, pi, agent);
     t -= P.tile0;
     const int tn = t % P.tiles_n, tm = t / P.tiles_n;
     const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
@@ -403,15 +466,145 @@ __global__ __launch_bounds__(LTHREADS, 2) void gemm_lds_kernel(GemmBatch gb)
     }
 }
 
+// Launches with many tiles (several agents): 128 x 128 workgroup tiles of
+// four 64 x 64 waves, k-chunks of 64 staged through LDS.  A wave's 4 x 4
+// tiles of 16 x 16 use each fragment four times, 0.5 KiB of LDS reads per
+// MFMA against 1.5 KiB in the eight-wave kernel above, whose reads exceed
+// the LDS bandwidth once every CU is busy.  Rows padded by 32 bytes
+// (measured faster than 16; two workgroups fill the 160 KiB of LDS).
+constexpr int BT = 128;               // workgroup tile (rows and columns)
+#ifndef GEMM_BPAD
+#define GEMM_BPAD 16                  // LDS row padding (bf16 elements)
+#endif
+constexpr int BBK = 64;               // k per chunk
+constexpr int BROW = BBK + GEMM_BPAD; // padded LDS row (bf16)
+constexpr int BTILE = BT * BROW;      // one operand's chunk (bf16)
+constexpr int BIG_MIN_TILES = 512;    // launches with fewer 128 x 128 tiles keep 64 x 64
+
+// Chunk loop: 256 threads move a 128 x 64 chunk of A and one of B (thread
+// t: rows (t / 8) + 32 j, 16-byte piece t % 8; a wave instruction reads
+// 8 rows x 128 contiguous bytes); wave (wm, wn) multiplies rows 64 wm ..
+// +63 by columns 64 wn .. +63.
+template <int NC>
+__device__ __forceinline__ void big_kloop(const __bf16 *const ga, const __bf16 *const gb,
+                                          int64_t lda, int64_t ldb, int Mr, int Nr,
+                                          __bf16 *smem, floatx4 (&acc)[4][4])
+{
+    const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
+    const int r16 = lane & 15, kq = lane >> 4;
+    const int lrow = tid >> 3, lpiece = tid & 7;
+    const __bf16 *la[4], *lb[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        la[j] = ga + (size_t)min(lrow + 32 * j, Mr - 1) * lda + lpiece * 8;
+        lb[j] = gb + (size_t)min(lrow + 32 * j, Nr - 1) * ldb + lpiece * 8;
+    }
+    constexpr int D = NC < GEMM_LD ? NC : GEMM_LD;   // chunks in flight in registers
+    v4u_t ra[D][4], rb[D][4];
+    auto load = [&](v4u_t (&xa)[4], v4u_t (&xb)[4], int c) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            xa[j] = *(const v4u_t *)(la[j] + c * BBK);
+            xb[j] = *(const v4u_t *)(lb[j] + c * BBK);
+        }
+    };
+    auto store = [&](const v4u_t (&xa)[4], const v4u_t (&xb)[4], int buf) {
+        __bf16 *As = smem + buf * 2 * BTILE, *Bs = As + BTILE;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            *(v4u_t *)(As + (lrow + 32 * j) * BROW + lpiece * 8) = xa[j];
+            *(v4u_t *)(Bs + (lrow + 32 * j) * BROW + lpiece * 8) = xb[j];
+        }
+    };
+    static_for<0, D>([&](auto c) { load(ra[c], rb[c], c); });
+    store(ra[0], rb[0], 0);
+    if constexpr (D < NC) load(ra[0], rb[0], D);
+    __syncthreads();
+    const int am = (wave >> 1) * 64, bn = (wave & 1) * 64;
+    // Per chunk c: read its fragments (both k-steps); store chunk c + 1 into
+    // the other LDS buffer (free since the last barrier: chunk c - 1's
+    // reads completed before it) and issue the load of chunk c + 1 + D;
+    // then the MFMAs, which overlap the stores and the second k-step's
+    // reads; one barrier.
+    static_for<0, NC>([&](auto c) {
+        constexpr int buf = c & 1;
+        const __bf16 *As = smem + buf * 2 * BTILE, *Bs = As + BTILE;
+        bf16x8 fa[BBK / 32][4], fb[BBK / 32][4];
+#pragma unroll
+        for (int q = 0; q < BBK / 32; ++q)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                fa[q][i] = *(const bf16x8 *)(As + (am + i * 16 + r16) * BROW + q * 32 + kq * 8);
+                fb[q][i] = *(const bf16x8 *)(Bs + (bn + i * 16 + r16) * BROW + q * 32 + kq * 8);
+            }
+        if constexpr (c + 1 < NC) {
+            // chunk c + 1 sits in register set (c + 1) % D; refill it with c + 1 + D
+            constexpr int slot = (c + 1) % D;
+            store(ra[slot], rb[slot], (c + 1) & 1);
+            if constexpr (c + 1 + D < NC) load(ra[slot], rb[slot], c + 1 + D);
+        }
+#pragma unroll
+        for (int q = 0; q < BBK / 32; ++q) {
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[q][i], fb[q][j],
+                                                                        acc[i][j], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (c + 1 < NC) __syncthreads();
+    });
+}
+
+__global__ __launch_bounds__(256, 2) void gemm_big_kernel(GemmBatch gb)
+{
+    __shared__ __attribute__((aligned(16))) __bf16 smem[2 * 2 * BTILE];
+    int agent, t;
+    if (!gemm_slot(gb, agent, t)) return;
+    const int pi = find_prob(gb, t);
+    const GemmProb P = agent_prob(gb, pi, agent);
+    t -= P.tile0;
+    const int tn = t % P.tiles_n, tm = t / P.tiles_n;
+    const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
+    const int m0 = tm * BT, n0 = tn * BT;
+    const int r16 = lane & 15, kq = lane >> 4;
+    const __bf16 *ga = (const __bf16 *)P.A + (size_t)m0 * P.lda;
+    const __bf16 *gbp = (const __bf16 *)P.B + (size_t)n0 * P.ldb;
+    floatx4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int Mr = P.M - m0, Nr = P.N - n0;     // rows left in this tile (>= 1)
+    switch (P.K / BBK) {
+    case 2: big_kloop<2>(ga, gbp, P.lda, P.ldb, Mr, Nr, smem, acc); break;
+    case 8: big_kloop<8>(ga, gbp, P.lda, P.ldb, Mr, Nr, smem, acc); break;
+    case 16: big_kloop<16>(ga, gbp, P.lda, P.ldb, Mr, Nr, smem, acc); break;
+    default: break;   // the launcher routes other K elsewhere
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    const int wm = m0 + (wave >> 1) * 64, wn = n0 + (wave & 1) * 64;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+            epi4<true>(P, wm + i * 16 + kq * 4, wn + j * 16 + r16, v);
+        }
+}
+
 // fp32: 16x16 threads, each a 4x4 block of the 64x64 tile; k-slices of 16
 // staged in LDS, k-major, so the inner loop reads broadcast-free rows.
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmBatch gb)
 {
     __shared__ float As[16][GT + 4];
     __shared__ float Bs[16][GT + 4];
-    int t = blockIdx.x;
+    int agent, t;
+    if (!gemm_slot(gb, agent, t)) return;
     const int pi = find_prob(gb, t);
-    const GemmProb &P = gb.p[pi];
+    const GemmProb P = agent_prob(gb, pi, agent);
     t -= P.tile0;
     const int tn = t % P.tiles_n, tm = t / P.tiles_n;
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
@@ -466,9 +659,17 @@ __global__ __launch_bounds__(256) void gather_kernel(
     const float *__restrict__ logp, const float *__restrict__ adv, const float *__restrict__ ret,
     const int64_t *__restrict__ idx, int64_t rows, int B, int S, int Kp, int n,
     Elem<BF> *__restrict__ X, Elem<BF> *__restrict__ Xt, float *__restrict__ Ag,
-    float *__restrict__ row_in)
+    float *__restrict__ row_in, int64_t aws, int64_t aidx)
 {
     typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+    {   // agent blockIdx.z: its workspace and its minibatch indices
+        const size_t w = (size_t)blockIdx.z * (size_t)aws;
+        idx += (size_t)blockIdx.z * (size_t)aidx;
+        X = shifted(X, w);
+        Xt = shifted(Xt, w);
+        Ag = shifted(Ag, w);
+        row_in = shifted(row_in, w);
+    }
     constexpr int VE = 16 / sizeof(Elem<BF>);   // elements per 16-byte vector
     constexpr int VPR = 64 / VE;                 // vectors per tile row
     __shared__ int64_t s_idx[64];
@@ -556,8 +757,23 @@ __global__ __launch_bounds__(256) void loss_kernel(
     const Elem<BF> *__restrict__ Hc2, const float *__restrict__ params, int64_t ols,
     int64_t owc3, int64_t obc3, int B, int n, int n_pad, int vsplit, int C2, float clip,
     float *__restrict__ row_out, Elem<BF> *__restrict__ dMU, Elem<BF> *__restrict__ dMUt,
-    float *__restrict__ LSt, Elem<BF> *__restrict__ dZc2, Elem<BF> *__restrict__ dZc2t)
+    float *__restrict__ LSt, Elem<BF> *__restrict__ dZc2, Elem<BF> *__restrict__ dZc2t,
+    int64_t aws, int64_t aprm)
 {
+    {   // agent blockIdx.z: its workspace and its parameters
+        const size_t w = (size_t)blockIdx.z * (size_t)aws;
+        mu = shifted(mu, w);
+        Ag = shifted(Ag, w);
+        row_in = shifted(row_in, w);
+        Hc2 = shifted(Hc2, w);
+        row_out = shifted(row_out, w);
+        dMU = shifted(dMU, w);
+        dMUt = shifted(dMUt, w);
+        LSt = shifted(LSt, w);
+        dZc2 = shifted(dZc2, w);
+        dZc2t = shifted(dZc2t, w);
+        params = shifted(params, (size_t)blockIdx.z * (size_t)aprm);
+    }
     __shared__ float t1[64][65];
     __shared__ float t2[64][65];
     __shared__ float s_row[64];    // g (actor tiles) or dL/dV (critic tiles)
@@ -790,30 +1006,40 @@ struct AdamBatch {
     const float *grad;
     float lr, b1, b2, eps, bc1, bc2;
     int do_adam;
+    int64_t aws, aprm, ast;   // bytes between agents: workspace, parameters, statistics
+};
+
+// One agent's parameters, moments and gradient
+struct AdamPtrs {
+    float *params, *m, *v;
+    const float *grad;
 };
 
 // One Adam step of one element (the moments and the master written back).
-__device__ __forceinline__ float adam_step(const AdamBatch &ab, int64_t p, float th, float g,
-                                           float m0, float v0)
+__device__ __forceinline__ float adam_step(const AdamBatch &ab, const AdamPtrs &q, int64_t p,
+                                           float th, float g, float m0, float v0)
 {
     const float m = ab.b1 * m0 + (1.0f - ab.b1) * g;
     const float v = ab.b2 * v0 + (1.0f - ab.b2) * (g * g);
-    ab.m[p] = m;
-    ab.v[p] = v;
+    q.m[p] = m;
+    q.v[p] = v;
     const float mh = m / ab.bc1, vh = v / ab.bc2;
     th = th - ab.lr * (mh / (sqrtf(vh) + ab.eps));
-    ab.params[p] = th;
+    q.params[p] = th;
     return th;
 }
 
 template <bool BF>
-__device__ __forceinline__ void adam_tile(const AdamBatch &ab, int t, Elem<BF> (*tile)[AT + 1])
+__device__ __forceinline__ void adam_tile(const AdamBatch &ab, const AdamPtrs &ap, int t,
+                                          Elem<BF> (*tile)[AT + 1])
 {
     int si = 0;
 #pragma unroll
     for (int q = 1; q < MAX_ASEGS; ++q)
         if (q < ab.ns && t >= ab.s[q].tile0) si = q;
-    const AdamSeg &S = ab.s[si];
+    AdamSeg S = ab.s[si];
+    S.copy = shifted(S.copy, (size_t)blockIdx.y * (size_t)ab.aws);
+    S.copyT = shifted(S.copyT, (size_t)blockIdx.y * (size_t)ab.aws);
     t -= S.tile0;
     const int tid = threadIdx.x;
     const int r0 = (t / S.tiles_c) * AT, c0 = (t % S.tiles_c) * AT;
@@ -825,11 +1051,11 @@ __device__ __forceinline__ void adam_tile(const AdamBatch &ab, int t, Elem<BF> (
         const int q = tid + 256 * j;
         const int r = min(r0 + q / AT, S.rows - 1), c = min(c0 + q % AT, S.cols - 1);
         const int64_t p = S.off + (int64_t)r * S.cols + c;
-        th[j] = ab.params[p];
+        th[j] = ap.params[p];
         if (ab.do_adam) {
-            gg[j] = ab.grad[p];
-            mm[j] = ab.m[p];
-            vv[j] = ab.v[p];
+            gg[j] = ap.grad[p];
+            mm[j] = ap.m[p];
+            vv[j] = ap.v[p];
         }
     }
 #pragma unroll
@@ -840,7 +1066,7 @@ __device__ __forceinline__ void adam_tile(const AdamBatch &ab, int t, Elem<BF> (
         if (r < S.rows && c < S.cols) {
             w = th[j];
             if (ab.do_adam)
-                w = adam_step(ab, S.off + (int64_t)r * S.cols + c, w, gg[j], mm[j], vv[j]);
+                w = adam_step(ab, ap, S.off + (int64_t)r * S.cols + c, w, gg[j], mm[j], vv[j]);
         }
         const Elem<BF> e = to_elem<BF>(w);
         if (r < S.rows_pad && c < S.cols_pad)
@@ -858,14 +1084,22 @@ __device__ __forceinline__ void adam_tile(const AdamBatch &ab, int t, Elem<BF> (
     }
 }
 
-__device__ __forceinline__ void reduce_row(const RedBatch &rb, const AdamBatch &ab, int g)
+__device__ __forceinline__ void reduce_row(const RedBatch &rb, const AdamBatch &ab,
+                                           const AdamPtrs &ap, int g)
 {
     const int lane = threadIdx.x % WAVE;
     int si = 0;
 #pragma unroll
     for (int q = 1; q < MAX_SEGS; ++q)
         if (q < rb.ns && g >= rb.s[q].row0) si = q;
-    const RedSeg &S = rb.s[si];
+    RedSeg S = rb.s[si];
+    {   // agent blockIdx.y: sources, weights and gradient in its workspace
+        const size_t w = (size_t)blockIdx.y * (size_t)ab.aws;
+        S.src = shifted(S.src, w);
+        S.w = shifted(S.w, w);
+        S.dst = shifted(S.dst, w);
+        S.dst64 = shifted(S.dst64, (size_t)blockIdx.y * (size_t)ab.ast);
+    }
     const int r = g - S.row0;
     double acc = 0.0;
     if (S.vec && S.bf) {   // 8 bf16 per lane per step
@@ -904,29 +1138,35 @@ __device__ __forceinline__ void reduce_row(const RedBatch &rb, const AdamBatch &
             S.dst[r] = (float)v;
             if (S.pidx >= 0 && ab.do_adam) {
                 const int64_t p = S.pidx + r;
-                adam_step(ab, p, ab.params[p], (float)v, ab.m[p], ab.v[p]);
+                adam_step(ab, ap, p, ap.params[p], (float)v, ap.m[p], ap.v[p]);
             }
         }
     }
 }
 
-// Blocks [0, 8 per) take the matrix tiles, XCD-aware: workgroups are
-// dealt round-robin over the 8 XCDs, so block b takes tile (b % 8) per +
-// b / 8 and each XCD walks a contiguous run of tiles (rows of W1 and Wc1
-// are not line-aligned: neighbouring tiles share lines, now in one L2).
+// blockIdx.y is the agent.  Blocks [0, 8 per) take the matrix tiles,
+// XCD-aware: workgroups are dealt round-robin over the 8 XCDs, so block b
+// takes tile (b % 8) per + b / 8 and each XCD walks a contiguous run of
+// tiles (rows of W1 and Wc1 are not line-aligned: neighbouring tiles share
+// lines, now in one L2).  For agent y the XCD of block b is that of b + y
+// gridDim.x, so blocks with equal b % 8 still share one.
 template <bool BF>
 __global__ __launch_bounds__(256) void adam_tail_kernel(AdamBatch ab, RedBatch rb, int mtiles)
 {
     __shared__ Elem<BF> tile[AT][AT + 1];
+    // agent blockIdx.y
+    const size_t q = (size_t)blockIdx.y * (size_t)ab.aprm;
+    const AdamPtrs ap{shifted(ab.params, q), shifted(ab.m, q), shifted(ab.v, q),
+                      shifted(ab.grad, (size_t)blockIdx.y * (size_t)ab.aws)};
     const int per = (mtiles + 7) / 8;
     const int b = blockIdx.x;
     if (b < 8 * per) {
         const int t = (b % 8) * per + b / 8;
-        if (t < mtiles) adam_tile<BF>(ab, t, tile);
+        if (t < mtiles) adam_tile<BF>(ab, ap, t, tile);
         return;
     }
     const int g = (b - 8 * per) * 4 + threadIdx.x / WAVE;
-    if (g < rb.total_rows) reduce_row(rb, ab, g);
+    if (g < rb.total_rows) reduce_row(rb, ab, ap, g);
 }
 
 // Minibatch rows: draw i of update counter c for agent g is word i % 4 of
@@ -1065,26 +1305,46 @@ GemmProb prob(const void *A, int64_t lda, const void *B, int64_t ldb, int M, int
     return p;
 }
 
-hipError_t run_gemms(bool bf, std::initializer_list<GemmProb> ps, hipStream_t s)
+// Agents of one call: count and byte strides between their workspaces and
+// parameter vectors.
+struct Agents {
+    int n;
+    int64_t aws, aprm;
+};
+
+hipError_t run_gemms(bool bf, const Agents &ag, std::initializer_list<GemmProb> ps, hipStream_t s)
 {
     GemmBatch gb{};
+    gb.aws = ag.aws;
+    gb.aprm = ag.aprm;
+    // kernel choice: bf16 products with K in {128, 512, 1024} go through
+    // LDS, in 128 x 128 tiles when the launch has enough of them
+    bool staged = bf, big = bf;
+    int tiles_big = 0;
+    for (const GemmProb &p : ps) {
+        const int nc = p.K / LBK, nb = p.K / BBK;
+        const bool ld_ok = p.lda % 8 == 0 && p.ldb % 8 == 0;
+        staged = staged && p.K % LBK == 0 && (nc == 1 || nc == 4 || nc == 8) && ld_ok;
+        big = big && p.K % BBK == 0 && (nb == 2 || nb == 8 || nb == 16) && ld_ok;
+        tiles_big += cdiv(p.M, BT) * cdiv(p.N, BT);
+    }
+    big = big && tiles_big * ag.n >= BIG_MIN_TILES;
+    const int T = big ? BT : GT;
     int tiles = 0;
     for (const GemmProb &p : ps) {
         GemmProb q = p;
-        q.tiles_n = cdiv(q.N, GT);
+        q.tiles_n = cdiv(q.N, T);
         q.tile0 = tiles;
-        tiles += q.tiles_n * cdiv(q.M, GT);
+        tiles += q.tiles_n * cdiv(q.M, T);
         gb.p[gb.np++] = q;
     }
-    bool staged = bf;   // K in {128, 512, 1024}: the LDS-staged kernel
-    for (int q = 0; q < gb.np; ++q) {
-        const int nc = gb.p[q].K / LBK;
-        staged = staged && gb.p[q].K % LBK == 0 && (nc == 1 || nc == 4 || nc == 8) &&
-                 gb.p[q].lda % 8 == 0 && gb.p[q].ldb % 8 == 0;
-    }
-    if (staged) hipLaunchKernelGGL(gemm_lds_kernel, dim3(tiles), dim3(LTHREADS), 0, s, gb);
-    else if (bf) hipLaunchKernelGGL(gemm_bf16_kernel, dim3(tiles), dim3(256), 0, s, gb);
-    else hipLaunchKernelGGL(gemm_f32_kernel, dim3(tiles), dim3(256), 0, s, gb);
+    gb.tiles = tiles;
+    gb.na = ag.n;
+    const dim3 grid(8 * cdiv(tiles * ag.n, 8));
+    if (big) hipLaunchKernelGGL(gemm_big_kernel, grid, dim3(256), 0, s, gb);
+    else if (staged) hipLaunchKernelGGL(gemm_lds_kernel, grid, dim3(LTHREADS), 0, s, gb);
+    else if (bf) hipLaunchKernelGGL(gemm_bf16_kernel, grid, dim3(256), 0, s, gb);
+    else hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, gb);
     return hipGetLastError();
 }
 
@@ -1100,6 +1360,11 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
     const int B = L.B;
     float *prm = a.params;
     float *grad = (float *)W(L.wG);
+    // agents: workspaces a.ws_stride bytes apart, parameter vectors (and
+    // moments) a.agent_stride floats apart; minibatch indices [A][U][B],
+    // statistics [A][U][4]
+    const int NA = a.n_agents;
+    const Agents ag{NA, a.ws_stride, a.agent_stride * (int64_t)sizeof(float)};
 
     // Adam / refresh segments
     AdamBatch ab{};
@@ -1111,6 +1376,9 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
     ab.b1 = a.beta1;
     ab.b2 = a.beta2;
     ab.eps = a.eps;
+    ab.aws = ag.aws;
+    ab.aprm = ag.aprm;
+    ab.ast = (int64_t)a.n_updates * 4 * (int64_t)sizeof(double);
     int atiles = 0;
     auto mseg = [&](int64_t off, int rows, int cols, int rows_pad, int cols_pad, void *copy,
                     int64_t ldc, int row0, void *copyT, int64_t ldt) {
@@ -1145,7 +1413,7 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
         ab.do_adam = do_adam;
         ab.bc1 = (float)(1.0 - pow((double)a.beta1, (double)step));
         ab.bc2 = (float)(1.0 - pow((double)a.beta2, (double)step));
-        const dim3 grid(8 * cdiv(mtiles, 8) + cdiv(rb.total_rows, 4));
+        const dim3 grid(8 * cdiv(mtiles, 8) + cdiv(rb.total_rows, 4), NA);
         if (bf) hipLaunchKernelGGL(adam_tail_kernel<true>, grid, dim3(256), 0, s, ab, rb, mtiles);
         else hipLaunchKernelGGL(adam_tail_kernel<false>, grid, dim3(256), 0, s, ab, rb, mtiles);
         return hipGetLastError();
@@ -1169,17 +1437,18 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
         const int64_t *idx = a.idx + (size_t)u * B;
         // gather
         {
-            const dim3 grid(cdiv(B, 64), cdiv(L.Kp, 64));
+            const dim3 grid(cdiv(B, 64), cdiv(L.Kp, 64), NA);
+            const int64_t aidx = (int64_t)a.n_updates * B;
             if (bf)
                 hipLaunchKernelGGL(gather_kernel<true>, grid, dim3(256), 0, s,
                                    (const __bf16 *)a.obs, a.ld_obs, vec_obs, a.action, a.logp,
                                    a.adv, a.ret, idx, a.rows, B, L.S, L.Kp, L.n, (__bf16 *)X,
-                                   (__bf16 *)Xt, Ag, row_in);
+                                   (__bf16 *)Xt, Ag, row_in, ag.aws, aidx);
             else
                 hipLaunchKernelGGL(gather_kernel<false>, grid, dim3(256), 0, s,
                                    (const float *)a.obs, a.ld_obs, vec_obs, a.action, a.logp,
                                    a.adv, a.ret, idx, a.rows, B, L.S, L.Kp, L.n, (float *)X,
-                                   (float *)Xt, Ag, row_in);
+                                   (float *)Xt, Ag, row_in, ag.aws, aidx);
         }
         // forward 1: [h1 | hc1] = tanh(X [W1; Wc1]^T + [b1 | bc1])
         {
@@ -1191,7 +1460,7 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             p.ldo = L.HC1;
             p.outT = H1t;
             p.ldt = B;
-            if ((e = run_gemms(bf, {p}, s)) != hipSuccess) return e;
+            if ((e = run_gemms(bf, ag, {p}, s)) != hipSuccess) return e;
         }
         // forward 2: h2 and hc2
         {
@@ -1207,7 +1476,7 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             pc.ldo = L.C2;
             pc.outT = Hc2t;
             pc.ldt = B;
-            if ((e = run_gemms(bf, {pa, pc}, s)) != hipSuccess) return e;
+            if ((e = run_gemms(bf, ag, {pa, pc}, s)) != hipSuccess) return e;
         }
         // forward 3: mu = h2 W3^T + b3
         {
@@ -1215,23 +1484,25 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             p.bias0 = prm + L.ob3;
             p.out = MU;
             p.ldo = L.n;
-            if ((e = run_gemms(bf, {p}, s)) != hipSuccess) return e;
+            if ((e = run_gemms(bf, ag, {p}, s)) != hipSuccess) return e;
         }
         // loss and its gradient tiles: actor columns [0, n_pad) in whole
         // tiles, then the critic's C2 columns
         {
             const int ntA = cdiv(L.n_pad, 64);
-            const dim3 grid(cdiv(B, 64), ntA + cdiv(L.C2, 64));
+            const dim3 grid(cdiv(B, 64), ntA + cdiv(L.C2, 64), NA);
             if (bf)
                 hipLaunchKernelGGL(loss_kernel<true>, grid, dim3(256), 0, s, MU, Ag, row_in,
                                    (const __bf16 *)Hc2, prm, L.ols, L.owc3, L.obc3, B, L.n,
                                    L.n_pad, ntA * 64, L.C2, a.clip, row_out, (__bf16 *)dMU,
-                                   (__bf16 *)dMUt, LSt, (__bf16 *)dZc2, (__bf16 *)dZc2t);
+                                   (__bf16 *)dMUt, LSt, (__bf16 *)dZc2, (__bf16 *)dZc2t, ag.aws,
+                                   ag.aprm);
             else
                 hipLaunchKernelGGL(loss_kernel<false>, grid, dim3(256), 0, s, MU, Ag, row_in,
                                    (const float *)Hc2, prm, L.ols, L.owc3, L.obc3, B, L.n,
                                    L.n_pad, ntA * 64, L.C2, a.clip, row_out, (float *)dMU,
-                                   (float *)dMUt, LSt, (float *)dZc2, (float *)dZc2t);
+                                   (float *)dMUt, LSt, (float *)dZc2, (float *)dZc2t, ag.aws,
+                                   ag.aprm);
         }
         // backward stage A: dW3, dZ2 (actor); dWc2, dZc1 (critic)
         {
@@ -1253,7 +1524,7 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             bc2.ldh = L.HC1;
             bc2.outT = at(dZ1t, (size_t)L.H1 * B);
             bc2.ldt = B;
-            if ((e = run_gemms(bf, {g3, b3, gc2, bc2}, s)) != hipSuccess) return e;
+            if ((e = run_gemms(bf, ag, {g3, b3, gc2, bc2}, s)) != hipSuccess) return e;
         }
         // backward stage B: dW2, dZ1 (actor)
         {
@@ -1265,7 +1536,7 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             b2.ldh = L.HC1;
             b2.outT = dZ1t;
             b2.ldt = B;
-            if ((e = run_gemms(bf, {g2, b2}, s)) != hipSuccess) return e;
+            if ((e = run_gemms(bf, ag, {g2, b2}, s)) != hipSuccess) return e;
         }
         // backward stage C: [dW1; dWc1] = [dZ1; dZc1]^T X
         {
@@ -1275,7 +1546,7 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             g1.gsplit = L.H1;
             g1.ldg = L.S;
             g1.gcols = L.S;
-            if ((e = run_gemms(bf, {g1}, s)) != hipSuccess) return e;
+            if ((e = run_gemms(bf, ag, {g1}, s)) != hipSuccess) return e;
         }
         // the tail: Adam over the matrices; row sums of the bias, log-std
         // and critic-head gradients (each with its element's Adam step) and
@@ -1327,9 +1598,10 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             if ((e = tail(1, a.step0 + u, rb)) != hipSuccess) return e;
         }
     }
-    if (a.grad_out)
-        return hipMemcpyAsync(a.grad_out, grad, sizeof(float) * (size_t)L.P,
-                              hipMemcpyDeviceToDevice, s);
+    if (a.grad_out)   // [A][P] from the agents' workspaces
+        return hipMemcpy2DAsync(a.grad_out, sizeof(float) * (size_t)L.P, grad,
+                                (size_t)a.ws_stride, sizeof(float) * (size_t)L.P, (size_t)NA,
+                                hipMemcpyDeviceToDevice, s);
     return hipSuccess;
 }
 

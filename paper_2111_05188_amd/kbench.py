@@ -26,6 +26,7 @@ Times, with HIP events on the launch stream:
     per call on a 390 x 4,096 trajectory; algorithmic FLOPs per update
     2B (2 S H1 + 3 H1 H2 + 3 H2 n + 2 S C1 + 3 C1 C2 + 3 C2) (forward of
     both networks, weight gradients, and input gradients except layer 1's);
+    then the same for 16 agents per call (tp_ppo_update_agents);
   * probes: the device ceilings the roofline figures are read against,
     from libtpprobe.so: the dense bf16 MFMA issue rate (back-to-back
     v_mfma_f32_16x16x32_bf16 or v_mfma_f32_32x32x16_bf16 on register
@@ -240,6 +241,26 @@ def main():
         out["learner"] = {"update_ms": sec * 1e3, "flops_per_update": flops,
                           "TFLOPs": flops / sec / 1e12,
                           "mfma_frac": flops / sec / 1e12 / PEAK_BF16_TFLOPS, "P": P}
+        del params, m, v, idx, ws
+        torch.cuda.empty_cache()
+        # the same updates for 16 agents in one call (tp_ppo_update_agents)
+        A = 16
+        print(f"[kbench] learner agents={A} B={B} updates={NU}", file=sys.stderr, flush=True)
+        params = torch.from_numpy(np.stack([W.make_flat_params(cc, agent=a)
+                                            for a in range(A)])).to(dev)
+        m = torch.zeros(A, P, device=dev)
+        v = torch.zeros(A, P, device=dev)
+        idx = torch.randint(0, rows, (A, NU, B), device=dev, generator=g)
+        ws = tp.ppo_workspace(c, n_agents=A)
+        step = [1]
+
+        def upd_agents():
+            tp.ppo_update_agents(c, params, m, v, step[0], obs, act, logp, adv, ret, idx, ws)
+            step[0] += NU
+        sec = _time(upd_agents, max(1, args.iters // 4), stream) / NU
+        out["learner"]["agents16"] = {"update_ms": sec * 1e3, "agent_update_ms": sec * 1e3 / A,
+                                      "TFLOPs": A * flops / sec / 1e12,
+                                      "mfma_frac": A * flops / sec / 1e12 / PEAK_BF16_TFLOPS}
         del obs, act, logp, adv, ret, params, m, v, idx, ws
         torch.cuda.empty_cache()
 

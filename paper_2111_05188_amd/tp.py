@@ -81,7 +81,7 @@ EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_backtest_metrics_work_bytes", "tp_ensemble_fuse", "tp_fitness",
            "tp_keep_best", "tp_select",
            "tp_ppo_param_count", "tp_ppo_workspace_bytes", "tp_ppo_update",
-           "tp_minibatch_rows", "tp_rollout_path",
+           "tp_ppo_update_agents", "tp_minibatch_rows", "tp_rollout_path",
            "tp_last_error", "tp_version")
 
 _lib = None
@@ -124,12 +124,14 @@ def load(path: str = LIB_PATH):
                                     vp]
     L.tp_ppo_update.argtypes = [vp, vp, vp, vp, i64, i32, vp, i64, vp, vp, vp, vp, i64, vp,
                                 vp, vp, vp, C.c_size_t, vp]
+    L.tp_ppo_update_agents.argtypes = [vp, i32, i64, vp, vp, vp, i64, i32, vp, i64, vp, vp, vp,
+                                       vp, i64, vp, vp, vp, vp, C.c_size_t, vp]
     L.tp_last_error.restype = C.c_char_p
     L.tp_version.restype = C.c_int
     for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae",
               "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
               "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
-              "tp_ppo_update", "tp_minibatch_rows"):
+              "tp_ppo_update", "tp_ppo_update_agents", "tp_minibatch_rows"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -445,11 +447,11 @@ def ppo_param_count(cfg: Ppo) -> int:
     return p
 
 
-def ppo_workspace(cfg: Ppo, device="cuda") -> torch.Tensor:
+def ppo_workspace(cfg: Ppo, device="cuda", n_agents: int = 1) -> torch.Tensor:
     nb = load().tp_ppo_workspace_bytes(C.byref(cfg))
     if nb == 0:
         raise TPError(TP_EINVAL, load().tp_last_error().decode())
-    return torch.empty(nb, dtype=torch.uint8, device=device)
+    return torch.empty(nb * n_agents, dtype=torch.uint8, device=device)
 
 
 def ppo_update(cfg: Ppo, params, adam_m, adam_v, step0: int, obs, action, logp, adv, ret,
@@ -464,6 +466,30 @@ def ppo_update(cfg: Ppo, params, adam_m, adam_v, step0: int, obs, action, logp, 
                                 _ptr(adv), _ptr(ret), rows, _ptr(idx), _ptr(grad),
                                 _ptr(stats), _ptr(workspace), workspace.numel(),
                                 _stream(stream)))
+
+
+def ppo_update_agents(cfg: Ppo, params, adam_m, adam_v, step0: int, obs, action, logp, adv,
+                      ret, idx, workspace, grad=None, stats=None, stream=None):
+    """ppo_update for A independent learners in one call: params, adam_m,
+    adam_v [A][stride] (stride >= P), idx [A][n_updates][B] int64, grad
+    [A][P] and stats [A][n_updates][4] optional, workspace from
+    ppo_workspace(cfg, n_agents=A)."""
+    A, nu, B = idx.shape
+    assert B == cfg.batch and idx.dtype == torch.int64
+    assert params.dim() == 2 and params.shape[0] == A
+    assert adam_m.shape == params.shape and adam_v.shape == params.shape
+    assert params.stride(1) == 1 and adam_m.stride() == params.stride()
+    assert adam_v.stride() == params.stride() and idx.is_contiguous()
+    P = ppo_param_count(cfg)
+    assert params.shape[1] >= P
+    assert grad is None or (grad.shape == (A, P) and grad.is_contiguous())
+    assert stats is None or (stats.shape == (A, nu, 4) and stats.is_contiguous())
+    rows, ld = obs.shape
+    _check(load().tp_ppo_update_agents(C.byref(cfg), A, params.stride(0), _ptr(params),
+                                       _ptr(adam_m), _ptr(adam_v), step0, nu, _ptr(obs), ld,
+                                       _ptr(action), _ptr(logp), _ptr(adv), _ptr(ret), rows,
+                                       _ptr(idx), _ptr(grad), _ptr(stats), _ptr(workspace),
+                                       workspace.numel(), _stream(stream)))
 
 
 def flat_segments(dims6):

@@ -189,3 +189,22 @@ def test_ppo_sizes_and_argument_errors_without_gpu():
     a = list(args)
     a[7] = 1000
     assert L.tp_ppo_update(*a) == tp.TP_EINVAL and "ld_obs" in tp.last_error()
+
+
+def test_ppo_agents_argument_errors_without_gpu():
+    L = tp.load()
+    dims = (1001, 512, 512, 100, 512, 512)
+    c = tp.ppo_cfg(dims, tp.TP_BF16, 1024)
+    P = tp.ppo_param_count(c)
+    nb = L.tp_ppo_workspace_bytes(C.byref(c))
+    x = 0x100000
+    # cfg, n_agents, agent_stride, params, m, v, step0, n_updates, obs, ld_obs, action, logp,
+    # adv, ret, rows, idx, grad, stats, workspace, workspace_bytes, stream
+    args = [C.byref(c), 4, P, x, x, x, 1, 1, x, 1024, x, x, x, x, 4096, x, None, None, x, 4 * nb,
+            None]
+    for i, v, msg in ((1, 0, "n_agents"), (1, 1025, "n_agents"), (2, P - 1, "overlap"),
+                      (19, 4 * nb - 1, "workspace"), (3, None, "NULL"), (6, 0, "step0")):
+        a = list(args)
+        a[i] = v
+        assert L.tp_ppo_update_agents(*a) == tp.TP_EINVAL, (i, v)
+        assert msg in tp.last_error(), tp.last_error()

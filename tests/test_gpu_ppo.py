@@ -188,3 +188,52 @@ def test_minimal_batch_and_rollout_rows():
     _, g_o = ppo.loss_and_grad(host["flat"].astype(np.float64), dims,
                                *_oracle_batch(host, idx[0], dims[0]))
     _check_grad(dims, grad.cpu().numpy(), g_o, GRAD_TOL["f32"], "tiny B=32")
+
+
+@pytest.mark.parametrize("name,rows,B,A", [("tiny", 512, 64, 3), ("nasdaq100", 4096, 1024, 3),
+                                            ("nasdaq100", 4096, 1024, 8)])
+def test_agents_in_one_call_equal_single_calls(name, rows, B, A):
+    """tp_ppo_update_agents: A agents with their own parameters, moments
+    and minibatches, laid out with a stride wider than P, give bit for bit
+    what A tp_ppo_update calls give (two updates, so the second reads
+    moments the first wrote); the padding between agents is left alone.
+    With eight 1001-512-512-100 agents the launches with at least 512
+    tiles of 128 x 128 (layer 1, the first backward group, the weight
+    gradient of layer 1) run the 128 x 128 product kernel, which keeps the
+    k order of the 64 x 64 one, so the bits still agree."""
+    cfg = W.get_config(name)
+    dims, bf, c, host, dev = _setup(cfg, rows, B)
+    P = tp.ppo_param_count(c)
+    U, stride = 2, P + 7
+    rng = np.random.default_rng(21)
+    idx = np.stack([np.stack([rng.choice(rows, B, replace=False) for _ in range(U)])
+                    for _ in range(A)])
+    start = np.stack([W.make_flat_params(cfg, agent=a) for a in range(A)])
+    say(f"[ppo-agents] {name} A={A} U={U} P={P} stride={stride} B={B}")
+    prm = torch.full((A, stride), 7.0, device="cuda")
+    prm[:, :P] = torch.from_numpy(start).cuda()
+    m = torch.full((A, stride), 5.0, device="cuda")
+    v = torch.full((A, stride), 3.0, device="cuda")
+    m[:, :P] = 0.0
+    v[:, :P] = 0.0
+    grad = torch.empty(A, P, device="cuda")
+    stats = torch.empty(A, U, 4, dtype=torch.float64, device="cuda")
+    tp.ppo_update_agents(c, prm, m, v, 1, dev["obs"], dev["action"], dev["logp"], dev["adv"],
+                         dev["ret"], torch.from_numpy(idx).cuda(), tp.ppo_workspace(c, n_agents=A),
+                         grad=grad, stats=stats)
+    torch.cuda.synchronize()
+    assert (prm[:, P:] == 7.0).all() and (m[:, P:] == 5.0).all() and (v[:, P:] == 3.0).all()
+    ws = tp.ppo_workspace(c)
+    for a in range(A):
+        p1 = torch.from_numpy(start[a].copy()).cuda()
+        m1, v1 = torch.zeros(P, device="cuda"), torch.zeros(P, device="cuda")
+        g1 = torch.empty(P, device="cuda")
+        s1 = torch.empty(U, 4, dtype=torch.float64, device="cuda")
+        tp.ppo_update(c, p1, m1, v1, 1, dev["obs"], dev["action"], dev["logp"], dev["adv"],
+                      dev["ret"], torch.from_numpy(idx[a]).cuda(), ws, grad=g1, stats=s1)
+        torch.cuda.synchronize()
+        assert torch.equal(prm[a, :P], p1), a
+        assert torch.equal(m[a, :P], m1) and torch.equal(v[a, :P], v1), a
+        assert torch.equal(grad[a], g1) and torch.equal(stats[a], s1), a
+    # the agents really differ
+    assert not torch.equal(prm[0, :P], prm[1, :P])
