@@ -27,6 +27,10 @@ Times, with HIP events on the launch stream:
     2B (2 S H1 + 3 H1 H2 + 3 H2 n + 2 S C1 + 3 C1 C2 + 3 C2) (forward of
     both networks, weight gradients, and input gradients except layer 1's);
     then the same for 16 agents per call (tp_ppo_update_agents);
+  * train: one generation of the ensemble workload (4 agents x 4 pods of
+    1,024 envs, L = 390): rollout, critic, GAE, the learners' 8 L envs / B
+    updates each in one agent-batched call, fusion, fitness, keep-best and
+    selection;
   * probes: the device ceilings the roofline figures are read against,
     from libtpprobe.so: the dense bf16 MFMA issue rate (back-to-back
     v_mfma_f32_16x16x32_bf16 or v_mfma_f32_32x32x16_bf16 on register
@@ -76,7 +80,7 @@ def main():
     ap.add_argument("--iters", type=int, default=20)
     ap.add_argument("--only", default=None,
                     choices=["env_step", "gae", "critic", "metrics", "evolution", "learner",
-                             "probes", "copy"])
+                             "train", "probes", "copy"])
     args = ap.parse_args()
     sys.path.insert(0, __file__.rsplit("/", 2)[0])
     import workloads as W
@@ -262,6 +266,31 @@ def main():
                                       "TFLOPs": A * flops / sec / 1e12,
                                       "mfma_frac": A * flops / sec / 1e12 / PEAK_BF16_TFLOPS}
         del obs, act, logp, adv, ret, params, m, v, idx, ws
+        torch.cuda.empty_cache()
+
+    if args.only in (None, "train"):
+        # one generation of the ensemble workload: 4 agents x 4 pods (16
+        # learners of 1,024 envs), rollout, critic, GAE, 8 L envs / B
+        # updates per learner in one agent-batched call, fusion, fitness,
+        # keep-best and selection
+        from paper_2111_05188_amd.train import Trainer
+        ce = W.get_config("ensemble")
+        NA, KP = 4, 4
+        print(f"[kbench] train: {NA} agents x {KP} pods, E={ce.E}, L={ce.L}", file=sys.stderr,
+              flush=True)
+        mk = W.make_market(ce)
+        flat = np.stack([W.make_flat_params(ce, agent=a) for a in range(NA * KP)])
+        tr = Trainer(ce, mk, W.make_t0(ce), flat, NA, KP, device=dev)
+        del mk, flat
+        sec = _time(lambda: tr.epoch(stream), 1, stream)
+        L16 = NA * KP
+        out["train"] = {"generation_ms": sec * 1e3, "learners": L16,
+                        "updates_per_learner": tr.updates, "env_steps": ce.E * ce.L,
+                        "agent_updates_per_s": L16 * tr.updates / sec,
+                        "learner_TFLOPs": L16 * tr.updates * 2.0 * 1024 * (
+                            2 * 1001 * 512 + 3 * 512 * 512 + 3 * 512 * 100 + 2 * 1001 * 512
+                            + 3 * 512 * 512 + 3 * 512) / sec / 1e12}
+        del tr
         torch.cuda.empty_cache()
 
     if args.only in (None, "probes"):

@@ -69,8 +69,8 @@ class Trainer:
         self.updates = (updates if updates is not None
                         else max(1, 8 * (cfg.L * self.epa) // batch))
         self.keep = keep if keep is not None else max(1, n_agents // 2)
-        self.idx = torch.empty(self.updates, batch, dtype=torch.int64, device=device)
-        self.ws = tp.ppo_workspace(self.ppo, device)
+        self.idx = torch.empty(A, self.updates, batch, dtype=torch.int64, device=device)
+        self.ws = tp.ppo_workspace(self.ppo, device, n_agents=A)
         self.stats = torch.empty(A, self.updates, 4, dtype=torch.float64, device=device)
         self.env_return = torch.empty(self.E, dtype=torch.float64, device=device)
         self.fitness = torch.empty(n_agents, dtype=torch.float64, device=device)
@@ -95,12 +95,13 @@ class Trainer:
         act = self.traj.action.reshape(self.rows, n)
         logp = self.traj.logp.reshape(self.rows)
         adv, ret = self.adv.reshape(self.rows), self.ret.reshape(self.rows)
+        # every learner (agent x pod) draws its own rows, then all of them
+        # update together, each launch covering every learner
         for q in range(A):
             tp.minibatch_rows(seed, self.counter, self.updates, self.ppo.batch, cfg.L, self.E,
-                              q, self.epa, out=self.idx, stream=stream)
-            tp.ppo_update(self.ppo, self.flat[q], self.m[q], self.v[q], self.step, obs, act,
-                          logp, adv, ret, self.idx, self.ws, stats=self.stats[q],
-                          stream=stream)
+                              q, self.epa, out=self.idx[q], stream=stream)
+        tp.ppo_update_agents(self.ppo, self.flat, self.m, self.v, self.step, obs, act, logp, adv,
+                             ret, self.idx, self.ws, stats=self.stats, stream=stream)
         self.counter += self.updates
         self.step += self.updates
         if evolve:
