@@ -27,10 +27,10 @@ Times, with HIP events on the launch stream:
     2B (2 S H1 + 3 H1 H2 + 3 H2 n + 2 S C1 + 3 C1 C2 + 3 C2) (forward of
     both networks, weight gradients, and input gradients except layer 1's);
     then the same for 16 agents per call (tp_ppo_update_agents);
-  * train: one generation of the ensemble workload (4 agents x 4 pods of
-    1,024 envs, L = 390): rollout, critic, GAE, the learners' 8 L envs / B
-    updates each in one agent-batched call, fusion, fitness, keep-best and
-    selection;
+  * train (only with --only train): one generation of the ensemble
+    workload (4 agents x 4 pods of 1,024 envs, L = 390): rollout, critic,
+    GAE, the learners' 8 L envs / B updates each in one agent-batched call,
+    fusion, fitness, keep-best and selection;
   * probes: the device ceilings the roofline figures are read against,
     from libtpprobe.so: the dense bf16 MFMA issue rate (back-to-back
     v_mfma_f32_16x16x32_bf16 or v_mfma_f32_32x32x16_bf16 on register
@@ -268,7 +268,7 @@ def main():
         del obs, act, logp, adv, ret, params, m, v, idx, ws
         torch.cuda.empty_cache()
 
-    if args.only in (None, "train"):
+    if args.only == "train":   # opt-in: one generation is ~50,000 launches
         # one generation of the ensemble workload: 4 agents x 4 pods (16
         # learners of 1,024 envs), rollout, critic, GAE, 8 L envs / B
         # updates per learner in one agent-batched call, fusion, fitness,
