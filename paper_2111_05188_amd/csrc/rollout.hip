@@ -109,6 +109,12 @@ __device__ __forceinline__ void mfma_layer(const bf16x8 *__restrict__ W,
 
 // fp32 VALU layer: thread o computes output o for all MB envs; weights are
 // k-blocked transposes so consecutive threads read consecutive 16 bytes.
+// A layer with at most half as many outputs as threads (the action means)
+// gives each output T consecutive lanes (T the largest power of two with
+// out * T <= nthr, at most 64) that split its k-blocks and combine by xor
+// shuffles in a fixed order: 10% faster on the 30-stock daily shape, where
+// 30 threads would otherwise walk 64 k-blocks each.  Deeper unrolling of
+// the k loop measured slower.
 template <int MB, bool HIDDEN>
 __device__ __forceinline__ void valu_layer(const float4 *__restrict__ Wt,
                                            const float *__restrict__ bias,
@@ -116,6 +122,42 @@ __device__ __forceinline__ void valu_layer(const float4 *__restrict__ Wt,
                                            int ldx, float *Y, int ldy, int tid,
                                            int nthr)
 {
+    if (out * 2 <= nthr) {
+        int T = 1;
+        while (T < WAVE && out * T * 2 <= nthr) T *= 2;
+        const int span = (out * T + nthr - 1) / nthr * nthr;
+        for (int q = tid; q < span; q += nthr) {
+            const int o = q / T, sub = q % T;
+            const bool live = o < out;
+            const int oc = live ? o : out - 1;
+            float acc[MB];
+#pragma unroll
+            for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+            for (int k4 = sub; k4 < K4; k4 += T) {
+                const float4 w = Wt[(size_t)k4 * out + oc];
+#pragma unroll
+                for (int m = 0; m < MB; ++m) {
+                    const float4 x = *(const float4 *)(Xs + m * ldx + 4 * k4);
+                    acc[m] = fmaf(w.x, x.x, acc[m]);
+                    acc[m] = fmaf(w.y, x.y, acc[m]);
+                    acc[m] = fmaf(w.z, x.z, acc[m]);
+                    acc[m] = fmaf(w.w, x.w, acc[m]);
+                }
+            }
+            for (int d = 1; d < T; d *= 2)
+#pragma unroll
+                for (int m = 0; m < MB; ++m) acc[m] += __shfl_xor(acc[m], d);
+            if (live && sub == 0) {
+                const float bo = bias[o];
+#pragma unroll
+                for (int m = 0; m < MB; ++m) {
+                    const float v = acc[m] + bo;
+                    Y[m * ldy + o] = HIDDEN ? tanhf(v) : v;
+                }
+            }
+        }
+        return;
+    }
     for (int o = tid; o < out; o += nthr) {
         float acc[MB];
 #pragma unroll
