@@ -46,9 +46,10 @@ def algorithmic_bytes_gae() -> int:
     return 4 + 4 + 1 + 4 + 4
 
 
-# Sources the rollout kernels are built from: counters taken on an older
-# version of any of them no longer describe the kernel.
-ROLLOUT_SOURCES = ("rollout_rs.hip", "rollout.hip", "env.hpp", "device.hpp")
+# Sources the role-split rollout kernel (the one the counters describe) is
+# built from: counters taken on an older version of any of them no longer
+# describe the kernel.
+ROLLOUT_SOURCES = ("rollout_rs.hip", "env.hpp", "device.hpp", "internal.hpp")
 
 
 def kernel_source_hash() -> str:
@@ -72,6 +73,8 @@ def counter_traffic(kernel_key: str):
     except (OSError, IndexError, ValueError):
         return None
     if data.get("source_sha256") != kernel_source_hash():
+        return None
+    if not kernel_key.startswith("rollout_rs_kernel "):
         return None
     k = data.get("kernels", {}).get(kernel_key)
     return None if k is None else k["traffic_bytes"]
