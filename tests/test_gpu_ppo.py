@@ -237,3 +237,34 @@ def test_agents_in_one_call_equal_single_calls(name, rows, B, A):
         assert torch.equal(grad[a], g1) and torch.equal(stats[a], s1), a
     # the agents really differ
     assert not torch.equal(prm[0, :P], prm[1, :P])
+
+
+def test_agents_at_the_maximum_count():
+    """1,024 learners (the documented maximum; a grid dimension of 1,024) of
+    the tiny fp32 shape in one call: sampled agents equal their own
+    tp_ppo_update calls bit for bit."""
+    cfg = W.get_config("tiny")
+    rows, B, A = 512, 64, 1024
+    dims, bf, c, host, dev = _setup(cfg, rows, B)
+    P = tp.ppo_param_count(c)
+    rng = np.random.default_rng(33)
+    idx = rng.integers(0, rows, (A, 1, B))
+    start = np.stack([host["flat"] * (1.0 + 1e-3 * (a % 7)) for a in range(A)]).astype(np.float32)
+    say(f"[ppo-agents] tiny A={A} P={P} B={B}")
+    prm = torch.from_numpy(start).cuda()
+    m, v = torch.zeros_like(prm), torch.zeros_like(prm)
+    grad = torch.empty(A, P, device="cuda")
+    tp.ppo_update_agents(c, prm, m, v, 1, dev["obs"], dev["action"], dev["logp"], dev["adv"],
+                         dev["ret"], torch.from_numpy(idx).cuda(), tp.ppo_workspace(c, n_agents=A),
+                         grad=grad)
+    torch.cuda.synchronize()
+    ws = tp.ppo_workspace(c)
+    for a in (0, 1, 517, 1023):
+        p1 = torch.from_numpy(start[a].copy()).cuda()
+        m1, v1 = torch.zeros(P, device="cuda"), torch.zeros(P, device="cuda")
+        g1 = torch.empty(P, device="cuda")
+        tp.ppo_update(c, p1, m1, v1, 1, dev["obs"], dev["action"], dev["logp"], dev["adv"],
+                      dev["ret"], torch.from_numpy(idx[a]).cuda(), ws, grad=g1)
+        torch.cuda.synchronize()
+        assert torch.equal(prm[a], p1) and torch.equal(grad[a], g1), a
+        assert torch.equal(m[a], m1) and torch.equal(v[a], v1), a
