@@ -268,3 +268,53 @@ def test_agents_at_the_maximum_count():
         torch.cuda.synchronize()
         assert torch.equal(prm[a], p1) and torch.equal(grad[a], g1), a
         assert torch.equal(m[a], m1) and torch.equal(v[a], v1), a
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_critic_widths_other_than_the_actors(dtype):
+    """The critic's widths are free (multiples of 32): the tiny 31-64-64-5
+    actor with a 96-32 critic, whose first layer joins the actor's in the
+    concatenated [W1; Wc1] product.  In bf16 these widths take the unstaged
+    product kernel (K not in {128, 512, 1024}).  Gradient against the
+    oracle, per segment."""
+    cfg = W.get_config("tiny").with_(dtype=dtype)
+    S, H1, H2, n = cfg.dims
+    dims = (S, H1, H2, n, 96, 32)
+    bf = dtype == "bf16"
+    rows, B = 512, 64
+    rng = np.random.default_rng(57)
+    parts = []
+    for name, shape in ppo.layout(*dims):
+        if name == "log_std":
+            parts.append(np.full(shape, -0.5))
+        elif len(shape) == 2:
+            parts.append(rng.uniform(-1, 1, shape) / np.sqrt(shape[1]))
+        else:
+            parts.append(rng.uniform(-0.1, 0.1, shape))
+    flat = np.concatenate([p.reshape(-1) for p in parts]).astype(np.float32)
+    obs, action, adv, ret, which = W.make_learner_data(cfg, rows)
+    obs_t = torch.from_numpy(obs)
+    if bf:
+        obs_t = obs_t.to(torch.bfloat16)
+    obs_vals = obs_t.float().numpy()
+    p = ppo.unflatten(flat.astype(np.float64), dims)
+    f = ppo.forward(p, obs_vals[:, :S], bf16=bf)
+    logp = (ppo.log_prob(action, f["mu"], p["log_std"])
+            - np.asarray(W.LOG_RATIO_OFFSETS)[which]).astype(np.float32)
+    c = tp.ppo_cfg(dims, tp.TP_BF16 if bf else tp.TP_F32, B)
+    P = tp.ppo_param_count(c)
+    assert P == flat.shape[0]
+    idx = rng.choice(rows, B, replace=False)[None]
+    say(f"[ppo] tiny actor, 96-32 critic, {dtype}, P={P}")
+    prm = torch.from_numpy(flat.copy()).cuda()
+    m, v = torch.zeros(P, device="cuda"), torch.zeros(P, device="cuda")
+    grad = torch.empty(P, device="cuda")
+    tp.ppo_update(c, prm, m, v, 1, obs_t.cuda(), torch.from_numpy(action).cuda(),
+                  torch.from_numpy(logp).cuda(), torch.from_numpy(adv).cuda(),
+                  torch.from_numpy(ret).cuda(), torch.from_numpy(idx).cuda(), tp.ppo_workspace(c),
+                  grad=grad)
+    torch.cuda.synchronize()
+    batch = ppo.gather(obs_vals, action, logp, adv, ret, idx[0], S)
+    _, _, _, _, g_o = ppo.update(flat.astype(np.float64), np.zeros(P), np.zeros(P), 1, dims,
+                                 batch, bf16=bf)
+    _check_grad(dims, grad.cpu().numpy(), g_o, GRAD_TOL[dtype], f"critic 96-32 {dtype}")
