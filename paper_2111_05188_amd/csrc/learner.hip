@@ -653,28 +653,49 @@ __device__ __forceinline__ int64_t clamp_row(int64_t r, int64_t rows)
 // observation rows idx[i] (columns >= S zeroed), plus the per-row
 // transition data.  Tiles of 64 rows x 64 columns through LDS.
 // ---------------------------------------------------------------------------
+// One update's minibatch gather, as a workgroup body: block (bx, by) of a
+// cdiv(B, 64) x cdiv(Kp, 64) grid, agent `agent`.
 template <bool BF>
-__global__ __launch_bounds__(256) void gather_kernel(
-    const Elem<BF> *__restrict__ obs, int64_t ld_obs, int vec_obs, const float *__restrict__ action,
-    const float *__restrict__ logp, const float *__restrict__ adv, const float *__restrict__ ret,
-    const int64_t *__restrict__ idx, int64_t rows, int B, int S, int Kp, int n,
-    Elem<BF> *__restrict__ X, Elem<BF> *__restrict__ Xt, float *__restrict__ Ag,
-    float *__restrict__ row_in, int64_t aws, int64_t aidx)
+struct GatherArgs {
+    const Elem<BF> *obs;
+    int64_t ld_obs;
+    int vec_obs;
+    const float *action, *logp, *adv, *ret;
+    const int64_t *idx;   // this update's rows of agent 0; agents aidx apart
+    int64_t rows;
+    int B, S, Kp, n;
+    Elem<BF> *X, *Xt;
+    float *Ag, *row_in;
+    int64_t aws, aidx;
+    int gx, gy;           // the grid: cdiv(B, 64) x cdiv(Kp, 64)
+};
+
+template <bool BF>
+struct GatherSmem {
+    int64_t s_idx[64];
+    Elem<BF> tile[64][64 + 16 / sizeof(Elem<BF>)];
+};
+
+template <bool BF>
+__device__ __forceinline__ void gather_block(const GatherArgs<BF> &ga, int bx, int by, int agent,
+                                             GatherSmem<BF> &sm)
 {
     typedef uint32_t v4u __attribute__((ext_vector_type(4)));
-    {   // agent blockIdx.z: its workspace and its minibatch indices
-        const size_t w = (size_t)blockIdx.z * (size_t)aws;
-        idx += (size_t)blockIdx.z * (size_t)aidx;
-        X = shifted(X, w);
-        Xt = shifted(Xt, w);
-        Ag = shifted(Ag, w);
-        row_in = shifted(row_in, w);
-    }
+    const size_t w = (size_t)agent * (size_t)ga.aws;
+    const Elem<BF> *__restrict__ obs = ga.obs;
+    const float *__restrict__ action = ga.action;
+    const int64_t *__restrict__ idx = shifted(ga.idx, (size_t)agent * (size_t)ga.aidx * 8);
+    Elem<BF> *__restrict__ X = shifted(ga.X, w);
+    Elem<BF> *__restrict__ Xt = shifted(ga.Xt, w);
+    float *__restrict__ Ag = shifted(ga.Ag, w);
+    float *__restrict__ row_in = shifted(ga.row_in, w);
+    const int64_t ld_obs = ga.ld_obs, rows = ga.rows;
+    const int B = ga.B, S = ga.S, Kp = ga.Kp, n = ga.n, vec_obs = ga.vec_obs;
     constexpr int VE = 16 / sizeof(Elem<BF>);   // elements per 16-byte vector
     constexpr int VPR = 64 / VE;                 // vectors per tile row
-    __shared__ int64_t s_idx[64];
-    __shared__ Elem<BF> tile[64][64 + VE];
-    const int i0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    int64_t *s_idx = sm.s_idx;
+    auto &tile = sm.tile;
+    const int i0 = bx * 64, c0 = by * 64;
     const int tid = threadIdx.x;
     if (tid < 64) s_idx[tid] = i0 + tid < B ? clamp_row(idx[i0 + tid], rows) : 0;
     __syncthreads();
@@ -718,18 +739,18 @@ __global__ __launch_bounds__(256) void gather_kernel(
         *(v4u *)(Xt + (size_t)col * B + i) = u.v;
     }
     // actions, spread over the column blocks; per-row scalars in the first
-    const int per = (n + gridDim.y - 1) / gridDim.y;
-    const int k0 = blockIdx.y * per, k1 = min(n, k0 + per);
+    const int per = (n + ga.gy - 1) / ga.gy;
+    const int k0 = by * per, k1 = min(n, k0 + per);
     for (int q = tid; q < 64 * (k1 - k0); q += 256) {
         const int r = q / (k1 - k0), k = k0 + q % (k1 - k0);
         if (i0 + r < B) Ag[(size_t)(i0 + r) * n + k] = action[(size_t)s_idx[r] * n + k];
     }
-    if (blockIdx.y == 0 && tid < 64 && i0 + tid < B) {
+    if (by == 0 && tid < 64 && i0 + tid < B) {
         const int i = i0 + tid;
         const int64_t g = s_idx[tid];
-        row_in[i] = logp[g];
-        row_in[B + i] = adv[g];
-        row_in[2 * B + i] = ret[g];
+        row_in[i] = ga.logp[g];
+        row_in[B + i] = ga.adv[g];
+        row_in[2 * B + i] = ga.ret[g];
     }
 }
 
@@ -1149,24 +1170,34 @@ __device__ __forceinline__ void reduce_row(const RedBatch &rb, const AdamBatch &
 // takes tile (b % 8) per + b / 8 and each XCD walks a contiguous run of
 // tiles (rows of W1 and Wc1 are not line-aligned: neighbouring tiles share
 // lines, now in one L2).  For agent y the XCD of block b is that of b + y
-// gridDim.x, so blocks with equal b % 8 still share one.
+// gridDim.x, so blocks with equal b % 8 still share one.  The next
+// cdiv(rows, 4) blocks take the row sums; the last gblocks blocks gather the
+// next update's minibatch (its X, X^T, actions and row data are read by
+// nothing in this launch, and by nothing of this update after it).
 template <bool BF>
-__global__ __launch_bounds__(256) void adam_tail_kernel(AdamBatch ab, RedBatch rb, int mtiles)
+__global__ __launch_bounds__(256) void adam_tail_kernel(AdamBatch ab, RedBatch rb, int mtiles,
+                                                        GatherArgs<BF> ga, int gblocks)
 {
     __shared__ Elem<BF> tile[AT][AT + 1];
+    __shared__ GatherSmem<BF> gsm;
     // agent blockIdx.y
     const size_t q = (size_t)blockIdx.y * (size_t)ab.aprm;
     const AdamPtrs ap{shifted(ab.params, q), shifted(ab.m, q), shifted(ab.v, q),
                       shifted(ab.grad, (size_t)blockIdx.y * (size_t)ab.aws)};
-    const int per = (mtiles + 7) / 8;
+    const int per = (mtiles + 7) / 8, rblocks = (rb.total_rows + 3) / 4;
     const int b = blockIdx.x;
     if (b < 8 * per) {
         const int t = (b % 8) * per + b / 8;
         if (t < mtiles) adam_tile<BF>(ab, ap, t, tile);
         return;
     }
-    const int g = (b - 8 * per) * 4 + threadIdx.x / WAVE;
-    if (g < rb.total_rows) reduce_row(rb, ab, ap, g);
+    if (b < 8 * per + rblocks) {
+        const int g = (b - 8 * per) * 4 + threadIdx.x / WAVE;
+        if (g < rb.total_rows) reduce_row(rb, ab, ap, g);
+        return;
+    }
+    const int g = b - 8 * per - rblocks;
+    if (g < gblocks) gather_block<BF>(ga, g % ga.gx, g / ga.gx, blockIdx.y, gsm);
 }
 
 // Minibatch rows: draw i of update counter c for agent g is word i % 4 of
@@ -1407,18 +1438,56 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
     // steps in the row sums that produce their gradients.
     const int mtiles = atiles;
 
-    // Adam (or, with do_adam = 0, only the operand-copy refresh) and the
-    // row sums, one launch
-    auto tail = [&](int do_adam, int64_t step, const RedBatch &rb) -> hipError_t {
+    // the minibatch gather of update u (it rides in the launch before that
+    // update: the initial refresh, or update u - 1's tail)
+    const int vec_obs = ((uintptr_t)a.obs % 16 == 0 && (a.ld_obs * (int64_t)es) % 16 == 0) ? 1 : 0;
+    GatherArgs<true> gab{};
+    GatherArgs<false> gaf{};
+    auto gather_args = [&](auto &g, int u) {
+        typedef std::remove_const_t<std::remove_reference_t<decltype(*g.obs)>> E;
+        g.obs = (const E *)a.obs;
+        g.ld_obs = a.ld_obs;
+        g.vec_obs = vec_obs;
+        g.action = a.action;
+        g.logp = a.logp;
+        g.adv = a.adv;
+        g.ret = a.ret;
+        g.idx = a.idx + (size_t)u * B;
+        g.rows = a.rows;
+        g.B = B;
+        g.S = L.S;
+        g.Kp = L.Kp;
+        g.n = L.n;
+        g.X = (E *)W(L.wX);
+        g.Xt = (E *)W(L.wXt);
+        g.Ag = (float *)W(L.wAg);
+        g.row_in = (float *)W(L.wRowIn);
+        g.aws = ag.aws;
+        g.aidx = (int64_t)a.n_updates * B;
+        g.gx = cdiv(B, 64);
+        g.gy = cdiv(L.Kp, 64);
+    };
+
+    // Adam (or, with do_adam = 0, only the operand-copy refresh), the row
+    // sums and the gather of update gu (none if gu < 0), one launch
+    auto tail = [&](int do_adam, int64_t step, const RedBatch &rb, int gu) -> hipError_t {
         ab.do_adam = do_adam;
         ab.bc1 = (float)(1.0 - pow((double)a.beta1, (double)step));
         ab.bc2 = (float)(1.0 - pow((double)a.beta2, (double)step));
-        const dim3 grid(8 * cdiv(mtiles, 8) + cdiv(rb.total_rows, 4), NA);
-        if (bf) hipLaunchKernelGGL(adam_tail_kernel<true>, grid, dim3(256), 0, s, ab, rb, mtiles);
-        else hipLaunchKernelGGL(adam_tail_kernel<false>, grid, dim3(256), 0, s, ab, rb, mtiles);
+        const int gblocks = gu >= 0 ? cdiv(B, 64) * cdiv(L.Kp, 64) : 0;
+        const dim3 grid(8 * cdiv(mtiles, 8) + cdiv(rb.total_rows, 4) + gblocks, NA);
+        if (bf) {
+            gather_args(gab, gu >= 0 ? gu : 0);
+            hipLaunchKernelGGL(adam_tail_kernel<true>, grid, dim3(256), 0, s, ab, rb, mtiles, gab,
+                               gblocks);
+        } else {
+            gather_args(gaf, gu >= 0 ? gu : 0);
+            hipLaunchKernelGGL(adam_tail_kernel<false>, grid, dim3(256), 0, s, ab, rb, mtiles, gaf,
+                               gblocks);
+        }
         return hipGetLastError();
     };
-    hipError_t e = tail(0, 1, RedBatch{});
+    hipError_t e = tail(0, 1, RedBatch{}, 0);
     if (e != hipSuccess) return e;
 
     void *X = W(L.wX), *Xt = W(L.wXt), *H1 = W(L.wH1), *H1t = W(L.wH1t);
@@ -1431,25 +1500,7 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
     void *dZ1t = W(L.wdZ1t);
     auto at = [&](void *base, size_t elems) { return (void *)((uint8_t *)base + elems * es); };
 
-    // observation rows take 16-byte loads when every row starts 16-byte aligned
-    const int vec_obs = ((uintptr_t)a.obs % 16 == 0 && (a.ld_obs * (int64_t)es) % 16 == 0) ? 1 : 0;
     for (int u = 0; u < a.n_updates; ++u) {
-        const int64_t *idx = a.idx + (size_t)u * B;
-        // gather
-        {
-            const dim3 grid(cdiv(B, 64), cdiv(L.Kp, 64), NA);
-            const int64_t aidx = (int64_t)a.n_updates * B;
-            if (bf)
-                hipLaunchKernelGGL(gather_kernel<true>, grid, dim3(256), 0, s,
-                                   (const __bf16 *)a.obs, a.ld_obs, vec_obs, a.action, a.logp,
-                                   a.adv, a.ret, idx, a.rows, B, L.S, L.Kp, L.n, (__bf16 *)X,
-                                   (__bf16 *)Xt, Ag, row_in, ag.aws, aidx);
-            else
-                hipLaunchKernelGGL(gather_kernel<false>, grid, dim3(256), 0, s,
-                                   (const float *)a.obs, a.ld_obs, vec_obs, a.action, a.logp,
-                                   a.adv, a.ret, idx, a.rows, B, L.S, L.Kp, L.n, (float *)X,
-                                   (float *)Xt, Ag, row_in, ag.aws, aidx);
-        }
         // forward 1: [h1 | hc1] = tanh(X [W1; Wc1]^T + [b1 | bc1])
         {
             GemmProb p = prob(X, L.Kp, W(L.wWcat1), L.Kp, B, L.HC1, L.Kp, EPI_TANH);
@@ -1595,7 +1646,8 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
                 add(row_out + 4 * B, B, 1, B, 0, nullptr, -1, st + 3, 1.0 / B, 0.0);
             }
             rb.total_rows = rows;
-            if ((e = tail(1, a.step0 + u, rb)) != hipSuccess) return e;
+            if ((e = tail(1, a.step0 + u, rb, u + 1 < a.n_updates ? u + 1 : -1)) != hipSuccess)
+                return e;
         }
     }
     if (a.grad_out)   // [A][P] from the agents' workspaces
