@@ -476,14 +476,37 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
 
         // slot L2: indicators of row t0+j+1 into x_{j+1} (the matrix waves
         // are done with x_j); the normals of step j
-        if (live) {
-            __bf16 *ri = xrow + 1 + 2 * n;
+        {
+            // 8-byte stores of columns 2n + 4k .. +3 for chunks k = hl + HALF mm
+            // <= nI / 4: indicator values 4k - 1 .. 4k + 2 (indicator i sits in
+            // column 2n + 1 + i).  Value 4k - 1 is element 3 of chunk k - 1, from
+            // the neighbouring lane of this half-wave.  Column 2n (the last
+            // holding) gets a placeholder that slot A overwrites before anything
+            // reads it; the columns past the last indicator are zero padding.
+            static_assert(n % 4 == 0, "chunk starts are 8-byte aligned");
+            constexpr int NCH = nI / 4 + 1;
+            constexpr int IPW = (NCH + HALF - 1) / HALF;
+            const int base = lane - hl;   // this half-wave's first lane
+            float prev[IPW];
 #pragma unroll
-            for (int mm = 0; mm < IPC; ++mm) {
-                const int kk = 4 * (hl + HALF * mm);
-                if (kk < nI) {
+            for (int mm = 0; mm < IPW; ++mm) {
+                const float up = mm < IPC ? __shfl(ind[mm < IPC ? mm : 0][3], lane - (hl > 0)) : 0.f;
+                const float wrap = mm > 0 ? __shfl(ind[mm - 1 < IPC ? mm - 1 : 0][3], base + HALF - 1)
+                                          : 0.f;
+                prev[mm] = hl > 0 ? up : wrap;
+            }
+            if (live) {
+                __bf16 *rc = xrow + 2 * n;
 #pragma unroll
-                    for (int c = 0; c < 4; ++c) ri[kk + c] = to_bf16(ind[mm][c]);
+                for (int mm = 0; mm < IPW; ++mm) {
+                    const int k = hl + HALF * mm;
+                    if (k < NCH) {
+                        const bool own = k < nI / 4;
+                        const f4v v = mm < IPC ? ind[mm < IPC ? mm : 0] : f4v{0.f, 0.f, 0.f, 0.f};
+                        *(bf16x4 *)(rc + 4 * k) =
+                            bf16x4{to_bf16(prev[mm]), to_bf16(own ? v[0] : 0.f),
+                                   to_bf16(own ? v[1] : 0.f), to_bf16(own ? v[2] : 0.f)};
+                    }
                 }
             }
         }
