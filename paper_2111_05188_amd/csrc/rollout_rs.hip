@@ -317,20 +317,36 @@ __device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
 // ---------------------------------------------------------------------------
 // Balance, prices and holdings of an observation row (the indicator part is
 // written separately, one slot earlier).
+// Balance, prices and holdings of an observation row (columns 0 .. 2n; the
+// indicator part is written separately, one slot earlier), in aligned
+// 8-byte stores: lane s (s < n / 4, owner of stocks 4s .. 4s+3) writes
+// columns 4s .. 4s+3 = [price 4s-1 (lane s-1's last), prices 4s .. 4s+2]
+// and columns n + 4s .. n + 4s + 3 = [holding 4s-1, holdings 4s .. 4s+2];
+// lane 0 starts the first with the balance and the second with the last
+// price; column 2n (the last holding) is one 2-byte store.  All lanes of
+// the wave call it (it shuffles); only `live` halves store.
 template <int n>
 __device__ __forceinline__ void write_obs_state(__bf16 *row, const EnvConst &C, double cash,
                                                 const int (&h)[SPL], const float (&p)[SPL],
-                                                int hl)
+                                                int lane, int hl, bool live)
 {
-    if (hl == 0) row[0] = to_bf16((float)(cash * (double)C.cash_scale));
+    static_assert(n % 4 == 0 && n / 4 <= HALF, "one chunk of each kind per lane");
+    float pv[SPL], hv[SPL];
 #pragma unroll
     for (int c = 0; c < SPL; ++c) {
-        const int i = SPL * hl + c;
-        if (i < n) {
-            row[1 + i] = to_bf16(p[c] * C.price_scale);
-            row[1 + n + i] = to_bf16((float)h[c] * C.share_scale);
-        }
+        pv[c] = p[c] * C.price_scale;
+        hv[c] = (float)h[c] * C.share_scale;
     }
+    const int base = lane - hl;
+    const float p_up = __shfl(pv[3], lane - (hl > 0)), h_up = __shfl(hv[3], lane - (hl > 0));
+    const float p_last = __shfl(pv[3], base + n / 4 - 1), h_last = __shfl(hv[3], base + n / 4 - 1);
+    if (!live || hl >= n / 4) return;
+    const float bal = (float)(cash * (double)C.cash_scale);
+    *(bf16x4 *)(row + 4 * hl) = bf16x4{to_bf16(hl > 0 ? p_up : bal), to_bf16(pv[0]), to_bf16(pv[1]),
+                                       to_bf16(pv[2])};
+    *(bf16x4 *)(row + n + 4 * hl) = bf16x4{to_bf16(hl > 0 ? h_up : p_last), to_bf16(hv[0]),
+                                           to_bf16(hv[1]), to_bf16(hv[2])};
+    if (hl == n / 4 - 1) row[2 * n] = to_bf16(h_last);
 }
 
 template <int NS, int NI, int KPAD>
@@ -423,7 +439,7 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
         float r = 0.f;
         if (wave_live) r = env_step_half<NS>(C, st, a, qq, live, lane, lp);
         lp -= half_log2pi_n;
-        if (live) write_obs_state<NS>(xrow, C, st.cash, st.h, st.p, hl);
+        write_obs_state<NS>(xrow, C, st.cash, st.h, st.p, lane, hl, live);
         if (!mine) return;
         const size_t row = (size_t)jj * E + e;
         const uint8_t done = (uint8_t)(A.step0 + (uint64_t)jj + 1 == (uint64_t)C.horizon);
