@@ -251,6 +251,62 @@ __device__ __forceinline__ void write_obs_half(T *row, const EnvConst &C, double
     for (int kk = S + hl; kk < C.K_pad; kk += HALF) row[kk] = obs_cvt<T>(0.0f);
 }
 
+// The same row for bf16 observations when n and nI are multiples of 4 and
+// the indicator rows are 16-byte aligned, in aligned 8-byte stores of
+// columns 4k .. 4k+3: the value of column 4k belongs to the neighbouring
+// chunk's owner and comes by shuffle.  Lane s < n/4 (stocks 4s .. 4s+3)
+// writes columns 4s .. +3 = [price 4s-1, prices 4s .. 4s+2] and n + 4s ..
+// +3 = [holding 4s-1, holdings 4s .. 4s+2] (lane 0: the balance, the last
+// price); indicator chunk k (lane k % 32) writes columns 2n + 4k .. +3 =
+// [indicator 4k-1, indicators 4k .. 4k+2] (chunk 0: the last holding),
+// zeros past the last indicator; then the zero padding.  Every lane of
+// the wave calls it (it shuffles; irow must be readable for every half);
+// halves with `live` false store nothing.
+__device__ __forceinline__ void write_obs_half_aligned(__bf16 *row, const EnvConst &C, double cash,
+                                                       const int (&h)[SPL],
+                                                       const float (&p)[SPL],
+                                                       const float *irow, int lane, int hl,
+                                                       bool live)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const int n = C.n, nI = C.nI, nq = n / 4, base = lane - hl;
+    float pv[SPL], hv[SPL];
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        pv[c] = p[c] * C.price_scale;
+        hv[c] = (float)h[c] * C.share_scale;
+    }
+    const int up = lane - (hl > 0);
+    const float p_up = __shfl(pv[3], up), h_up = __shfl(hv[3], up);
+    const float p_last = __shfl(pv[3], base + nq - 1), h_last = __shfl(hv[3], base + nq - 1);
+    const int nch = nI / 4 + 1, rounds = (nch + HALF - 1) / HALF;
+    float last3 = 0.f;
+    for (int m = 0; m < rounds; ++m) {   // the same trip count in every lane
+        const int k = hl + HALF * m;
+        const f4 v = *(const f4 *)(irow + 4 * min(k, nI / 4 - 1));
+        const float v_up = __shfl(v[3], up), v_wrap = __shfl(last3, base + HALF - 1);
+        const float first = hl > 0 ? v_up : (m > 0 ? v_wrap : h_last);
+        if (live && k < nch) {
+            const bool own = k < nI / 4;
+            *(bf16x4 *)(row + 2 * n + 4 * k) =
+                bf16x4{to_bf16(first), to_bf16(own ? v[0] : 0.f), to_bf16(own ? v[1] : 0.f),
+                       to_bf16(own ? v[2] : 0.f)};
+        }
+        last3 = v[3];
+    }
+    if (!live) return;
+    if (hl < nq) {
+        const float bal = (float)(cash * (double)C.cash_scale);
+        *(bf16x4 *)(row + 4 * hl) = bf16x4{to_bf16(hl > 0 ? p_up : bal), to_bf16(pv[0]),
+                                           to_bf16(pv[1]), to_bf16(pv[2])};
+        *(bf16x4 *)(row + n + 4 * hl) = bf16x4{to_bf16(hl > 0 ? h_up : p_last), to_bf16(hv[0]),
+                                               to_bf16(hv[1]), to_bf16(hv[2])};
+    }
+    const bf16x4 zero = {to_bf16(0.f), to_bf16(0.f), to_bf16(0.f), to_bf16(0.f)};
+    for (int c4 = (2 * n) / 4 + nch + hl; c4 < C.K_pad / 4; c4 += HALF)
+        *(bf16x4 *)(row + 4 * c4) = zero;
+}
+
 // Copy `bytes` (a multiple of 16) with 16-byte accesses, lanes l = 0..nl-1
 // of the calling group participating.
 __device__ __forceinline__ void copy16(void *dst, const void *src, size_t bytes,

@@ -92,6 +92,9 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
     }
     double none = 0.0;
     const float r = env_step_half(C, s, a, q, live, lane, none);
+    // bf16 rows of 4k stocks and 4k indicator values go out in aligned stores
+    const bool aligned_obs = sizeof(OT) == 2 && C.n % 4 == 0 && C.nI % 4 == 0 &&
+                             (uintptr_t)C.ind % 16 == 0;
     if (live) {
 #pragma unroll
         for (int c = 0; c < SPL; ++c) {
@@ -103,7 +106,7 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
             t[e] = tt + 1;
             reward[e] = r;
         }
-        if (obs) {
+        if (obs && !aligned_obs) {
             const float *irow = C.ind + (size_t)(tt + 1) * C.nI;
             float ind1[1];
             ind1[0] = hl < C.nI ? irow[hl] : 0.f;
@@ -113,6 +116,11 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
         if (hl == 0) reward[e] = __builtin_nanf("");
         if (obs)
             for (int k = hl; k < C.K_pad; k += HALF) row[k] = obs_cvt<OT>(__builtin_nanf(""));
+    }
+    if constexpr (sizeof(OT) == 2) {
+        if (obs && aligned_obs)   // every lane (shuffles); only live halves store
+            write_obs_half_aligned(row, C, s.cash, s.h, q, C.ind + (size_t)(live ? tt + 1 : 0) * C.nI,
+                                   lane, hl, live);
     }
     __syncthreads();
     if (in && obs)

@@ -116,3 +116,30 @@ def test_env_reset(name):
         g = bits16(obs[e]) if cfg.dtype == "bf16" else obs[e].cpu().numpy()
         assert np.array_equal(g, o)
     assert (obs[5].float() == 0).all()
+
+
+def test_env_step_bf16_rows_with_envs_not_stepped():
+    """bf16 observation rows of the 100-stock shape (the aligned-store path)
+    when envs that are not stepped (t = -1 or the last market row) share
+    waves and workgroups with envs that are: the stepped envs' rows equal
+    the oracle's bit for bit, the others are all NaN, rewards NaN."""
+    rows = 300
+    cfg, mk, cash, shares, _, act = _setup("nasdaq100", 10, rows, 23)
+    t = np.array([-1, rows - 1, 10, 11, -1, 12, rows - 1, 3, 4, 5], np.int64)
+    live = (t >= 0) & (t < rows - 1)
+    say("[env_step] nasdaq100 bf16 rows, envs not stepped mixed in")
+    dev = "cuda"
+    mkt = tp.MarketT(torch.from_numpy(mk.price).to(dev), torch.from_numpy(mk.ind).to(dev))
+    st = tp.StateT(torch.from_numpy(cash).to(dev), torch.from_numpy(shares).to(dev),
+                   torch.from_numpy(t).to(dev))
+    rew = torch.empty(10, dtype=torch.float32, device=dev)
+    obs = torch.full((10, cfg.K_pad), 7.0, dtype=torch.bfloat16, device=dev)
+    tp.env_step(mkt, problem.env_cfg(cfg), st, torch.from_numpy(act).to(dev), rew, obs)
+    torch.cuda.synchronize()
+    m, oc = oracle.market(mk.price, mk.ind), oracle.env_cfg(cfg)
+    c_cash, c_sh, c_t = cash[live].copy(), shares[live].copy(), t[live].copy()
+    r_o, obs_o = oracle.env_step(m, oc, c_cash, c_sh, c_t, act[live], cfg.K_pad, True)
+    assert np.array_equal(bits16(obs[torch.from_numpy(live).to(dev)]), obs_o)
+    rel_check("reward", rew.cpu().numpy()[live], r_o, TOL_REWARD)
+    assert np.isnan(rew.cpu().numpy()[~live]).all()
+    assert torch.isnan(obs[torch.from_numpy(~live).to(dev)].float()).all()
