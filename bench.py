@@ -12,8 +12,9 @@ Prints one JSON line:
   roofline   the fused rollout kernel against the bf16 MFMA peak (its
              algorithmic FLOPs / its average duration, measured with HIP
              events on its stream), plus its HBM figure (algorithmic bytes)
-  cpu_baseline  the oracle on the host cores on a bounded sample of the same
-             workload (32 envs x one 390-step episode)
+  cpu_baseline  the oracle on one host core on a bounded sample of the same
+             workload (64 envs x one 390-step episode by default), with the
+             host's CPU model
 """
 
 from __future__ import annotations
@@ -211,29 +212,48 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(cfg, mk, params, t0, n_envs):
+def host_cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(cfg, mk, params, t0, n_envs, chunk=64):
     """The oracle, as it stands, on a bounded sample: n_envs envs of the same
-    workload for one full episode (free-running, single thread)."""
+    workload for one full episode (free-running, single thread).  Envs are
+    independent, so the sample runs in chunks of `chunk` envs, each chunk's
+    rollout + GAE timed and the times summed; a progress line follows each
+    chunk."""
     import numpy as np
 
     import oracle
     m = oracle.market(mk.price, mk.ind, mk.row0)
     ec = oracle.env_cfg(cfg)
     act = oracle.actor(*params, cfg.dims, cfg.dtype == "bf16", cfg.envs_per_agent)
-    ids = np.arange(n_envs)
-    cash, sh, t = oracle.env_reset(ec, t0[ids], cfg.n)
     print(f"[bench] oracle sample: {n_envs} envs x {cfg.L} steps", file=sys.stderr, flush=True)
-    t1 = time.time()
-    out = oracle.rollout(m, ec, act, cash, sh, t, SEED, 0, cfg.L, cfg.K_pad, env_ids=ids,
-                         want=("reward", "done"))
-    v = np.zeros((cfg.L + 1, n_envs), np.float32)
-    oracle.gae(out["reward"], v, out["done"], cfg.gamma, cfg.lam)
-    dt = time.time() - t1
+    dt = 0.0
+    for c0 in range(0, n_envs, chunk):
+        ids = np.arange(c0, min(n_envs, c0 + chunk))
+        cash, sh, t = oracle.env_reset(ec, t0[ids], cfg.n)
+        t1 = time.time()
+        out = oracle.rollout(m, ec, act, cash, sh, t, SEED, 0, cfg.L, cfg.K_pad, env_ids=ids,
+                             want=("reward", "done"))
+        v = np.zeros((cfg.L + 1, len(ids)), np.float32)
+        oracle.gae(out["reward"], v, out["done"], cfg.gamma, cfg.lam)
+        dt += time.time() - t1
+        if n_envs > chunk:
+            print(f"[bench] oracle envs {c0}..{ids[-1]} done, {dt:.1f}s so far",
+                  file=sys.stderr, flush=True)
     return {"value": n_envs * cfg.L / dt, "unit": "env-steps/s", "cores": 1,
-            "kind": "oracle", "seconds": dt,
+            "kind": "oracle", "seconds": dt, "cpu_model": host_cpu_model(),
+            "host_cpus": len(os.sched_getaffinity(0)),
             "sample": f"{n_envs} envs x {cfg.L} steps of the same workload (full actor), "
                       f"free-running rollout + GAE, one thread"}
-
 
 if __name__ == "__main__":
     main()
