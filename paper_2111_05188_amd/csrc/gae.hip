@@ -9,7 +9,8 @@
 // the carries are combined through LDS, pass 2 re-runs each chunk from its
 // true carry and writes A and ret.  Chunks of up to 28 steps keep their
 // inputs in registers between the passes (each input is read once); longer
-// ones read them again.  fp64 arithmetic, fp32 I/O.
+// ones read them again.  fp64 arithmetic, fp32 I/O.  This kernel serves
+// rollouts longer than gae_wide_kernel (below) takes.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -115,10 +116,134 @@ __global__ __launch_bounds__(GAE_NCH *WAVE) void gae_kernel(
     }
 }
 
+// Rollouts of up to GW_NCH * GW_CL steps: a workgroup takes GW_E envs and
+// GW_NCH chunks of at most GW_CL steps, one thread per (env, chunk), so
+// that even a few thousand envs fill every CU.  Lane l of wave w holds env
+// l % GW_E of chunk w * GW_K + l / GW_E; each wave reads GW_K row pieces of
+// GW_E consecutive envs per step.  The chunk maps x -> A + P x (x: the
+// value carried in from the chunk after) are composed within a wave by
+// shuffles, across waves through LDS; every input is read once and kept in
+// registers between the two passes.
+constexpr int GW_E = 16;                 // envs per workgroup
+constexpr int GW_K = WAVE / GW_E;        // chunks per wave
+constexpr int GW_W = 16;                 // waves per workgroup
+constexpr int GW_NCH = GW_K * GW_W;      // chunks per workgroup
+constexpr int GW_CL = 8;                 // longest chunk
+
+__global__ __launch_bounds__(GW_W *WAVE) void gae_wide_kernel(
+    const float *__restrict__ r, const float *__restrict__ v,
+    const uint8_t *__restrict__ d, int L, int E, int nblk, double g, double gl,
+    float *__restrict__ adv, float *__restrict__ ret)
+{
+    __shared__ double sA[GW_W][GW_E], sP[GW_W][GW_E];
+    // XCD-aware order: consecutive env groups (which share 128-byte lines)
+    // go to one XCD's L2
+    const int logical = (blockIdx.x % 8) * (gridDim.x / 8) + blockIdx.x / 8;
+    if (logical >= nblk) return;   // whole workgroup: no barrier is skipped by part of it
+    const int w = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
+    const int le = lane % GW_E, k = lane / GW_E;
+    const int e = logical * GW_E + le;
+    const int c = w * GW_K + k;
+    const int cl = (L + GW_NCH - 1) / GW_NCH;
+    const int lo = min(L, c * cl), hi = min(L, lo + cl);
+    const bool ok = e < E && hi > lo;
+    const size_t sE = (size_t)E;
+
+    // pass 1: the chunk's inputs (step hi-1-i in slot i) and its map
+    float cr[GW_CL], cv[GW_CL];
+    uint32_t cd = 0;
+    double vend = 0.0;
+    if (ok) {
+        vend = (double)v[(size_t)hi * sE + e];
+#pragma unroll
+        for (int i = 0; i < GW_CL; ++i) {
+            const int j = hi - 1 - i;
+            if (j >= lo) {
+                const size_t x = (size_t)j * sE + e;
+                cr[i] = r[x];
+                cv[i] = v[x];
+                cd |= (uint32_t)(d[x] != 0) << i;
+            }
+        }
+    }
+    double A = 0.0, P = 1.0;
+    if (ok) {
+        double vn = vend;
+#pragma unroll
+        for (int i = 0; i < GW_CL; ++i) {
+            if (hi - 1 - i >= lo) {
+                const double nd = (cd >> i) & 1u ? 0.0 : 1.0;
+                const double vj = (double)cv[i];
+                const double delta = (double)cr[i] + g * nd * vn - vj;
+                const double cj = gl * nd;
+                A = delta + cj * A;
+                P *= cj;
+                vn = vj;
+            }
+        }
+    }
+
+    // suffix composition over the wave's GW_K chunks of this env: after
+    // it, (A, P) maps the value entering chunk GW_K-1's end to chunk k's
+    // start through chunks k .. GW_K-1 (chunks past the rollout are the
+    // identity)
+#pragma unroll
+    for (int sh = 1; sh < GW_K; sh *= 2) {
+        const double An = __shfl_down(A, sh * GW_E), Pn = __shfl_down(P, sh * GW_E);
+        if (k + sh < GW_K) {
+            A = A + P * An;
+            P = P * Pn;
+        }
+    }
+    if (k == 0) {
+        sA[w][le] = A;
+        sP[w][le] = P;
+    }
+    __syncthreads();
+    // value entering this wave's last chunk: the later waves' maps applied
+    // to 0, last wave first
+    double carry = 0.0;
+    for (int ww = GW_W - 1; ww > w; --ww) carry = sA[ww][le] + sP[ww][le] * carry;
+    // value entering this chunk: the suffix map of chunk k + 1 applied to it
+    {
+        const double An = __shfl_down(A, GW_E), Pn = __shfl_down(P, GW_E);
+        if (k + 1 < GW_K) carry = An + Pn * carry;
+    }
+
+    // pass 2: the chunk again from its true carry
+    if (ok) {
+        A = carry;
+        double vn = vend;
+#pragma unroll
+        for (int i = 0; i < GW_CL; ++i) {
+            const int j = hi - 1 - i;
+            if (j >= lo) {
+                const size_t x = (size_t)j * sE + e;
+                const double nd = (cd >> i) & 1u ? 0.0 : 1.0;
+                const double vj = (double)cv[i];
+                const double delta = (double)cr[i] + g * nd * vn - vj;
+                A = delta + gl * nd * A;
+                adv[x] = (float)A;
+                ret[x] = (float)(A + vj);
+                vn = vj;
+            }
+        }
+    }
+}
+
 hipError_t launch_gae(const float *r, const float *v, const uint8_t *d, int L,
                       int E, double g, double gl, float *adv, float *ret,
                       hipStream_t s)
 {
+    // the wide kernel where the other would leave CUs idle (fewer than 256
+    // of its 64-env workgroups); at 16,384 envs and more the other one's
+    // whole-line rows measured as fast or faster
+    if (L <= GW_NCH * GW_CL && (E + WAVE - 1) / WAVE < 256) {
+        const int nblk = (E + GW_E - 1) / GW_E;
+        hipLaunchKernelGGL(gae_wide_kernel, dim3((nblk + 7) / 8 * 8), dim3(GW_W * WAVE), 0, s,
+                           r, v, d, L, E, nblk, g, gl, adv, ret);
+        return hipGetLastError();
+    }
     const int cl = (L + GAE_NCH - 1) / GAE_NCH;
     if (cl <= GAE_CACHE)
         hipLaunchKernelGGL(gae_kernel<true>, dim3((E + WAVE - 1) / WAVE), dim3(GAE_NCH * WAVE), 0,

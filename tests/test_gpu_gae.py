@@ -1,6 +1,7 @@
 """GPU parity of tp_gae against the oracle (seeded generator inputs), at
 small and full sizes, ragged env counts, L = 1, episode ends inside the
-rollout, and the lambda = 0 / 1 special cases."""
+rollout, the lambda = 0 / 1 special cases, and shapes on both sides of the
+switch between the two GAE kernels."""
 
 import numpy as np
 import pytest
@@ -24,7 +25,11 @@ def _inputs(L, E, seed, p_done=0.02):
 @pytest.mark.parametrize("L,E,gamma,lam", [
     (1, 1, 0.99, 0.95), (3, 5, 0.9, 0.5), (256, 64, 0.99, 0.95),
     (390, 100, 0.99, 0.95), (390, 4096, 0.99, 0.95), (2520, 1024, 0.99, 0.95),
-    (17, 130, 0.99, 0.0), (45, 65, 0.97, 1.0), (1000, 3, 1.0, 1.0)])
+    (17, 130, 0.99, 0.0), (45, 65, 0.97, 1.0), (1000, 3, 1.0, 1.0),
+    # both sides of the boundary between the two kernels: rollouts of 512
+    # steps (8-step chunks) and 513; 16,383 envs and 16,384
+    (512, 1000, 0.99, 0.95), (513, 200, 0.99, 0.95), (64, 16383, 0.99, 0.95),
+    (7, 16384, 0.99, 0.95)])
 def test_gae_parity(L, E, gamma, lam):
     say(f"[gae] L={L} E={E} gamma={gamma} lambda={lam}")
     r, v, d = _inputs(L, E, L * 7 + E)
