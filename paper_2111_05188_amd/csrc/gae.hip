@@ -116,25 +116,26 @@ __global__ __launch_bounds__(GAE_NCH *WAVE) void gae_kernel(
     }
 }
 
-// Rollouts of up to GW_NCH * GW_CL steps: a workgroup takes GW_E envs and
-// GW_NCH chunks of at most GW_CL steps, one thread per (env, chunk), so
-// that even a few thousand envs fill every CU.  Lane l of wave w holds env
-// l % GW_E of chunk w * GW_K + l / GW_E; each wave reads GW_K row pieces of
-// GW_E consecutive envs per step.  The chunk maps x -> A + P x (x: the
+// Rollouts of up to GW_LMAX steps: a workgroup takes GW_E envs and GW_NCH
+// chunks of at most GW_CL steps, one thread per (env, chunk), so that even
+// a few thousand envs fill every CU.  Lane l of wave w holds env l % GW_E
+// of chunk w * GW_K + l / GW_E; each wave reads GW_K row pieces of GW_E
+// consecutive envs per step (64 or 128 bytes).  The chunk maps x -> A + P x (x: the
 // value carried in from the chunk after) are composed within a wave by
 // shuffles, across waves through LDS; every input is read once and kept in
 // registers between the two passes.
-constexpr int GW_E = 16;                 // envs per workgroup
-constexpr int GW_K = WAVE / GW_E;        // chunks per wave
 constexpr int GW_W = 16;                 // waves per workgroup
-constexpr int GW_NCH = GW_K * GW_W;      // chunks per workgroup
-constexpr int GW_CL = 8;                 // longest chunk
+constexpr int GW_LMAX = 512;             // longest rollout
 
+template <int GW_E>   // envs per workgroup (16 or 32)
 __global__ __launch_bounds__(GW_W *WAVE) void gae_wide_kernel(
     const float *__restrict__ r, const float *__restrict__ v,
     const uint8_t *__restrict__ d, int L, int E, int nblk, double g, double gl,
     float *__restrict__ adv, float *__restrict__ ret)
 {
+    constexpr int GW_K = WAVE / GW_E;                  // chunks per wave
+    constexpr int GW_NCH = GW_K * GW_W;                // chunks per workgroup
+    constexpr int GW_CL = GW_LMAX / GW_NCH;            // longest chunk
     __shared__ double sA[GW_W][GW_E], sP[GW_W][GW_E];
     // XCD-aware order: consecutive env groups (which share 128-byte lines)
     // go to one XCD's L2
@@ -235,13 +236,18 @@ hipError_t launch_gae(const float *r, const float *v, const uint8_t *d, int L,
                       int E, double g, double gl, float *adv, float *ret,
                       hipStream_t s)
 {
-    // the wide kernel where the other would leave CUs idle (fewer than 256
-    // of its 64-env workgroups); at 16,384 envs and more the other one's
-    // whole-line rows measured as fast or faster
-    if (L <= GW_NCH * GW_CL && (E + WAVE - 1) / WAVE < 256) {
-        const int nblk = (E + GW_E - 1) / GW_E;
-        hipLaunchKernelGGL(gae_wide_kernel, dim3((nblk + 7) / 8 * 8), dim3(GW_W * WAVE), 0, s,
-                           r, v, d, L, E, nblk, g, gl, adv, ret);
+    // rollouts up to GW_LMAX steps: 16-env workgroups below 16,384 envs
+    // (so that every CU gets one), whole-line 32-env ones from there on
+    if (L <= GW_LMAX) {
+        if (E >= 16384) {
+            const int nblk = (E + 31) / 32;
+            hipLaunchKernelGGL(gae_wide_kernel<32>, dim3((nblk + 7) / 8 * 8), dim3(GW_W * WAVE), 0, s,
+                               r, v, d, L, E, nblk, g, gl, adv, ret);
+        } else {
+            const int nblk = (E + 15) / 16;
+            hipLaunchKernelGGL(gae_wide_kernel<16>, dim3((nblk + 7) / 8 * 8), dim3(GW_W * WAVE), 0, s,
+                               r, v, d, L, E, nblk, g, gl, adv, ret);
+        }
         return hipGetLastError();
     }
     const int cl = (L + GAE_NCH - 1) / GAE_NCH;

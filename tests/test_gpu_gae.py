@@ -26,10 +26,11 @@ def _inputs(L, E, seed, p_done=0.02):
     (1, 1, 0.99, 0.95), (3, 5, 0.9, 0.5), (256, 64, 0.99, 0.95),
     (390, 100, 0.99, 0.95), (390, 4096, 0.99, 0.95), (2520, 1024, 0.99, 0.95),
     (17, 130, 0.99, 0.0), (45, 65, 0.97, 1.0), (1000, 3, 1.0, 1.0),
-    # both sides of the boundary between the two kernels: rollouts of 512
-    # steps (8-step chunks) and 513; 16,383 envs and 16,384
+    # both sides of the boundaries between the kernels: rollouts of 512
+    # steps (the longest chunks) and 513; 16,383 envs and 16,384 (and a
+    # ragged count above it)
     (512, 1000, 0.99, 0.95), (513, 200, 0.99, 0.95), (64, 16383, 0.99, 0.95),
-    (7, 16384, 0.99, 0.95)])
+    (7, 16384, 0.99, 0.95), (512, 16400, 0.99, 0.95)])
 def test_gae_parity(L, E, gamma, lam):
     say(f"[gae] L={L} E={E} gamma={gamma} lambda={lam}")
     r, v, d = _inputs(L, E, L * 7 + E)
