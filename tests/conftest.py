@@ -16,7 +16,7 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests are never silently skipped on a GPU machine: they fail loudly if
+    # GPU tests are never silently skipped on a machine with a GPU: they fail loudly if
     # the HIP library is missing.  Without a GPU they are skipped.
     try:
         import torch
