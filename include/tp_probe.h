@@ -32,6 +32,11 @@ double tpp_mfma32_issue_flops(int blocks, int iters);
 int tpp_l2_stream(const void *buf, size_t buf_bytes, int frags_per_wave, int reps, int blocks,
                   void *out, void *stream);
 
+/* A plain copy of `bytes` (a multiple of 16; both pointers 16-byte
+ * aligned) from src to dst by `blocks` workgroups of 256 threads, 16 bytes
+ * per lane per access, four loads in flight, non-temporal. */
+int tpp_copy(const void *src, void *dst, size_t bytes, int blocks, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -8,8 +8,10 @@
 //     the pattern of the rollout's weight stream (a wave instruction reads
 //     1 KiB: lane l the 16 bytes at 16 l), 16 loads in flight per wave: the
 //     L2 -> CU bandwidth one CU can pull.
-// Both write to `out` only under a condition the data never meets, so the
-// results stay live without memory traffic.
+//   * tpp_copy: a plain device copy, 16 bytes per lane, four loads in flight
+//     per lane, non-temporal: the HBM rate a streaming kernel can reach.
+// The first two write to `out` only under a condition the data never meets,
+// so the results stay live without memory traffic.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -105,6 +107,22 @@ __global__ __launch_bounds__(512) void l2_stream_kernel(const u32x4 *__restrict_
     if (acc.x == 0x12345678u && acc.y == 0x9abcdef0u) out[blockIdx.x * 512 + threadIdx.x] = acc;
 }
 
+
+__global__ __launch_bounds__(256) void copy_kernel(const u32x4 *__restrict__ src,
+                                                   u32x4 *__restrict__ dst, size_t n)
+{
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        u32x4 v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = __builtin_nontemporal_load(src + i + k * stride);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(v[k], dst + i + k * stride);
+    }
+    for (; i < n; i += stride) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+}
+
 }  // namespace
 
 extern "C" {
@@ -142,6 +160,15 @@ int tpp_l2_stream(const void *buf, size_t buf_bytes, int frags_per_wave, int rep
     if ((size_t)8 * frags_per_wave * 1024 > buf_bytes) return -1;
     hipLaunchKernelGGL(l2_stream_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream,
                        (const u32x4 *)buf, frags_per_wave, reps, (u32x4 *)out);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int tpp_copy(const void *src, void *dst, size_t bytes, int blocks, void *stream)
+{
+    if (!src || !dst || bytes % 16 || blocks < 1 || (uintptr_t)src % 16 || (uintptr_t)dst % 16)
+        return -1;
+    hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream,
+                       (const u32x4 *)src, (u32x4 *)dst, bytes / 16);
     return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 

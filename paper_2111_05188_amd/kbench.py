@@ -333,6 +333,21 @@ def main():
         a.fill_(1.0)
         sec = _time(lambda: b.copy_(a), args.iters, stream)
         out["copy_1GiB"] = {"launch_ms": sec * 1e3, "GBs": 2 * a.numel() * 4 / sec / 1e9}
+        # the probe library's plain copy (16 bytes per lane, four loads in
+        # flight, non-temporal) over a few grid sizes
+        import ctypes as C
+        import os
+        pl = C.CDLL(os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpprobe.so"))
+        pl.tpp_copy.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int, C.c_void_p]
+        sp = stream.cuda_stream
+        nbytes = a.numel() * 4
+        probe = {}
+        for nb in (2048, 8192, 16384, 32768, 65536):
+            assert pl.tpp_copy(a.data_ptr(), b.data_ptr(), nbytes, nb, sp) == 0
+            sec = _time(lambda: pl.tpp_copy(a.data_ptr(), b.data_ptr(), nbytes, nb, sp),
+                        args.iters, stream)
+            probe[f"{nb}wg_GBs"] = 2 * nbytes / sec / 1e9
+        out["copy_1GiB_probe"] = probe
 
     print(json.dumps(out), flush=True)
 
