@@ -36,6 +36,28 @@ def test_library_exports_every_declared_symbol():
     assert L.tp_version() == 1
 
 
+PROBE_HEADER = os.path.join(ROOT, "include", "tp_probe.h")
+PROBE_LIB = os.path.join(ROOT, "paper_2111_05188_amd", "libtpprobe.so")
+
+
+def test_probe_library_exports_every_declared_symbol():
+    """include/tp_probe.h (the measurement probes) against libtpprobe.so."""
+    src = re.sub(r"/\*.*?\*/", "", open(PROBE_HEADER).read(), flags=re.S)
+    declared = sorted(set(re.findall(r"\b(tpp_[a-z_0-9]+)\s*\(", src)))
+    assert declared, "no probe declared"
+    out = subprocess.check_output(["nm", "-D", "--defined-only", PROBE_LIB]).decode()
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    missing = [f for f in declared if f not in exported]
+    assert not missing, missing
+    L = C.CDLL(PROBE_LIB)
+    for f in declared:
+        assert hasattr(L, f)
+    # argument checks return -1 before anything is launched
+    L.tpp_copy.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int, C.c_void_p]
+    assert L.tpp_copy(None, None, 16, 1, None) == -1
+    assert L.tpp_copy(0x1000, 0x2000, 15, 1, None) == -1
+
+
 def _nasdaq_actor(dtype=tp.TP_BF16, dims=(1001, 512, 512, 100), A=1):
     a = tp.Actor()
     a.n_agents, a.envs_per_agent, a.dtype = A, 4096, dtype
