@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define TP_VERSION 1
+#define TP_VERSION 2
 
 typedef enum {
     TP_OK = 0,
@@ -97,6 +97,13 @@ typedef struct tp_env_state {
     int32_t *shares;       /* [E][n] holdings h (>= 0)                       */
     int64_t *t;            /* [E] current market row                         */
     int32_t E;             /* envs, >= 1                                     */
+    int32_t *n_invalid;    /* optional device int32 [1], or NULL: every call
+                              that takes the state sets it to the number of
+                              envs it could not start (tp_env_reset: t0
+                              outside [0, T1-1)) or step (tp_env_step,
+                              tp_rollout: not enough market rows left).  The
+                              host cannot read device-side time indices;
+                              this count is how such envs are reported.     */
 } tp_env_state;
 
 /* Actor: the PPO Gaussian policy (PPO is named in Section 5.2):
@@ -143,6 +150,10 @@ typedef struct tp_traj {
                               the prices of the new row (the account value
                               of eq. (2)), or NULL; NaN for an env that is
                               not stepped                                    */
+    float *mu_tap;         /* [L][E][n] the actor's output mu_j (the mean of
+                              the Gaussian policy) that a_j was drawn
+                              around, or NULL; NaN for an env that is not
+                              stepped                                        */
 } tp_traj;
 
 /*
@@ -153,7 +164,10 @@ typedef struct tp_traj {
  *   columns zero).  t0 is a device int64 [E].  The host cannot read t0, so
  *   the kernel checks it: an env with t0[e] outside [0, T1-1) gets
  *   t[e] = -1 (an invalid env: every later step or rollout leaves it
- *   untouched and reports NaN for it) and a zero observation row.
+ *   untouched and reports NaN for it) and a zero observation row; the
+ *   number of such envs goes to st->n_invalid when that is not NULL.
+ *   Callers that hold t0 on the host check it first with tp_check_starts,
+ *   which returns TP_ERANGE for a start without enough market rows.
  *   obs_dtype: tp_dtype of obs0.
  */
 int tp_env_reset(const tp_market *mkt, const tp_env_cfg *cfg,
@@ -172,7 +186,8 @@ int tp_env_reset(const tp_market *mkt, const tp_env_cfg *cfg,
  *   ([E][ld_obs], obs_dtype).
  *   Every t[e] + 1 must be < T1: the host cannot read device t, so the
  *   kernel checks it; an env with t[e] < 0 or t[e] + 1 >= T1 is left
- *   unchanged, gets reward NaN and (if requested) a NaN observation row.
+ *   unchanged, gets reward NaN and (if requested) a NaN observation row,
+ *   and is counted in st->n_invalid when that is not NULL.
  */
 int tp_env_step(const tp_market *mkt, const tp_env_cfg *cfg,
                 const tp_env_state *st, const float *action, float *reward,
@@ -189,6 +204,27 @@ int tp_env_step(const tp_market *mkt, const tp_env_cfg *cfg,
 size_t tp_actor_packed_bytes(const tp_actor *actor);
 int tp_actor_pack(const tp_actor *actor, void *packed, size_t packed_bytes,
                   void *stream);
+
+/*
+ * tp_actor_release / tp_critic_release -- forget a packed buffer (host
+ * only; nothing is freed).  The library records, per packed buffer, the
+ * shape it was filled with, and tp_rollout / tp_critic_value accept only
+ * buffers so recorded.  Call this before freeing a packed buffer, so that
+ * a later allocation at the same address is not taken for it.  Packing
+ * into a buffer also forgets every recorded buffer it overlaps.  Returns
+ * TP_EINVAL for a pointer that is not recorded.
+ */
+int tp_actor_release(const void *packed);
+int tp_critic_release(const void *packed);
+
+/*
+ * tp_check_starts -- host-side check of episode start rows (Section 3: the
+ * MDP steps through consecutive bars of the market).  t0_host [E] is a
+ * HOST array; every env must have L market rows after its start:
+ * 0 <= t0[e] and t0[e] + L <= T1 - 1.  Returns TP_OK, or TP_ERANGE with
+ * the first offending env in tp_last_error(); TP_EINVAL for bad sizes.
+ */
+int tp_check_starts(const int64_t *t0_host, int32_t E, int64_t T1, int32_t L);
 
 /*
  * tp_rollout -- L lockstep steps of the batched env driven by the actor
@@ -208,9 +244,11 @@ int tp_actor_pack(const tp_actor *actor, void *packed, size_t packed_bytes,
  *   pieces with matching step0 reproduces the unsplit one bit for bit.
  *   Requires step0 + L <= horizon.  Device-side t is not visible to the
  *   host: an env with t < 0 or t + L > T1 - 1 is not stepped: its state is
- *   left unchanged, its action / logp / reward rows are NaN, done is 0, the
- *   taps hold the unchanged state and its observation rows are not written.
- *   `packed` must come from tp_actor_pack with the same actor shape.
+ *   left unchanged, its action / logp / reward / mu rows are NaN, done is
+ *   0, the taps hold the unchanged state, its observation rows are not
+ *   written, and it is counted in st->n_invalid when that is not NULL.
+ *   `packed` must come from tp_actor_pack with the same actor shape and
+ *   must not have been released (tp_actor_release) since.
  */
 int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg,
                const tp_env_state *st, const tp_actor *actor,

@@ -48,8 +48,8 @@ int check_market(const tp_market *m)
     if (!m->price) return fail(TP_EINVAL, "market.price is NULL");
     if (m->n < 1 || m->n > 128) return fail(TP_EINVAL, "market.n = %d outside 1..128", m->n);
     if (m->n_ind < 0) return fail(TP_EINVAL, "market.n_ind = %d < 0", m->n_ind);
-    if ((int64_t)m->n * m->n_ind > 16384)
-        return fail(TP_EUNSUPPORTED, "market.n * n_ind = %lld > 16384", (long long)m->n * m->n_ind);
+    if ((int64_t)m->n * m->n_ind > 1024)
+        return fail(TP_EUNSUPPORTED, "market.n * n_ind = %lld > 1024", (long long)m->n * m->n_ind);
     if (m->n_ind > 0 && !m->ind) return fail(TP_EINVAL, "market.ind is NULL");
     if (m->T1 < 2) return fail(TP_EINVAL, "market.T1 = %lld < 2", (long long)m->T1);
     if (!aligned(m->price, 4) || !aligned(m->ind, 4))
@@ -77,7 +77,8 @@ int check_state(const tp_env_state *s, int n)
     if (!s) return fail(TP_EINVAL, "state is NULL");
     if (s->E < 1) return fail(TP_EINVAL, "state.E = %d < 1", s->E);
     if (!s->cash || !s->shares || !s->t) return fail(TP_EINVAL, "state array is NULL");
-    if (!aligned(s->cash, 8) || !aligned(s->t, 8) || !aligned(s->shares, 4))
+    if (!aligned(s->cash, 8) || !aligned(s->t, 8) || !aligned(s->shares, 4) ||
+        !aligned(s->n_invalid, 4))
         return fail(TP_EINVAL, "state arrays are not naturally aligned");
     (void)n;
     return TP_OK;
@@ -122,6 +123,11 @@ struct PackSig {
     size_t total;
 };
 
+// Packed buffers filled by tp_actor_pack / tp_critic_pack, keyed by their
+// device address, with the shape they hold (guarded by g_mu).  A buffer is
+// forgotten by tp_*_release, or when a later pack writes over any of its
+// bytes (the caller has freed it and the allocator handed out the memory
+// again).
 std::mutex g_mu;
 std::map<const void *, PackSig> g_packed;
 
@@ -154,6 +160,26 @@ struct CriticSig {
 };
 
 std::map<const void *, CriticSig> g_packed_critic;
+
+// Forget every recorded buffer that overlaps [p, p + bytes) (g_mu held).
+template <class M>
+void forget_overlapping(M &m, const void *p, size_t bytes)
+{
+    const uintptr_t lo = (uintptr_t)p, hi = lo + bytes;
+    for (auto it = m.begin(); it != m.end();) {
+        const uintptr_t a = (uintptr_t)it->first, b = a + it->second.total;
+        if (a < hi && lo < b)
+            it = m.erase(it);
+        else
+            ++it;
+    }
+}
+
+void forget_all_overlapping(const void *p, size_t bytes)
+{
+    forget_overlapping(g_packed, p, bytes);
+    forget_overlapping(g_packed_critic, p, bytes);
+}
 
 int check_ppo(const tp_ppo *c, PpoLayout *lay)
 {
@@ -296,6 +322,37 @@ const char *tp_last_error(void) { return g_err.c_str(); }
 
 int tp_version(void) { return TP_VERSION; }
 
+int tp_actor_release(const void *packed)
+{
+    std::lock_guard<std::mutex> g(g_mu);
+    if (!g_packed.erase(packed)) return fail(TP_EINVAL, "%p is not a packed actor buffer", packed);
+    return ok();
+}
+
+int tp_critic_release(const void *packed)
+{
+    std::lock_guard<std::mutex> g(g_mu);
+    if (!g_packed_critic.erase(packed))
+        return fail(TP_EINVAL, "%p is not a packed critic buffer", packed);
+    return ok();
+}
+
+int tp_check_starts(const int64_t *t0_host, int32_t E, int64_t T1, int32_t L)
+{
+    if (!t0_host) return fail(TP_EINVAL, "t0_host is NULL");
+    if (E < 1 || L < 1 || T1 < 2)
+        return fail(TP_EINVAL, "E = %d, L = %d, T1 = %lld (need E, L >= 1, T1 >= 2)", E, L,
+                    (long long)T1);
+    for (int32_t e = 0; e < E; ++e) {
+        const int64_t t0 = t0_host[e];
+        if (t0 < 0 || t0 > T1 - 1 - L)
+            return fail(TP_ERANGE,
+                        "env %d starts at row %lld: %d steps need rows up to %lld of %lld", e,
+                        (long long)t0, L, (long long)t0 + L, (long long)T1);
+    }
+    return ok();
+}
+
 int tp_env_reset(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *st,
                  const int64_t *t0, void *obs0, int64_t ld_obs, int32_t obs_dtype, void *stream)
 {
@@ -306,7 +363,9 @@ int tp_env_reset(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state
     if ((rc = check_obs(obs0, ld_obs, obs_dtype, K_pad_of(mkt), "obs0"))) return rc;
     const EnvConst c = make_env(mkt, cfg);
     hipError_t e = launch_env_reset(c, st->cash, st->shares, st->t, t0, st->E, obs0, ld_obs,
-                                    obs_dtype == TP_BF16, (hipStream_t)stream);
+                                    obs_dtype == TP_BF16, st->n_invalid, (hipStream_t)stream);
+    if (e == hipErrorInvalidConfiguration)
+        return fail(TP_EUNSUPPORTED, "observation rows of K_pad = %d exceed the LDS limit", c.K_pad);
     if (e != hipSuccess) return hip_fail(e, "env_reset launch");
     return ok();
 }
@@ -324,7 +383,10 @@ int tp_env_step(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state 
     if ((rc = check_obs(obs_next, ld_obs, obs_dtype, K_pad_of(mkt), "obs_next"))) return rc;
     const EnvConst c = make_env(mkt, cfg);
     hipError_t e = launch_env_step(c, st->cash, st->shares, st->t, action, reward, st->E, obs_next,
-                                   ld_obs, obs_dtype == TP_BF16, (hipStream_t)stream);
+                                   ld_obs, obs_dtype == TP_BF16, st->n_invalid,
+                                   (hipStream_t)stream);
+    if (e == hipErrorInvalidConfiguration)
+        return fail(TP_EUNSUPPORTED, "observation rows of K_pad = %d exceed the LDS limit", c.K_pad);
     if (e != hipSuccess) return hip_fail(e, "env_step launch");
     return ok();
 }
@@ -354,6 +416,7 @@ int tp_actor_pack(const tp_actor *actor, void *packed, size_t packed_bytes, void
         sig.dtype = actor->dtype;
         sig.n_agents = actor->n_agents;
         sig.total = L.total;
+        forget_all_overlapping(packed, L.total);
         g_packed[packed] = sig;
     }
     return ok();
@@ -394,7 +457,7 @@ int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *
         return fail(TP_EINVAL, "traj.action/logp/reward/done must not be NULL");
     if (!aligned(traj->action, 4) || !aligned(traj->logp, 4) || !aligned(traj->reward, 4) ||
         !aligned(traj->cash_tap, 8) || !aligned(traj->shares_tap, 4) ||
-        !aligned(traj->asset_tap, 8))
+        !aligned(traj->asset_tap, 8) || !aligned(traj->mu_tap, 4))
         return fail(TP_EINVAL, "traj arrays are not naturally aligned");
     const int K_pad = K_pad_of(mkt);
     if ((rc = check_obs(traj->obs, traj->ld_obs, actor->dtype, K_pad, "traj.obs")) ||
@@ -440,6 +503,8 @@ int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg, const tp_env_state *
     a.shares_tap = traj->shares_tap;
     a.obs_last = traj->obs_last;
     a.asset_tap = traj->asset_tap;
+    a.mu_tap = traj->mu_tap;
+    a.n_invalid = st->n_invalid;
     hipError_t e = launch_rollout(a, (hipStream_t)stream);
     if (e == hipErrorInvalidConfiguration)
         return fail(TP_EUNSUPPORTED, "rollout working set (%zu bytes of LDS) exceeds the limit",
@@ -473,6 +538,7 @@ int tp_critic_pack(const tp_critic *critic, void *packed, size_t packed_bytes, v
         sig.dtype = critic->dtype;
         sig.n_agents = critic->n_agents;
         sig.total = L.total;
+        forget_all_overlapping(packed, L.total);
         g_packed_critic[packed] = sig;
     }
     return ok();

@@ -16,10 +16,19 @@ __device__ __forceinline__ int obs_ld_lds(const EnvConst &C)
     return (C.K_pad * (int)sizeof(OT) + 15) / 16 * 16 / (int)sizeof(OT);
 }
 
+// An env the call cannot start or step adds one to *n_invalid (lane 0 of
+// its half; an integer count, so the total does not depend on the order).
+__device__ __forceinline__ void count_invalid(int32_t *n_invalid, bool bad, int hl)
+{
+    if (n_invalid && bad && hl == 0) atomicAdd(n_invalid, 1);
+}
+
+__global__ void zero_i32_kernel(int32_t *p) { *p = 0; }
+
 template <typename OT>
 __global__ __launch_bounds__(ENV_WPB *WAVE) void env_reset_kernel(
     EnvConst C, double *cash, int32_t *shares, int64_t *t, const int64_t *t0,
-    int E, OT *obs, int64_t ld_obs)
+    int E, OT *obs, int64_t ld_obs, int32_t *n_invalid)
 {
     extern __shared__ __align__(16) uint8_t smem[];
     const int lane = threadIdx.x % WAVE, hl = lane % HALF;
@@ -30,6 +39,7 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_reset_kernel(
         const int n = C.n;
         const int64_t tt = t0[e];
         const bool ok = tt >= 0 && tt < C.T1 - 1;
+        count_invalid(n_invalid, !ok, hl);
         for (int i = hl; i < n; i += HALF) shares[(size_t)e * n + i] = 0;
         if (hl == 0) {
             cash[e] = C.cash0;
@@ -62,7 +72,7 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_reset_kernel(
 template <typename OT>
 __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
     EnvConst C, double *cash, int32_t *shares, int64_t *t, const float *action,
-    float *reward, int E, OT *obs, int64_t ld_obs)
+    float *reward, int E, OT *obs, int64_t ld_obs, int32_t *n_invalid)
 {
     extern __shared__ __align__(16) uint8_t smem[];
     const int lane = threadIdx.x % WAVE, hl = lane % HALF;
@@ -75,6 +85,7 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
     const bool in = e < E;
     const int64_t tt = in ? t[e] : -1;
     const bool live = in && tt >= 0 && tt + 1 < C.T1;
+    count_invalid(n_invalid, in && !live, hl);
     const int64_t trow = live ? tt : 0;
     const float *p0 = C.price + (size_t)trow * n;
     const float *p1 = p0 + (live ? n : 0);
@@ -92,8 +103,10 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
     }
     double none = 0.0;
     const float r = env_step_half(C, s, a, q, live, lane, none);
-    // bf16 rows of 4k stocks and 4k indicator values go out in aligned stores
-    const bool aligned_obs = sizeof(OT) == 2 && C.n % 4 == 0 && C.nI % 4 == 0 &&
+    // bf16 rows of 4k stocks and 4k > 0 indicator values go out in aligned
+    // stores (the aligned writer reads indicator chunks, so a market without
+    // indicators takes the per-value writer)
+    const bool aligned_obs = sizeof(OT) == 2 && C.n % 4 == 0 && C.nI > 0 && C.nI % 4 == 0 &&
                              (uintptr_t)C.ind % 16 == 0;
     if (live) {
 #pragma unroll
@@ -132,32 +145,53 @@ static size_t row_lds(const EnvConst &c, int esz)
     return (size_t)ENV_EPB * (((size_t)c.K_pad * esz + 15) / 16 * 16);
 }
 
+bool env_rows_fit(const EnvConst &c, int obs_bf16) { return row_lds(c, obs_bf16 ? 2 : 4) <= LDS_LIMIT; }
+
+hipError_t launch_zero_i32(int32_t *p, hipStream_t s)
+{
+    hipLaunchKernelGGL(zero_i32_kernel, dim3(1), dim3(1), 0, s, p);
+    return hipGetLastError();
+}
+
 hipError_t launch_env_reset(const EnvConst &c, double *cash, int32_t *shares,
                             int64_t *t, const int64_t *t0, int E, void *obs,
-                            int64_t ld_obs, int obs_bf16, hipStream_t s)
+                            int64_t ld_obs, int obs_bf16, int32_t *n_invalid,
+                            hipStream_t s)
 {
+    if (!env_rows_fit(c, obs_bf16)) return hipErrorInvalidConfiguration;
+    if (n_invalid) {
+        const hipError_t e = launch_zero_i32(n_invalid, s);
+        if (e != hipSuccess) return e;
+    }
     const dim3 grid((E + ENV_EPB - 1) / ENV_EPB), block(ENV_WPB * WAVE);
     if (obs_bf16)
         hipLaunchKernelGGL(env_reset_kernel<__bf16>, grid, block, row_lds(c, 2), s, c,
-                           cash, shares, t, t0, E, (__bf16 *)obs, ld_obs);
+                           cash, shares, t, t0, E, (__bf16 *)obs, ld_obs, n_invalid);
     else
         hipLaunchKernelGGL(env_reset_kernel<float>, grid, block, row_lds(c, 4), s, c,
-                           cash, shares, t, t0, E, (float *)obs, ld_obs);
+                           cash, shares, t, t0, E, (float *)obs, ld_obs, n_invalid);
     return hipGetLastError();
 }
 
 hipError_t launch_env_step(const EnvConst &c, double *cash, int32_t *shares,
                            int64_t *t, const float *action, float *reward,
                            int E, void *obs, int64_t ld_obs, int obs_bf16,
-                           hipStream_t s)
+                           int32_t *n_invalid, hipStream_t s)
 {
+    if (!env_rows_fit(c, obs_bf16)) return hipErrorInvalidConfiguration;
+    if (n_invalid) {
+        const hipError_t e = launch_zero_i32(n_invalid, s);
+        if (e != hipSuccess) return e;
+    }
     const dim3 grid((E + ENV_EPB - 1) / ENV_EPB), block(ENV_WPB * WAVE);
     if (obs_bf16)
         hipLaunchKernelGGL(env_step_kernel<__bf16>, grid, block, row_lds(c, 2), s, c,
-                           cash, shares, t, action, reward, E, (__bf16 *)obs, ld_obs);
+                           cash, shares, t, action, reward, E, (__bf16 *)obs, ld_obs,
+                           n_invalid);
     else
         hipLaunchKernelGGL(env_step_kernel<float>, grid, block, row_lds(c, 4), s, c,
-                           cash, shares, t, action, reward, E, (float *)obs, ld_obs);
+                           cash, shares, t, action, reward, E, (float *)obs, ld_obs,
+                           n_invalid);
     return hipGetLastError();
 }
 

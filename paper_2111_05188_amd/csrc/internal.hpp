@@ -67,6 +67,8 @@ struct RolloutArgs {
     int32_t *shares_tap;
     void *obs_last;
     double *asset_tap;
+    float *mu_tap;
+    int32_t *n_invalid;   // count of envs not stepped (zeroed before the launch), or NULL
     // LDS carve-up (bytes / elements), filled by the launcher
     int ldx, ldh, ldmu, ldz, ldh2;
     size_t lds_X, lds_H, lds_MU, lds_OS, lds_PT, lds_scal, lds_Z, lds_B, lds_bytes;
@@ -79,11 +81,17 @@ hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s);
 bool rollout_rs_shape(const PackedLayout &P, int nI);
 hipError_t launch_env_reset(const EnvConst &c, double *cash, int32_t *shares,
                             int64_t *t, const int64_t *t0, int E, void *obs,
-                            int64_t ld_obs, int obs_bf16, hipStream_t s);
+                            int64_t ld_obs, int obs_bf16, int32_t *n_invalid,
+                            hipStream_t s);
 hipError_t launch_env_step(const EnvConst &c, double *cash, int32_t *shares,
                            int64_t *t, const float *action, float *reward,
                            int E, void *obs, int64_t ld_obs, int obs_bf16,
-                           hipStream_t s);
+                           int32_t *n_invalid, hipStream_t s);
+// *p = 0 by a one-thread kernel (a fill kernel rather than a memset node, so
+// the call sequence stays safe to capture in a graph)
+hipError_t launch_zero_i32(int32_t *p, hipStream_t s);
+// the env step's LDS observation rows for this market fit the device
+bool env_rows_fit(const EnvConst &c, int obs_bf16);
 size_t backtest_metrics_work_bytes(int T, int E);
 hipError_t launch_backtest_metrics(const double *v0, const double *v, int T, int E,
                                    double periods_per_year, double risk_free, double *out,

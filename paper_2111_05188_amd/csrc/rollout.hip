@@ -259,6 +259,7 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
         const int e = ebase + sl;
         const int64_t tt = A.t[e];
         live = tt >= 0 && tt + A.L <= C.T1 - 1;
+        if (A.n_invalid && !live && hl == 0) atomicAdd(A.n_invalid, 1);
         // state (also for envs that are not stepped: their taps repeat it)
         for (int i = hl; i < n; i += HALF) OS[sl * n + i] = A.shares[(size_t)e * n + i];
         if (hl == 0) {
@@ -373,11 +374,13 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
         if (mine) {
             const size_t row = (size_t)j * E + e;
             float *ga = A.action + row * n;
+            float *gm = A.mu_tap ? A.mu_tap + row * n : nullptr;
             int32_t *gs = A.shares_tap ? A.shares_tap + row * n : nullptr;
             if (!live) {
                 // not stepped: NaN rows, done = 0, taps repeat the state
                 for (int i = hl; i < n; i += HALF) {
                     ga[i] = qnan;
+                    if (gm) gm[i] = qnan;
                     if (gs) gs[i] = OS[sl * n + i];
                 }
                 if (hl == 0) {
@@ -393,6 +396,7 @@ __global__ __launch_bounds__(NWM *WAVE) void rollout_kernel(RolloutArgs A)
                     const int i = SPL * hl + c;
                     if (i < n) {
                         ga[i] = a[c];
+                        if (gm) gm[i] = mu[i];
                         if (gs) gs[i] = st.h[c];
                     }
                 }
@@ -470,6 +474,10 @@ static hipError_t launch_cfg(RolloutArgs &a, hipStream_t s)
 
 hipError_t launch_rollout(RolloutArgs &a, hipStream_t s)
 {
+    if (a.n_invalid) {
+        const hipError_t e = launch_zero_i32(a.n_invalid, s);
+        if (e != hipSuccess) return e;
+    }
     if (a.lay.dtype == TP_BF16) {
         const hipError_t e = launch_rollout_rs(a, s);
         if (e != hipErrorNotSupported) return e;

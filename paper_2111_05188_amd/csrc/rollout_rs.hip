@@ -393,6 +393,7 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
     if (mine) {
         t0 = A.t[e];
         live = t0 >= 0 && t0 + A.L <= C.T1 - 1;
+        if (A.n_invalid && !live && hl == 0) atomicAdd(A.n_invalid, 1);
         st.cash = A.cash[e];
 #pragma unroll
         for (int c = 0; c < SPL; ++c) {
@@ -447,6 +448,9 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
         if (hl < NS / SPL) {
             const f4v av = live ? f4v{a[0], a[1], a[2], a[3]} : f4v{qnan, qnan, qnan, qnan};
             store_stream(av, (f4v *)(A.action + row * n) + hl);
+            if (A.mu_tap)
+                store_stream(live ? *(const f4v *)(mu + SPL * hl) : f4v{qnan, qnan, qnan, qnan},
+                             (f4v *)(A.mu_tap + row * n) + hl);
             if (A.shares_tap)
                 store_stream(i4v{st.h[0], st.h[1], st.h[2], st.h[3]},
                              (i4v *)(A.shares_tap + row * n) + hl);
@@ -652,7 +656,7 @@ hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
     // the env waves move prices, indicators, actions and holdings in
     // 16-byte accesses
     if ((uintptr_t)a.env.price % 16 || (uintptr_t)a.env.ind % 16 || (uintptr_t)a.action % 16 ||
-        (uintptr_t)a.shares_tap % 16)
+        (uintptr_t)a.shares_tap % 16 || (uintptr_t)a.mu_tap % 16)
         return hipErrorNotSupported;
     if (P.H1 == 512 && P.H2 == 512) return rs::launch<rs::Shape<100, 800, 32, 7, 32, 32, 8, 16>>(a, s);
     if (P.H1 == 1024 && P.H2 == 1024) return rs::launch<rs::Shape<100, 800, 32, 7, 64, 64, 8, 16>>(a, s);

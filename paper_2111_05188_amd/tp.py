@@ -44,7 +44,7 @@ class EnvCfg(C.Structure):
 
 class EnvState(C.Structure):
     _fields_ = [("cash", C.c_void_p), ("shares", C.c_void_p),
-                ("t", C.c_void_p), ("E", C.c_int32)]
+                ("t", C.c_void_p), ("E", C.c_int32), ("n_invalid", C.c_void_p)]
 
 
 class Actor(C.Structure):
@@ -72,7 +72,8 @@ class Traj(C.Structure):
                 ("action", C.c_void_p), ("logp", C.c_void_p),
                 ("reward", C.c_void_p), ("done", C.c_void_p),
                 ("cash_tap", C.c_void_p), ("shares_tap", C.c_void_p),
-                ("obs_last", C.c_void_p), ("asset_tap", C.c_void_p)]
+                ("obs_last", C.c_void_p), ("asset_tap", C.c_void_p),
+                ("mu_tap", C.c_void_p)]
 
 
 EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
@@ -82,6 +83,7 @@ EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_keep_best", "tp_select",
            "tp_ppo_param_count", "tp_ppo_workspace_bytes", "tp_ppo_update",
            "tp_ppo_update_agents", "tp_minibatch_rows", "tp_rollout_path",
+           "tp_actor_release", "tp_critic_release", "tp_check_starts",
            "tp_last_error", "tp_version")
 
 _lib = None
@@ -126,12 +128,16 @@ def load(path: str = LIB_PATH):
                                 vp, vp, vp, C.c_size_t, vp]
     L.tp_ppo_update_agents.argtypes = [vp, i32, i64, vp, vp, vp, i64, i32, vp, i64, vp, vp, vp,
                                        vp, i64, vp, vp, vp, vp, C.c_size_t, vp]
+    L.tp_actor_release.argtypes = [vp]
+    L.tp_critic_release.argtypes = [vp]
+    L.tp_check_starts.argtypes = [vp, i32, i64, i32]
     L.tp_last_error.restype = C.c_char_p
     L.tp_version.restype = C.c_int
     for f in ("tp_env_reset", "tp_env_step", "tp_actor_pack", "tp_rollout", "tp_gae",
               "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
               "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
-              "tp_ppo_update", "tp_ppo_update_agents", "tp_minibatch_rows"):
+              "tp_ppo_update", "tp_ppo_update_agents", "tp_minibatch_rows",
+              "tp_actor_release", "tp_critic_release", "tp_check_starts"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -180,15 +186,20 @@ def env_cfg(hmax, horizon, fee, cash0, reward_scale, cash_scale, price_scale,
 
 
 class StateT:
-    def __init__(self, cash: torch.Tensor, shares: torch.Tensor, t: torch.Tensor):
-        self.cash, self.shares, self.t = cash, shares, t
-        self.s = EnvState(_ptr(cash), _ptr(shares), _ptr(t), cash.shape[0])
+    """Env state arrays; ``n_invalid`` (optional int32 [1]) receives the
+    number of envs each call could not start or step."""
+
+    def __init__(self, cash: torch.Tensor, shares: torch.Tensor, t: torch.Tensor,
+                 n_invalid: torch.Tensor | None = None):
+        self.cash, self.shares, self.t, self.n_invalid = cash, shares, t, n_invalid
+        self.s = EnvState(_ptr(cash), _ptr(shares), _ptr(t), cash.shape[0], _ptr(n_invalid))
 
     @staticmethod
-    def empty(E: int, n: int, device="cuda"):
+    def empty(E: int, n: int, device="cuda", count_invalid: bool = False):
         return StateT(torch.zeros(E, dtype=torch.float64, device=device),
                       torch.zeros(E, n, dtype=torch.int32, device=device),
-                      torch.zeros(E, dtype=torch.int64, device=device))
+                      torch.zeros(E, dtype=torch.int64, device=device),
+                      torch.zeros(1, dtype=torch.int32, device=device) if count_invalid else None)
 
 
 class ActorT:
@@ -222,10 +233,23 @@ class ActorT:
         """(Re)build the packed copy the rollout kernel reads."""
         nb = self.packed_bytes()
         if self.packed is None or self.packed.numel() < nb:
+            self.release()
             self.packed = torch.empty(nb, dtype=torch.uint8, device=self.W[0].device)
         _check(load().tp_actor_pack(C.byref(self.s), _ptr(self.packed), nb,
                                     _stream(stream)))
         return self.packed
+
+    def release(self):
+        """Forget the packed copy (the library stops accepting its address)."""
+        if self.packed is not None:
+            load().tp_actor_release(_ptr(self.packed))
+            self.packed = None
+
+    def __del__(self):
+        try:
+            self.release()
+        except Exception:  # interpreter shutdown
+            pass
 
 
 class CriticT:
@@ -257,24 +281,39 @@ class CriticT:
     def pack(self, stream=None):
         nb = self.packed_bytes()
         if self.packed is None or self.packed.numel() < nb:
+            self.release()
             self.packed = torch.empty(nb, dtype=torch.uint8, device=self.W[0].device)
         _check(load().tp_critic_pack(C.byref(self.s), _ptr(self.packed), nb,
                                      _stream(stream)))
         return self.packed
 
+    def release(self):
+        if self.packed is not None:
+            load().tp_critic_release(_ptr(self.packed))
+            self.packed = None
+
+    def __del__(self):
+        try:
+            self.release()
+        except Exception:  # interpreter shutdown
+            pass
+
 
 class TrajT:
     def __init__(self, action, logp, reward, done, obs=None, ld_obs=0,
-                 cash_tap=None, shares_tap=None, obs_last=None, asset_tap=None):
+                 cash_tap=None, shares_tap=None, obs_last=None, asset_tap=None,
+                 mu_tap=None):
         self.t = (action, logp, reward, done, obs, cash_tap, shares_tap, obs_last,
-                  asset_tap)
+                  asset_tap, mu_tap)
         self.s = Traj(_ptr(obs), ld_obs, _ptr(action), _ptr(logp), _ptr(reward),
                       _ptr(done), _ptr(cash_tap), _ptr(shares_tap), _ptr(obs_last),
-                      _ptr(asset_tap))
+                      _ptr(asset_tap), _ptr(mu_tap))
 
     @staticmethod
     def alloc(L, E, n, K_pad=None, obs_dtype=None, taps=False, obs_last=False,
               device="cuda"):
+        """Trajectory buffers; ``taps`` adds the parity taps (balance,
+        holdings, total asset and the actor's output mu)."""
         kw = {}
         obs_all = None
         if K_pad is not None:
@@ -291,6 +330,7 @@ class TrajT:
             kw["cash_tap"] = torch.empty(L, E, dtype=torch.float64, device=device)
             kw["shares_tap"] = torch.empty(L, E, n, dtype=torch.int32, device=device)
             kw["asset_tap"] = torch.empty(L, E, dtype=torch.float64, device=device)
+            kw["mu_tap"] = torch.empty(L, E, n, dtype=torch.float32, device=device)
         tr = TrajT(torch.empty(L, E, n, dtype=torch.float32, device=device),
                    torch.empty(L, E, dtype=torch.float32, device=device),
                    torch.empty(L, E, dtype=torch.float32, device=device),
@@ -307,6 +347,7 @@ class TrajT:
     shares_tap = property(lambda self: self.t[6])
     obs_last = property(lambda self: self.t[7])
     asset_tap = property(lambda self: self.t[8])
+    mu_tap = property(lambda self: self.t[9])
 
 
 def _dtype_code(t: torch.Tensor | None, default=TP_F32) -> int:
@@ -350,6 +391,13 @@ def gae(reward, value, done, gamma, lam, adv, ret, stream=None):
     L, E = reward.shape
     _check(load().tp_gae(_ptr(reward), _ptr(value), _ptr(done), L, E, gamma,
                          lam, _ptr(adv), _ptr(ret), _stream(stream)))
+
+
+def check_starts(t0, T1: int, L: int):
+    """Host-side check that every start row t0 (host int64 array) leaves L
+    market rows; raises TPError(TP_ERANGE) naming the first bad env."""
+    t0 = np.ascontiguousarray(t0, dtype=np.int64)
+    _check(load().tp_check_starts(t0.ctypes.data, t0.shape[0], T1, L))
 
 
 def last_error() -> str:

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
     L = tp.load()
     for f in declared_functions():
         assert hasattr(L, f)
-    assert L.tp_version() == 1
+    assert L.tp_version() == 2
 
 
 PROBE_HEADER = os.path.join(ROOT, "include", "tp_probe.h")
@@ -230,3 +230,40 @@ def test_ppo_agents_argument_errors_without_gpu():
         a[i] = v
         assert L.tp_ppo_update_agents(*a) == tp.TP_EINVAL, (i, v)
         assert msg in tp.last_error(), tp.last_error()
+
+
+def test_boundary_hygiene_without_gpu():
+    """Host-only parts of the boundary: the start-row check (TP_ERANGE with
+    the first offending env), the packed-buffer registry's release, the
+    indicator-count limit and the alignment of the invalid-env counter."""
+    import numpy as np
+    L = tp.load()
+    t0 = np.array([0, 10, 390 * 5, 42], np.int64)
+    tp.check_starts(t0, 390 * 6 + 1, 390)           # every start has 390 rows
+    with pytest.raises(tp.TPError) as ei:
+        tp.check_starts(t0, 390 * 6, 390)           # env 2 is one row short
+    assert ei.value.code == tp.TP_ERANGE and "env 2" in str(ei.value)
+    bad = np.array([5, -1], np.int64)
+    with pytest.raises(tp.TPError) as ei:
+        tp.check_starts(bad, 1000, 10)
+    assert ei.value.code == tp.TP_ERANGE and "env 1" in str(ei.value)
+    assert L.tp_check_starts(None, 4, 100, 10) == tp.TP_EINVAL
+    assert L.tp_check_starts(t0.ctypes.data, 4, 100, 0) == tp.TP_EINVAL
+    # release of a buffer that was never packed
+    assert L.tp_actor_release(0x123400) == tp.TP_EINVAL
+    assert "not a packed actor" in tp.last_error()
+    assert L.tp_critic_release(0x123400) == tp.TP_EINVAL
+    # more indicator values than the kernels hold: TP_EUNSUPPORTED
+    x = 0x100000
+    cfg = tp.env_cfg(100, 10, 1e-3, 1e6, 2 ** -12, 2 ** -20, 2 ** -7, 2 ** -7)
+    st = tp.EnvState(x, x, x, 4, None)
+    m = tp.Market(x, x, 100, 100, 11)
+    assert L.tp_env_step(C.byref(m), C.byref(cfg), C.byref(st), x, x, None, 0, 0,
+                         None) == tp.TP_EUNSUPPORTED
+    assert "1024" in tp.last_error()
+    # a misaligned invalid-env counter
+    m = tp.Market(x, x, 100, 10, 8)
+    st = tp.EnvState(x, x, x, 4, x + 2)
+    assert L.tp_env_step(C.byref(m), C.byref(cfg), C.byref(st), x, x, None, 0, 0,
+                         None) == tp.TP_EINVAL
+    assert "aligned" in tp.last_error()

@@ -72,7 +72,8 @@ def test_env_step_out_of_range_env_is_noop():
     mk = W.make_market(cfg)
     dev = "cuda"
     mkt = tp.MarketT(torch.from_numpy(mk.price).to(dev), torch.from_numpy(mk.ind).to(dev))
-    st = tp.StateT.empty(3, cfg.n)
+    st = tp.StateT.empty(3, cfg.n, count_invalid=True)
+    st.n_invalid.fill_(77)
     st.cash.fill_(5.0)
     st.t.copy_(torch.tensor([-1, cfg.T1 - 1, 10]))
     a = torch.full((3, cfg.n), 0.5, device=dev)
@@ -83,6 +84,7 @@ def test_env_step_out_of_range_env_is_noop():
     assert np.isnan(r[0]) and np.isnan(r[1]) and np.isfinite(r[2])
     assert st.t.cpu().tolist() == [-1, cfg.T1 - 1, 11]
     assert st.cash.cpu().numpy()[0] == 5.0
+    assert st.n_invalid.item() == 2        # the two envs that were not stepped
 
 
 @pytest.mark.parametrize("name", ["tiny", "nasdaq100"])
@@ -97,7 +99,7 @@ def test_env_reset(name):
     t0[6] = rows - 1        # no next row: invalid
     dev = "cuda"
     mkt = tp.MarketT(torch.from_numpy(mk.price).to(dev), torch.from_numpy(mk.ind).to(dev))
-    st = tp.StateT.empty(E, cfg.n)
+    st = tp.StateT.empty(E, cfg.n, count_invalid=True)
     st.shares.fill_(9)
     obs = torch.empty(E, cfg.K_pad, dtype=problem.obs_torch_dtype(cfg), device=dev)
     tp.env_reset(mkt, problem.env_cfg(cfg), st, torch.from_numpy(t0).to(dev), obs)
@@ -107,6 +109,7 @@ def test_env_reset(name):
     assert (st.cash.cpu().numpy() == cfg.cash0).all() and (st.shares.cpu().numpy() == 0).all()
     tt = st.t.cpu().numpy()
     assert tt[5] == -1 and tt[6] == -1
+    assert st.n_invalid.item() == 2
     for e in range(E):
         if e in (5, 6):
             continue
@@ -143,3 +146,49 @@ def test_env_step_bf16_rows_with_envs_not_stepped():
     rel_check("reward", rew.cpu().numpy()[live], r_o, TOL_REWARD)
     assert np.isnan(rew.cpu().numpy()[~live]).all()
     assert torch.isnan(obs[torch.from_numpy(~live).to(dev)].float()).all()
+
+
+@pytest.mark.parametrize("obs_dtype", [torch.bfloat16, torch.float32])
+def test_env_step_market_without_indicators(obs_dtype):
+    """A market with no indicators (n_ind = 0: the state is balance, prices
+    and holdings only) and 8 stocks: reset and chained steps against the
+    oracle, observation rows bit for bit.  With bf16 rows and a stock count
+    divisible by 4 this once took the aligned row writer, which reads
+    indicator chunks and has none to read."""
+    say(f"[env_step] n_ind = 0, {obs_dtype}")
+    cfg = W.get_config("tiny").with_(n=8, n_ind=0)
+    rows = 200
+    mk = W.make_market(cfg, rows=(0, rows))
+    assert mk.ind.shape == (rows, 8, 0)
+    E = 21
+    dev = "cuda"
+    mkt = tp.MarketT(torch.from_numpy(mk.price).to(dev),
+                     torch.empty(rows, 8, 0, dtype=torch.float32, device=dev))
+    ecfg = problem.env_cfg(cfg)
+    K = cfg.K_pad
+    bf = obs_dtype == torch.bfloat16
+    t0 = np.random.default_rng(5).integers(0, rows - 10, E).astype(np.int64)
+    st = tp.StateT.empty(E, cfg.n, count_invalid=True)
+    obs = torch.full((E, K), 7.0, dtype=obs_dtype, device=dev)
+    tp.env_reset(mkt, ecfg, st, torch.from_numpy(t0).to(dev), obs)
+    m, oc = oracle.market(mk.price, mk.ind), oracle.env_cfg(cfg)
+    c_cash, c_sh, c_t = oracle.env_reset(oc, t0, cfg.n)
+    torch.cuda.synchronize()
+    for e in range(E):
+        o = oracle.obs(m, oc, int(t0[e]), cfg.cash0, np.zeros(cfg.n, np.int32), K, bf)
+        g = bits16(obs[e]) if bf else obs[e].cpu().numpy()
+        assert np.array_equal(g, o)
+    assert st.n_invalid.item() == 0
+    for k in range(5):
+        a = W.make_actions(40 + k, E, cfg.n)
+        rew = torch.empty(E, dtype=torch.float32, device=dev)
+        obs = torch.full((E, K), 7.0, dtype=obs_dtype, device=dev)
+        tp.env_step(mkt, ecfg, st, torch.from_numpy(a).to(dev), rew, obs)
+        torch.cuda.synchronize()
+        r_o, obs_o = oracle.env_step(m, oc, c_cash, c_sh, c_t, a, K, bf)
+        assert np.array_equal(st.shares.cpu().numpy(), c_sh), "shares"
+        assert np.array_equal(st.cash.cpu().numpy(), c_cash), "cash"
+        rel_check("reward", rew.cpu().numpy(), r_o, TOL_REWARD)
+        g = bits16(obs) if bf else obs.cpu().numpy()
+        assert np.array_equal(g, obs_o)
+        assert st.n_invalid.item() == 0

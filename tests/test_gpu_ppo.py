@@ -8,9 +8,9 @@ Inputs are seeded and synthetic (workloads.make_learner_data); the stored
 log-probabilities are the oracle's log-density of the stored action under
 the starting parameters, shifted by log-ratio offsets that keep every row
 clearly inside or clearly outside the clip (so both sides take the same
-branch).  Tolerances: gradients are compared per segment by relative L2
-error, 1e-4 for fp32 (the tanh and summation order differ) and 2e-2 for
-bf16 (operands rounded to bf16 as the kernels do); parameters by the Adam
+branch).  Tolerances: every gradient element is held to 1e-4 (fp32: the
+tanh and summation order differ) or 2e-2 (bf16: operands rounded to bf16
+as the kernels do) of max(|g|, RMS of its segment); parameters by the Adam
 step they moved, in units of the learning rate.
 
 Several updates in a row are compared as two independent chains.  At the
@@ -73,13 +73,24 @@ def _rel(a, b):
 
 
 def _check_grad(dims, g_gpu, g_orc, tol, what):
+    """Every gradient element within tol * max(|g|, RMS of its segment)
+    (the relative tolerance read per compared tensor); the per-segment
+    relative L2 error is printed beside it as a diagnostic."""
     seg_g, seg_o = ppo.unflatten(g_gpu.astype(np.float64), dims), ppo.unflatten(g_orc, dims)
-    worst = 0.0
+    worst = worst_l2 = 0.0
     for name, _ in ppo.layout(*dims):
-        e = _rel(seg_g[name], seg_o[name])
+        g, o = np.asarray(seg_g[name]).ravel(), np.asarray(seg_o[name]).ravel()
+        scale = np.maximum(np.abs(o), max(np.sqrt(np.mean(o * o)), 1e-30))
+        ratio = np.abs(g - o) / scale
+        k = int(np.argmax(ratio))
+        e = float(ratio[k])
         worst = max(worst, e)
-        assert e < tol, f"{what}: gradient of {name}: relative error {e:.3g} >= {tol}"
-    say(f"[ppo] {what}: worst segment relative error {worst:.3g}")
+        worst_l2 = max(worst_l2, _rel(g, o))
+        assert e <= tol, (f"{what}: gradient of {name}: {(ratio > tol).sum()} of {ratio.size} "
+                          f"elements outside {tol}; worst {e:.3g} at {k} (gpu {g[k]:.6g}, "
+                          f"oracle {o[k]:.6g})")
+    say(f"[ppo] {what}: worst element error {worst:.3g} (tol {tol:g}); "
+        f"worst segment L2 error {worst_l2:.3g}")
 
 
 def _run(cfg, rows, B, n_updates, seed=7, lr=2.0 ** -14):

@@ -120,7 +120,9 @@ def test_env_without_room_is_not_stepped():
     mk = W.make_market(cfg)
     t0 = np.zeros(20, np.int64)
     pb, _ = build_problem(cfg.with_(E=20), mk, t0, E=20, envs_per_agent=20)
+    pb.state = tp.StateT.empty(20, cfg.n, count_invalid=True)
     pb.reset()
+    assert pb.state.n_invalid.item() == 0
     # env 3 starts too late for L steps; env 4 has an invalid (negative) row
     pb.state.t[3] = cfg.T1 - 10
     pb.state.t[4] = -1
@@ -132,8 +134,41 @@ def test_env_without_room_is_not_stepped():
     assert np.isfinite(r[:, [0, 1, 2, 5]]).all()
     assert (pb.traj.done[:50].cpu().numpy()[:, 3] == 0).all()
     assert np.isnan(pb.traj.action[:50, 3].cpu().numpy()).all()
+    assert np.isnan(pb.traj.mu_tap[:50, [3, 4]].cpu().numpy()).all()
+    assert np.isfinite(pb.traj.mu_tap[:50, [0, 1, 2, 5]].cpu().numpy()).all()
     assert pb.state.t[3].item() == cfg.T1 - 10 and pb.state.t[4].item() == -1
     assert pb.state.t[0].item() == 50
+    assert pb.state.n_invalid.item() == 2
+    # the host check names the first env without room
+    with pytest.raises(tp.TPError) as ei:
+        tp.check_starts(pb.state.t.cpu().numpy(), cfg.T1, 50)
+    assert ei.value.code == tp.TP_ERANGE and "env 3" in str(ei.value)
+
+
+def test_env_without_room_role_split_kernel():
+    """The same on the role-split kernel (100-stock bf16 actor): an env
+    whose start row leaves no room is counted, its rows are NaN, and the
+    envs sharing its waves are stepped as usual."""
+    cfg = W.get_config("nasdaq100").with_(N=4 * 390, E=20)
+    mk = W.make_market(cfg)
+    t0 = W.make_t0(cfg)
+    pb, params = build_problem(cfg, mk, t0)
+    assert tp.rollout_path(pb.mkt, pb.actor) == 1
+    pb.state = tp.StateT.empty(20, cfg.n, count_invalid=True)
+    pb.reset()
+    pb.state.t[6] = cfg.T1 - 5
+    pb.state.t[9] = -7
+    say("[rollout] role-split kernel, envs without room")
+    pb.rollout(SEED, 0, 30)
+    torch.cuda.synchronize()
+    assert pb.state.n_invalid.item() == 2
+    r = pb.traj.reward[:30].cpu().numpy()
+    assert np.isnan(r[:, [6, 9]]).all() and np.isfinite(np.delete(r, [6, 9], axis=1)).all()
+    assert np.isnan(pb.traj.mu_tap[:30, [6, 9]].cpu().numpy()).all()
+    ids = np.array([0, 7, 8, 19])
+    teacher = pb.traj.action[:30].index_select(1, torch.as_tensor(ids, device="cuda")).cpu().numpy()
+    out = oracle_replay(cfg, mk, params, t0[ids], ids, SEED, 30, teacher, cfg.envs_per_agent)
+    compare_rollout(cfg, pb, out, ids, 30)
 
 
 def test_rollout_errors():

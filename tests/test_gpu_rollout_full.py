@@ -47,23 +47,41 @@ def _full(cfg, mk, ids, store_obs=True, taps=True):
     return pb
 
 
+def _spread(blocks, per_block, block_envs, seed):
+    """One env from each of `blocks` workgroup-sized blocks of `block_envs`
+    envs (every `per_block`-th block), at a varying position in the block."""
+    rng = np.random.default_rng(seed)
+    return [b * block_envs + int(rng.integers(block_envs)) for b in range(0, blocks, per_block)]
+
+
 def test_dow30_full():
     cfg = W.get_config("dow30")
     mk = W.make_market(cfg)
-    _full(cfg, mk, [0, 1, 511, 777, 1023])
+    # 4 envs per workgroup on the generic kernel: 32 envs spread over all 256
+    _full(cfg, mk, [0, 1, 1023] + _spread(256, 9, 4, 1))
 
 
 def test_nasdaq100_full(minute_market):
     cfg = W.get_config("nasdaq100")
-    _full(cfg, minute_market, [0, 15, 16, 2047, 4095])
+    # one env from every one of the 256 workgroups (16 envs each)
+    _full(cfg, minute_market, sorted(set([0, 15, 16, 4095] + _spread(256, 1, 16, 2))))
 
 
 def test_ensemble_full(minute_market):
     cfg = W.get_config("ensemble")
-    # envs of agents 0, 5, 15 (first/last env of an agent, mid-block env)
-    _full(cfg, minute_market, [0, 5 * 1024 + 17, 16 * 1024 - 1], store_obs=True)
+    # 8 envs of each of the 16 agents, including each agent's first and
+    # last env
+    ids = []
+    rng = np.random.default_rng(3)
+    for a in range(16):
+        base = a * 1024
+        ids += [base, base + 1023] + [base + int(x) for x in rng.choice(np.arange(1, 1023), 6,
+                                                                         replace=False)]
+    _full(cfg, minute_market, sorted(ids))
 
 
 def test_stress_full(minute_market):
     cfg = W.get_config("stress")
-    _full(cfg, minute_market, [0, 40000, 65535], store_obs=False, taps=True)
+    # 64 envs spread over the 4,096 workgroups, observations stored and checked
+    _full(cfg, minute_market, sorted(set([0, 65535] + _spread(4096, 64, 16, 4))),
+          store_obs=True, taps=True)

@@ -378,3 +378,26 @@ def test_observation_layout_and_power_of_two_scales():
     # bf16 = RNE of the fp32 observation
     want = torch.from_numpy(base).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(obs(bf16=True), want)
+
+
+def test_parallel_replay_equals_serial():
+    """The GPU tests replay sampled envs through the oracle in chunks on a
+    thread pool; the joined result equals one serial call bit for bit."""
+    import workloads as W
+    from gpu_common import oracle_replay
+    cfg = W.get_config("tiny")
+    mk = W.make_market(cfg)
+    t0 = W.make_t0(cfg)
+    params = W.make_actor(cfg)
+    ids = np.array([0, 3, 5, 9, 17, 33, 40, 41, 50, 63])
+    teacher = np.random.default_rng(1).normal(0, 0.7, (60, len(ids), cfg.n)).astype(np.float32)
+    a = oracle_replay(cfg, mk, params, t0[ids], ids, 99, 60, teacher, cfg.envs_per_agent, chunk=3)
+    b = oracle_replay(cfg, mk, params, t0[ids], ids, 99, 60, teacher, cfg.envs_per_agent,
+                      chunk=100)
+    assert a.keys() == b.keys()
+    for k in a:
+        if k == "final":
+            for x, y in zip(a[k], b[k]):
+                assert np.array_equal(x, y)
+        else:
+            assert np.array_equal(a[k], b[k], equal_nan=True), k
