@@ -343,6 +343,25 @@ int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
                         double periods_per_year, double risk_free, double *out,
                         void *work, size_t work_bytes, void *stream);
 
+/*
+ * tp_backtest_metrics_noalloc -- tp_backtest_metrics for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same kernels and the same results,
+ * bit for bit, with the segment partials in a static device scratch array
+ * of 4.5 MiB that the library holds on each GPU it runs on until the
+ * process ends, instead of a caller workspace.  Nothing is allocated.
+ * Every shape within the limits of tp_backtest_metrics fits (the largest
+ * needs about 4.1 MiB); a request that would not fit returns
+ * TP_EUNSUPPORTED.  All calls on one GPU share its scratch, which keeps the
+ * last call's contents (nothing in it needs clearing): calls that may
+ * overlap on one GPU (different streams, or different host threads) race
+ * and must be serialised by the caller.  The stream must belong to the
+ * current device.  Arguments otherwise as tp_backtest_metrics.
+ */
+int tp_backtest_metrics_noalloc(const double *v0, const double *v, int32_t T, int32_t E,
+                                double periods_per_year, double risk_free, double *out,
+                                void *stream);
+
 /* Bytes of the caller-owned device workspace tp_backtest_metrics needs for
  * T steps of E series (8-byte aligned; segment partial sums and maxima), or
  * 0 for T < 1 or E outside 1 .. 64 * 65535.  Host only. */

@@ -623,6 +623,32 @@ int tp_backtest_metrics(const double *v0, const double *v, int32_t T, int32_t E,
     return ok();
 }
 
+int tp_backtest_metrics_noalloc(const double *v0, const double *v, int32_t T, int32_t E,
+                                double periods_per_year, double risk_free, double *out,
+                                void *stream)
+{
+    if (!v0 || !v || !out) return fail(TP_EINVAL, "a metrics array is NULL");
+    if (!aligned(v0, 8) || !aligned(v, 8) || !aligned(out, 8))
+        return fail(TP_EINVAL, "metrics arrays are not 8-byte aligned");
+    if (T < 1 || E < 1 || E > 64 * 65535)
+        return fail(TP_EINVAL, "T = %d, E = %d (1 <= E <= %d)", T, E, 64 * 65535);
+    if (!(periods_per_year > 0.0))
+        return fail(TP_EINVAL, "periods_per_year = %g must be > 0", periods_per_year);
+    if (!std::isfinite(risk_free)) return fail(TP_EINVAL, "risk_free = %g", risk_free);
+    const size_t need = backtest_metrics_scratch_needed(T, E);
+    if (need > backtest_metrics_scratch_capacity())
+        return fail(TP_EUNSUPPORTED, "T = %d, E = %d needs %zu bytes of scratch; the static "
+                    "scratch holds %zu (use tp_backtest_metrics with a workspace)", T, E, need,
+                    backtest_metrics_scratch_capacity());
+    void *work = nullptr;
+    hipError_t e = backtest_metrics_scratch(&work);
+    if (e != hipSuccess) return hip_fail(e, "metrics scratch address");
+    e = launch_backtest_metrics(v0, v, T, E, periods_per_year, risk_free, out, work,
+                                (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "metrics launch");
+    return ok();
+}
+
 int64_t tp_ppo_param_count(const tp_ppo *cfg)
 {
     PpoLayout L;

@@ -93,6 +93,12 @@ hipError_t launch_zero_i32(int32_t *p, hipStream_t s);
 // the env step's LDS observation rows for this market fit the device
 bool env_rows_fit(const EnvConst &c, int obs_bf16);
 size_t backtest_metrics_work_bytes(int T, int E);
+// the no-allocation variant: bytes of scratch the call needs (0 on the
+// one-launch path), the static scratch's size, and its device address on
+// the current device
+size_t backtest_metrics_scratch_needed(int T, int E);
+size_t backtest_metrics_scratch_capacity();
+hipError_t backtest_metrics_scratch(void **ptr);
 hipError_t launch_backtest_metrics(const double *v0, const double *v, int T, int E,
                                    double periods_per_year, double risk_free, double *out,
                                    void *work, hipStream_t s);

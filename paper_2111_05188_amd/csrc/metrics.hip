@@ -23,10 +23,21 @@
 //   3. per env: the segments' squared deviations summed in segment order,
 //      their largest drawdown, and the five metrics.
 // Only the sums are reassociated (fixed order, deterministic).
+#include <mutex>
+
 #include "device.hpp"
 #include "internal.hpp"
 
 namespace tpk {
+
+// Static device scratch for tp_backtest_metrics_noalloc (callers that cannot
+// allocate).  Every shape the three-launch path takes needs at most
+// 8 (4 s + s TC + E) bytes with s = nseg E <= 1024 EB and s TC <= 2^18, i.e.
+// below 4.2 MiB; 4.5 MiB covers it.  Each GPU holds its own copy until the
+// process ends.  In host code `scratch` names a host-side stand-in: its
+// device address is taken once per device with hipGetSymbolAddress.
+constexpr size_t METRICS_SCRATCH_BYTES = (size_t)9 << 19;   // 4.5 MiB
+static __device__ __align__(256) double scratch[METRICS_SCRATCH_BYTES / sizeof(double)];
 
 namespace {
 
@@ -377,6 +388,39 @@ size_t backtest_metrics_work_bytes(int T, int E)
     return sizeof(double) * (4 * se + se * g.TC + (size_t)E);
 }
 
+static bool metrics_one_launch(int T, int E)
+{
+    const int lg = metrics_eb_log2(T, E);
+    return ((E + (1 << lg) - 1) >> lg) >= 256;
+}
+
+size_t backtest_metrics_scratch_needed(int T, int E)
+{
+    return metrics_one_launch(T, E) ? 0 : backtest_metrics_work_bytes(T, E);
+}
+
+size_t backtest_metrics_scratch_capacity() { return METRICS_SCRATCH_BYTES; }
+
+hipError_t backtest_metrics_scratch(void **ptr)
+{
+    constexpr int MAX_DEV = 64;
+    static std::mutex mu;
+    static void *addr[MAX_DEV] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= MAX_DEV) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> g(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
+
 hipError_t launch_backtest_metrics(const double *v0, const double *v, int T, int E,
                                    double periods_per_year, double risk_free, double *out,
                                    void *work, hipStream_t s)
@@ -384,7 +428,7 @@ hipError_t launch_backtest_metrics(const double *v0, const double *v, int T, int
     {
         const int lg = metrics_eb_log2(T, E);
         const int blocks = (E + (1 << lg) - 1) >> lg;
-        if (blocks >= 256) {
+        if (blocks >= 256) {   // metrics_one_launch
             hipLaunchKernelGGL(metrics_onepass_kernel, dim3(blocks), dim3(MET_THREADS), 0, s, v0, v,
                                T, E, periods_per_year, risk_free, out, lg);
             return hipGetLastError();

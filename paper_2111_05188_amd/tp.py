@@ -84,6 +84,7 @@ EXPORTS = ("tp_env_reset", "tp_env_step", "tp_actor_packed_bytes",
            "tp_ppo_param_count", "tp_ppo_workspace_bytes", "tp_ppo_update",
            "tp_ppo_update_agents", "tp_minibatch_rows", "tp_rollout_path",
            "tp_actor_release", "tp_critic_release", "tp_check_starts",
+           "tp_backtest_metrics_noalloc",
            "tp_last_error", "tp_version")
 
 _lib = None
@@ -111,6 +112,8 @@ def load(path: str = LIB_PATH):
     L.tp_critic_value.argtypes = [vp, vp, sz, vp, i64, i64, i32, vp, vp]
     L.tp_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp, vp,
                                       C.c_size_t, vp]
+    L.tp_backtest_metrics_noalloc.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp,
+                                              vp]
     L.tp_backtest_metrics_work_bytes.restype = C.c_size_t
     L.tp_backtest_metrics_work_bytes.argtypes = [i32, i32]
     L.tp_ensemble_fuse.argtypes = [vp, i32, i32, i64, vp]
@@ -137,7 +140,8 @@ def load(path: str = LIB_PATH):
               "tp_critic_pack", "tp_critic_value", "tp_backtest_metrics",
               "tp_ensemble_fuse", "tp_fitness", "tp_keep_best", "tp_select",
               "tp_ppo_update", "tp_ppo_update_agents", "tp_minibatch_rows",
-              "tp_actor_release", "tp_critic_release", "tp_check_starts"):
+              "tp_actor_release", "tp_critic_release", "tp_check_starts",
+              "tp_backtest_metrics_noalloc"):
         getattr(L, f).restype = C.c_int
     _lib = L
     return L
@@ -439,6 +443,19 @@ def backtest_metrics(v0: torch.Tensor, v: torch.Tensor, periods_per_year: float,
     _check(load().tp_backtest_metrics(_ptr(v0), _ptr(v), T, E, periods_per_year,
                                       risk_free, _ptr(out), _ptr(work), work.numel(),
                                       _stream(stream)))
+    return out
+
+
+def backtest_metrics_noalloc(v0: torch.Tensor, v: torch.Tensor, periods_per_year: float,
+                             risk_free: float = 0.0, out: torch.Tensor | None = None,
+                             stream=None):
+    """backtest_metrics without a workspace: the library's static device
+    scratch holds the partials (calls on one GPU must not overlap)."""
+    T, E = v.shape
+    if out is None:
+        out = torch.empty(E, 5, dtype=torch.float64, device=v.device)
+    _check(load().tp_backtest_metrics_noalloc(_ptr(v0), _ptr(v), T, E, periods_per_year,
+                                              risk_free, _ptr(out), _stream(stream)))
     return out
 
 
