@@ -12,8 +12,10 @@ Prints one JSON line:
   roofline   the fused rollout kernel against the bf16 MFMA peak (its
              algorithmic FLOPs / its average duration, measured with HIP
              events on its stream), plus its HBM figure (algorithmic bytes)
-  cpu_baseline  the oracle on one host core on a bounded sample of the same
-             workload (64 envs x one 390-step episode by default), with the
+  cpu_baseline  the oracle on bounded samples of the same workload: all
+             host cores (OpenMP over envs, 32 envs per thread by default; the
+             reported value), one thread (64 envs), one thread with the fp32
+             actor (32 envs); each a full 390-step episode per env, with the
              host's CPU model
 """
 
@@ -89,7 +91,10 @@ def main():
     ap.add_argument("--workload", default="nasdaq100",
                     choices=["nasdaq100", "ensemble", "stress", "dow30", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-envs", type=int, default=64)
+    ap.add_argument("--cpu-envs", type=int, default=64,
+                    help="envs of the one-thread oracle sample")
+    ap.add_argument("--cpu-envs-all", type=int, default=0,
+                    help="envs of the all-core oracle sample (default 32 per thread)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -164,7 +169,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, mk, params, t0, args.cpu_envs)
+        cpu = cpu_baseline(cfg, mk, params, t0, args.cpu_envs, args.cpu_envs_all)
 
     line = {
         "metric": METRIC,
@@ -223,37 +228,75 @@ def host_cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(cfg, mk, params, t0, n_envs, chunk=64):
-    """The oracle, as it stands, on a bounded sample: n_envs envs of the same
-    workload for one full episode (free-running, single thread).  Envs are
-    independent, so the sample runs in chunks of `chunk` envs, each chunk's
-    rollout + GAE timed and the times summed; a progress line follows each
-    chunk."""
+def _oracle_leg(cfg, mk, params, t0, ids, bf16, omp, chunk, label):
+    """One timed oracle run: free-running rollout + GAE of the envs `ids`
+    for one full episode, in chunks of `chunk` envs (a progress line after
+    each); returns (env-steps/s, seconds, threads)."""
     import numpy as np
 
     import oracle
     m = oracle.market(mk.price, mk.ind, mk.row0)
     ec = oracle.env_cfg(cfg)
-    act = oracle.actor(*params, cfg.dims, cfg.dtype == "bf16", cfg.envs_per_agent)
-    print(f"[bench] oracle sample: {n_envs} envs x {cfg.L} steps", file=sys.stderr, flush=True)
+    act = oracle.actor(*params, cfg.dims, bf16, cfg.envs_per_agent)
     dt = 0.0
-    for c0 in range(0, n_envs, chunk):
-        ids = np.arange(c0, min(n_envs, c0 + chunk))
-        cash, sh, t = oracle.env_reset(ec, t0[ids], cfg.n)
+    for c0 in range(0, len(ids), chunk):
+        sub = ids[c0:c0 + chunk]
+        cash, sh, t = oracle.env_reset(ec, t0[sub], cfg.n)
         t1 = time.time()
-        out = oracle.rollout(m, ec, act, cash, sh, t, SEED, 0, cfg.L, cfg.K_pad, env_ids=ids,
-                             want=("reward", "done"))
-        v = np.zeros((cfg.L + 1, len(ids)), np.float32)
+        out = oracle.rollout(m, ec, act, cash, sh, t, SEED, 0, cfg.L, cfg.K_pad, env_ids=sub,
+                             want=("reward", "done"), omp=omp)
+        v = np.zeros((cfg.L + 1, len(sub)), np.float32)
         oracle.gae(out["reward"], v, out["done"], cfg.gamma, cfg.lam)
         dt += time.time() - t1
-        if n_envs > chunk:
-            print(f"[bench] oracle envs {c0}..{ids[-1]} done, {dt:.1f}s so far",
-                  file=sys.stderr, flush=True)
-    return {"value": n_envs * cfg.L / dt, "unit": "env-steps/s", "cores": 1,
-            "kind": "oracle", "seconds": dt, "cpu_model": host_cpu_model(),
+        print(f"[bench] oracle {label}: envs {sub[0]}..{sub[-1]} done, {dt:.1f}s so far",
+              file=sys.stderr, flush=True)
+    return len(ids) * cfg.L / dt, dt, oracle.threads(omp)
+
+
+def cpu_baseline(cfg, mk, params, t0, n_envs, all_core_envs=None):
+    """The oracle, as it stands, on bounded samples of the same workload
+    (free-running rollout + GAE, one full episode per env):
+      - all cores: the OpenMP build of the same source (envs split over
+        threads, results identical), all_core_envs envs (default 32 per
+        thread) -- the reported value;
+      - one thread: n_envs envs with the workload's actor precision;
+      - one thread, fp32 actor: n_envs / 2 envs of the same shape with the
+        fp32 masters used as they are (no bf16 rounding)."""
+    import numpy as np
+
+    import oracle
+    threads = oracle.threads(True)
+    n_all = all_core_envs if all_core_envs else 32 * threads
+    n_all = min(n_all, cfg.E)
+    print(f"[bench] oracle samples: {n_all} envs on {threads} threads, {n_envs} envs on one "
+          f"thread, {max(1, n_envs // 2)} envs fp32 on one thread", file=sys.stderr, flush=True)
+    bf = cfg.dtype == "bf16"
+    all_ids = np.arange(n_all)
+    v_all, s_all, thr = _oracle_leg(cfg, mk, params, t0, all_ids, bf, True,
+                                    max(thr_chunk(threads), 1), "all cores")
+    v_one, s_one, _ = _oracle_leg(cfg, mk, params, t0, np.arange(n_envs), bf, False, 64,
+                                  "one thread")
+    n32 = max(1, n_envs // 2)
+    v_32, s_32, _ = _oracle_leg(cfg, mk, params, t0, np.arange(n32), False, False, 64,
+                                "one thread fp32")
+    return {"value": v_all, "unit": "env-steps/s", "cores": thr, "kind": "oracle",
+            "seconds": s_all, "cpu_model": host_cpu_model(),
             "host_cpus": len(os.sched_getaffinity(0)),
-            "sample": f"{n_envs} envs x {cfg.L} steps of the same workload (full actor), "
-                      f"free-running rollout + GAE, one thread"}
+            "sample": f"{n_all} envs x {cfg.L} steps of the same workload (full actor, "
+                      f"{'bf16-emulated' if bf else 'fp32'}), free-running rollout + GAE, "
+                      f"OpenMP over envs on {thr} threads",
+            "single_thread": {"value": v_one, "seconds": s_one, "cores": 1,
+                              "sample": f"{n_envs} envs x {cfg.L} steps, one thread"},
+            "single_thread_fp32_actor": {"value": v_32, "seconds": s_32, "cores": 1,
+                                         "sample": f"{n32} envs x {cfg.L} steps, fp32 actor, "
+                                                   "one thread"}}
+
+
+def thr_chunk(threads):
+    """Envs per timed chunk of the all-core leg: a few per thread, so the
+    progress lines keep coming and every thread has work."""
+    return 8 * threads
+
 
 if __name__ == "__main__":
     main()

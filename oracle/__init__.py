@@ -21,17 +21,27 @@ _SRC = os.path.join(_HERE, "oracle.c")
 # ORACLE_LIB points the wrapper at another build of oracle.c (used to check
 # that the pins fail when a mistake is planted in the oracle).
 _LIB = os.environ.get("ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
+# The same source built with OpenMP: the rollout's envs run on all cores
+# (the CPU baseline's all-core leg); results are identical to the plain build.
+_LIB_OMP = os.path.join(_HERE, "liboracle_omp.so")
 
 CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC",
           "-shared", "-Wall", "-Wextra"]
 
 
+def _compile(out, extra=()):
+    tmp = out + ".tmp"
+    subprocess.check_call(["gcc", *CFLAGS, *extra, "-o", tmp, _SRC, "-lm"])
+    os.replace(tmp, out)
+
+
 def build(force: bool = True) -> str:
-    """Compile liboracle.so with gcc (no fast-math, no fp contraction)."""
+    """Compile liboracle.so (and the OpenMP build liboracle_omp.so) with gcc
+    (no fast-math, no fp contraction)."""
     if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp"
-        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
-        os.replace(tmp, _LIB)
+        _compile(_LIB, ["-Wno-unknown-pragmas"])
+    if force or not os.path.exists(_LIB_OMP):
+        _compile(_LIB_OMP, ["-fopenmp"])
     return _LIB
 
 
@@ -64,47 +74,61 @@ class Traj(C.Structure):
 
 
 _lib = None
+_lib_omp = None
 
 
-def lib():
-    global _lib
+def lib(omp: bool = False):
+    """The oracle library; omp=True gives the OpenMP build (the rollout's
+    envs over OMP_NUM_THREADS threads, results identical)."""
+    global _lib, _lib_omp
+    if omp:
+        if _lib_omp is None:
+            if not os.path.exists(_LIB_OMP) or os.path.getmtime(_LIB_OMP) < os.path.getmtime(_SRC):
+                build()
+            _lib_omp = _declare(C.CDLL(_LIB_OMP))
+        return _lib_omp
     if _lib is None:
         if not os.environ.get("ORACLE_LIB") and (
                 not os.path.exists(_LIB)
                 or os.path.getmtime(_LIB) < os.path.getmtime(_SRC)):
             build()
-        L = C.CDLL(_LIB)
-        vp, i32, i64, u32, u64 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64
-        L.orc_bf16_bits.restype = C.c_uint16
-        L.orc_bf16_bits.argtypes = [C.c_float]
-        L.orc_bf16_value.restype = C.c_float
-        L.orc_bf16_value.argtypes = [C.c_uint16]
-        L.orc_philox4x32_10.argtypes = [vp, vp, vp]
-        L.orc_uniform.restype = C.c_float
-        L.orc_uniform.argtypes = [u32]
-        L.orc_normals.argtypes = [u64, u32, u32, u32, i32, vp]
-        L.orc_obs.argtypes = [vp, vp, i64, C.c_double, vp, i32, vp, vp]
-        L.orc_env_reset.argtypes = [vp, i32, i32, vp, vp, vp, vp]
-        L.orc_clip_action.restype = C.c_float
-        L.orc_clip_action.argtypes = [C.c_float]
-        L.orc_shares_from_action.restype = i32
-        L.orc_shares_from_action.argtypes = [C.c_float, i32]
-        L.orc_env_step_one.restype = C.c_float
-        L.orc_env_step_one.argtypes = [vp, vp, vp, vp, vp, vp, vp]
-        L.orc_env_step.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp, i32, vp, vp]
-        L.orc_mlp.argtypes = [vp, i32, i32, vp, i32, vp]
-        L.orc_rollout.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, u64, u64,
-                                  i32, i32, vp, vp]
-        L.orc_gae.argtypes = [vp, vp, vp, i32, i32, C.c_float, C.c_float, vp, vp]
-        L.orc_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp]
-        L.orc_ensemble_fuse.argtypes = [vp, i32, i32, C.c_int64]
-        L.orc_fitness.argtypes = [vp, i32, i32, i32, C.c_double, vp]
-        L.orc_keep_best.argtypes = [vp, vp, vp, vp, vp, i32, C.c_int64]
-        L.orc_select.argtypes = [vp, vp, i32, C.c_int64, i32, vp]
-        L.orc_minibatch_rows.argtypes = [u64, u64, i32, i32, i32, i32, i32, i32, vp]
-        L.orc_version.restype = C.c_int
-        _lib = L
+        _lib = _declare(C.CDLL(_LIB))
     return _lib
+
+
+def _declare(L):
+    """Argument and result types of the oracle's functions."""
+    vp, i32, i64, u32, u64 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64
+    L.orc_bf16_bits.restype = C.c_uint16
+    L.orc_bf16_bits.argtypes = [C.c_float]
+    L.orc_bf16_value.restype = C.c_float
+    L.orc_bf16_value.argtypes = [C.c_uint16]
+    L.orc_philox4x32_10.argtypes = [vp, vp, vp]
+    L.orc_uniform.restype = C.c_float
+    L.orc_uniform.argtypes = [u32]
+    L.orc_normals.argtypes = [u64, u32, u32, u32, i32, vp]
+    L.orc_obs.argtypes = [vp, vp, i64, C.c_double, vp, i32, vp, vp]
+    L.orc_env_reset.argtypes = [vp, i32, i32, vp, vp, vp, vp]
+    L.orc_clip_action.restype = C.c_float
+    L.orc_clip_action.argtypes = [C.c_float]
+    L.orc_shares_from_action.restype = i32
+    L.orc_shares_from_action.argtypes = [C.c_float, i32]
+    L.orc_env_step_one.restype = C.c_float
+    L.orc_env_step_one.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+    L.orc_env_step.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp, i32, vp, vp]
+    L.orc_mlp.argtypes = [vp, i32, i32, vp, i32, vp]
+    L.orc_rollout.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, u64, u64,
+                              i32, i32, vp, vp]
+    L.orc_gae.argtypes = [vp, vp, vp, i32, i32, C.c_float, C.c_float, vp, vp]
+    L.orc_backtest_metrics.argtypes = [vp, vp, i32, i32, C.c_double, C.c_double, vp]
+    L.orc_ensemble_fuse.argtypes = [vp, i32, i32, C.c_int64]
+    L.orc_fitness.argtypes = [vp, i32, i32, i32, C.c_double, vp]
+    L.orc_keep_best.argtypes = [vp, vp, vp, vp, vp, i32, C.c_int64]
+    L.orc_select.argtypes = [vp, vp, i32, C.c_int64, i32, vp]
+    L.orc_minibatch_rows.argtypes = [u64, u64, i32, i32, i32, i32, i32, i32, vp]
+    L.orc_version.restype = C.c_int
+    L.orc_threads.restype = C.c_int
+    return L
 
 
 def _p(a):
@@ -260,11 +284,12 @@ def mlp(act, agent, x):
 def rollout(mkt, ecfg, act, cash, shares, t, seed, step0, L, K_pad,
             env_ids=None, teacher=None, want=("obs", "act", "logp", "reward",
                                               "done", "cash", "shares", "mu",
-                                              "asset")):
+                                              "asset"), omp=False):
     """Run O9 over the envs in (cash, shares, t) (updated in place).
 
     env_ids: global env index of each row (Philox counter and agent id);
-    teacher: raw actions [L][E][n] that drive the env step (teacher forcing).
+    teacher: raw actions [L][E][n] that drive the env step (teacher forcing);
+    omp: run on the OpenMP build (envs over threads, same results).
     Returns a dict of time-major arrays."""
     E, n = shares.shape
     ids = None if env_ids is None else _c(env_ids, np.int32)
@@ -289,10 +314,15 @@ def rollout(mkt, ecfg, act, cash, shares, t, seed, step0, L, K_pad,
         if key in want:
             out[key] = np.zeros(shape, dtype=dt)
             setattr(tr, fld, _p(out[key]))
-    lib().orc_rollout(C.byref(mkt.s), C.byref(ecfg), C.byref(act.s), E,
+    lib(omp).orc_rollout(C.byref(mkt.s), C.byref(ecfg), C.byref(act.s), E,
                       _p(ids), _p(cash), _p(shares), _p(t), seed, step0, L,
                       K_pad, _p(tch), C.byref(tr))
     return out
+
+
+def threads(omp: bool = False) -> int:
+    """Threads the rollout uses in the plain (1) or the OpenMP build."""
+    return lib(omp).orc_threads()
 
 
 def gae(r, v, d, gamma, lam):

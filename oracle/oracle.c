@@ -83,6 +83,15 @@ typedef struct {
 
 int orc_version(void) { return ORC_VERSION; }
 
+/* Threads the rollout's envs are split over: 1 for the plain build, the
+ * OpenMP team size for the OpenMP build. */
+#ifdef _OPENMP
+#include <omp.h>
+int orc_threads(void) { return omp_get_max_threads(); }
+#else
+int orc_threads(void) { return 1; }
+#endif
+
 /* ------------------------------------------------------------------------ */
 /* bf16 rounding (IEEE round-to-nearest-even on the upper 16 bits)           */
 /* ------------------------------------------------------------------------ */
@@ -473,6 +482,17 @@ void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
             W[3 * ag + l] = rounded_copy(a->W[l] + (size_t)ag * cnt, cnt, a->bf16);
         }
 
+    /* an env without market rows for all L steps is not stepped: its
+     * state stays, its rows hold NaN (done = 0, obs untouched) */
+    uint8_t *active = (uint8_t *)malloc((size_t)E + 1);
+    for (int32_t e = 0; e < E; ++e) active[e] = (uint8_t)has_rows(m, t[e], L);
+
+    /* Envs share nothing, so each env runs its L steps on its own; the
+     * OpenMP build (liboracle_omp.so, the CPU baseline over all cores) splits
+     * the envs over threads, the plain build runs them one after another.
+     * Either way every env sees the same operations in the same order. */
+#pragma omp parallel
+    {
     float *x = (float *)malloc(sizeof(float) * K_pad);
     uint16_t *xb = (uint16_t *)malloc(sizeof(uint16_t) * K_pad);
     float *h1 = (float *)malloc(sizeof(float) * d[1]);
@@ -480,15 +500,10 @@ void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
     float *mu = (float *)malloc(sizeof(float) * n);
     float *z = (float *)malloc(sizeof(float) * n);
     float *act = (float *)malloc(sizeof(float) * n);
-
-    /* an env without market rows for all L steps is not stepped: its
-     * state stays, its rows hold NaN (done = 0, obs untouched) */
-    uint8_t *active = (uint8_t *)malloc((size_t)E + 1);
-    for (int32_t e = 0; e < E; ++e) active[e] = (uint8_t)has_rows(m, t[e], L);
-
-    for (int32_t j = 0; j < L; ++j) {
-        const uint32_t step = (uint32_t)(step0 + (uint64_t)j);
-        for (int32_t e = 0; e < E; ++e) {
+#pragma omp for schedule(dynamic, 1)
+    for (int32_t e = 0; e < E; ++e) {
+        for (int32_t j = 0; j < L; ++j) {
+            const uint32_t step = (uint32_t)(step0 + (uint64_t)j);
             const int32_t gid = env_ids ? env_ids[e] : e;
             const int32_t ag = gid / a->envs_per_agent;
             int32_t *h = &shares[(size_t)e * n];
@@ -554,8 +569,9 @@ void orc_rollout(const orc_market *m, const orc_env_cfg *cfg,
             }
         }
     }
-    free(active);
     free(x); free(xb); free(h1); free(h2); free(mu); free(z); free(act);
+    }
+    free(active);
     for (int32_t i = 0; i < 3 * A; ++i) free(W[i]);
     free(W);
 }

@@ -16,7 +16,9 @@ import numpy as np
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libtp.so")
+# TP_LIB_PATH selects another build of the same library (the CPU sanitizer
+# test loads a host-instrumented build); default: the in-tree libtp.so.
+LIB_PATH = os.environ.get("TP_LIB_PATH") or os.path.join(HERE, "libtp.so")
 
 TP_OK, TP_EINVAL, TP_ERANGE, TP_EUNSUPPORTED, TP_EHIP = 0, -1, -2, -3, -4
 TP_F32, TP_BF16 = 0, 1

@@ -1,6 +1,6 @@
 """Host-side logic of bench.py (no GPU): the single-GPU refusal, the per
 env-step work figures the roofline divides by, the counter lookup's source
-gate and the oracle sample's chunking."""
+gate and the oracle samples (all cores, one thread, fp32 actor)."""
 
 import json
 import os
@@ -47,11 +47,17 @@ def test_counter_traffic_is_gated_by_the_kernel_sources():
     assert bench.counter_traffic("no_such_kernel x") is None
 
 
-def test_oracle_sample_runs_in_chunks_and_names_the_host():
+def test_oracle_samples_name_the_host_and_the_threads():
+    import oracle
     cfg = W.get_config("tiny")
     mk, t0, params = W.make_market(cfg), W.make_t0(cfg), W.make_actor(cfg)
-    r = bench.cpu_baseline(cfg, mk, params, t0, 24, chunk=10)
-    assert r["kind"] == "oracle" and r["cores"] == 1 and r["unit"] == "env-steps/s"
+    r = bench.cpu_baseline(cfg, mk, params, t0, 24, all_core_envs=40)
+    assert r["kind"] == "oracle" and r["unit"] == "env-steps/s"
+    assert r["cores"] == oracle.threads(True) >= 1
     assert r["value"] > 0 and np.isfinite(r["value"]) and r["seconds"] > 0
     assert r["cpu_model"] and r["host_cpus"] >= 1
-    assert "24 envs" in r["sample"]
+    assert "40 envs" in r["sample"] and "OpenMP" in r["sample"]
+    one = r["single_thread"]
+    assert one["cores"] == 1 and one["value"] > 0 and "24 envs" in one["sample"]
+    f32 = r["single_thread_fp32_actor"]
+    assert f32["cores"] == 1 and f32["value"] > 0 and "12 envs" in f32["sample"]

@@ -401,3 +401,33 @@ def test_parallel_replay_equals_serial():
                 assert np.array_equal(x, y)
         else:
             assert np.array_equal(a[k], b[k], equal_nan=True), k
+
+
+def test_openmp_build_equals_plain_build():
+    """The CPU baseline's all-core leg runs the OpenMP build of the same
+    oracle source; its free-running rollout equals the plain build's bit
+    for bit (envs are independent), here on 24 envs of the 100-stock shape
+    with a small actor and on the tiny workload."""
+    import oracle
+    import workloads as W
+    assert oracle.threads(False) == 1 and oracle.threads(True) >= 1
+    for cfg in (W.get_config("nasdaq100").with_(N=3 * 390, E=24, hidden=(128, 128)),
+                W.get_config("tiny")):
+        mk = W.make_market(cfg)
+        t0 = W.make_t0(cfg)
+        params = W.make_actor(cfg)
+        m = oracle.market(mk.price, mk.ind)
+        ec = oracle.env_cfg(cfg)
+        act = oracle.actor(*params, cfg.dims, cfg.dtype == "bf16", cfg.envs_per_agent)
+        outs = []
+        for omp in (False, True):
+            cash, sh, t = oracle.env_reset(ec, t0, cfg.n)
+            o = oracle.rollout(m, ec, act, cash, sh, t, 5, 0, 40, cfg.K_pad, omp=omp)
+            o["state"] = (cash, sh, t)
+            outs.append(o)
+        a, b = outs
+        for k in a:
+            if k == "state":
+                assert all(np.array_equal(x, y) for x, y in zip(a[k], b[k]))
+            else:
+                assert np.array_equal(a[k], b[k], equal_nan=True), k
