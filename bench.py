@@ -83,6 +83,22 @@ def counter_traffic(kernel_key: str):
     return None if k is None else k["traffic_bytes"]
 
 
+def mfma_busy(kernel_key: str):
+    """MFMA busy fraction per launch (SQ_VALU_MFMA_BUSY_CYCLES over the SIMD
+    cycles) from the committed counter summary, or None once the kernel
+    sources differ from the ones the counters were taken on."""
+    path = os.path.join(ROOT, "profiles", "mfma_busy_counters.md")
+    try:
+        text = open(path).read()
+        data = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    except (OSError, IndexError, ValueError):
+        return None
+    if data.get("source_sha256") != kernel_source_hash():
+        return None
+    k = data.get("kernels", {}).get(kernel_key)
+    return None if k is None else k["mfma_busy_frac"]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -201,6 +217,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved_tflops / peak_flops,
             "traffic": counter_traffic(f"{kname} {cfg.name}"),
+            "mfma_busy_frac": mfma_busy(f"{kname} {cfg.name}"),
             "launch_ms": t_roll * 1e3,
             "flops_per_launch": flops,
             "hbm_achieved_GBs": roll_bytes / t_roll / 1e9,

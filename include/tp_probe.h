@@ -23,6 +23,18 @@ double tpp_mfma_issue_flops(int blocks, int iters);
 int tpp_mfma32_issue(int blocks, int iters, float *out, void *stream);
 double tpp_mfma32_issue_flops(int blocks, int iters);
 
+/* Issue-rate sweep: `blocks` workgroups of `waves` waves (1..16), each wave
+ * issuing iters x nacc back-to-back MFMAs of shape m (16:
+ * v_mfma_f32_16x16x32_bf16, 32: v_mfma_f32_32x32x16_bf16) into nacc
+ * (1, 2, 4 or 8) independent accumulators, with one A/B operand pair per
+ * accumulator (distinct != 0) or one pair shared by all.  out:
+ * blocks * waves * 64 floats (written only under a condition the data never
+ * meets); clk[0..1] (device): the shader-clock and the 100 MHz-clock ticks
+ * wave 0 of workgroup 0 spent in its loop. */
+int tpp_mfma_sweep(int m, int nacc, int distinct, int blocks, int waves, int iters, float *out,
+                   unsigned long long *clk, void *stream);
+double tpp_mfma_sweep_flops(int m, int nacc, int blocks, int waves, int iters);
+
 /* `blocks` workgroups of eight waves; wave w streams 1-KiB fragments
  * f = 0 .. frags_per_wave-1 of buf + w * frags_per_wave KiB, reps times,
  * 16 loads in flight.  buf >= 8 * frags_per_wave KiB (every workgroup reads

@@ -1,5 +1,8 @@
 // Hardware probes for the roofline ceilings the design notes quote
 // (measurement tooling, built as libtpprobe.so; not part of the method):
+//   * tpp_mfma_sweep: the same issue rates over accumulators per wave
+//     (1-8), operands shared or one pair per accumulator, and waves per
+//     workgroup, with the shader clock the loop ran at;
 //   * tpp_mfma_issue / tpp_mfma32_issue: waves issuing
 //     v_mfma_f32_16x16x32_bf16 (eight independent accumulators per wave) or
 //     v_mfma_f32_32x32x16_bf16 (four) back to back on register operands:
@@ -78,6 +81,80 @@ __global__ __launch_bounds__(256) void mfma32_issue_kernel(int iters, float *out
     if (s == 1234567.0f) out[blockIdx.x * 256 + threadIdx.x] = s;
 }
 
+// The issue-rate sweep: NACC independent accumulators per wave, each with
+// its own A and B operand registers (DISTINCT) or all sharing one pair, on
+// v_mfma_f32_16x16x32_bf16 (M = 16) or v_mfma_f32_32x32x16_bf16 (M = 32).
+// Wave 0 of workgroup 0 also records the shader clock (s_memtime) and the
+// constant 100 MHz clock (s_memrealtime) around its loop, so the host can
+// tell the clock the MFMAs ran at.
+template <int M, int NACC, bool DISTINCT>
+__global__ __launch_bounds__(256) void mfma_sweep_kernel(int iters, float *out,
+                                                          unsigned long long *clk)
+{
+    constexpr int NA = DISTINCT ? NACC : 1;
+    constexpr int NV = M == 16 ? 4 : 16;
+    typedef float accv __attribute__((ext_vector_type(NV)));
+    const int lane = threadIdx.x % 64;
+    bf16x8 a[NA], b[NA];
+#pragma unroll
+    for (int j = 0; j < NA; ++j)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            a[j][e] = (__bf16)(0.001f * (float)(lane + e + j));
+            b[j][e] = (__bf16)(0.002f * (float)(lane - e - j));
+        }
+    accv acc[NACC];
+#pragma unroll
+    for (int j = 0; j < NACC; ++j)
+#pragma unroll
+        for (int q = 0; q < NV; ++q) acc[j][q] = 0.f;
+    const unsigned long long c0 = clock64(), w0 = wall_clock64();
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int j = 0; j < NACC; ++j) {
+            if constexpr (M == 16)
+                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[DISTINCT ? j : 0],
+                                                                 b[DISTINCT ? j : 0], acc[j], 0, 0, 0);
+            else
+                acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[DISTINCT ? j : 0],
+                                                                 b[DISTINCT ? j : 0], acc[j], 0, 0, 0);
+        }
+    }
+    const unsigned long long c1 = clock64(), w1 = wall_clock64();
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < NACC; ++j)
+#pragma unroll
+        for (int q = 0; q < NV; ++q) s += acc[j][q];
+    if (s == 1234567.0f) out[blockIdx.x * blockDim.x + threadIdx.x] = s;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        clk[0] = c1 - c0;
+        clk[1] = w1 - w0;
+    }
+}
+
+template <int M, int NACC, bool D>
+hipError_t launch_sweep(int blocks, int waves, int iters, float *out, unsigned long long *clk,
+                        hipStream_t st)
+{
+    hipLaunchKernelGGL((mfma_sweep_kernel<M, NACC, D>), dim3(blocks), dim3(64 * waves), 0, st,
+                       iters, out, clk);
+    return hipGetLastError();
+}
+
+template <int M, bool D>
+hipError_t sweep_nacc(int nacc, int blocks, int waves, int iters, float *out,
+                      unsigned long long *clk, hipStream_t st)
+{
+    switch (nacc) {
+    case 1: return launch_sweep<M, 1, D>(blocks, waves, iters, out, clk, st);
+    case 2: return launch_sweep<M, 2, D>(blocks, waves, iters, out, clk, st);
+    case 4: return launch_sweep<M, 4, D>(blocks, waves, iters, out, clk, st);
+    case 8: return launch_sweep<M, 8, D>(blocks, waves, iters, out, clk, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 constexpr int SD = 16;   // loads in flight per wave
 
 __global__ __launch_bounds__(512) void l2_stream_kernel(const u32x4 *__restrict__ buf,
@@ -151,6 +228,29 @@ int tpp_mfma32_issue(int blocks, int iters, float *out, void *stream)
 double tpp_mfma32_issue_flops(int blocks, int iters)
 {
     return (double)blocks * 4.0 * iters * 4 * (2.0 * 32 * 32 * 16);
+}
+
+int tpp_mfma_sweep(int m, int nacc, int distinct, int blocks, int waves, int iters, float *out,
+                   unsigned long long *clk, void *stream)
+{
+    if ((m != 16 && m != 32) || !(nacc == 1 || nacc == 2 || nacc == 4 || nacc == 8) ||
+        blocks < 1 || waves < 1 || waves > 4 || iters < 1 || !out || !clk)
+        return -1;
+    const hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    if (m == 16)
+        e = distinct ? sweep_nacc<16, true>(nacc, blocks, waves, iters, out, clk, st)
+                     : sweep_nacc<16, false>(nacc, blocks, waves, iters, out, clk, st);
+    else
+        e = distinct ? sweep_nacc<32, true>(nacc, blocks, waves, iters, out, clk, st)
+                     : sweep_nacc<32, false>(nacc, blocks, waves, iters, out, clk, st);
+    return e == hipSuccess ? 0 : -4;
+}
+
+double tpp_mfma_sweep_flops(int m, int nacc, int blocks, int waves, int iters)
+{
+    const double per = m == 16 ? 2.0 * 16 * 16 * 32 : 2.0 * 32 * 32 * 16;
+    return (double)blocks * waves * iters * nacc * per;
 }
 
 int tpp_l2_stream(const void *buf, size_t buf_bytes, int frags_per_wave, int reps, int blocks,

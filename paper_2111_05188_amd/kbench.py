@@ -36,6 +36,10 @@ Times, with HIP events on the launch stream:
     v_mfma_f32_16x16x32_bf16 or v_mfma_f32_32x32x16_bf16 on register
     operands, 4 workgroups of four waves per CU) and the L2 -> CU stream one CU can pull in the rollout's
     weight-stream pattern (256 workgroups, one per CU, and 8 workgroups);
+  * mfma_sweep (only with --only mfma_sweep): the issue rate of both bf16
+    MFMA shapes over 1-8 accumulators per wave, operands shared or one pair
+    per accumulator, and 1-4 waves per SIMD, with the shader clock the
+    loops ran at;
   * copy: a plain device-to-device copy of 1 GiB (the reference kernel used
     to calibrate HBM byte counters: FETCH_SIZE and WRITE_SIZE of this copy
     should each read 1 GiB per launch).
@@ -80,7 +84,7 @@ def main():
     ap.add_argument("--iters", type=int, default=20)
     ap.add_argument("--only", default=None,
                     choices=["env_step", "gae", "critic", "metrics", "evolution", "learner",
-                             "train", "probes", "copy"])
+                             "train", "probes", "copy", "mfma_sweep"])
     args = ap.parse_args()
     sys.path.insert(0, __file__.rsplit("/", 2)[0])
     import workloads as W
@@ -326,6 +330,43 @@ def main():
             per_cu = 8 * fpw * 1024 * reps / sec / 1e9
             probes[f"l2_stream_GBs_per_CU_{nb}wg"] = per_cu
         out["probes"] = probes
+
+    if args.only == "mfma_sweep":
+        # issue rate of the two bf16 MFMA shapes over accumulators per wave,
+        # shared or per-accumulator operands and waves per SIMD, with the
+        # shader clock the loops ran at (s_memtime ticks over s_memrealtime's
+        # 100 MHz ticks)
+        import ctypes as C
+        import os
+        pl = C.CDLL(os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpprobe.so"))
+        pl.tpp_mfma_sweep.argtypes = [C.c_int] * 6 + [C.c_void_p, C.c_void_p, C.c_void_p]
+        pl.tpp_mfma_sweep_flops.restype = C.c_double
+        pl.tpp_mfma_sweep_flops.argtypes = [C.c_int] * 5
+        sp = stream.cuda_stream
+        clk = torch.zeros(2, dtype=torch.int64, device=dev)
+        rows = []
+        for m in (16, 32):
+            for distinct in (0, 1):
+                for nacc in (1, 2, 4, 8):
+                    for blocks, waves in ((256, 4), (512, 4), (1024, 4), (2048, 4)):
+                        # 2^28 (16x16x32) or 2^27 (32x32x16) instructions per launch
+                        total = (1 << 28) if m == 16 else (1 << 27)
+                        iters = max(1, total // (blocks * waves * nacc))
+                        sink = torch.empty(blocks * waves * 64, device=dev)
+                        fn = lambda: pl.tpp_mfma_sweep(m, nacc, distinct, blocks, waves, iters,
+                                                       sink.data_ptr(), clk.data_ptr(), sp)
+                        assert fn() == 0
+                        sec = _time(fn, 3, stream)
+                        c = clk.cpu().tolist()
+                        tf = pl.tpp_mfma_sweep_flops(m, nacc, blocks, waves, iters) / sec / 1e12
+                        rows.append({"shape": f"{m}x{m}x{512 // m}", "acc_per_wave": nacc,
+                                     "operands": "per accumulator" if distinct else "shared",
+                                     "waves_per_simd": blocks * waves // 1024,
+                                     "TFLOPs": round(tf, 1),
+                                     "frac_of_2500": round(tf / PEAK_BF16_TFLOPS, 3),
+                                     "clock_GHz": round(0.1 * c[0] / max(c[1], 1), 3)})
+                        print(f"[kbench] mfma sweep {rows[-1]}", file=sys.stderr, flush=True)
+        out["mfma_sweep"] = rows
 
     if args.only in (None, "copy"):
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
