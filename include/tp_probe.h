@@ -44,6 +44,30 @@ double tpp_mfma_sweep_flops(int m, int nacc, int blocks, int waves, int iters);
 int tpp_l2_stream(const void *buf, size_t buf_bytes, int frags_per_wave, int reps, int blocks,
                   void *out, void *stream);
 
+/* Workgroup handoff latency: 2 * pairs workgroups of one wave; b and
+ * b ^ stride (stride a power of two, 2 * stride dividing 2 * pairs) pass a
+ * counter back and forth `rounds` times through one flag word (flags:
+ * pairs * 32 ints, zeroed by the caller) with agent-scope release/acquire
+ * (mode 0) or relaxed agent-scope atomics (mode 1).  Every wait gives up
+ * after spin_limit polls.  out: 2 * pairs records {uint32 xcc, uint32
+ * timeouts, uint64 ticks of the 100 MHz clock over the loop}. */
+int tpp_pingpong(int mode, int pairs, int stride, int rounds, int spin_limit, int *flags,
+                 void *out, void *stream);
+
+/* The handoff with a 16 KiB payload per turn (1024 16-byte words written by
+ * one side, read and checked by the other): payload accesses plain stores
+ * and L1-bypassing loads (mode 0) or device-scope stores and loads (mode 1);
+ * the flag as mode 1 of tpp_pingpong.  flags: pairs * 32 ints (zeroed);
+ * data: pairs * 2 * 1024 16-byte words; out: 2 * pairs records {uint32 xcc,
+ * uint32 timeouts, uint64 ticks, uint32 stale words read, uint32 pad}. */
+int tpp_pingpong_data(int mode, int pairs, int stride, int rounds, int spin_limit, int *flags,
+                      void *data, void *out, void *stream);
+
+/* tpp_l2_stream with an agent-scope acquire (mode 1) or release (mode 2)
+ * fence every `every` fragments of each wave (mode 0: none). */
+int tpp_l2_stream_fence(const void *buf, size_t buf_bytes, int frags_per_wave, int reps,
+                        int blocks, int mode, int every, void *out, void *stream);
+
 /* A plain copy of `bytes` (a multiple of 16; both pointers 16-byte
  * aligned) from src to dst by `blocks` workgroups of 256 threads, 16 bytes
  * per lane per access, four loads in flight, non-temporal. */

@@ -155,6 +155,183 @@ hipError_t sweep_nacc(int nacc, int blocks, int waves, int iters, float *out,
     }
 }
 
+// Workgroup-to-workgroup handoff: workgroup b (of 2 * pairs, one wave
+// each) and its partner b ^ stride pass a counter back and forth `rounds`
+// times through one flag word, with agent-scope release stores and acquire
+// loads (mode 0) or relaxed agent-scope atomics (mode 1).  Every wait is
+// bounded by spin_limit polls; a wait that runs out sets out[b].timeouts and
+// the workgroup leaves its loop, so every wave exits.  out[b]: the XCD the
+// workgroup ran on (hardware register XCC_ID), the 100 MHz ticks of its
+// loop, the timeouts.
+struct PingOut {
+    unsigned int xcc, timeouts;
+    unsigned long long ticks;
+};
+
+__device__ __forceinline__ unsigned int xcc_id()
+{
+    // HW_REG_XCC_ID (20), bits [3:0]
+    return __builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11));
+}
+
+__global__ __launch_bounds__(64) void pingpong_kernel(int mode, int stride, int rounds,
+                                                      int spin_limit, int *flags, PingOut *out)
+{
+    const int b = blockIdx.x;
+    const int partner = b ^ stride;
+    const bool ping = b < partner;
+    // pair index in [0, pairs): b = q (2 stride) + r, r < 2 stride
+    const int pair = (b / (2 * stride)) * stride + (b % stride);
+    int *flag = flags + pair * 32;   // one 128-byte line per pair
+    unsigned int timeouts = 0;
+    const unsigned long long w0 = wall_clock64();
+    if (threadIdx.x == 0) {
+        for (int r = 0; r < rounds && timeouts == 0; ++r) {
+            const int want = ping ? 2 * r : 2 * r + 1;   // value that lets this side go
+            int spins = 0;
+            for (;;) {
+                const int v = mode == 0
+                                  ? __hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT)
+                                  : __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (v >= want) break;
+                if (++spins >= spin_limit) {
+                    ++timeouts;
+                    break;
+                }
+            }
+            if (timeouts) break;
+            if (mode == 0)
+                __hip_atomic_store(flag, want + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            else
+                __hip_atomic_store(flag, want + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        const unsigned long long w1 = wall_clock64();
+        out[b].xcc = xcc_id();
+        out[b].timeouts = timeouts;
+        out[b].ticks = w1 - w0;
+    }
+}
+
+// The same handoff carrying a payload: each side, on its turn, writes
+// PW 16-byte words (round-dependent values) to its half of the pair's data
+// block, then raises the flag (relaxed agent-scope atomic store, after all
+// its stores have completed); the other side, once it sees the flag, reads
+// the payload and counts words that differ from what was written (stale
+// data).  Cache policy of the payload accesses: mode 0 plain stores and
+// loads that bypass the CU's L1 (sc0; the L2 of one XCD is shared by its
+// CUs), mode 1 stores and loads at device scope (sc1).  data: pairs * 2 *
+// PW 16-byte words.  out as for pingpong_kernel, plus the mismatch count.
+constexpr int PW = 1024;
+
+struct PingDataOut {
+    unsigned int xcc, timeouts;
+    unsigned long long ticks;
+    unsigned int mismatches, pad;
+};
+
+__global__ __launch_bounds__(64) void pingpong_data_kernel(int mode, int stride, int rounds,
+                                                           int spin_limit, int *flags,
+                                                           uint32_t *data, PingDataOut *out)
+{
+    typedef uint32_t v4 __attribute__((ext_vector_type(4)));
+    const int b = blockIdx.x, lane = threadIdx.x;
+    const int partner = b ^ stride;
+    const bool ping = b < partner;
+    const int pair = (b / (2 * stride)) * stride + (b % stride);
+    int *flag = flags + pair * 32;
+    // this side writes its own half, reads the partner's
+    uint32_t *base = data + (size_t)pair * 2 * PW * 4;
+    const __amdgpu_buffer_rsrc_t mine = __builtin_amdgcn_make_buffer_rsrc(
+        base + (ping ? 0 : PW * 4), (short)0, PW * 16, 0x00020000);
+    const __amdgpu_buffer_rsrc_t theirs = __builtin_amdgcn_make_buffer_rsrc(
+        base + (ping ? PW * 4 : 0), (short)0, PW * 16, 0x00020000);
+    unsigned int timeouts = 0, bad = 0;
+    const unsigned long long w0 = wall_clock64();
+    for (int r = 0; r < rounds && timeouts == 0; ++r) {
+        const int want = ping ? 2 * r : 2 * r + 1;
+        if (want > 0) {
+            // wait for the partner's turn, then read its payload of value want - 1
+            int spins = 0, v = 0;
+            for (;;) {
+                if (lane == 0) v = __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                v = __shfl(v, 0);
+                if (v >= want) break;
+                if (++spins >= spin_limit) {
+                    ++timeouts;
+                    break;
+                }
+            }
+            if (timeouts) break;
+            const uint32_t expect = (uint32_t)(want - 1);
+#pragma unroll 4
+            for (int k = 0; k < PW / 64; ++k) {
+                const int w = lane + 64 * k;
+                const v4 x = mode == 0 ? __builtin_amdgcn_raw_buffer_load_b128(theirs, w * 16, 0, 1)
+                                       : __builtin_amdgcn_raw_buffer_load_b128(theirs, w * 16, 0, 16);
+                bad += (x.x != expect * 4096u + (uint32_t)w) + (x.w != expect);
+            }
+        }
+        // this side's payload for value `want`
+#pragma unroll 4
+        for (int k = 0; k < PW / 64; ++k) {
+            const int w = lane + 64 * k;
+            const v4 x = {(uint32_t)want * 4096u + (uint32_t)w, 1u, 2u, (uint32_t)want};
+            if (mode == 0)
+                __builtin_amdgcn_raw_buffer_store_b128(x, mine, w * 16, 0, 0);
+            else
+                __builtin_amdgcn_raw_buffer_store_b128(x, mine, w * 16, 0, 16);
+        }
+        __builtin_amdgcn_s_waitcnt(0);   // every store of this wave has completed
+        if (lane == 0) __hip_atomic_store(flag, want + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const unsigned long long w1 = wall_clock64();
+    // lane totals of stale words
+    for (int o = 32; o >= 1; o >>= 1) bad += __shfl_xor(bad, o);
+    if (lane == 0) {
+        out[b].xcc = __builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11));
+        out[b].timeouts = timeouts;
+        out[b].ticks = w1 - w0;
+        out[b].mismatches = bad;
+    }
+}
+
+// The rollout's weight stream (1 KiB per wave instruction, 16 loads in
+// flight) from an L2-resident buffer, with an agent-scope acquire fence
+// (mode 1) or release fence (mode 2) every `every` fragments, or none
+// (mode 0): what such fences cost a concurrent weight stream.
+__global__ __launch_bounds__(512) void l2_stream_fence_kernel(const uint32_t *__restrict__ buf,
+                                                              int frags_per_wave, int reps,
+                                                              int mode, int every, uint32_t *out)
+{
+    typedef uint32_t v4 __attribute__((ext_vector_type(4)));
+    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+    const v4 *p = (const v4 *)buf + (size_t)wave * frags_per_wave * 64 + lane;
+    v4 acc = {0u, 0u, 0u, 0u};
+    constexpr int D = 16;
+    for (int r = 0; r < reps; ++r) {
+        v4 b[D];
+#pragma unroll
+        for (int d = 0; d < D; ++d) b[d] = p[(size_t)(d % frags_per_wave) * 64];
+        for (int f0 = 0; f0 < frags_per_wave; f0 += D) {
+#pragma unroll
+            for (int d = 0; d < D; ++d) {
+                acc ^= b[d];
+                int nf = f0 + d + D;
+                while (nf >= frags_per_wave) nf -= frags_per_wave;
+                b[d] = p[(size_t)nf * 64];
+                if ((f0 + d) % every == 0) {
+                    if (mode == 1) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                    if (mode == 2) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < D; ++d) acc ^= b[d];
+    }
+    if (acc.x == 0x12345678u && acc.y == 0x9abcdef0u) ((v4 *)out)[blockIdx.x * 512 + threadIdx.x] = acc;
+}
+
 constexpr int SD = 16;   // loads in flight per wave
 
 __global__ __launch_bounds__(512) void l2_stream_kernel(const u32x4 *__restrict__ buf,
@@ -260,6 +437,47 @@ int tpp_l2_stream(const void *buf, size_t buf_bytes, int frags_per_wave, int rep
     if ((size_t)8 * frags_per_wave * 1024 > buf_bytes) return -1;
     hipLaunchKernelGGL(l2_stream_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream,
                        (const u32x4 *)buf, frags_per_wave, reps, (u32x4 *)out);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int tpp_pingpong(int mode, int pairs, int stride, int rounds, int spin_limit, int *flags,
+                 void *out, void *stream)
+{
+    // 2 * pairs workgroups; partners b and b ^ stride (stride a power of two
+    // below 2 * pairs); flags: pairs * 32 ints, zeroed by the caller
+    if ((mode != 0 && mode != 1) || pairs < 1 || stride < 1 || (stride & (stride - 1)) ||
+        stride >= 2 * pairs || (2 * pairs) % (2 * stride) || rounds < 1 || spin_limit < 1 ||
+        !flags || !out)
+        return -1;
+    hipLaunchKernelGGL(pingpong_kernel, dim3(2 * pairs), dim3(64), 0, (hipStream_t)stream, mode,
+                       stride, rounds, spin_limit, flags, (PingOut *)out);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int tpp_pingpong_data(int mode, int pairs, int stride, int rounds, int spin_limit, int *flags,
+                      void *data, void *out, void *stream)
+{
+    // flags: pairs * 32 ints (zeroed); data: pairs * 2 * 1024 16-byte words;
+    // out: 2 * pairs records of 24 bytes
+    if ((mode != 0 && mode != 1) || pairs < 1 || stride < 1 || (stride & (stride - 1)) ||
+        stride >= 2 * pairs || (2 * pairs) % (2 * stride) || rounds < 1 || spin_limit < 1 ||
+        !flags || !data || !out)
+        return -1;
+    hipLaunchKernelGGL(pingpong_data_kernel, dim3(2 * pairs), dim3(64), 0, (hipStream_t)stream,
+                       mode, stride, rounds, spin_limit, flags, (uint32_t *)data,
+                       (PingDataOut *)out);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int tpp_l2_stream_fence(const void *buf, size_t buf_bytes, int frags_per_wave, int reps,
+                        int blocks, int mode, int every, void *out, void *stream)
+{
+    if (!buf || !out || frags_per_wave < 1 || reps < 1 || blocks < 1 || mode < 0 || mode > 2 ||
+        every < 1)
+        return -1;
+    if ((size_t)8 * frags_per_wave * 1024 > buf_bytes) return -1;
+    hipLaunchKernelGGL(l2_stream_fence_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream,
+                       (const uint32_t *)buf, frags_per_wave, reps, mode, every, (uint32_t *)out);
     return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 

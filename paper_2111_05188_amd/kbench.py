@@ -84,7 +84,7 @@ def main():
     ap.add_argument("--iters", type=int, default=20)
     ap.add_argument("--only", default=None,
                     choices=["env_step", "gae", "critic", "metrics", "evolution", "learner",
-                             "train", "probes", "copy", "mfma_sweep"])
+                             "train", "probes", "copy", "mfma_sweep", "sync"])
     args = ap.parse_args()
     sys.path.insert(0, __file__.rsplit("/", 2)[0])
     import workloads as W
@@ -367,6 +367,75 @@ def main():
                                      "clock_GHz": round(0.1 * c[0] / max(c[1], 1), 3)})
                         print(f"[kbench] mfma sweep {rows[-1]}", file=sys.stderr, flush=True)
         out["mfma_sweep"] = rows
+
+    if args.only == "sync":
+        # workgroup handoff latency through one flag word (agent-scope
+        # release/acquire, or relaxed agent-scope atomics), partners 8 apart
+        # (the same XCD under round-robin dispatch) or 1 apart; and what
+        # agent-scope fences cost a concurrent L2 weight stream
+        import ctypes as C
+        import os
+        pl = C.CDLL(os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpprobe.so"))
+        pl.tpp_pingpong.argtypes = [C.c_int] * 5 + [C.c_void_p, C.c_void_p, C.c_void_p]
+        pl.tpp_l2_stream_fence.argtypes = [C.c_void_p, C.c_size_t, C.c_int, C.c_int, C.c_int,
+                                           C.c_int, C.c_int, C.c_void_p, C.c_void_p]
+        sp = stream.cuda_stream
+        res = []
+        pairs, rounds = 128, 2000
+        for mode in (0, 1):
+            for stride in (8, 1):
+                flags = torch.zeros(pairs * 32, dtype=torch.int32, device=dev)
+                rec = torch.zeros(2 * pairs, 2, dtype=torch.int64, device=dev)
+                assert pl.tpp_pingpong(mode, pairs, stride, rounds, 1 << 20, flags.data_ptr(),
+                                       rec.data_ptr(), sp) == 0
+                torch.cuda.synchronize()
+                r = rec.cpu().numpy()
+                xcc = (r[:, 0] & 0xFFFFFFFF).astype(np.int64)
+                tmo = (r[:, 0] >> 32).astype(np.int64)
+                ticks = r[:, 1].astype(np.float64)
+                b = np.arange(2 * pairs)
+                same = float(np.mean(xcc == xcc[b ^ stride]))
+                rt_us = ticks / rounds * 0.01     # 100 MHz ticks -> us per round trip
+                res.append({"mode": "release/acquire" if mode == 0 else "relaxed",
+                            "partner_stride": stride, "same_xcd_frac": same,
+                            "timeouts": int(tmo.sum()),
+                            "round_trip_us_median": float(np.median(rt_us)),
+                            "round_trip_us_max": float(rt_us.max()),
+                            "xcc_of_first_16": xcc[:16].tolist()})
+                print(f"[kbench] sync {res[-1]}", file=sys.stderr, flush=True)
+        pl.tpp_pingpong_data.argtypes = [C.c_int] * 5 + [C.c_void_p] * 4
+        for mode in (0, 1):
+            for stride in (8, 1):
+                flags = torch.zeros(pairs * 32, dtype=torch.int32, device=dev)
+                data = torch.zeros(pairs * 2 * 1024 * 4, dtype=torch.int32, device=dev)
+                rec = torch.zeros(2 * pairs, 6, dtype=torch.int32, device=dev)
+                assert pl.tpp_pingpong_data(mode, pairs, stride, 500, 1 << 20, flags.data_ptr(),
+                                            data.data_ptr(), rec.data_ptr(), sp) == 0
+                torch.cuda.synchronize()
+                r = rec.cpu().numpy().astype(np.int64)
+                xcc, tmo = r[:, 0], r[:, 1]
+                ticks = (r[:, 2] & 0xFFFFFFFF) + (r[:, 3] << 32)
+                b = np.arange(2 * pairs)
+                rt_us = ticks / 500 * 0.01
+                res.append({"payload": "16 KiB", "mode": "plain store + sc0 load" if mode == 0
+                            else "sc1 store + sc1 load", "partner_stride": stride,
+                            "same_xcd_frac": float(np.mean(xcc == xcc[b ^ stride])),
+                            "timeouts": int(tmo.sum()), "stale_words": int(r[:, 4].sum()),
+                            "round_trip_us_median": float(np.median(rt_us)),
+                            "round_trip_us_max": float(rt_us.max())})
+                print(f"[kbench] sync {res[-1]}", file=sys.stderr, flush=True)
+        fpw, reps = 200, 20
+        buf = torch.ones(8 * fpw * 1024 // 4 + 16384, dtype=torch.int32, device=dev)
+        so = torch.empty(256 * 512 * 4, dtype=torch.int32, device=dev)
+        fence = []
+        for mode, every in ((0, 1), (1, 64), (1, 16), (2, 64), (2, 16)):
+            sec = _time(lambda: pl.tpp_l2_stream_fence(buf.data_ptr(), buf.numel() * 4, fpw,
+                                                       reps, 256, mode, every, so.data_ptr(), sp),
+                        5, stream)
+            fence.append({"fence": ["none", "acquire", "release"][mode], "every_frags": every,
+                          "GBs_per_CU": 8 * fpw * 1024 * reps / sec / 1e9})
+            print(f"[kbench] stream {fence[-1]}", file=sys.stderr, flush=True)
+        out["sync"] = {"pingpong": res, "l2_stream_with_fences": fence}
 
     if args.only in (None, "copy"):
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
