@@ -262,11 +262,45 @@ __device__ __forceinline__ void write_obs_half(T *row, const EnvConst &C, double
 // zeros past the last indicator; then the zero padding.  Every lane of
 // the wave calls it (it shuffles; irow must be readable for every half);
 // halves with `live` false store nothing.
+// Indicator chunks of the aligned writer below, loaded ahead of use: round
+// m holds chunk hl + 32 m of the row (clamped to the last chunk), for up to
+// MAXR rounds (nI / 4 + 1 <= 32 MAXR).  Issuing these loads before the env
+// step lets their latency overlap the step's arithmetic.
+template <int MAXR>
+struct IndChunks {
+    float __attribute__((ext_vector_type(4))) v[MAXR];
+};
+
+template <int MAXR>
+__device__ __forceinline__ IndChunks<MAXR> load_ind_chunks(const EnvConst &C, const float *irow, int hl)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    IndChunks<MAXR> r;
+    const int nch = C.nI / 4 + 1, rounds = (nch + HALF - 1) / HALF;
+#pragma unroll
+    for (int m = 0; m < MAXR; ++m)
+        r.v[m] = m < rounds ? *(const f4 *)(irow + 4 * min(hl + HALF * m, C.nI / 4 - 1))
+                            : f4{0.f, 0.f, 0.f, 0.f};
+    return r;
+}
+
+// The same row for bf16 observations when n and nI are multiples of 4 (nI
+// > 0) and the indicator rows are 16-byte aligned, in aligned 8-byte stores
+// of columns 4k .. 4k+3: the value of column 4k belongs to the neighbouring
+// chunk's owner and comes by shuffle.  Lane s < n/4 (stocks 4s .. 4s+3)
+// writes columns 4s .. +3 = [price 4s-1, prices 4s .. 4s+2] and n + 4s ..
+// +3 = [holding 4s-1, holdings 4s .. 4s+2] (lane 0: the balance, the last
+// price); indicator chunk k (lane k % 32) writes columns 2n + 4k .. +3 =
+// [indicator 4k-1, indicators 4k .. 4k+2] (chunk 0: the last holding),
+// zeros past the last indicator; then the zero padding.  `ind` holds the
+// row's chunks (load_ind_chunks).  Every lane of the wave calls it (it
+// shuffles); halves with `live` false store nothing.
+template <int MAXR>
 __device__ __forceinline__ void write_obs_half_aligned(__bf16 *row, const EnvConst &C, double cash,
                                                        const int (&h)[SPL],
                                                        const float (&p)[SPL],
-                                                       const float *irow, int lane, int hl,
-                                                       bool live)
+                                                       const IndChunks<MAXR> &ind, int lane,
+                                                       int hl, bool live)
 {
     typedef float f4 __attribute__((ext_vector_type(4)));
     const int n = C.n, nI = C.nI, nq = n / 4, base = lane - hl;
@@ -281,9 +315,11 @@ __device__ __forceinline__ void write_obs_half_aligned(__bf16 *row, const EnvCon
     const float p_last = __shfl(pv[3], base + nq - 1), h_last = __shfl(hv[3], base + nq - 1);
     const int nch = nI / 4 + 1, rounds = (nch + HALF - 1) / HALF;
     float last3 = 0.f;
-    for (int m = 0; m < rounds; ++m) {   // the same trip count in every lane
+#pragma unroll
+    for (int m = 0; m < MAXR; ++m) {   // the same trip count in every lane
+        if (m >= rounds) break;
         const int k = hl + HALF * m;
-        const f4 v = *(const f4 *)(irow + 4 * min(k, nI / 4 - 1));
+        const f4 v = ind.v[m];
         const float v_up = __shfl(v[3], up), v_wrap = __shfl(last3, base + HALF - 1);
         const float first = hl > 0 ? v_up : (m > 0 ? v_wrap : h_last);
         if (live && k < nch) {

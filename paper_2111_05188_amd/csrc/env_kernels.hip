@@ -8,6 +8,9 @@
 namespace tpk {
 
 constexpr int ENV_WPB = 4;              // waves per workgroup
+// rounds of 16-byte indicator chunks a lane holds: n * n_ind <= 1024 gives
+// at most 257 chunks of 4 (with the shifted first column), 9 rounds of 32
+constexpr int ENV_IND_ROUNDS = 9;
 constexpr int ENV_EPB = 2 * ENV_WPB;    // envs per workgroup
 
 template <typename OT>
@@ -92,27 +95,59 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
     HalfEnv s;
     s.cash = live ? cash[e] : 0.0;
     float a[SPL], q[SPL];
+    // a lane's 4 stocks are 16 contiguous bytes of the action, holdings and
+    // price rows when n is a multiple of 4 and the arrays are 16-byte
+    // aligned: one 16-byte access each instead of four
+    const bool vec = n % SPL == 0 && ((uintptr_t)action | (uintptr_t)shares | (uintptr_t)C.price) % 16 == 0;
+    if (vec) {
+        typedef float f4 __attribute__((ext_vector_type(4)));
+        typedef int i4 __attribute__((ext_vector_type(4)));
+        const bool v = live && SPL * hl < n;
+        const size_t o = (size_t)e * n + SPL * hl;
+        const i4 hv = v ? *(const i4 *)(shares + o) : i4{0, 0, 0, 0};
+        const f4 av = v ? *(const f4 *)(action + o) : f4{0.f, 0.f, 0.f, 0.f};
+        const f4 pv = v ? *(const f4 *)(p0 + SPL * hl) : f4{0.f, 0.f, 0.f, 0.f};
+        const f4 qv = v ? *(const f4 *)(p1 + SPL * hl) : f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < SPL; ++c) {
-        const int i = SPL * hl + c;
-        const bool v = live && i < n;
-        s.h[c] = v ? shares[(size_t)e * n + i] : 0;
-        s.p[c] = v ? p0[i] : 0.f;
-        a[c] = v ? action[(size_t)e * n + i] : 0.f;
-        q[c] = v ? p1[i] : 0.f;
-    }
-    double none = 0.0;
-    const float r = env_step_half(C, s, a, q, live, lane, none);
-    // bf16 rows of 4k stocks and 4k > 0 indicator values go out in aligned
-    // stores (the aligned writer reads indicator chunks, so a market without
-    // indicators takes the per-value writer)
-    const bool aligned_obs = sizeof(OT) == 2 && C.n % 4 == 0 && C.nI > 0 && C.nI % 4 == 0 &&
-                             (uintptr_t)C.ind % 16 == 0;
-    if (live) {
+        for (int c = 0; c < SPL; ++c) {
+            s.h[c] = hv[c];
+            a[c] = av[c];
+            s.p[c] = pv[c];
+            q[c] = qv[c];
+        }
+    } else {
 #pragma unroll
         for (int c = 0; c < SPL; ++c) {
             const int i = SPL * hl + c;
-            if (i < n) shares[(size_t)e * n + i] = s.h[c];
+            const bool v = live && i < n;
+            s.h[c] = v ? shares[(size_t)e * n + i] : 0;
+            s.p[c] = v ? p0[i] : 0.f;
+            a[c] = v ? action[(size_t)e * n + i] : 0.f;
+            q[c] = v ? p1[i] : 0.f;
+        }
+    }
+    // bf16 rows of 4k stocks and 4k > 0 indicator values go out in aligned
+    // stores (the aligned writer reads indicator chunks, so a market without
+    // indicators takes the per-value writer); their indicator chunks are
+    // loaded before the step's arithmetic
+    const bool aligned_obs = sizeof(OT) == 2 && C.n % 4 == 0 && C.nI > 0 && C.nI % 4 == 0 &&
+                             (uintptr_t)C.ind % 16 == 0;
+    IndChunks<ENV_IND_ROUNDS> ind;
+    if (sizeof(OT) == 2 && obs && aligned_obs)
+        ind = load_ind_chunks<ENV_IND_ROUNDS>(C, C.ind + (size_t)(live ? tt + 1 : 0) * C.nI, hl);
+    double none = 0.0;
+    const float r = env_step_half(C, s, a, q, live, lane, none);
+    if (live) {
+        if (vec) {
+            typedef int i4 __attribute__((ext_vector_type(4)));
+            if (SPL * hl < n)
+                *(i4 *)(shares + (size_t)e * n + SPL * hl) = i4{s.h[0], s.h[1], s.h[2], s.h[3]};
+        } else {
+#pragma unroll
+            for (int c = 0; c < SPL; ++c) {
+                const int i = SPL * hl + c;
+                if (i < n) shares[(size_t)e * n + i] = s.h[c];
+            }
         }
         if (hl == 0) {
             cash[e] = s.cash;
@@ -132,8 +167,7 @@ __global__ __launch_bounds__(ENV_WPB *WAVE) void env_step_kernel(
     }
     if constexpr (sizeof(OT) == 2) {
         if (obs && aligned_obs)   // every lane (shuffles); only live halves store
-            write_obs_half_aligned(row, C, s.cash, s.h, q, C.ind + (size_t)(live ? tt + 1 : 0) * C.nI,
-                                   lane, hl, live);
+            write_obs_half_aligned<ENV_IND_ROUNDS>(row, C, s.cash, s.h, q, ind, lane, hl, live);
     }
     __syncthreads();
     if (in && obs)

@@ -232,12 +232,147 @@ __global__ __launch_bounds__(GW_W *WAVE) void gae_wide_kernel(
     }
 }
 
+// Many envs (E a multiple of 4, 16-byte aligned rows): the same two passes
+// with four envs per lane, so every access is one 16-byte load or store of
+// r, v, adv, ret (4-byte for done) and a wave instruction moves whole
+// 256-byte row pieces.  A workgroup takes GV_E = 64 envs (16 lanes per row
+// piece) and GV_W * 4 = 32 chunks of at most GV_CL steps; chunk maps
+// compose by shuffles within a wave (4 chunks) and through LDS across the
+// 8 waves.
+constexpr int GV_W = 8;
+constexpr int GV_E = 64;
+constexpr int GV_RL = GV_E / 4;               // lanes per row piece
+constexpr int GV_K = WAVE / GV_RL;            // chunks per wave
+constexpr int GV_NCH = GV_K * GV_W;           // chunks per workgroup
+constexpr int GV_LMAX = 416;                  // longest rollout
+constexpr int GV_CL = GV_LMAX / GV_NCH;       // longest chunk (13 steps)
+
+typedef float f4g __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(GV_W *WAVE) void gae_vec_kernel(
+    const float *__restrict__ r, const float *__restrict__ v,
+    const uint8_t *__restrict__ d, int L, int E, int nblk, double g, double gl,
+    float *__restrict__ adv, float *__restrict__ ret)
+{
+    __shared__ double sA[GV_W][GV_E], sP[GV_W][GV_E];
+    const int logical = (blockIdx.x % 8) * (gridDim.x / 8) + blockIdx.x / 8;
+    if (logical >= nblk) return;   // whole workgroup
+    const int w = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
+    const int lr = lane % GV_RL, k = lane / GV_RL;
+    const int e0 = logical * GV_E + 4 * lr;     // this lane's first env (E % 4 == 0)
+    const int c = w * GV_K + k;
+    const int cl = (L + GV_NCH - 1) / GV_NCH;
+    const int lo = min(L, c * cl), hi = min(L, lo + cl);
+    const bool ok = e0 < E && hi > lo;
+    const size_t sE = (size_t)E;
+
+    f4g cr[GV_CL], cv[GV_CL];
+    uint32_t cd[GV_CL];   // done bytes of the 4 envs at step hi-1-i
+    f4g vend = {0.f, 0.f, 0.f, 0.f};
+    if (ok) {
+        vend = __builtin_nontemporal_load((const f4g *)(v + (size_t)hi * sE + e0));
+#pragma unroll
+        for (int i = 0; i < GV_CL; ++i) {
+            const int j = hi - 1 - i;
+            if (j >= lo) {
+                const size_t x = (size_t)j * sE + e0;
+                cr[i] = __builtin_nontemporal_load((const f4g *)(r + x));
+                cv[i] = __builtin_nontemporal_load((const f4g *)(v + x));
+                cd[i] = __builtin_nontemporal_load((const uint32_t *)(d + x));
+            }
+        }
+    }
+    double A[4] = {0.0, 0.0, 0.0, 0.0}, P[4] = {1.0, 1.0, 1.0, 1.0};
+    if (ok) {
+        double vn[4] = {(double)vend[0], (double)vend[1], (double)vend[2], (double)vend[3]};
+#pragma unroll
+        for (int i = 0; i < GV_CL; ++i) {
+            if (hi - 1 - i >= lo) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const double nd = (cd[i] >> (8 * q)) & 0xFFu ? 0.0 : 1.0;
+                    const double vj = (double)cv[i][q];
+                    const double delta = (double)cr[i][q] + g * nd * vn[q] - vj;
+                    const double cj = gl * nd;
+                    A[q] = delta + cj * A[q];
+                    P[q] *= cj;
+                    vn[q] = vj;
+                }
+            }
+        }
+    }
+    // suffix composition over the wave's GV_K chunks of each env
+#pragma unroll
+    for (int sh = 1; sh < GV_K; sh *= 2) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const double An = __shfl_down(A[q], sh * GV_RL), Pn = __shfl_down(P[q], sh * GV_RL);
+            if (k + sh < GV_K) {
+                A[q] = A[q] + P[q] * An;
+                P[q] = P[q] * Pn;
+            }
+        }
+    }
+    if (k == 0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            sA[w][4 * lr + q] = A[q];
+            sP[w][4 * lr + q] = P[q];
+        }
+    }
+    __syncthreads();
+    double carry[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        double cq = 0.0;
+        for (int ww = GV_W - 1; ww > w; --ww) cq = sA[ww][4 * lr + q] + sP[ww][4 * lr + q] * cq;
+        const double An = __shfl_down(A[q], GV_RL), Pn = __shfl_down(P[q], GV_RL);
+        carry[q] = k + 1 < GV_K ? An + Pn * cq : cq;
+    }
+
+    // pass 2 from the true carries
+    if (ok) {
+        double vn[4] = {(double)vend[0], (double)vend[1], (double)vend[2], (double)vend[3]};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) A[q] = carry[q];
+#pragma unroll
+        for (int i = 0; i < GV_CL; ++i) {
+            const int j = hi - 1 - i;
+            if (j >= lo) {
+                f4g a4, r4;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const double nd = (cd[i] >> (8 * q)) & 0xFFu ? 0.0 : 1.0;
+                    const double vj = (double)cv[i][q];
+                    const double delta = (double)cr[i][q] + g * nd * vn[q] - vj;
+                    A[q] = delta + gl * nd * A[q];
+                    a4[q] = (float)A[q];
+                    r4[q] = (float)(A[q] + vj);
+                    vn[q] = vj;
+                }
+                const size_t x = (size_t)j * sE + e0;
+                __builtin_nontemporal_store(a4, (f4g *)(adv + x));
+                __builtin_nontemporal_store(r4, (f4g *)(ret + x));
+            }
+        }
+    }
+}
+
 hipError_t launch_gae(const float *r, const float *v, const uint8_t *d, int L,
                       int E, double g, double gl, float *adv, float *ret,
                       hipStream_t s)
 {
     // rollouts up to GW_LMAX steps: 16-env workgroups below 16,384 envs
     // (so that every CU gets one), whole-line 32-env ones from there on
+    const bool vec_ok = E % 4 == 0 && (uintptr_t)r % 16 == 0 && (uintptr_t)v % 16 == 0 &&
+                        (uintptr_t)d % 4 == 0 && (uintptr_t)adv % 16 == 0 &&
+                        (uintptr_t)ret % 16 == 0;
+    if (L <= GV_LMAX && E >= 16384 && vec_ok) {
+        const int nblk = (E + GV_E - 1) / GV_E;
+        hipLaunchKernelGGL(gae_vec_kernel, dim3((nblk + 7) / 8 * 8), dim3(GV_W * WAVE), 0, s, r, v,
+                           d, L, E, nblk, g, gl, adv, ret);
+        return hipGetLastError();
+    }
     if (L <= GW_LMAX) {
         if (E >= 16384) {
             const int nblk = (E + 31) / 32;

@@ -30,7 +30,13 @@ def _inputs(L, E, seed, p_done=0.02):
     # steps (the longest chunks) and 513; 16,383 envs and 16,384 (and a
     # ragged count above it)
     (512, 1000, 0.99, 0.95), (513, 200, 0.99, 0.95), (64, 16383, 0.99, 0.95),
-    (7, 16384, 0.99, 0.95), (512, 16400, 0.99, 0.95)])
+    (7, 16384, 0.99, 0.95), (512, 16400, 0.99, 0.95),
+    # the four-envs-per-lane kernel (E a multiple of 4 from 16,384 envs,
+    # rollouts up to 416 steps): full and ragged chunk counts, a ragged
+    # last workgroup, one step, lambda 1, and both sides of its length limit
+    (390, 16384, 0.99, 0.95), (416, 16388, 0.99, 0.95), (417, 16384, 0.99, 0.95),
+    (33, 20000, 0.97, 0.9), (1, 16388, 0.99, 0.95), (390, 32772, 0.99, 1.0),
+    (390, 16386, 0.99, 0.95)])
 def test_gae_parity(L, E, gamma, lam):
     say(f"[gae] L={L} E={E} gamma={gamma} lambda={lam}")
     r, v, d = _inputs(L, E, L * 7 + E)
@@ -46,7 +52,8 @@ def test_gae_parity(L, E, gamma, lam):
 
 
 def test_gae_stress_shape_sampled():
-    """Full stress size (L=390, E=65536): GPU vs oracle on sampled columns."""
+    """Full stress size (L=390, E=65536): GPU vs oracle on every column (the
+    name is historical) -- the oracle's scan takes well under a second."""
     L, E = 390, 65536
     say(f"[gae] stress L={L} E={E}")
     r, v, d = _inputs(L, E, 5)
@@ -56,11 +63,9 @@ def test_gae_stress_shape_sampled():
     ret = torch.empty(L, E, device=dev)
     tp.gae(gr, gv, gd, 0.99, 0.95, adv, ret)
     torch.cuda.synchronize()
-    cols = np.random.default_rng(1).choice(E, 64, replace=False)
-    cols = np.sort(np.concatenate([cols, [0, E - 1]]))
-    a_o, r_o = oracle.gae(r[:, cols], v[:, cols], d[:, cols], 0.99, 0.95)
-    rel_check("adv", adv.cpu().numpy()[:, cols], a_o, TOL_GAE)
-    rel_check("ret", ret.cpu().numpy()[:, cols], r_o, TOL_GAE)
+    a_o, r_o = oracle.gae(r, v, d, 0.99, 0.95)
+    rel_check("adv", adv.cpu().numpy(), a_o, TOL_GAE)
+    rel_check("ret", ret.cpu().numpy(), r_o, TOL_GAE)
 
 
 def test_gae_deterministic():
