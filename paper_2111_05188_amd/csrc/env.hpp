@@ -118,16 +118,21 @@ __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
     extra = half_value(extra, HALF - 1, HALF - 1, upper);
     const double b_s = fma(S, C.f_s, s.cash);
 
-    // buys: resolve the greedy in ascending stock order in rounds.  A round
-    // first drops every pending stock that cannot pay for one share at the
-    // current G (G only grows, so it never will), then finds the first
-    // pending stock whose full order no longer fits (the misfit): every
-    // pending stock before it is bought in full, the lane holding it buys
-    // its largest affordable q, and the next round continues after it.
-    // Both halves run their rounds together; a half without pending stocks
-    // idles.
-    // pending stocks as a 4-bit mask per lane (bit c = stock 4 hl + c);
-    // everything below is branch-free except the misfit's own search
+    // buys: the greedy in ascending stock order, each stock buying the
+    // largest q <= k the balance still covers.  Both halves run the same
+    // instruction stream; a half without work idles.
+    //
+    // (1) One bulk round.  Drop every stock that cannot pay for one share
+    // (at G = 0 it buys nothing), then find the first pending stock whose
+    // full order no longer fits (the misfit): every pending stock before it
+    // is bought in full, the misfit buys its largest affordable q < k.
+    // (2) The tail, after a misfit: the remaining balance is below one
+    // share of the misfit, so few stocks can still buy.  Each iteration
+    // takes the lowest-index pending stock that can pay for one share and
+    // buys its largest affordable q <= k.  Every purchase so far is of a
+    // lower-index stock, so a stock skipped as unaffordable sees the G the
+    // serial greedy would give it, and G only grows: it stays at zero.
+    // Pending stocks as a 4-bit mask per lane (bit c = stock 4 hl + c).
     double cost[SPL];
     int pm = 0;
 #pragma unroll
@@ -135,14 +140,25 @@ __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
         cost[c] = k[c] > 0 ? pd[c] * (double)k[c] : 0.0;
         pm |= k[c] > 0 ? 1 << c : 0;
     }
+    // largest q in [lo, hi] with f_b (g + p q) <= b_s, the answer known to
+    // lie in [lo, hi]: an fp32 estimate of (b_s - f_b g) / (f_b p) (off by at
+    // most one: the quotient is below 2^15, after a misfit the balance is
+    // below one share of it, and the relative error of the estimate is about
+    // 2^-21), then one step up and one step down with the sign-exact test
+    // (g + p q is exact in fp64)
+    auto largest_q = [&](double g, double p, int lo, int hi) {
+        const float rem = (float)fma(-fb, g, b_s);
+        const float est = floorf(rem * __builtin_amdgcn_rcpf((float)(p * fb)));
+        int qq = (int)fminf(fmaxf(est, (float)lo), (float)hi);
+        qq += (qq < hi && fma(fb, g + p * (double)(qq + 1), -b_s) <= 0.0) ? 1 : 0;
+        qq -= (qq > lo && fma(fb, g + p * (double)qq, -b_s) > 0.0) ? 1 : 0;
+        return qq;
+    };
     double G = 0.0;
-    for (;;) {
-        // drop what cannot pay for one share (at G = 0 such a stock buys
-        // nothing either, so the first round may drop too)
 #pragma unroll
-        for (int c = 0; c < SPL; ++c)
-            pm &= fma(fb, G + pd[c], -b_s) > 0.0 ? ~(1 << c) : ~0;
-        if (__ballot(pm != 0) == 0) break;
+    for (int c = 0; c < SPL; ++c)
+        pm &= fma(fb, pd[c], -b_s) > 0.0 ? ~(1 << c) : ~0;
+    if (__ballot(pm != 0) != 0) {
         // lane-local inclusive prefix of the pending full costs, then the
         // half's exclusive prefix of lane totals (all exact)
         double pre[SPL], acc = 0.0;
@@ -151,7 +167,7 @@ __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
             acc += (pm >> c) & 1 ? cost[c] : 0.0;
             pre[c] = acc;
         }
-        const double base = G + (half_inclusive_scan(acc) - acc);
+        const double base = half_inclusive_scan(acc) - acc;
         int bad = 0;   // pending stocks whose prefix no longer fits
 #pragma unroll
         for (int c = 0; c < SPL; ++c)
@@ -160,45 +176,70 @@ __device__ __forceinline__ float env_step_half(const EnvConst &C, HalfEnv &s,
         const uint64_t m = __ballot(bad != 0);
         const uint32_t ma = (uint32_t)m, mb = (uint32_t)(m >> 32);
         // the misfit's lane in each half (the last lane when there is none:
-        // its running total is then the half's new G)
+        // its running total is then the half's G)
         const int fla = ma ? __ffs(ma) - 1 : HALF - 1;
         const int flb = mb ? __ffs(mb) - 1 : HALF - 1;
         const bool has = (upper ? mb : ma) != 0;
         const int fl = upper ? flb : fla;
         const bool at = has && hl == fl;
-        const int cf = __ffs(bad) - 1;   // on the misfit's lane: its stock
+        const int cf = bad ? __ffs(bad) - 1 : 0;   // on the misfit's lane: its stock
         // every pending stock before the misfit is bought in full
         const int full = pm & (!has || hl < fl ? 0xF : (at ? (1 << cf) - 1 : 0));
 #pragma unroll
         for (int c = 0; c < SPL; ++c) h[c] += (full >> c) & 1 ? k[c] : 0;
         pm &= ~full;
+        // the misfit's purchase, computed by every lane for its own first
+        // misfitting stock (uniform code) and kept on the misfit's lane
+        double gf = base, pf = pd[0];
+        int kf = k[0];
+#pragma unroll
+        for (int c = 0; c < SPL; ++c)
+            if (c == cf) {
+                pf = pd[c];
+                kf = k[c];
+                gf = base + pre[c] - cost[c];
+            }
+        const int qf = largest_q(gf, pf, 0, kf > 0 ? kf - 1 : 0);
         double gnew = base + acc;
         if (at) {
-            // the misfit: largest q in [0, kf - 1] with f_b (Gf + pf q) <= b_s.
-            // An fp32 estimate (off by at most one) is stepped to the exact
-            // boundary with the sign-exact fma test.
-            double gf = base, pf = pd[0];
-            int kf = k[0];
-#pragma unroll
-            for (int c = 1; c < SPL; ++c)
-                if (c == cf) {
-                    pf = pd[c];
-                    kf = k[c];
-                }
-#pragma unroll
-            for (int c = 0; c < SPL; ++c)
-                if (c == cf) gf = base + pre[c] - cost[c];
-            const float rem = (float)fma(-fb, gf, b_s);
-            const float est = floorf(rem * __builtin_amdgcn_rcpf((float)(pf * fb)));
-            int qf = (int)fminf(fmaxf(est, 0.0f), (float)(kf - 1));
-            while (qf < kf - 1 && fma(fb, gf + pf * (double)(qf + 1), -b_s) <= 0.0) ++qf;
-            while (qf > 0 && fma(fb, gf + pf * (double)qf, -b_s) > 0.0) --qf;
 #pragma unroll
             for (int c = 0; c < SPL; ++c) h[c] += c == cf ? qf : 0;
             pm &= ~(1 << cf);
             gnew = gf + pf * (double)qf;
         }
         G = half_value(gnew, fla, flb, upper);
+        // the tail (no iteration runs for a half without a misfit: its
+        // pending mask is empty)
+        for (;;) {
+            int aff = 0;
+#pragma unroll
+            for (int c = 0; c < SPL; ++c)
+                aff |= ((pm >> c) & 1) && fma(fb, G + pd[c], -b_s) <= 0.0 ? 1 << c : 0;
+            pm = aff;
+            const uint64_t mt = __ballot(aff != 0);
+            if (mt == 0) break;
+            const uint32_t ta = (uint32_t)mt, tb = (uint32_t)(mt >> 32);
+            const int la = ta ? __ffs(ta) - 1 : 0, lb = tb ? __ffs(tb) - 1 : 0;
+            const bool hit = (upper ? tb : ta) != 0 && hl == (upper ? lb : la);
+            const int ct = aff ? __ffs(aff) - 1 : 0;
+            double pt = pd[0];
+            int kt = k[0];
+#pragma unroll
+            for (int c = 1; c < SPL; ++c)
+                if (c == ct) {
+                    pt = pd[c];
+                    kt = k[c];
+                }
+            const int qt = largest_q(G, pt, 1, kt > 0 ? kt : 1);
+            double dg = 0.0;
+            if (hit) {
+#pragma unroll
+                for (int c = 0; c < SPL; ++c) h[c] += c == ct ? qt : 0;
+                pm &= ~(1 << ct);
+                dg = pt * (double)qt;
+            }
+            G += half_value(dg, la, lb, upper);
+        }
     }
     double nb = fma(-fb, G, b_s);
     if (nb < 0.0) nb = 0.0;
