@@ -1,63 +1,73 @@
-// Role-split fused rollout kernel for bf16 actors of the shapes in use
-// (1001 inputs from 100 stocks with 8 indicators each, 512- or 1024-wide
-// hidden layers).  One launch runs all L lockstep steps of a block of 16 envs.
+// Role-split fused rollout kernel for bf16 actors of the 100-stock shapes in
+// use (1001 inputs from 100 stocks with 8 indicators each, 512- or
+// 1024-wide hidden layers).  One launch runs all L lockstep steps of a block
+// of 16 envs.
 //
 // Why split roles.  A workgroup owns 16 envs, the N dimension of one MFMA
-// tile, so every step streams the whole actor (1.65 MB at 1001-512-512-100)
-// from L2 into the CU.  That stream, not the MFMAs, bounds the actor, and the
-// env step is VALU work of about the same length.  Run back to back they add
-// up; here they overlap.  The observation is [balance, prices, holdings,
-// indicators] (Section 3, "State space"), and layer 1's columns past the
-// first KSB k-steps of 32 hold only indicators of the market row.  Those do
-// not depend on the actions, so their share of layer 1 for step j+1 can be
-// computed while the env step of step j runs.  Only the first KSB k-steps of
-// layer 1, layers 2 and 3 remain on the step-to-step chain.
+// tile, so every step streams the actor's weights from L2 into the CU.  That
+// stream, not the MFMAs, bounds the actor, and the env step is VALU work
+// that would add to it if the two ran one after the other.  Here they
+// overlap.  The observation is [balance, prices, holdings, indicators]
+// (Section 3, "State space").  Only the balance and the holdings depend on
+// the actions; the k-steps of 32 layer-1 inputs that hold neither (the
+// market k-steps: prices and indicators only) can be multiplied as soon as
+// the market row is known, which is before the env step that completes the
+// observation.  Only the other k-steps of layer 1 (the action k-steps),
+// layers 2 and 3 remain on the step-to-step chain.
 //
-// Waves.  Four matrix waves (one per SIMD) compute every actor layer; eight
-// env waves (two per SIMD) own two envs each, one per 32-lane half, four
-// stocks per lane.  Each role runs its own loop with the same barrier
-// sequence: per step, four slots separated by workgroup barriers:
+// Market k-steps in pairs.  With J = 2 the market k-steps of two consecutive
+// steps are multiplied together, each weight fragment against both steps'
+// rows (two MFMAs per fragment), so the market part of layer 1 streams once
+// per pair of steps.  The pair's partial sums wait in accumulator registers
+// for their step's action k-steps.
 //
-//   slot   matrix waves                         env waves
-//   A      Z = W1[:, KSB..] x_j  (indicators)   env step j-1, trajectory row j-1,
-//                                               balance/prices/holdings of x_j;
-//                                               x_j to HBM; loads of row t+j+1
-//   B      h1 = tanh(Z + W1[:, ..KSB] x_j + b1) -
-//   L2     h2 = tanh(W2 h1 + b2)                indicators of row t+j+1 into x_{j+1};
-//                                               Philox + Box-Muller normals of step j
-//   L3     mu = W3 h2 + b3                      -
+// Waves.  Four matrix waves (one per SIMD) compute every actor layer; four
+// env waves (one per SIMD) own four envs each, one per 16-lane row, eight
+// stocks per lane (env_row.hpp).  Each role runs its own loop with the same
+// barrier sequence: per step j, four slots separated by workgroup barriers:
 //
-// LDS: x rows (bf16), h1 (bf16), Z (fp32) sharing its space with h2 (their
-// lifetimes, slots A->B and L2->L3, do not overlap), mu (fp32), biases.
+//   slot  matrix waves                             env waves
+//   A     market k-steps of x_j and x_{j+1}        env step j-1: balance and holdings
+//         (even j when J = 2; every j when J = 1)   of x_j, trajectory row j-1
+//   B     h1 = tanh(Z_j + W1[:, action] x_j + b1)   x_j to HBM; loads of row t0+j+2
+//   L2    h2 = tanh(W2 h1 + b2)                    prices and indicators of row t0+j+2
+//                                                  into x_{j+2}; normals of step j
+//   L3    mu = W3 h2 + b3                          -
 //
-// Weight stream.  A matrix wave consumes a fixed sequence of F weight
-// fragments per step (1 KiB each: one 16x32 A-operand of
-// v_mfma_f32_16x16x32_bf16, 16 bytes per lane) through a ring of R fragment
-// registers: consuming fragment f issues the load of fragment f + R, wrapping
-// into the next step's sequence (the weights do not change during a
-// rollout), so loads stay in flight across group ends, layer ends and
-// barriers, and nothing is read twice.  Fragments come through buffer loads
-// with a wave-uniform scalar offset.
+// LDS: two observation rows per env (x_j lives in buffer j & 1: its market
+// columns are written two steps ahead, the balance and holdings by the env
+// step that completes it), h1, h2 (bf16), mu (fp32), biases.
+//
+// Weight stream.  A matrix wave consumes a fixed sequence of weight
+// fragments (1 KiB each: one 16x32 A-operand of v_mfma_f32_16x16x32_bf16, 16
+// bytes per lane) through a ring of R fragment registers: consuming fragment
+// f issues the load of fragment f + R - 1, wrapping into the next period
+// (the weights do not change during a rollout), so loads stay in flight
+// across layer ends and barriers, and nothing is read twice.  Fragments come
+// through buffer loads with a wave-uniform scalar offset.
 #include <type_traits>
 
 #include "device.hpp"
-#include "env.hpp"
+#include "env_row.hpp"
 #include "internal.hpp"
 
 namespace tpk {
 namespace rs {
 
 constexpr int MW = 4;            // matrix waves
-constexpr int VW = 8;            // env waves
+constexpr int VW = 4;            // env waves
 constexpr int NWAVES = MW + VW;
-constexpr int MB = 2 * VW;       // envs per workgroup
+constexpr int EPW = WAVE / RL;   // envs per env wave
+constexpr int MB = EPW * VW;     // envs per workgroup
 constexpr int G = 4;             // output tiles per group in layers 1 and 2
+static_assert(MB == 16, "one MFMA tile of envs per workgroup");
 
 template <int I> using ic = std::integral_constant<int, I>;
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 typedef int i4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Market rows and trajectory rows are touched once per step; streaming
 // (non-temporal) accesses keep them from evicting the actor's weights,
@@ -82,39 +92,73 @@ __device__ __forceinline__ void static_for(Fn &&fn)
 }
 
 // Actor shape.  NS stocks with NI indicator values per market row; KS1
-// k-steps of 32 inputs in layer 1, the first KSB of which hold the balance,
-// prices and holdings; NT1, NT2, NT3 output tiles of 16; a ring of R weight
-// fragments per matrix wave.
-template <int NS_, int NI_, int KS1_, int KSB_, int NT1_, int NT2_, int NT3_, int R_>
+// k-steps of 32 inputs in layer 1; NT1, NT2, NT3 output tiles of 16; a ring
+// of R weight fragments per matrix wave; market k-steps of J steps (1 or 2)
+// multiplied together.
+template <int NS_, int NI_, int KS1_, int NT1_, int NT2_, int NT3_, int R_, int J_>
 struct Shape {
     static constexpr int NS = NS_, NI = NI_;   // stocks, indicator values per row
-    static constexpr int R = R_;
-    static constexpr int KS1 = KS1_, KSB = KSB_, KSA = KS1_ - KSB_;
+    static constexpr int R = R_, J = J_;
+    static constexpr int KS1 = KS1_;
     static constexpr int NT1 = NT1_, NT2 = NT2_, NT3 = NT3_;
     static constexpr int KS2 = NT1 / 2, KS3 = NT2 / 2;
     static constexpr int NG1 = NT1 / (MW * G), NG2 = NT2 / (MW * G), NG3 = NT3 / MW;
     static_assert(NT1 % (MW * G) == 0 && NT2 % (MW * G) == 0 && NT3 % MW == 0,
                   "tiles must split evenly over the matrix waves");
-    // fragments per step of one matrix wave, in consumption order A, B, L2, L3
-    static constexpr int FA = NG1 * KSA * G, FB = NG1 * KSB * G;
+    static_assert(J == 1 || J == 2, "one or two steps per market pass");
+
+    // k-step s holds the balance (column 0) or a holding (columns NS+1 .. 2NS)
+    static constexpr bool is_action(int s) { return s == 0 || (32 * s <= 2 * NS && 32 * s + 31 >= NS + 1); }
+    static constexpr int count_action()
+    {
+        int c = 0;
+        for (int s = 0; s < KS1; ++s) c += is_action(s);
+        return c;
+    }
+    static constexpr int KSB = count_action(), KSA = KS1 - KSB;
+    // the i-th action / market k-step
+    static constexpr int aks(int i)
+    {
+        for (int s = 0; s < KS1; ++s)
+            if (is_action(s) && i-- == 0) return s;
+        return -1;
+    }
+    static constexpr int mks(int i)
+    {
+        for (int s = 0; s < KS1; ++s)
+            if (!is_action(s) && i-- == 0) return s;
+        return -1;
+    }
+
+    // fragments of one matrix wave, in consumption order: the market
+    // k-steps (once per J steps), then per step the action k-steps, layer 2
+    // and layer 3
+    static constexpr int FM = NG1 * KSA * G, FB = NG1 * KSB * G;
     static constexpr int F2 = NG2 * KS2 * G, F3 = NG3 * KS3;
-    static constexpr int F = FA + FB + F2 + F3;
+    static constexpr int FS = FB + F2 + F3;
+    static constexpr int F = FM + J * FS;   // one period
     static_assert(F % R == 0, "the ring must map every fragment to a fixed slot");
+    static_assert(KSB >= G, "the deferred epilogue needs a k-step per tile");
 
     // layer of fragment f, and its byte offset from the wave's base in that
     // layer (the wave's first tile; groups are MW * G tiles apart in layers
     // 1 and 2, MW tiles apart in layer 3)
-    static constexpr int layer(int f) { return f < FA + FB ? 0 : (f < FA + FB + F2 ? 1 : 2); }
+    static constexpr int layer(int f)
+    {
+        if (f < FM) return 0;
+        f = (f - FM) % FS;
+        return f < FB ? 0 : (f < FB + F2 ? 1 : 2);
+    }
     static constexpr int offset(int f)
     {
-        if (f < FA) {
+        if (f < FM) {
             const int g = f / (KSA * G), r = f % (KSA * G);
-            return ((g * MW * G + r % G) * KS1 + KSB + r / G) * 1024;
+            return ((g * MW * G + r % G) * KS1 + mks(r / G)) * 1024;
         }
-        f -= FA;
+        f = (f - FM) % FS;
         if (f < FB) {
             const int g = f / (KSB * G), r = f % (KSB * G);
-            return ((g * MW * G + r % G) * KS1 + r / G) * 1024;
+            return ((g * MW * G + r % G) * KS1 + aks(r / G)) * 1024;
         }
         f -= FB;
         if (f < F2) {
@@ -132,21 +176,33 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint32_t __attribute__((ext_vector_t
 }
 
 struct Lds {
-    __bf16 *X;      // [MB][ldx]   observations
+    __bf16 *X;      // [2][MB][ldx] observation rows (x_j in buffer j & 1)
     __bf16 *H1;     // [MB][ldh1]  hidden layer 1
-    float *Z;       // [MB][ldz]   indicator part of layer 1 (shares space with H2)
     __bf16 *H2;     // [MB][ldh2]  hidden layer 2
     float *MU;      // [MB][ldmu]  action means
     float *BIAS;    // b1 | b2 | b3
-    int ldx, ldh1, ldz, ldh2, ldmu;
+    int ldx, ldh1, ldh2, ldmu;
+    // row `sl` of observation buffer b & 1
+    __device__ __forceinline__ __bf16 *xrow(int b, int sl) const { return X + ((b & 1) * MB + sl) * ldx; }
+};
+
+// k-step k of a segment at input column 32 * col(k)
+struct KPlain {
+    static constexpr int col(int k) { return k; }
+};
+template <class S> struct KAction {
+    static constexpr int col(int k) { return S::aks(k); }
+};
+template <class S> struct KMarket {
+    static constexpr int col(int k) { return S::mks(k); }
 };
 
 // ---------------------------------------------------------------------------
 // Matrix role
 // ---------------------------------------------------------------------------
-// One matrix wave's weight stream.  Fragment i of the step sequence lives in
-// ring slot i % R; consuming fragment i first refills the slot fragment i-1
-// left (its MFMA has issued), then multiplies, so R-1 loads stay in flight.
+// One matrix wave's weight stream.  Fragment i of the period lives in ring
+// slot i % R; consuming fragment i first refills the slot fragment i-1 left
+// (its MFMAs have issued), then multiplies, so R-1 loads stay in flight.
 template <class S>
 struct Stream {
     static constexpr int R = S::R;
@@ -171,18 +227,28 @@ struct Stream {
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[I % R], x, acc, 0, 0, 0);
     }
 
+    // fragment I against two input tiles
+    template <int I>
+    __device__ __forceinline__ void mma2(const bf16x8 &x0, const bf16x8 &x1, floatx4 &a0, floatx4 &a1)
+    {
+        fetch<I + R - 1>();
+        a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[I % R], x0, a0, 0, 0, 0);
+        a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[I % R], x1, a1, 0, 0, 0);
+    }
+
     // The fragment offsets base + constant are loop-invariant; hoisted out
     // of the step loop they would need one scalar register each.  Hiding
     // the bases from the optimiser at every slot keeps each offset next to
     // its load.
     __device__ __forceinline__ void launder() { asm volatile("" : "+s"(wb0), "+s"(wb1), "+s"(wb2)); }
 
-    // One slot's work: NG groups of GT output tiles over KS k-steps that
-    // start at k-step K0 of the input rows `xb` (this lane's row and column
-    // offset).  init(g, acc) and epi(g, t, acc) set up and store group g.
-    // With DEFER the epilogue of group g runs tile by tile inside the first
-    // GT k-steps of group g+1, so the weight stream keeps moving through it.
-    template <int FB0, int NG, int KS, int K0, int GT, bool DEFER, class InitF, class EpiF>
+    // One slot's work: NG groups of GT output tiles over KS k-steps (k-step
+    // k at input column 32 * KM::col(k) of the rows `xb`, this lane's row and
+    // column offset).  init(g, acc) and epi(g, t, acc) set up and store group
+    // g.  With DEFER the epilogue of group g runs tile by tile inside the
+    // first GT k-steps of group g+1, so the weight stream keeps moving
+    // through it.
+    template <int FB0, int NG, int KS, class KM, int GT, bool DEFER, class InitF, class EpiF>
     __device__ __forceinline__ void seg(const __bf16 *xb, InitF &&init, EpiF &&epi)
     {
         static_assert(!DEFER || KS >= GT, "deferred epilogue needs a k-step per tile");
@@ -190,11 +256,11 @@ struct Stream {
         static_for<0, NG>([&](auto gi) {
             constexpr int g = decltype(gi)::value;
             init(g, acc);
-            bf16x8 x = *(const bf16x8 *)(xb + K0 * 32);
+            bf16x8 x = *(const bf16x8 *)(xb + KM::col(0) * 32);
             static_for<0, KS>([&](auto ki) {
                 constexpr int k = decltype(ki)::value;
                 bf16x8 xn;
-                if constexpr (k + 1 < KS) xn = *(const bf16x8 *)(xb + (K0 + k + 1) * 32);
+                if constexpr (k + 1 < KS) xn = *(const bf16x8 *)(xb + KM::col(k + 1) * 32);
                 static_for<0, GT>([&](auto ti) {
                     constexpr int t = decltype(ti)::value;
                     mma<FB0 + (g * KS + k) * GT + t>(x, acc[t]);
@@ -210,6 +276,45 @@ struct Stream {
 #pragma unroll
                 for (int t = 0; t < GT; ++t) epi(g, t, acc[t]);
             }
+        });
+    }
+
+    // The market k-steps of layer 1 for one (x0 -> Z0) or two (x0 -> Z0,
+    // x1 -> Z1) steps' rows, no bias.
+    template <int FB0, bool TWO>
+    __device__ __forceinline__ void market(const __bf16 *x0b, const __bf16 *x1b,
+                                           floatx4 (&Z0)[S::NG1][G], floatx4 (&Z1)[S::NG1][G])
+    {
+        static_for<0, S::NG1>([&](auto gi) {
+            constexpr int g = decltype(gi)::value;
+#pragma unroll
+            for (int t = 0; t < G; ++t) {
+                Z0[g][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+                if constexpr (TWO) Z1[g][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+            }
+            bf16x8 x0 = *(const bf16x8 *)(x0b + S::mks(0) * 32), x1;
+            if constexpr (TWO) x1 = *(const bf16x8 *)(x1b + S::mks(0) * 32);
+            static_for<0, S::KSA>([&](auto ki) {
+                constexpr int k = decltype(ki)::value;
+                bf16x8 xn0, xn1;
+                if constexpr (k + 1 < S::KSA) {
+                    xn0 = *(const bf16x8 *)(x0b + S::mks(k + 1) * 32);
+                    if constexpr (TWO) xn1 = *(const bf16x8 *)(x1b + S::mks(k + 1) * 32);
+                }
+                static_for<0, G>([&](auto ti) {
+                    constexpr int t = decltype(ti)::value;
+                    constexpr int f = FB0 + (g * S::KSA + k) * G + t;
+                    if constexpr (TWO)
+                        mma2<f>(x0, x1, Z0[g][t], Z1[g][t]);
+                    else
+                        mma<f>(x0, Z0[g][t]);
+                });
+                if constexpr (k + 1 < S::KSA) {
+                    x0 = xn0;
+                    if constexpr (TWO) x1 = xn1;
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            });
         });
     }
 };
@@ -239,7 +344,8 @@ __device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
     st.wb2 = (int)P.off_W[2] + m * S::KS3 * 1024;
     st.voff = lane * 16;
 
-    const __bf16 *xb = s.X + r16 * s.ldx + kq * 8;
+    const __bf16 *xb0 = s.xrow(0, r16) + kq * 8;
+    const __bf16 *xb1 = s.xrow(1, r16) + kq * 8;
     const __bf16 *h1b = s.H1 + r16 * s.ldh1 + kq * 8;
     const __bf16 *h2b = s.H2 + r16 * s.ldh2 + kq * 8;
     // output column of tile t of group g, for this lane, in layers 1-2 / 3
@@ -258,32 +364,33 @@ __device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
         *(bf16x4 *)(Y + o) = h;
     };
 
-    // slot A: Z = W1[:, KSB..] x (fp32, no bias)
-    auto seg_A = [&]() {
-        st.template seg<0, S::NG1, S::KSA, S::KSB, G, false>(
-            xb, zero, [&](int g, int t, const floatx4 &a) {
-                *(floatx4 *)(s.Z + r16 * s.ldz + col12(g, t)) = a;
-            });
-    };
-    // slot B: h1 = tanh(Z + W1[:, ..KSB] x + b1)
-    auto seg_B = [&]() {
-        st.template seg<S::FA, S::NG1, S::KSB, 0, G, true>(
+    // market partial sums of layer 1 for the pending steps (Z[1] only with
+    // J = 2)
+    floatx4 Z[2][S::NG1][G];
+
+    // one step's chain from fragment FB0 on: h1 from the action k-steps of
+    // the rows `xb` on top of Zs, then layers 2 and 3
+    auto chain = [&](auto fb0, const __bf16 *xb, floatx4 (&Zs)[S::NG1][G]) {
+        constexpr int F0 = decltype(fb0)::value;
+        // slot B: h1 = tanh(Z + W1[:, action] x + b1)
+        st.launder();
+        st.template seg<F0, S::NG1, S::KSB, KAction<S>, G, true>(
             xb,
             [&](int g, floatx4 *acc) {
 #pragma unroll
-                for (int t = 0; t < G; ++t) acc[t] = *(const floatx4 *)(s.Z + r16 * s.ldz + col12(g, t));
+                for (int t = 0; t < G; ++t) acc[t] = Zs[g][t];
             },
             [&](int g, int t, const floatx4 &a) { tanh_store(a, b1, s.H1 + r16 * s.ldh1, col12(g, t)); });
-    };
-    // slot L2: h2 = tanh(W2 h1 + b2)
-    auto seg_L2 = [&]() {
-        st.template seg<S::FA + S::FB, S::NG2, S::KS2, 0, G, true>(
+        __syncthreads();
+        // slot L2: h2 = tanh(W2 h1 + b2)
+        st.launder();
+        st.template seg<F0 + S::FB, S::NG2, S::KS2, KPlain, G, true>(
             h1b, zero,
             [&](int g, int t, const floatx4 &a) { tanh_store(a, b2, s.H2 + r16 * s.ldh2, col12(g, t)); });
-    };
-    // slot L3: mu = W3 h2 + b3
-    auto seg_L3 = [&]() {
-        st.template seg<S::FA + S::FB + S::F2, S::NG3, S::KS3, 0, 1, false>(
+        __syncthreads();
+        // slot L3: mu = W3 h2 + b3
+        st.launder();
+        st.template seg<F0 + S::FB + S::F2, S::NG3, S::KS3, KPlain, 1, false>(
             h2b, [&](int, floatx4 *acc) { acc[0] = floatx4{0.f, 0.f, 0.f, 0.f}; },
             [&](int g, int, const floatx4 &a) {
                 const int o = col3(g);
@@ -291,251 +398,275 @@ __device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
                 *(floatx4 *)(s.MU + r16 * s.ldmu + o) =
                     floatx4{a[0] + bv[0], a[1] + bv[1], a[2] + bv[2], a[3] + bv[3]};
             });
+        __syncthreads();
     };
 
     // the first R-1 fragments; the rest is fetched one slot behind use
     static_for<0, S::R - 1>([&](auto i) { st.template fetch<decltype(i)::value>(); });
-    __syncthreads();   // observations of step 0 and the biases are in LDS
-    for (int j = 0; j < A.L; ++j) {
+    __syncthreads();   // observation rows of steps 0 and 1 and the biases are in LDS
+    for (int j = 0; j < A.L; j += S::J) {
+        // slot A of step j
         st.launder();
-        seg_A();
+        st.template market<0, S::J == 2>((S::J == 1 && (j & 1)) ? xb1 : xb0, xb1, Z[0], Z[1]);
         __syncthreads();
-        st.launder();
-        seg_B();
-        __syncthreads();
-        st.launder();
-        seg_L2();
-        __syncthreads();
-        st.launder();
-        seg_L3();
-        __syncthreads();
+        if constexpr (S::J == 1) {
+            chain(ic<S::FM>{}, (j & 1) ? xb1 : xb0, Z[0]);
+        } else {
+            chain(ic<S::FM>{}, xb0, Z[0]);
+            if (j + 1 < A.L) {
+                __syncthreads();   // slot A of step j+1: nothing for the matrix waves
+                chain(ic<S::FM + S::FS>{}, xb1, Z[1]);
+            }
+        }
     }
 }
 
 // ---------------------------------------------------------------------------
 // Env role
 // ---------------------------------------------------------------------------
-// Balance, prices and holdings of an observation row (the indicator part is
-// written separately, one slot earlier).
-// Balance, prices and holdings of an observation row (columns 0 .. 2n; the
-// indicator part is written separately, one slot earlier), in aligned
-// 8-byte stores: lane s (s < n / 4, owner of stocks 4s .. 4s+3) writes
-// columns 4s .. 4s+3 = [price 4s-1 (lane s-1's last), prices 4s .. 4s+2]
-// and columns n + 4s .. n + 4s + 3 = [holding 4s-1, holdings 4s .. 4s+2];
-// lane 0 starts the first with the balance and the second with the last
-// price; column 2n (the last holding) is one 2-byte store.  All lanes of
-// the wave call it (it shuffles); only `live` halves store.
-template <int n>
-__device__ __forceinline__ void write_obs_state(__bf16 *row, const EnvConst &C, double cash,
-                                                const int (&h)[SPL], const float (&p)[SPL],
-                                                int lane, int hl, bool live)
-{
-    static_assert(n % 4 == 0 && n / 4 <= HALF, "one chunk of each kind per lane");
-    float pv[SPL], hv[SPL];
-#pragma unroll
-    for (int c = 0; c < SPL; ++c) {
-        pv[c] = p[c] * C.price_scale;
-        hv[c] = (float)h[c] * C.share_scale;
-    }
-    const int base = lane - hl;
-    const float p_up = __shfl(pv[3], lane - (hl > 0)), h_up = __shfl(hv[3], lane - (hl > 0));
-    const float p_last = __shfl(pv[3], base + n / 4 - 1), h_last = __shfl(hv[3], base + n / 4 - 1);
-    if (!live || hl >= n / 4) return;
-    const float bal = (float)(cash * (double)C.cash_scale);
-    *(bf16x4 *)(row + 4 * hl) = bf16x4{to_bf16(hl > 0 ? p_up : bal), to_bf16(pv[0]), to_bf16(pv[1]),
-                                       to_bf16(pv[2])};
-    *(bf16x4 *)(row + n + 4 * hl) = bf16x4{to_bf16(hl > 0 ? h_up : p_last), to_bf16(hv[0]),
-                                           to_bf16(hv[1]), to_bf16(hv[2])};
-    if (hl == n / 4 - 1) row[2 * n] = to_bf16(h_last);
-}
-
-template <int NS, int NI, int KPAD>
+template <class S>
 __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, const uint8_t *pk,
                                          int agent, int ebase, int nenv, int v, int lane)
 {
-    // NS stocks (a multiple of 4, at most 128), NI = NS * indicators (a
-    // multiple of 4), observation rows of KPAD elements
-    static_assert(NS % SPL == 0 && NS <= SPL * HALF && NI % 4 == 0, "shape");
-    constexpr int IPC = (NI / 4 + HALF - 1) / HALF;   // 16-byte indicator chunks per lane
-    constexpr int OBS_CHUNKS = KPAD * 2 / 16;         // 16-byte chunks of an observation row
+    constexpr int n = S::NS, nI = S::NI;
+    constexpr int KPAD = S::KS1 * 32;
+    static_assert(n % 4 == 0 && n <= RL * SPR && nI % 4 == 0 && nI > 0, "shape");
+    constexpr int NPC = n / 4;                         // 16-byte price chunks of a row
+    constexpr int NICH = nI / 4;                       // 16-byte indicator chunks of a row
+    constexpr int IPL = (NICH + RL - 1) / RL;          // indicator chunks per lane
+    constexpr int OBS_CHUNKS = KPAD * 2 / 16;          // 16-byte chunks of an observation row
+    static_assert(OBS_CHUNKS % RL == 0, "whole observation chunks per lane");
     const EnvConst &C = A.env;
     const PackedLayout &P = A.lay;
-    constexpr int n = NS, nI = NI;
-    const int half = lane / HALF, hl = lane % HALF;
-    const int sl = 2 * v + half;
+    const int r = lane / RL, sl16 = lane % RL;
+    const int sl = EPW * v + r;   // env slot in the workgroup
     const bool mine = sl < nenv;
     const int e = ebase + sl;
-    __bf16 *xrow = s.X + sl * s.ldx;
     const size_t E = (size_t)A.E;
     const float qnan = __builtin_nanf("");
+    // this lane's two 16-byte price chunks (clamped to the row; stocks past
+    // n read as zero)
+    const int pc0 = min(2 * sl16, NPC - 1), pc1 = min(2 * sl16 + 1, NPC - 1);
+    const bool pv0 = 2 * sl16 < NPC, pv1 = 2 * sl16 + 1 < NPC;
 
-    float ls[SPL], sg[SPL];
+    float ls[SPR], sg[SPR];
     {
         const float *lsd = (const float *)(pk + P.off_ls);
 #pragma unroll
-        for (int c = 0; c < SPL; ++c) {
-            const int i = SPL * hl + c;
+        for (int c = 0; c < SPR; ++c) {
+            const int i = SPR * sl16 + c;
             ls[c] = i < n ? lsd[i] : 0.f;
             sg[c] = expf(ls[c]);
         }
     }
 
-    // state of this half's env, kept in registers for the whole rollout
-    HalfEnv st;
+    // state of this row's env, kept in registers for the whole rollout
+    RowEnv st;
     st.cash = 0.0;
+    st.value = 0.0;
     int64_t t0 = 0;
     bool live = false;
 #pragma unroll
-    for (int c = 0; c < SPL; ++c) {
+    for (int c = 0; c < SPR; ++c) {
         st.h[c] = 0;
-        st.p[c] = 0.f;
+        st.pd[c] = 0.0;
     }
     if (mine) {
         t0 = A.t[e];
         live = t0 >= 0 && t0 + A.L <= C.T1 - 1;
-        if (A.n_invalid && !live && hl == 0) atomicAdd(A.n_invalid, 1);
+        if (A.n_invalid && !live && sl16 == 0) atomicAdd(A.n_invalid, 1);
         st.cash = A.cash[e];
 #pragma unroll
-        for (int c = 0; c < SPL; ++c) {
-            const int i = SPL * hl + c;
+        for (int c = 0; c < SPR; ++c) {
+            const int i = SPR * sl16 + c;
             st.h[c] = i < n ? A.shares[(size_t)e * n + i] : 0;
-        }
-        if (live) {
-            const float *prow = C.price + (size_t)t0 * n;
-            const float *irow = C.ind + (size_t)t0 * nI;
-#pragma unroll
-            for (int c = 0; c < SPL; ++c) {
-                const int i = SPL * hl + c;
-                st.p[c] = i < n ? prow[i] : 0.f;
-            }
-            float ind1[1];
-            ind1[0] = hl < nI ? irow[hl] : 0.f;
-            write_obs_half<__bf16, 1>(xrow, C, st.cash, st.h, st.p, ind1, irow, hl);
         }
     }
     const bool wave_live = __ballot(live) != 0;
     const double half_log2pi_n = 0.5 * (double)n * 1.8378770664093454836;
-    const int obs_bytes = C.K_pad * 2;
 
-    float z[SPL], q[SPL];
+    // prices of row t (8 per lane, zero past n); row 0 for envs not stepped
+    auto load_prices = [&](int64_t t, float (&p)[SPR]) {
+        const float *pr = C.price + (size_t)(live ? t : 0) * n;
+        const f4v a = load_stream(pr + 4 * pc0), b = load_stream(pr + 4 * pc1);
 #pragma unroll
-    for (int c = 0; c < SPL; ++c) z[c] = q[c] = 0.f;
-
-    // env step of step jj: action, log-density, trade, trajectory row jj and
-    // the balance / prices / holdings of observation jj + 1
-    auto step_env = [&](int jj) {
-        const float *mu = s.MU + sl * s.ldmu;
-        float a[SPL];
-        double lp = 0.0;
-#pragma unroll
-        for (int c = 0; c < SPL; ++c) {
-            const int i = SPL * hl + c;
-            const bool ok = live && i < n;
-            a[c] = ok ? mu[i] + sg[c] * z[c] : 0.f;
-            if (ok) lp += -0.5 * (double)z[c] * (double)z[c] - (double)ls[c];
+        for (int c = 0; c < 4; ++c) {
+            p[c] = pv0 ? a[c] : 0.f;
+            p[4 + c] = pv1 ? b[c] : 0.f;
         }
-        float qq[SPL];
+    };
+    // indicator chunks sl16 + 16 m of row t (clamped to the row)
+    auto load_ind = [&](int64_t t, f4v (&ind)[IPL]) {
+        const float *ir = C.ind + (size_t)(live ? t : 0) * nI;
 #pragma unroll
-        for (int c = 0; c < SPL; ++c) qq[c] = (live && SPL * hl + c < n) ? q[c] : 0.f;
-        float r = 0.f;
-        if (wave_live) r = env_step_half<NS>(C, st, a, qq, live, lane, lp);
-        lp -= half_log2pi_n;
-        write_obs_state<NS>(xrow, C, st.cash, st.h, st.p, lane, hl, live);
+        for (int mm = 0; mm < IPL; ++mm) ind[mm] = load_stream(ir + 4 * min(sl16 + RL * mm, NICH - 1));
+    };
+    // the market columns of an observation row (prices 1 .. n, indicators
+    // 2n+1 .. 2n+nI) in bf16; the balance, the holdings and the zero padding
+    // are left alone.  Indicators go in aligned 8-byte stores of columns
+    // 2n + 4w .. +3 = [indicator 4w-1, indicators 4w .. 4w+2] (chunk w of the
+    // row; value 4w-1 is the last of chunk w-1, held by the previous lane of
+    // the row, or by lane 15 one round earlier); chunk 0 skips column 2n
+    // (the last holding) and the last indicator is one 2-byte store.  All
+    // lanes call it (it moves values between lanes); only live rows store.
+    auto write_market = [&](__bf16 *row, const float (&p)[SPR], const f4v (&ind)[IPL]) {
+        float last = 0.f;   // element 3 of this lane's previous chunk
+#pragma unroll
+        for (int mm = 0; mm < IPL; ++mm) {
+            const f4v vv = ind[mm];
+            const float src = sl16 == RL - 1 ? last : vv[3];
+            const float prev = dpp32f<DPP_ROW_ROR1>(src);
+            last = vv[3];
+            const int w = sl16 + RL * mm;
+            if (live && w < NICH) {
+                __bf16 *q = row + 2 * n + 4 * w;
+                if (w > 0) {
+                    *(bf16x4 *)q = bf16x4{to_bf16(prev), to_bf16(vv[0]), to_bf16(vv[1]), to_bf16(vv[2])};
+                } else {
+                    q[1] = to_bf16(vv[0]);
+                    *(bf16x2 *)(q + 2) = bf16x2{to_bf16(vv[1]), to_bf16(vv[2])};
+                }
+                if (w == NICH - 1) q[4] = to_bf16(vv[3]);
+            }
+        }
+        if (live) {
+#pragma unroll
+            for (int c = 0; c < SPR; ++c) {
+                const int i = SPR * sl16 + c;
+                if (i < n) row[1 + i] = to_bf16(p[c] * C.price_scale);
+            }
+        }
+    };
+    // the balance and the holdings of an observation row
+    auto write_state = [&](__bf16 *row) {
+        if (!live) return;
+        if (sl16 == 0) row[0] = to_bf16((float)(st.cash * (double)C.cash_scale));
+#pragma unroll
+        for (int c = 0; c < SPR; ++c) {
+            const int i = SPR * sl16 + c;
+            if (i < n) row[1 + n + i] = to_bf16((float)st.h[c] * C.share_scale);
+        }
+    };
+
+    // observation rows of steps 0 (complete) and 1 (market columns); the
+    // total asset at the start row; prices of rows t0 and t0 + 1
+    float pn[SPR], pnn[SPR];
+    f4v ind[IPL];
+    {
+        float p0[SPR];
+        load_prices(t0, p0);
+        load_ind(t0, ind);
+        write_market(s.xrow(0, sl), p0, ind);
+        write_state(s.xrow(0, sl));
+        double hv = 0.0;
+#pragma unroll
+        for (int c = 0; c < SPR; ++c) {
+            st.pd[c] = (double)p0[c];
+            hv = fma((double)st.h[c], st.pd[c], hv);
+        }
+        st.value = st.cash + row_sum(hv);
+        load_prices(t0 + 1, pn);
+        load_ind(t0 + 1, ind);
+        write_market(s.xrow(1, sl), pn, ind);
+#pragma unroll
+        for (int c = 0; c < SPR; ++c) pnn[c] = 0.f;
+    }
+
+    float sz[SPR];
+    double lp = 0.0;
+#pragma unroll
+    for (int c = 0; c < SPR; ++c) sz[c] = 0.f;
+
+    // env step of step jj (the prices of row t0 + jj + 1 in pn): action,
+    // trade, the balance and holdings of x_{jj+1}, trajectory row jj
+    auto step_env = [&](int jj) {
+        const float *mu = s.MU + sl * s.ldmu + SPR * sl16;
+        const f4v m0 = *(const f4v *)mu, m1 = *(const f4v *)(mu + 4);
+        float a[SPR], ain[SPR];
+        double qd[SPR];
+#pragma unroll
+        for (int c = 0; c < SPR; ++c) {
+            const float mc = c < 4 ? m0[c] : m1[c - 4];
+            a[c] = mc + sz[c];
+            ain[c] = (live && SPR * sl16 + c < n) ? a[c] : 0.f;
+            qd[c] = (double)pn[c];
+        }
+        float rw = 0.f;
+        if (wave_live) rw = env_step_row(C, st, ain, qd);
+        write_state(s.xrow(jj + 1, sl));
         if (!mine) return;
         const size_t row = (size_t)jj * E + e;
         const uint8_t done = (uint8_t)(A.step0 + (uint64_t)jj + 1 == (uint64_t)C.horizon);
-        // this lane's 4 stocks are 16 contiguous bytes of the action row
-        if (hl < NS / SPL) {
-            const f4v av = live ? f4v{a[0], a[1], a[2], a[3]} : f4v{qnan, qnan, qnan, qnan};
-            store_stream(av, (f4v *)(A.action + row * n) + hl);
-            if (A.mu_tap)
-                store_stream(live ? *(const f4v *)(mu + SPL * hl) : f4v{qnan, qnan, qnan, qnan},
-                             (f4v *)(A.mu_tap + row * n) + hl);
-            if (A.shares_tap)
-                store_stream(i4v{st.h[0], st.h[1], st.h[2], st.h[3]},
-                             (i4v *)(A.shares_tap + row * n) + hl);
+        // this lane's stocks are 16-byte chunks pc0, pc1 of the row
+        float *arow = A.action + row * n;
+        const f4v nanv = {qnan, qnan, qnan, qnan};
+        if (pv0) store_stream(live ? f4v{a[0], a[1], a[2], a[3]} : nanv, (f4v *)arow + pc0);
+        if (pv1) store_stream(live ? f4v{a[4], a[5], a[6], a[7]} : nanv, (f4v *)arow + pc1);
+        if (A.mu_tap) {
+            float *mrow = A.mu_tap + row * n;
+            if (pv0) store_stream(live ? m0 : nanv, (f4v *)mrow + pc0);
+            if (pv1) store_stream(live ? m1 : nanv, (f4v *)mrow + pc1);
         }
-        if (hl == 0) {
+        if (A.shares_tap) {
+            int32_t *srow = A.shares_tap + row * n;
+            if (pv0) store_stream(i4v{st.h[0], st.h[1], st.h[2], st.h[3]}, (i4v *)srow + pc0);
+            if (pv1) store_stream(i4v{st.h[4], st.h[5], st.h[6], st.h[7]}, (i4v *)srow + pc1);
+        }
+        if (sl16 == 0) {
             store_stream(live ? (float)lp : qnan, A.logp + row);
-            store_stream(live ? r : qnan, A.reward + row);
+            store_stream(live ? rw : qnan, A.reward + row);
             store_stream(live ? done : (uint8_t)0, A.done + row);
             if (A.cash_tap) store_stream(st.cash, A.cash_tap + row);
             if (A.asset_tap) store_stream(live ? st.value : (double)qnan, A.asset_tap + row);
         }
     };
 
-    __syncthreads();   // observations of step 0 are in LDS
-    f4v ind[IPC];
+    __syncthreads();   // observation rows of steps 0 and 1 are in LDS
     for (int j = 0; j < A.L; ++j) {
         // slot A: env step of step j-1, which completes x_j (the matrix
-        // waves read only the indicator columns of x_j meanwhile); then
-        // this step's memory traffic, kept out of the short slot B where
-        // it would hold up the weight stream: x_j to HBM, loads of row
-        // t0+j+1 (which exists for a stepped env; others read row 0)
-        if (j > 0) step_env(j - 1);
+        // waves read only the market k-steps meanwhile)
+        if (j > 0) {
+            step_env(j - 1);
+#pragma unroll
+            for (int c = 0; c < SPR; ++c) pn[c] = pnn[c];
+        }
+        __syncthreads();
+
+        // slot B: x_j to HBM; loads of row t0 + j + 2 (when a later step
+        // needs it)
         if (live && A.obs) {
-            const u4v *src = (const u4v *)xrow;
+            const u4v *src = (const u4v *)(s.xrow(j, sl));
             u4v *dst = (u4v *)((__bf16 *)A.obs + ((size_t)j * E + e) * A.ld_obs);
 #pragma unroll
-            for (int c = hl; c < OBS_CHUNKS; c += HALF) store_stream(src[c], dst + c);
+            for (int c = sl16; c < OBS_CHUNKS; c += RL) store_stream(src[c], dst + c);
         }
-        {
-            const int64_t t1 = live ? t0 + j + 1 : 0;
-            const float *pr = C.price + (size_t)t1 * NS;
-            const float *ir = C.ind + (size_t)t1 * NI;
-            const f4v qv = load_stream(pr + SPL * min(hl, NS / SPL - 1));
-#pragma unroll
-            for (int c = 0; c < SPL; ++c) q[c] = qv[c];
-#pragma unroll
-            for (int mm = 0; mm < IPC; ++mm) ind[mm] = load_stream(ir + 4 * min(hl + HALF * mm, NI / 4 - 1));
+        const bool ahead = j + 2 <= A.L;
+        if (ahead) {
+            load_prices(t0 + j + 2, pnn);
+            load_ind(t0 + j + 2, ind);
         }
         __syncthreads();
 
-        // slot B: nothing for the env waves
-        __syncthreads();
-
-        // slot L2: indicators of row t0+j+1 into x_{j+1} (the matrix waves
-        // are done with x_j); the normals of step j
+        // slot L2: market columns of x_{j+2}; the normals of step j and
+        // their log-density
+        if (ahead) write_market(s.xrow(j, sl), pnn, ind);
         {
-            // 8-byte stores of columns 2n + 4k .. +3 for chunks k = hl + HALF mm
-            // <= nI / 4: indicator values 4k - 1 .. 4k + 2 (indicator i sits in
-            // column 2n + 1 + i).  Value 4k - 1 is element 3 of chunk k - 1, from
-            // the neighbouring lane of this half-wave.  Column 2n (the last
-            // holding) gets a placeholder that slot A overwrites before anything
-            // reads it; the columns past the last indicator are zero padding.
-            static_assert(n % 4 == 0, "chunk starts are 8-byte aligned");
-            constexpr int NCH = nI / 4 + 1;
-            constexpr int IPW = (NCH + HALF - 1) / HALF;
-            const int base = lane - hl;   // this half-wave's first lane
-            float prev[IPW];
+            float z[SPR];
 #pragma unroll
-            for (int mm = 0; mm < IPW; ++mm) {
-                const float up = mm < IPC ? __shfl(ind[mm < IPC ? mm : 0][3], lane - (hl > 0)) : 0.f;
-                const float wrap = mm > 0 ? __shfl(ind[mm - 1 < IPC ? mm - 1 : 0][3], base + HALF - 1)
-                                          : 0.f;
-                prev[mm] = hl > 0 ? up : wrap;
+            for (int h = 0; h < 2; ++h) {
+                const U4 w = philox4x32_10(U4{(uint32_t)(2 * sl16 + h), (uint32_t)e,
+                                              (uint32_t)(A.step0 + (uint64_t)j), (uint32_t)agent},
+                                           A.key_lo, A.key_hi);
+                box_muller_hw(uniform_open01(w.x), uniform_open01(w.y), z[4 * h], z[4 * h + 1]);
+                box_muller_hw(uniform_open01(w.z), uniform_open01(w.w), z[4 * h + 2], z[4 * h + 3]);
             }
-            if (live) {
-                __bf16 *rc = xrow + 2 * n;
+            double l = 0.0;
 #pragma unroll
-                for (int mm = 0; mm < IPW; ++mm) {
-                    const int k = hl + HALF * mm;
-                    if (k < NCH) {
-                        const bool own = k < nI / 4;
-                        const f4v v = mm < IPC ? ind[mm < IPC ? mm : 0] : f4v{0.f, 0.f, 0.f, 0.f};
-                        *(bf16x4 *)(rc + 4 * k) =
-                            bf16x4{to_bf16(prev[mm]), to_bf16(own ? v[0] : 0.f),
-                                   to_bf16(own ? v[1] : 0.f), to_bf16(own ? v[2] : 0.f)};
-                    }
-                }
+            for (int c = 0; c < SPR; ++c) {
+                sz[c] = sg[c] * z[c];
+                if (SPR * sl16 + c < n) l += -0.5 * (double)z[c] * (double)z[c] - (double)ls[c];
             }
-        }
-        {
-            const U4 w = philox4x32_10(
-                U4{(uint32_t)hl, (uint32_t)e, (uint32_t)(A.step0 + (uint64_t)j), (uint32_t)agent},
-                A.key_lo, A.key_hi);
-            box_muller_hw(uniform_open01(w.x), uniform_open01(w.y), z[0], z[1]);
-            box_muller_hw(uniform_open01(w.z), uniform_open01(w.w), z[2], z[3]);
+            lp = row_sum(l) - half_log2pi_n;
         }
         __syncthreads();
 
@@ -545,14 +676,19 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
     step_env(A.L - 1);
 
     if (mine && live) {
-        if (A.obs_last) copy16((__bf16 *)A.obs_last + (size_t)e * A.ld_obs, xrow, obs_bytes, hl, HALF);
-        if (hl == 0) {
+        if (A.obs_last) {
+            const u4v *src = (const u4v *)(s.xrow(A.L, sl));
+            u4v *dst = (u4v *)((__bf16 *)A.obs_last + (size_t)e * A.ld_obs);
+#pragma unroll
+            for (int c = sl16; c < OBS_CHUNKS; c += RL) dst[c] = src[c];
+        }
+        if (sl16 == 0) {
             A.cash[e] = st.cash;
             A.t[e] = t0 + A.L;
         }
 #pragma unroll
-        for (int c = 0; c < SPL; ++c) {
-            const int i = SPL * hl + c;
+        for (int c = 0; c < SPR; ++c) {
+            const int i = SPR * sl16 + c;
             if (i < n) A.shares[(size_t)e * n + i] = st.h[c];
         }
     }
@@ -579,26 +715,24 @@ __global__ __launch_bounds__(NWAVES *WAVE) void rollout_rs_kernel(RolloutArgs A)
     Lds s;
     s.X = (__bf16 *)(smem + A.lds_X);
     s.H1 = (__bf16 *)(smem + A.lds_H);
-    s.Z = (float *)(smem + A.lds_Z);
     s.H2 = (__bf16 *)(smem + A.lds_Z);
     s.MU = (float *)(smem + A.lds_MU);
     s.BIAS = (float *)(smem + A.lds_B);
     s.ldx = A.ldx;
     s.ldh1 = A.ldh;
-    s.ldz = A.ldz;
     s.ldh2 = A.ldh2;
     s.ldmu = A.ldmu;
 
-    // zero the observation rows (padding columns and rows of absent envs
-    // stay zero)
-    for (int i = threadIdx.x; i < MB * s.ldx * 2 / 16; i += NWAVES * WAVE)
+    // zero both observation buffers (padding columns and rows of absent
+    // envs stay zero)
+    for (int i = threadIdx.x; i < 2 * MB * s.ldx * 2 / 16; i += NWAVES * WAVE)
         ((uint4 *)s.X)[i] = uint4{0, 0, 0, 0};
     __syncthreads();
 
     if (wave < MW)
         matrix_role<S>(A, s, pk, wave, lane);
     else
-        env_role<S::NS, S::NI, S::KS1 * 32>(A, s, pk, agent, ebase, nenv, wave - MW, lane);
+        env_role<S>(A, s, pk, agent, ebase, nenv, wave - MW, lane);
 }
 
 template <class S>
@@ -607,18 +741,14 @@ hipError_t launch(RolloutArgs &a, hipStream_t st)
     const PackedLayout &P = a.lay;
     a.ldx = S::KS1 * 32 + 8;
     a.ldh = S::NT1 * 16 + 8;
-    a.ldz = S::NT1 * 16 + 4;
     a.ldh2 = S::NT2 * 16 + 8;
     a.ldmu = S::NT3 * 16 + 4;
+    a.ldz = 0;
     auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
     size_t off = 0;
-    a.lds_X = off;  off = al(off + (size_t)MB * a.ldx * 2);
+    a.lds_X = off;  off = al(off + (size_t)2 * MB * a.ldx * 2);
     a.lds_H = off;  off = al(off + (size_t)MB * a.ldh * 2);
-    a.lds_Z = off;
-    {
-        const size_t z = (size_t)MB * a.ldz * 4, h2 = (size_t)MB * a.ldh2 * 2;
-        off = al(off + (z > h2 ? z : h2));
-    }
+    a.lds_Z = off;  off = al(off + (size_t)MB * a.ldh2 * 2);
     a.lds_MU = off; off = al(off + (size_t)MB * a.ldmu * 4);
     a.lds_B = off;  off = al(off + (size_t)(S::NT1 + S::NT2 + S::NT3) * 16 * 4);
     a.lds_bytes = off;
@@ -640,9 +770,8 @@ hipError_t launch(RolloutArgs &a, hipStream_t st)
 }  // namespace rs
 
 // The role-split kernel covers bf16 actors with 100 stocks of 8 indicators
-// (1001 inputs: KS1 = 32, the balance/prices/holdings in the first 7
-// k-steps) and hidden widths 512 or 1024; returns hipErrorNotSupported for
-// other shapes.
+// (1001 inputs: KS1 = 32) and hidden widths 512 or 1024; returns
+// hipErrorNotSupported for other shapes.
 bool rollout_rs_shape(const PackedLayout &P, int nI)
 {
     return P.dtype == TP_BF16 && P.n == 100 && P.S == 1001 && nI == 800 && P.KS[0] == 32 &&
@@ -658,8 +787,10 @@ hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
     if ((uintptr_t)a.env.price % 16 || (uintptr_t)a.env.ind % 16 || (uintptr_t)a.action % 16 ||
         (uintptr_t)a.shares_tap % 16 || (uintptr_t)a.mu_tap % 16)
         return hipErrorNotSupported;
-    if (P.H1 == 512 && P.H2 == 512) return rs::launch<rs::Shape<100, 800, 32, 7, 32, 32, 8, 16>>(a, s);
-    if (P.H1 == 1024 && P.H2 == 1024) return rs::launch<rs::Shape<100, 800, 32, 7, 64, 64, 8, 16>>(a, s);
+    if (P.H1 == 512 && P.H2 == 512)
+        return rs::launch<rs::Shape<100, 800, 32, 32, 32, 8, 22, 2>>(a, s);
+    if (P.H1 == 1024 && P.H2 == 1024)
+        return rs::launch<rs::Shape<100, 800, 32, 64, 64, 8, 16, 1>>(a, s);
     return hipErrorNotSupported;
 }
 
