@@ -15,11 +15,11 @@
 // observation.  Only the other k-steps of layer 1 (the action k-steps),
 // layers 2 and 3 remain on the step-to-step chain.
 //
-// Market k-steps in pairs.  With J = 2 the market k-steps of two consecutive
-// steps are multiplied together, each weight fragment against both steps'
-// rows (two MFMAs per fragment), so the market part of layer 1 streams once
-// per pair of steps.  The pair's partial sums wait in accumulator registers
-// for their step's action k-steps.
+// Market k-steps in batches.  The market k-steps of J consecutive steps
+// (J = 3 for the 512-wide actor) are multiplied together, each weight
+// fragment against every step's rows (J MFMAs per fragment), so the market
+// part of layer 1 streams once per J steps.  The batch's partial sums wait
+// in accumulator registers for their step's action k-steps.
 //
 // Waves.  Four matrix waves (one per SIMD) compute every actor layer; four
 // env waves (one per SIMD) own four envs each, one per 16-lane row, eight
@@ -27,15 +27,15 @@
 // barrier sequence: per step j, four slots separated by workgroup barriers:
 //
 //   slot  matrix waves                             env waves
-//   A     market k-steps of x_j and x_{j+1}        env step j-1: balance and holdings
-//         (even j when J = 2; every j when J = 1)   of x_j, trajectory row j-1
-//   B     h1 = tanh(Z_j + W1[:, action] x_j + b1)   x_j to HBM; loads of row t0+j+2
-//   L2    h2 = tanh(W2 h1 + b2)                    prices and indicators of row t0+j+2
-//                                                  into x_{j+2}; normals of step j
-//   L3    mu = W3 h2 + b3                          -
+//   A     market k-steps of x_j .. x_{j+J-1}       env step j-1: balance and holdings
+//         (once every J steps)                     of x_j, trajectory row j-1
+//   B     h1 = tanh(Z_j + W1[:, action] x_j + b1)   loads of row t0+j+J
+//   L2    h2 = tanh(W2 h1 + b2)                    x_j to HBM; normals of step j
+//   L3    mu = W3 h2 + b3                          prices and indicators of row t0+j+J
+//                                                  into x_{j+J}
 //
-// LDS: two observation rows per env (x_j lives in buffer j & 1: its market
-// columns are written two steps ahead, the balance and holdings by the env
+// LDS: J observation rows per env (x_j lives in buffer j % J: its market
+// columns are written J steps ahead, the balance and holdings by the env
 // step that completes it), h1, h2 (bf16), mu (fp32), biases.
 //
 // Weight stream.  A matrix wave consumes a fixed sequence of weight
@@ -105,7 +105,7 @@ struct Shape {
     static constexpr int NG1 = NT1 / (MW * G), NG2 = NT2 / (MW * G), NG3 = NT3 / MW;
     static_assert(NT1 % (MW * G) == 0 && NT2 % (MW * G) == 0 && NT3 % MW == 0,
                   "tiles must split evenly over the matrix waves");
-    static_assert(J == 1 || J == 2, "one or two steps per market pass");
+    static_assert(J >= 1 && J <= 3, "one to three steps per market pass");
 
     // k-step s holds the balance (column 0) or a holding (columns NS+1 .. 2NS)
     static constexpr bool is_action(int s) { return s == 0 || (32 * s <= 2 * NS && 32 * s + 31 >= NS + 1); }
@@ -176,14 +176,14 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint32_t __attribute__((ext_vector_t
 }
 
 struct Lds {
-    __bf16 *X;      // [2][MB][ldx] observation rows (x_j in buffer j & 1)
+    __bf16 *X;      // [J][MB][ldx] observation rows (x_j in buffer j % J)
     __bf16 *H1;     // [MB][ldh1]  hidden layer 1
     __bf16 *H2;     // [MB][ldh2]  hidden layer 2
     float *MU;      // [MB][ldmu]  action means
     float *BIAS;    // b1 | b2 | b3
     int ldx, ldh1, ldh2, ldmu;
-    // row `sl` of observation buffer b & 1
-    __device__ __forceinline__ __bf16 *xrow(int b, int sl) const { return X + ((b & 1) * MB + sl) * ldx; }
+    // row `sl` of observation buffer b (0 <= b < J)
+    __device__ __forceinline__ __bf16 *xrow(int b, int sl) const { return X + (b * MB + sl) * ldx; }
 };
 
 // k-step k of a segment at input column 32 * col(k)
@@ -225,15 +225,6 @@ struct Stream {
     {
         fetch<I + R - 1>();
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[I % R], x, acc, 0, 0, 0);
-    }
-
-    // fragment I against two input tiles
-    template <int I>
-    __device__ __forceinline__ void mma2(const bf16x8 &x0, const bf16x8 &x1, floatx4 &a0, floatx4 &a1)
-    {
-        fetch<I + R - 1>();
-        a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[I % R], x0, a0, 0, 0, 0);
-        a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[I % R], x1, a1, 0, 0, 0);
     }
 
     // The fragment offsets base + constant are loop-invariant; hoisted out
@@ -279,39 +270,41 @@ struct Stream {
         });
     }
 
-    // The market k-steps of layer 1 for one (x0 -> Z0) or two (x0 -> Z0,
-    // x1 -> Z1) steps' rows, no bias.
-    template <int FB0, bool TWO>
-    __device__ __forceinline__ void market(const __bf16 *x0b, const __bf16 *x1b,
-                                           floatx4 (&Z0)[S::NG1][G], floatx4 (&Z1)[S::NG1][G])
+    // The market k-steps of layer 1 for the rows of NT consecutive steps
+    // (tile i from the rows x0b + i * bstride into Z[i]), no bias: every
+    // weight fragment is multiplied against all NT tiles.
+    template <int FB0, int NT>
+    __device__ __forceinline__ void market(const __bf16 *x0b, int bstride,
+                                           floatx4 (&Z)[S::J][S::NG1][G])
     {
         static_for<0, S::NG1>([&](auto gi) {
             constexpr int g = decltype(gi)::value;
 #pragma unroll
-            for (int t = 0; t < G; ++t) {
-                Z0[g][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-                if constexpr (TWO) Z1[g][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-            }
-            bf16x8 x0 = *(const bf16x8 *)(x0b + S::mks(0) * 32), x1;
-            if constexpr (TWO) x1 = *(const bf16x8 *)(x1b + S::mks(0) * 32);
+            for (int i = 0; i < NT; ++i)
+#pragma unroll
+                for (int t = 0; t < G; ++t) Z[i][g][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+            bf16x8 x[NT];
+#pragma unroll
+            for (int i = 0; i < NT; ++i) x[i] = *(const bf16x8 *)(x0b + i * bstride + S::mks(0) * 32);
             static_for<0, S::KSA>([&](auto ki) {
                 constexpr int k = decltype(ki)::value;
-                bf16x8 xn0, xn1;
+                bf16x8 xn[NT];
                 if constexpr (k + 1 < S::KSA) {
-                    xn0 = *(const bf16x8 *)(x0b + S::mks(k + 1) * 32);
-                    if constexpr (TWO) xn1 = *(const bf16x8 *)(x1b + S::mks(k + 1) * 32);
+#pragma unroll
+                    for (int i = 0; i < NT; ++i)
+                        xn[i] = *(const bf16x8 *)(x0b + i * bstride + S::mks(k + 1) * 32);
                 }
                 static_for<0, G>([&](auto ti) {
                     constexpr int t = decltype(ti)::value;
                     constexpr int f = FB0 + (g * S::KSA + k) * G + t;
-                    if constexpr (TWO)
-                        mma2<f>(x0, x1, Z0[g][t], Z1[g][t]);
-                    else
-                        mma<f>(x0, Z0[g][t]);
+                    fetch<f + R - 1>();
+#pragma unroll
+                    for (int i = 0; i < NT; ++i)
+                        Z[i][g][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ring[f % R], x[i], Z[i][g][t], 0, 0, 0);
                 });
                 if constexpr (k + 1 < S::KSA) {
-                    x0 = xn0;
-                    if constexpr (TWO) x1 = xn1;
+#pragma unroll
+                    for (int i = 0; i < NT; ++i) x[i] = xn[i];
                 }
                 __builtin_amdgcn_sched_barrier(0);
             });
@@ -344,8 +337,8 @@ __device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
     st.wb2 = (int)P.off_W[2] + m * S::KS3 * 1024;
     st.voff = lane * 16;
 
-    const __bf16 *xb0 = s.xrow(0, r16) + kq * 8;
-    const __bf16 *xb1 = s.xrow(1, r16) + kq * 8;
+    const __bf16 *xb0 = s.xrow(0, r16) + kq * 8;   // buffer i: xb0 + i * bstride
+    const int bstride = MB * s.ldx;
     const __bf16 *h1b = s.H1 + r16 * s.ldh1 + kq * 8;
     const __bf16 *h2b = s.H2 + r16 * s.ldh2 + kq * 8;
     // output column of tile t of group g, for this lane, in layers 1-2 / 3
@@ -364,9 +357,8 @@ __device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
         *(bf16x4 *)(Y + o) = h;
     };
 
-    // market partial sums of layer 1 for the pending steps (Z[1] only with
-    // J = 2)
-    floatx4 Z[2][S::NG1][G];
+    // market partial sums of layer 1 for the J steps of a period
+    floatx4 Z[S::J][S::NG1][G];
 
     // one step's chain from fragment FB0 on: h1 from the action k-steps of
     // the rows `xb` on top of Zs, then layers 2 and 3
@@ -405,19 +397,18 @@ __device__ __forceinline__ void matrix_role(const RolloutArgs &A, const Lds &s,
     static_for<0, S::R - 1>([&](auto i) { st.template fetch<decltype(i)::value>(); });
     __syncthreads();   // observation rows of steps 0 and 1 and the biases are in LDS
     for (int j = 0; j < A.L; j += S::J) {
-        // slot A of step j
+        // slot A of step j: the market k-steps of steps j .. j+J-1 (their
+        // rows are in buffers 0 .. J-1)
         st.launder();
-        st.template market<0, S::J == 2>((S::J == 1 && (j & 1)) ? xb1 : xb0, xb1, Z[0], Z[1]);
+        st.template market<0, S::J>(xb0, bstride, Z);
         __syncthreads();
-        if constexpr (S::J == 1) {
-            chain(ic<S::FM>{}, (j & 1) ? xb1 : xb0, Z[0]);
-        } else {
-            chain(ic<S::FM>{}, xb0, Z[0]);
-            if (j + 1 < A.L) {
-                __syncthreads();   // slot A of step j+1: nothing for the matrix waves
-                chain(ic<S::FM + S::FS>{}, xb1, Z[1]);
+        static_for<0, S::J>([&](auto ii) {
+            constexpr int i = decltype(ii)::value;
+            if (i == 0 || j + i < A.L) {
+                if constexpr (i > 0) __syncthreads();   // slot A of step j+i: nothing here
+                chain(ic<S::FM + i * S::FS>{}, xb0 + i * bstride, Z[i]);
             }
-        }
+        });
     }
 }
 
@@ -428,7 +419,7 @@ template <class S>
 __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, const uint8_t *pk,
                                          int agent, int ebase, int nenv, int v, int lane)
 {
-    constexpr int n = S::NS, nI = S::NI;
+    constexpr int n = S::NS, nI = S::NI, J = S::J;
     constexpr int KPAD = S::KS1 * 32;
     static_assert(n % 4 == 0 && n <= RL * SPR && nI % 4 == 0 && nI > 0, "shape");
     constexpr int NPC = n / 4;                         // 16-byte price chunks of a row
@@ -444,10 +435,11 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
     const int e = ebase + sl;
     const size_t E = (size_t)A.E;
     const float qnan = __builtin_nanf("");
-    // this lane's two 16-byte price chunks (clamped to the row; stocks past
-    // n read as zero)
+    // this lane's stocks SPR * sl16 + c: all eight, the first four (the
+    // lane holding the row's last four stocks when n % 8 == 4) or none
+    const bool has8 = SPR * sl16 + 8 <= n, has4 = SPR * sl16 + 4 <= n;
+    // ... which are 16-byte chunks pc0, pc1 of a row (clamped to the row)
     const int pc0 = min(2 * sl16, NPC - 1), pc1 = min(2 * sl16 + 1, NPC - 1);
-    const bool pv0 = 2 * sl16 < NPC, pv1 = 2 * sl16 + 1 < NPC;
 
     float ls[SPR], sg[SPR];
     {
@@ -485,14 +477,18 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
     const bool wave_live = __ballot(live) != 0;
     const double half_log2pi_n = 0.5 * (double)n * 1.8378770664093454836;
 
-    // prices of row t (8 per lane, zero past n); row 0 for envs not stepped
+    // prices of row t, 8 per lane; row 0 for envs not stepped.  Slots of
+    // stocks past n repeat the row's last chunk: such a stock holds no
+    // shares and its order is zero, so its price never enters a sum (and
+    // leaving the loaded values as they are lets the loads stay in flight
+    // until first use)
     auto load_prices = [&](int64_t t, float (&p)[SPR]) {
         const float *pr = C.price + (size_t)(live ? t : 0) * n;
         const f4v a = load_stream(pr + 4 * pc0), b = load_stream(pr + 4 * pc1);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            p[c] = pv0 ? a[c] : 0.f;
-            p[4 + c] = pv1 ? b[c] : 0.f;
+            p[c] = a[c];
+            p[4 + c] = b[c];
         }
     };
     // indicator chunks sl16 + 16 m of row t (clamped to the row)
@@ -500,6 +496,22 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
         const float *ir = C.ind + (size_t)(live ? t : 0) * nI;
 #pragma unroll
         for (int mm = 0; mm < IPL; ++mm) ind[mm] = load_stream(ir + 4 * min(sl16 + RL * mm, NICH - 1));
+    };
+    // this lane's stock values v[c] as bf16 at columns col0 + SPR * sl16 + c
+    // (col0 odd): 2-, 4-, 4-, 4- and 2-byte stores for eight stocks
+    auto put_stocks = [&](__bf16 *row, int col0, const float (&v)[SPR]) {
+        __bf16 *q = row + col0 + SPR * sl16;
+        if (has8) {
+            q[0] = to_bf16(v[0]);
+            *(bf16x2 *)(q + 1) = bf16x2{to_bf16(v[1]), to_bf16(v[2])};
+            *(bf16x2 *)(q + 3) = bf16x2{to_bf16(v[3]), to_bf16(v[4])};
+            *(bf16x2 *)(q + 5) = bf16x2{to_bf16(v[5]), to_bf16(v[6])};
+            q[7] = to_bf16(v[7]);
+        } else if (has4) {
+            q[0] = to_bf16(v[0]);
+            *(bf16x2 *)(q + 1) = bf16x2{to_bf16(v[1]), to_bf16(v[2])};
+            q[3] = to_bf16(v[3]);
+        }
     };
     // the market columns of an observation row (prices 1 .. n, indicators
     // 2n+1 .. 2n+nI) in bf16; the balance, the holdings and the zero padding
@@ -529,47 +541,49 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
                 if (w == NICH - 1) q[4] = to_bf16(vv[3]);
             }
         }
-        if (live) {
+        float ps[SPR];
 #pragma unroll
-            for (int c = 0; c < SPR; ++c) {
-                const int i = SPR * sl16 + c;
-                if (i < n) row[1 + i] = to_bf16(p[c] * C.price_scale);
-            }
-        }
+        for (int c = 0; c < SPR; ++c) ps[c] = p[c] * C.price_scale;
+        if (live) put_stocks(row, 1, ps);
     };
     // the balance and the holdings of an observation row
     auto write_state = [&](__bf16 *row) {
+        float hs[SPR];
+#pragma unroll
+        for (int c = 0; c < SPR; ++c) hs[c] = (float)st.h[c] * C.share_scale;
         if (!live) return;
         if (sl16 == 0) row[0] = to_bf16((float)(st.cash * (double)C.cash_scale));
-#pragma unroll
-        for (int c = 0; c < SPR; ++c) {
-            const int i = SPR * sl16 + c;
-            if (i < n) row[1 + n + i] = to_bf16((float)st.h[c] * C.share_scale);
-        }
+        put_stocks(row, 1 + n, hs);
     };
+    auto xr = [&](int b) { return s.xrow(b, sl); };
 
-    // observation rows of steps 0 (complete) and 1 (market columns); the
-    // total asset at the start row; prices of rows t0 and t0 + 1
-    float pn[SPR], pnn[SPR];
+    // Prices the coming env steps need: at the start of step j, pj[i]
+    // holds row t0 + j + i (pj[0]: the next row of env step j-1).  Rows are
+    // loaded J steps ahead, with the market columns of x_{j+J}.
+    float pj[J][SPR];
     f4v ind[IPL];
     {
-        float p0[SPR];
-        load_prices(t0, p0);
+        // observation rows of steps 0 (complete) and 1 .. J-1 (market
+        // columns); the total asset at the start row
+        load_prices(t0, pj[0]);
         load_ind(t0, ind);
-        write_market(s.xrow(0, sl), p0, ind);
-        write_state(s.xrow(0, sl));
+        write_market(xr(0), pj[0], ind);
+        write_state(xr(0));
         double hv = 0.0;
 #pragma unroll
         for (int c = 0; c < SPR; ++c) {
-            st.pd[c] = (double)p0[c];
+            st.pd[c] = (double)pj[0][c];
             hv = fma((double)st.h[c], st.pd[c], hv);
         }
         st.value = st.cash + row_sum(hv);
-        load_prices(t0 + 1, pn);
-        load_ind(t0 + 1, ind);
-        write_market(s.xrow(1, sl), pn, ind);
 #pragma unroll
-        for (int c = 0; c < SPR; ++c) pnn[c] = 0.f;
+        for (int m = 1; m < J; ++m) {
+            if (m <= A.L) {
+                load_prices(t0 + m, pj[m]);
+                load_ind(t0 + m, ind);
+                write_market(xr(m), pj[m], ind);
+            }
+        }
     }
 
     float sz[SPR];
@@ -577,40 +591,46 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
 #pragma unroll
     for (int c = 0; c < SPR; ++c) sz[c] = 0.f;
 
-    // env step of step jj (the prices of row t0 + jj + 1 in pn): action,
-    // trade, the balance and holdings of x_{jj+1}, trajectory row jj
-    auto step_env = [&](int jj) {
-        const float *mu = s.MU + sl * s.ldmu + SPR * sl16;
-        const f4v m0 = *(const f4v *)mu, m1 = *(const f4v *)(mu + 4);
-        float a[SPR], ain[SPR];
+    // env step of step jj (pn: the prices of row t0 + jj + 1): action and
+    // mean rows, the trade, the balance and holdings of x_{jj+1}, the rest
+    // of trajectory row jj
+    auto step_env = [&](int jj, const float (&pn)[SPR]) {
+        const size_t row = (size_t)jj * E + e;
+        float ain[SPR];
+        {
+            const float *mu = s.MU + sl * s.ldmu + SPR * sl16;
+            const f4v m0 = *(const f4v *)mu, m1 = *(const f4v *)(mu + 4);
+            float a[SPR];
+#pragma unroll
+            for (int c = 0; c < SPR; ++c) {
+                a[c] = (c < 4 ? m0[c] : m1[c - 4]) + sz[c];
+                ain[c] = (live && SPR * sl16 + c < n) ? a[c] : 0.f;
+            }
+            // this lane's stocks are 16-byte chunks pc0, pc1 of the rows
+            if (mine && has4) {
+                const f4v nanv = {qnan, qnan, qnan, qnan};
+                f4v *arow = (f4v *)(A.action + row * n);
+                store_stream(live ? f4v{a[0], a[1], a[2], a[3]} : nanv, arow + pc0);
+                if (has8) store_stream(live ? f4v{a[4], a[5], a[6], a[7]} : nanv, arow + pc1);
+                if (A.mu_tap) {
+                    f4v *mrow = (f4v *)(A.mu_tap + row * n);
+                    store_stream(live ? m0 : nanv, mrow + pc0);
+                    if (has8) store_stream(live ? m1 : nanv, mrow + pc1);
+                }
+            }
+        }
         double qd[SPR];
 #pragma unroll
-        for (int c = 0; c < SPR; ++c) {
-            const float mc = c < 4 ? m0[c] : m1[c - 4];
-            a[c] = mc + sz[c];
-            ain[c] = (live && SPR * sl16 + c < n) ? a[c] : 0.f;
-            qd[c] = (double)pn[c];
-        }
+        for (int c = 0; c < SPR; ++c) qd[c] = (double)pn[c];
         float rw = 0.f;
         if (wave_live) rw = env_step_row(C, st, ain, qd);
-        write_state(s.xrow(jj + 1, sl));
+        write_state(xr((jj + 1) % J));
         if (!mine) return;
-        const size_t row = (size_t)jj * E + e;
         const uint8_t done = (uint8_t)(A.step0 + (uint64_t)jj + 1 == (uint64_t)C.horizon);
-        // this lane's stocks are 16-byte chunks pc0, pc1 of the row
-        float *arow = A.action + row * n;
-        const f4v nanv = {qnan, qnan, qnan, qnan};
-        if (pv0) store_stream(live ? f4v{a[0], a[1], a[2], a[3]} : nanv, (f4v *)arow + pc0);
-        if (pv1) store_stream(live ? f4v{a[4], a[5], a[6], a[7]} : nanv, (f4v *)arow + pc1);
-        if (A.mu_tap) {
-            float *mrow = A.mu_tap + row * n;
-            if (pv0) store_stream(live ? m0 : nanv, (f4v *)mrow + pc0);
-            if (pv1) store_stream(live ? m1 : nanv, (f4v *)mrow + pc1);
-        }
-        if (A.shares_tap) {
-            int32_t *srow = A.shares_tap + row * n;
-            if (pv0) store_stream(i4v{st.h[0], st.h[1], st.h[2], st.h[3]}, (i4v *)srow + pc0);
-            if (pv1) store_stream(i4v{st.h[4], st.h[5], st.h[6], st.h[7]}, (i4v *)srow + pc1);
+        if (A.shares_tap && has4) {
+            i4v *srow = (i4v *)(A.shares_tap + row * n);
+            store_stream(i4v{st.h[0], st.h[1], st.h[2], st.h[3]}, srow + pc0);
+            if (has8) store_stream(i4v{st.h[4], st.h[5], st.h[6], st.h[7]}, srow + pc1);
         }
         if (sl16 == 0) {
             store_stream(live ? (float)lp : qnan, A.logp + row);
@@ -621,35 +641,40 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
         }
     };
 
-    __syncthreads();   // observation rows of steps 0 and 1 are in LDS
+    __syncthreads();   // observation rows of steps 0 .. J-1 are in LDS
+    int bj = 0;        // j % J: the buffer of x_j
     for (int j = 0; j < A.L; ++j) {
-        // slot A: env step of step j-1, which completes x_j (the matrix
+        // slot A: the env step of step j-1, which completes x_j (the matrix
         // waves read only the market k-steps meanwhile)
-        if (j > 0) {
-            step_env(j - 1);
+        float pnext[SPR];
 #pragma unroll
-            for (int c = 0; c < SPR; ++c) pn[c] = pnn[c];
+        for (int c = 0; c < SPR; ++c) pnext[c] = pj[0][c];
+#pragma unroll
+        for (int i = 0; i + 1 < J; ++i)
+#pragma unroll
+            for (int c = 0; c < SPR; ++c) pj[i][c] = pj[i + 1][c];
+        const bool ahead = j + J <= A.L;
+        if (j > 0) step_env(j - 1, pnext);
+        __syncthreads();
+
+        // slot B: loads of row t0 + j + J (when a step of this rollout needs
+        // it; written two slots later).  These rows miss in L2 and hold
+        // their memory requests for a full HBM round trip; measured against
+        // issuing them at the start or the end of slot A or in slot L2, this
+        // slot costs the weight stream least
+        if (ahead) {
+            load_prices(t0 + j + J, pj[J - 1]);
+            load_ind(t0 + j + J, ind);
         }
         __syncthreads();
 
-        // slot B: x_j to HBM; loads of row t0 + j + 2 (when a later step
-        // needs it)
+        // slot L2: x_j to HBM; the normals of step j and their log-density
         if (live && A.obs) {
-            const u4v *src = (const u4v *)(s.xrow(j, sl));
+            const u4v *src = (const u4v *)xr(bj);
             u4v *dst = (u4v *)((__bf16 *)A.obs + ((size_t)j * E + e) * A.ld_obs);
 #pragma unroll
             for (int c = sl16; c < OBS_CHUNKS; c += RL) store_stream(src[c], dst + c);
         }
-        const bool ahead = j + 2 <= A.L;
-        if (ahead) {
-            load_prices(t0 + j + 2, pnn);
-            load_ind(t0 + j + 2, ind);
-        }
-        __syncthreads();
-
-        // slot L2: market columns of x_{j+2}; the normals of step j and
-        // their log-density
-        if (ahead) write_market(s.xrow(j, sl), pnn, ind);
         {
             float z[SPR];
 #pragma unroll
@@ -670,14 +695,18 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
         }
         __syncthreads();
 
-        // slot L3: nothing for the env waves
+        // slot L3: market columns of x_{j+J} into buffer j % J (x_j has left
+        // it: its action k-steps were read in slot B, its copy went out in
+        // slot L2)
+        if (ahead) write_market(xr(bj), pj[J - 1], ind);
         __syncthreads();
+        bj = bj + 1 == J ? 0 : bj + 1;
     }
-    step_env(A.L - 1);
+    step_env(A.L - 1, pj[0]);
 
     if (mine && live) {
         if (A.obs_last) {
-            const u4v *src = (const u4v *)(s.xrow(A.L, sl));
+            const u4v *src = (const u4v *)xr(A.L % J);
             u4v *dst = (u4v *)((__bf16 *)A.obs_last + (size_t)e * A.ld_obs);
 #pragma unroll
             for (int c = sl16; c < OBS_CHUNKS; c += RL) dst[c] = src[c];
@@ -723,9 +752,9 @@ __global__ __launch_bounds__(NWAVES *WAVE) void rollout_rs_kernel(RolloutArgs A)
     s.ldh2 = A.ldh2;
     s.ldmu = A.ldmu;
 
-    // zero both observation buffers (padding columns and rows of absent
+    // zero the observation buffers (padding columns and rows of absent
     // envs stay zero)
-    for (int i = threadIdx.x; i < 2 * MB * s.ldx * 2 / 16; i += NWAVES * WAVE)
+    for (int i = threadIdx.x; i < S::J * MB * s.ldx * 2 / 16; i += NWAVES * WAVE)
         ((uint4 *)s.X)[i] = uint4{0, 0, 0, 0};
     __syncthreads();
 
@@ -746,7 +775,7 @@ hipError_t launch(RolloutArgs &a, hipStream_t st)
     a.ldz = 0;
     auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
     size_t off = 0;
-    a.lds_X = off;  off = al(off + (size_t)2 * MB * a.ldx * 2);
+    a.lds_X = off;  off = al(off + (size_t)S::J * MB * a.ldx * 2);
     a.lds_H = off;  off = al(off + (size_t)MB * a.ldh * 2);
     a.lds_Z = off;  off = al(off + (size_t)MB * a.ldh2 * 2);
     a.lds_MU = off; off = al(off + (size_t)MB * a.ldmu * 4);
@@ -788,7 +817,7 @@ hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
         (uintptr_t)a.shares_tap % 16 || (uintptr_t)a.mu_tap % 16)
         return hipErrorNotSupported;
     if (P.H1 == 512 && P.H2 == 512)
-        return rs::launch<rs::Shape<100, 800, 32, 32, 32, 8, 22, 2>>(a, s);
+        return rs::launch<rs::Shape<100, 800, 32, 32, 32, 8, 16, 3>>(a, s);
     if (P.H1 == 1024 && P.H2 == 1024)
         return rs::launch<rs::Shape<100, 800, 32, 64, 64, 8, 16, 1>>(a, s);
     return hipErrorNotSupported;
