@@ -27,9 +27,11 @@
 // barrier sequence: per step j, four slots separated by workgroup barriers:
 //
 //   slot  matrix waves                             env waves
-//   A     market k-steps of x_j .. x_{j+J-1}       env step j-1: balance and holdings
-//         (once every J steps)                     of x_j, trajectory row j-1
-//   B     h1 = tanh(Z_j + W1[:, action] x_j + b1)   loads of row t0+j+J
+//   A     market k-steps of x_j .. x_{j+J-1}       loads of row t0+j+J (in slot B when the
+//         (once every J steps)                     step starts a batch); env step j-1:
+//                                                  balance and holdings of x_j, trajectory
+//                                                  row j-1
+//   B     h1 = tanh(Z_j + W1[:, action] x_j + b1)   -
 //   L2    h2 = tanh(W2 h1 + b2)                    x_j to HBM; normals of step j
 //   L3    mu = W3 h2 + b3                          prices and indicators of row t0+j+J
 //                                                  into x_{j+J}
@@ -653,16 +655,22 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
         for (int i = 0; i + 1 < J; ++i)
 #pragma unroll
             for (int c = 0; c < SPR; ++c) pj[i][c] = pj[i + 1][c];
+        // Loads of row t0 + j + J (when a step of this rollout needs it;
+        // written in slot L3).  These rows miss in L2 and hold their memory
+        // requests for a full HBM round trip, which slows a weight stream
+        // running beside them: they go out first in slot A, where the
+        // matrix waves stream nothing, except in the steps that start a
+        // market batch, where they wait for slot B.
         const bool ahead = j + J <= A.L;
+        if (ahead && bj != 0) {
+            load_prices(t0 + j + J, pj[J - 1]);
+            load_ind(t0 + j + J, ind);
+        }
         if (j > 0) step_env(j - 1, pnext);
         __syncthreads();
 
-        // slot B: loads of row t0 + j + J (when a step of this rollout needs
-        // it; written two slots later).  These rows miss in L2 and hold
-        // their memory requests for a full HBM round trip; measured against
-        // issuing them at the start or the end of slot A or in slot L2, this
-        // slot costs the weight stream least
-        if (ahead) {
+        // slot B: the row loads of a step that starts a market batch
+        if (ahead && bj == 0) {
             load_prices(t0 + j + J, pj[J - 1]);
             load_ind(t0 + j + J, ind);
         }
