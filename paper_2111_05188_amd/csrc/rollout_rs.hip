@@ -825,7 +825,7 @@ hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
         (uintptr_t)a.shares_tap % 16 || (uintptr_t)a.mu_tap % 16)
         return hipErrorNotSupported;
     if (P.H1 == 512 && P.H2 == 512)
-        return rs::launch<rs::Shape<100, 800, 32, 32, 32, 8, 16, 3>>(a, s);
+        return rs::launch<rs::Shape<100, 800, 32, 32, 32, 8, 24, 3>>(a, s);
     if (P.H1 == 1024 && P.H2 == 1024)
         return rs::launch<rs::Shape<100, 800, 32, 64, 64, 8, 16, 1>>(a, s);
     return hipErrorNotSupported;
