@@ -52,7 +52,7 @@ def algorithmic_bytes_gae() -> int:
 # Sources the role-split rollout kernel (the one the counters describe) is
 # built from: counters taken on an older version of any of them no longer
 # describe the kernel.
-ROLLOUT_SOURCES = ("rollout_rs.hip", "env.hpp", "device.hpp", "internal.hpp")
+ROLLOUT_SOURCES = ("rollout_rs.hip", "env_row.hpp", "device.hpp", "internal.hpp")
 
 
 def kernel_source_hash() -> str:
@@ -223,8 +223,10 @@ def main():
             "hbm_achieved_GBs": roll_bytes / t_roll / 1e9,
             "hbm_frac": roll_bytes / t_roll / 1e9 / PEAK_HBM_GBS,
             "bytes_per_launch": roll_bytes,
-            "note": "fused kernel: the actor's weights stream from L2 to every CU each step; "
-                    "the measured per-CU L2->CU ceiling (~124 GB/s) bounds the MLP phase",
+            "note": "fused kernel: every CU streams the actor's weights from L2 (layer 1's "
+                    "market columns once per three steps, the rest every step) at a measured "
+                    "per-CU ceiling of ~124 GB/s, and the env step sits on the step-to-step "
+                    "chain between layer 3 and the next layer 1",
         },
         "gae": {"launch_ms": t_gae * 1e3, "GBs": gae_bytes / t_gae / 1e9,
                 "hbm_frac": gae_bytes / t_gae / 1e9 / PEAK_HBM_GBS},
