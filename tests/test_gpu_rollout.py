@@ -63,6 +63,14 @@ def test_ensemble_shape_three_agents_ragged():
     _run_case(W.get_config("ensemble"), 60, 40, rows=20 * 390 + 1, n_agents=3)
 
 
+@pytest.mark.parametrize("L", [1, 2, 4, 5])
+def test_nasdaq_shape_short_rollouts(L):
+    """Rollouts shorter than, or not a multiple of, the role-split kernel's
+    market batch of three steps: the partial final batch, the bootstrap
+    observation row and the final state."""
+    _run_case(W.get_config("nasdaq100"), 20, L, rows=6 * 390 + 1)
+
+
 def test_stress_shape_small():
     _run_case(W.get_config("stress"), 20, 30, rows=20 * 390 + 1)
 
