@@ -1,7 +1,7 @@
-// Role-split fused rollout kernel for bf16 actors of the 100-stock shapes in
-// use (1001 inputs from 100 stocks with 8 indicators each, 512- or
-// 1024-wide hidden layers).  One launch runs all L lockstep steps of a block
-// of 16 envs.
+// Role-split fused rollout kernel for bf16 actors of the 100-stock market
+// (1001 inputs from 100 stocks with 8 indicators each) with two hidden
+// layers of the same width, 256, 512, 768 or 1024.  One launch runs all L
+// lockstep steps of a block of 16 envs.
 //
 // Why split roles.  A workgroup owns 16 envs, the N dimension of one MFMA
 // tile, so every step streams the actor's weights from L2 into the CU.  That
@@ -16,7 +16,8 @@
 // layers 2 and 3 remain on the step-to-step chain.
 //
 // Market k-steps in batches.  The market k-steps of J consecutive steps
-// (J = 3 for the 512-wide actor) are multiplied together, each weight
+// (J = 3 up to 512 wide, 2 at 768 and 1024: the batch's partial sums
+// must fit the registers) are multiplied together, each weight
 // fragment against every step's rows (J MFMAs per fragment), so the market
 // part of layer 1 streams once per J steps.  The batch's partial sums wait
 // in accumulator registers for their step's action k-steps.
@@ -95,7 +96,7 @@ __device__ __forceinline__ void static_for(Fn &&fn)
 
 // Actor shape.  NS stocks with NI indicator values per market row; KS1
 // k-steps of 32 inputs in layer 1; NT1, NT2, NT3 output tiles of 16; a ring
-// of R weight fragments per matrix wave; market k-steps of J steps (1 or 2)
+// of R weight fragments per matrix wave; market k-steps of J steps (1 to 3)
 // multiplied together.
 template <int NS_, int NI_, int KS1_, int NT1_, int NT2_, int NT3_, int R_, int J_>
 struct Shape {
@@ -807,12 +808,13 @@ hipError_t launch(RolloutArgs &a, hipStream_t st)
 }  // namespace rs
 
 // The role-split kernel covers bf16 actors with 100 stocks of 8 indicators
-// (1001 inputs: KS1 = 32) and hidden widths 512 or 1024; returns
-// hipErrorNotSupported for other shapes.
+// (1001 inputs: KS1 = 32) and two hidden layers of one width, 256, 512, 768
+// or 1024; returns hipErrorNotSupported for other shapes.
 bool rollout_rs_shape(const PackedLayout &P, int nI)
 {
+    const bool width = P.H1 == P.H2 && (P.H1 == 256 || P.H1 == 512 || P.H1 == 768 || P.H1 == 1024);
     return P.dtype == TP_BF16 && P.n == 100 && P.S == 1001 && nI == 800 && P.KS[0] == 32 &&
-           P.NT[2] == 8 && ((P.H1 == 512 && P.H2 == 512) || (P.H1 == 1024 && P.H2 == 1024));
+           P.NT[2] == 8 && width;
 }
 
 hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
@@ -824,10 +826,16 @@ hipError_t launch_rollout_rs(RolloutArgs &a, hipStream_t s)
     if ((uintptr_t)a.env.price % 16 || (uintptr_t)a.env.ind % 16 || (uintptr_t)a.action % 16 ||
         (uintptr_t)a.shares_tap % 16 || (uintptr_t)a.mu_tap % 16)
         return hipErrorNotSupported;
-    if (P.H1 == 512 && P.H2 == 512)
-        return rs::launch<rs::Shape<100, 800, 32, 32, 32, 8, 24, 3>>(a, s);
-    if (P.H1 == 1024 && P.H2 == 1024)
-        return rs::launch<rs::Shape<100, 800, 32, 64, 64, 8, 16, 1>>(a, s);
+    // per width: the ring depth R and the market batch J that fit 256
+    // registers per matrix wave (J * NT1 / 4 accumulator registers, 4 R ring
+    // registers) and the 160 KiB of LDS (J observation rows per env); the
+    // period of fragments J FS + FM a multiple of R
+    switch (P.H1) {
+    case 256: return rs::launch<rs::Shape<100, 800, 32, 16, 16, 8, 24, 3>>(a, s);
+    case 512: return rs::launch<rs::Shape<100, 800, 32, 32, 32, 8, 24, 3>>(a, s);
+    case 768: return rs::launch<rs::Shape<100, 800, 32, 48, 48, 8, 18, 2>>(a, s);
+    case 1024: return rs::launch<rs::Shape<100, 800, 32, 64, 64, 8, 16, 2>>(a, s);
+    }
     return hipErrorNotSupported;
 }
 

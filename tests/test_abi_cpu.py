@@ -84,6 +84,24 @@ def test_packed_bytes_host_only():
     assert "multiples of 128" in tp.last_error()
 
 
+def test_rollout_path_host_only():
+    """Which rollout kernel a market and actor shape get, decided on the
+    host: the role-split kernel for the 100 x 8 market with two equal bf16
+    hidden layers of 256 to 1024 (multiples of 256), the generic one
+    otherwise."""
+    L = tp.load()
+    x = 0x100000
+    m = tp.Market(x, x, 100, 100, 8)
+    for H in (256, 512, 768, 1024):
+        assert L.tp_rollout_path(C.byref(m), C.byref(_nasdaq_actor(dims=(1001, H, H, 100)))) == 1
+    for dims in ((1001, 384, 384, 100), (1001, 512, 256, 100), (1001, 1280, 1280, 100)):
+        assert L.tp_rollout_path(C.byref(m), C.byref(_nasdaq_actor(dims=dims))) == 0
+    assert L.tp_rollout_path(C.byref(m), C.byref(_nasdaq_actor(dtype=tp.TP_F32))) == 0
+    m10 = tp.Market(x, x, 100, 100, 10)
+    assert L.tp_rollout_path(C.byref(m10), C.byref(_nasdaq_actor(dims=(1201, 512, 512, 100)))) == 0
+    assert L.tp_rollout_path(C.byref(m), C.byref(_nasdaq_actor(dims=(1001, 500, 512, 100)))) < 0
+
+
 def test_argument_errors_without_gpu():
     L = tp.load()
     assert L.tp_gae(None, None, None, 1, 1, 0.99, 0.95, None, None, None) == tp.TP_EINVAL

@@ -1,7 +1,7 @@
 """GPU parity of tp_rollout (fused actor + sampling + env step + trajectory
 store) against a teacher-forced oracle replay, at sizes the oracle finishes
 in seconds: several workgroups of envs, ragged tails, every actor shape
-family (fp32 VALU, bf16 MFMA 512-wide and 1024-wide on the role-split kernel,
+family (fp32 VALU, bf16 MFMA 256- to 1024-wide on the role-split kernel,
 bf16 of another shape on the generic kernel, multi-agent), plus
 determinism, split/resume, and envs whose start row leaves no room."""
 
@@ -73,6 +73,15 @@ def test_nasdaq_shape_short_rollouts(L):
 
 def test_stress_shape_small():
     _run_case(W.get_config("stress"), 20, 30, rows=20 * 390 + 1)
+
+
+@pytest.mark.parametrize("H,L", [(256, 50), (256, 4), (768, 50), (768, 3)])
+def test_role_split_other_widths(H, L):
+    """The role-split kernel at its other hidden widths (256: market batches
+    of three steps; 768: of two), three workgroups with a ragged tail, and
+    rollouts that end inside a batch."""
+    pb = _run_case(W.get_config("nasdaq100").with_(hidden=(H, H)), 37, L, rows=20 * 390 + 1)
+    assert tp.rollout_path(pb.mkt, pb.actor) == 1
 
 
 def test_dow_shape_small():
