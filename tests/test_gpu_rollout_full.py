@@ -67,6 +67,14 @@ def test_nasdaq100_full(minute_market):
     _full(cfg, minute_market, sorted(set([0, 15, 16, 4095] + _spread(256, 1, 16, 2))))
 
 
+@pytest.mark.parametrize("H", [256, 768])
+def test_nasdaq_other_widths_full(minute_market, H):
+    # the role-split kernel at its other widths (market batches of three
+    # steps at 256, two at 768): 32 envs spread over all 256 workgroups
+    cfg = W.get_config("nasdaq100").with_(hidden=(H, H))
+    _full(cfg, minute_market, sorted(set([0, 4095] + _spread(256, 8, 16, 5 + H))))
+
+
 def test_ensemble_full(minute_market):
     cfg = W.get_config("ensemble")
     # 8 envs of each of the 16 agents, including each agent's first and
