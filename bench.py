@@ -52,7 +52,7 @@ def algorithmic_bytes_gae() -> int:
 # Sources the role-split rollout kernel (the one the counters describe) is
 # built from: counters taken on an older version of any of them no longer
 # describe the kernel.
-ROLLOUT_SOURCES = ("rollout_rs.hip", "env_row.hpp", "device.hpp", "internal.hpp")
+ROLLOUT_SOURCES = ("rollout_rs.hip", "rollout_rs.hpp", "env_row.hpp", "device.hpp", "internal.hpp")
 
 
 def kernel_source_hash() -> str:

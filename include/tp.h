@@ -257,10 +257,11 @@ int tp_rollout(const tp_market *mkt, const tp_env_cfg *cfg,
 
 /*
  * tp_rollout_path -- which rollout kernel tp_rollout launches for this
- * market and actor shape: 1 = the role-split kernel (bf16, 100 stocks x 8
- * indicators, 1001-H-H-100 with H = 256, 512, 768 or 1024, given 16-byte
- * aligned market, action and holdings-tap buffers), 0 = the generic kernel,
- * or a negative tp_status for an invalid market or actor.  Host only.
+ * market and actor shape: 1 = the role-split kernel (bf16, 100 stocks x 4,
+ * 8 or 10 indicators, S-H-H-100 with H = 256, 512, 768 or 1024, given
+ * 16-byte aligned market, action and holdings-tap buffers), 0 = the generic
+ * kernel, or a negative tp_status for an invalid market or actor.  Host
+ * only.
  */
 int tp_rollout_path(const tp_market *market, const tp_actor *actor);
 

@@ -11,8 +11,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libtp.so")
-SOURCES = ["api.cpp", "rollout.hip", "rollout_rs.hip", "critic.hip", "metrics.hip",
-           "evolution.hip", "learner.hip", "env_kernels.hip", "gae.hip", "pack.hip"]
+SOURCES = ["api.cpp", "rollout.hip", "rollout_rs.hip", "rollout_rs_i4.hip", "rollout_rs_i10.hip",
+           "rollout_rs_i10_wide.hip", "critic.hip", "metrics.hip", "evolution.hip", "learner.hip",
+           "env_kernels.hip", "gae.hip", "pack.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -86,9 +86,9 @@ def test_packed_bytes_host_only():
 
 def test_rollout_path_host_only():
     """Which rollout kernel a market and actor shape get, decided on the
-    host: the role-split kernel for the 100 x 8 market with two equal bf16
-    hidden layers of 256 to 1024 (multiples of 256), the generic one
-    otherwise."""
+    host: the role-split kernel for 100 stocks with 4, 8 or 10 indicators
+    each and two equal bf16 hidden layers of 256 to 1024 (multiples of 256),
+    the generic one otherwise."""
     L = tp.load()
     x = 0x100000
     m = tp.Market(x, x, 100, 100, 8)
@@ -97,8 +97,15 @@ def test_rollout_path_host_only():
     for dims in ((1001, 384, 384, 100), (1001, 512, 256, 100), (1001, 1280, 1280, 100)):
         assert L.tp_rollout_path(C.byref(m), C.byref(_nasdaq_actor(dims=dims))) == 0
     assert L.tp_rollout_path(C.byref(m), C.byref(_nasdaq_actor(dtype=tp.TP_F32))) == 0
-    m10 = tp.Market(x, x, 100, 100, 10)
-    assert L.tp_rollout_path(C.byref(m10), C.byref(_nasdaq_actor(dims=(1201, 512, 512, 100)))) == 0
+    for I in (4, 10):
+        mI = tp.Market(x, x, 100, 100, I)
+        for H in (256, 512, 768, 1024):
+            a = _nasdaq_actor(dims=(201 + 100 * I, H, H, 100))
+            assert L.tp_rollout_path(C.byref(mI), C.byref(a)) == 1
+    m6 = tp.Market(x, x, 100, 100, 6)
+    assert L.tp_rollout_path(C.byref(m6), C.byref(_nasdaq_actor(dims=(801, 512, 512, 100)))) == 0
+    m30 = tp.Market(x, x, 100, 32, 8)
+    assert L.tp_rollout_path(C.byref(m30), C.byref(_nasdaq_actor(dims=(321, 512, 512, 32)))) == 0
     assert L.tp_rollout_path(C.byref(m), C.byref(_nasdaq_actor(dims=(1001, 500, 512, 100)))) < 0
 
 

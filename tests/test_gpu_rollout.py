@@ -75,6 +75,18 @@ def test_stress_shape_small():
     _run_case(W.get_config("stress"), 20, 30, rows=20 * 390 + 1)
 
 
+@pytest.mark.parametrize("I,H,L", [(4, 512, 50), (4, 256, 4), (4, 768, 5), (4, 1024, 3),
+                                   (10, 512, 50), (10, 256, 4), (10, 768, 5), (10, 1024, 3)])
+def test_role_split_other_markets(I, H, L):
+    """The role-split kernel on the 100-stock markets with 4 and 10
+    indicators per stock (601 and 1201 inputs: 20 and 40 k-steps, observation
+    rows of 608 and 1,216 columns), at every width, three workgroups with a
+    ragged tail, rollouts that end inside a market batch."""
+    cfg = W.get_config("nasdaq100").with_(n_ind=I, hidden=(H, H))
+    pb = _run_case(cfg, 37, L, rows=20 * 390 + 1)
+    assert tp.rollout_path(pb.mkt, pb.actor) == 1
+
+
 @pytest.mark.parametrize("H,L", [(256, 50), (256, 4), (768, 50), (768, 3)])
 def test_role_split_other_widths(H, L):
     """The role-split kernel at its other hidden widths (256: market batches

@@ -75,6 +75,17 @@ def test_nasdaq_other_widths_full(minute_market, H):
     _full(cfg, minute_market, sorted(set([0, 4095] + _spread(256, 8, 16, 5 + H))))
 
 
+@pytest.mark.parametrize("I", [4, 10])
+def test_other_markets_full_launch(I):
+    # the bench's launch (4,096 envs x 390 steps, 256 workgroups) on the
+    # markets with 4 and 10 indicators per stock (a 60-day market: the
+    # start rows, not the market's length, decide what the kernel does):
+    # 32 envs spread over all 256 workgroups
+    cfg = W.get_config("nasdaq100").with_(n_ind=I, N=60 * 390)
+    mk = W.make_market(cfg)
+    _full(cfg, mk, sorted(set([0, 4095] + _spread(256, 8, 16, 7 + I))))
+
+
 def test_ensemble_full(minute_market):
     cfg = W.get_config("ensemble")
     # 8 envs of each of the 16 agents, including each agent's first and
