@@ -2,8 +2,8 @@
 // (4, 8 or 10 indicators per stock: 601, 1001 or 1201 inputs) with two
 // hidden layers of the same width, 256, 512, 768 or 1024.  One launch runs
 // all L lockstep steps of a block of 16 envs.  The kernel is a template over
-// the shape; rollout_rs.hip and one translation unit per market instantiate
-// it.
+// the shape; rollout_rs.hip (8 indicators) and rollout_rs_i4.hip,
+// rollout_rs_i10.hip, rollout_rs_i10_wide.hip instantiate it.
 //
 // Why split roles.  A workgroup owns 16 envs, the N dimension of one MFMA
 // tile, so every step streams the actor's weights from L2 into the CU.  That
@@ -19,10 +19,10 @@
 //
 // Market k-steps in batches.  The market k-steps of J consecutive steps
 // (1 to 3, as the registers and the LDS allow: Pick below) are multiplied
-// together, each weight
-// fragment against every step's rows (J MFMAs per fragment), so the market
-// part of layer 1 streams once per J steps.  The batch's partial sums wait
-// in accumulator registers for their step's action k-steps.
+// together, each weight fragment against every step's rows (J MFMAs per
+// fragment), so the market part of layer 1 streams once per J steps.  The
+// batch's partial sums wait in accumulator registers for their step's
+// action k-steps.
 //
 // Waves.  Four matrix waves (one per SIMD) compute every actor layer; four
 // env waves (one per SIMD) own four envs each, one per 16-lane row, eight
