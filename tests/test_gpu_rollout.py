@@ -87,6 +87,17 @@ def test_role_split_other_markets(I, H, L):
     assert tp.rollout_path(pb.mkt, pb.actor) == 1
 
 
+@pytest.mark.parametrize("I,H,agents,E", [(10, 768, 3, 60), (4, 512, 2, 34), (10, 512, 1, 1),
+                                          (10, 1024, 1, 17)])
+def test_role_split_agents_and_env_counts(I, H, agents, E):
+    """Several agents per launch (each agent's blocks in its own run of
+    workgroups, ragged per agent), a single env, and one env past a
+    workgroup, on the market-batch and single-step paths."""
+    cfg = W.get_config("nasdaq100").with_(n_ind=I, hidden=(H, H))
+    pb = _run_case(cfg, E, 20, rows=20 * 390 + 1, n_agents=agents)
+    assert tp.rollout_path(pb.mkt, pb.actor) == 1
+
+
 @pytest.mark.parametrize("H,L", [(256, 50), (256, 4), (768, 50), (768, 3)])
 def test_role_split_other_widths(H, L):
     """The role-split kernel at its other hidden widths (256: market batches
