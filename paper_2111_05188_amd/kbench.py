@@ -27,6 +27,12 @@ Times, with HIP events on the launch stream:
     2B (2 S H1 + 3 H1 H2 + 3 H2 n + 2 S C1 + 3 C1 C2 + 3 C2) (forward of
     both networks, weight gradients, and input gradients except layer 1's);
     then the same for 16 agents per call (tp_ppo_update_agents);
+  * rollout_shapes (only with --only rollout_shapes): the fused rollout
+    step (reset, rollout with observations stored, GAE) of 4,096 envs x 390
+    steps on each shape the role-split kernel takes: 100 stocks with 4, 8
+    or 10 indicators, hidden widths 256, 512, 768 and 1024, on a 60-day
+    minute market (the start rows, not the market's length, decide what
+    the kernel does); FLOPs 2 (S H + H H + H n) per env-step;
   * train (only with --only train): one generation of the ensemble
     workload (4 agents x 4 pods of 1,024 envs, L = 390): rollout, critic,
     GAE, the learners' 8 L envs / B updates each in one agent-batched call,
@@ -84,7 +90,7 @@ def main():
     ap.add_argument("--iters", type=int, default=20)
     ap.add_argument("--only", default=None,
                     choices=["env_step", "gae", "critic", "metrics", "evolution", "learner",
-                             "train", "probes", "copy", "mfma_sweep", "sync"])
+                             "train", "probes", "copy", "mfma_sweep", "sync", "rollout_shapes"])
     args = ap.parse_args()
     sys.path.insert(0, __file__.rsplit("/", 2)[0])
     import workloads as W
@@ -271,6 +277,37 @@ def main():
                                       "mfma_frac": A * flops / sec / 1e12 / PEAK_BF16_TFLOPS}
         del obs, act, logp, adv, ret, params, m, v, idx, ws
         torch.cuda.empty_cache()
+
+    if args.only == "rollout_shapes":
+        shapes = {}
+        for ni in (4, 8, 10):
+            base = W.get_config("nasdaq100").with_(n_ind=ni, N=60 * W.MINUTES_PER_DAY)
+            print(f"[kbench] rollout shapes: {base.n} stocks x {ni} indicators", file=sys.stderr,
+                  flush=True)
+            mk = W.make_market(base)
+            t0 = W.make_t0(base)
+            for H in (256, 512, 768, 1024):
+                c = base.with_(hidden=(H, H))
+                pb = problem.Problem(c, mk, W.make_actor(c), t0, store_obs=True, taps=False)
+                pb.set_values(W.make_values(c))
+                k = [0]
+
+                def step():
+                    pb.step(1000 + k[0], stream)
+                    k[0] += 1
+                sec = _time(step, max(2, args.iters // 4), stream)
+                es = c.E * c.L / sec
+                fl = es * c.flops_per_env_step()
+                shapes[f"I{ni}_H{H}"] = {"S": c.S, "path": tp.rollout_path(pb.mkt, pb.actor),
+                                         "step_ms": sec * 1e3, "env_steps_per_s": es,
+                                         "us_per_lockstep_step": sec * 1e6 / c.L,
+                                         "TFLOPs": fl / 1e12, "mfma_frac": fl / 1e12 / PEAK_BF16_TFLOPS}
+                print(f"[kbench]   I={ni} H={H}: {es / 1e6:.1f} M env-steps/s", file=sys.stderr,
+                      flush=True)
+                del pb
+                torch.cuda.empty_cache()
+            del mk
+        out["rollout_shapes"] = shapes
 
     if args.only == "train":   # opt-in: one generation is ~50,000 launches
         # one generation of the ensemble workload: 4 agents x 4 pods (16
