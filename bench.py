@@ -115,7 +115,7 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}): the rollout "
-              "shards by env with no communication on the hot path, and this build "
+              "shards by env with no communication on the hot path; this benchmark "
               "runs and reports the single-GPU path.", file=sys.stderr)
         sys.exit(2)
 
