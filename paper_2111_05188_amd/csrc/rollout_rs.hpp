@@ -188,6 +188,7 @@ struct Lds {
     __bf16 *H2;     // [MB][ldh2]  hidden layer 2
     float *MU;      // [MB][ldmu]  action means
     float *BIAS;    // b1 | b2 | b3
+    float *LS;      // log sigma | sigma of the actor, per stock slot (RL * SPR each)
     int ldx, ldh1, ldh2, ldmu;
     // row `sl` of observation buffer b (0 <= b < J)
     __device__ __forceinline__ __bf16 *xrow(int b, int sl) const { return X + (b * MB + sl) * ldx; }
@@ -456,14 +457,15 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
     // ... which are 16-byte chunks pc0, pc1 of a row (clamped to the row)
     const int pc0 = min(2 * sl16, NPC - 1), pc1 = min(2 * sl16 + 1, NPC - 1);
 
-    float ls[SPR], sg[SPR];
-    {
+    // log sigma and sigma per stock slot (0 and 1 past n) go to LDS once;
+    // the normals' slot reads them back each step (16 registers the env
+    // waves do not hold through the trade)
+    if (v == 0) {
         const float *lsd = (const float *)(pk + P.off_ls);
-#pragma unroll
-        for (int c = 0; c < SPR; ++c) {
-            const int i = SPR * sl16 + c;
-            ls[c] = i < n ? lsd[i] : 0.f;
-            sg[c] = expf(ls[c]);
+        for (int i = lane; i < RL * SPR; i += WAVE) {
+            const float l = i < n ? lsd[i] : 0.f;
+            s.LS[i] = l;
+            s.LS[RL * SPR + i] = expf(l);
         }
     }
 
@@ -712,11 +714,15 @@ __device__ __forceinline__ void env_role(const RolloutArgs &A, const Lds &s, con
                 box_muller_hw(uniform_open01(w.x), uniform_open01(w.y), z[4 * h], z[4 * h + 1]);
                 box_muller_hw(uniform_open01(w.z), uniform_open01(w.w), z[4 * h + 2], z[4 * h + 3]);
             }
+            const float *lsr = s.LS + SPR * sl16;
+            const f4v l0 = *(const f4v *)lsr, l1 = *(const f4v *)(lsr + 4);
+            const f4v g0 = *(const f4v *)(lsr + RL * SPR), g1 = *(const f4v *)(lsr + RL * SPR + 4);
             double l = 0.0;
 #pragma unroll
             for (int c = 0; c < SPR; ++c) {
-                sz[c] = sg[c] * z[c];
-                if (SPR * sl16 + c < n) l += -0.5 * (double)z[c] * (double)z[c] - (double)ls[c];
+                const float lsc = c < 4 ? l0[c] : l1[c - 4], sgc = c < 4 ? g0[c] : g1[c - 4];
+                sz[c] = sgc * z[c];
+                if (SPR * sl16 + c < n) l += -0.5 * (double)z[c] * (double)z[c] - (double)lsc;
             }
             lp = row_sum(l) - half_log2pi_n;
         }
@@ -780,6 +786,7 @@ __global__ __launch_bounds__(NWAVES *WAVE) void rollout_rs_kernel(RolloutArgs A)
     s.H2 = (__bf16 *)(smem + A.lds_Z);
     s.MU = (float *)(smem + A.lds_MU);
     s.BIAS = (float *)(smem + A.lds_B);
+    s.LS = s.BIAS + (S::NT1 + S::NT2 + S::NT3) * 16;
     s.ldx = A.ldx;
     s.ldh1 = A.ldh;
     s.ldh2 = A.ldh2;
@@ -812,7 +819,7 @@ hipError_t launch(RolloutArgs &a, hipStream_t st)
     a.lds_H = off;  off = al(off + (size_t)MB * a.ldh * 2);
     a.lds_Z = off;  off = al(off + (size_t)MB * a.ldh2 * 2);
     a.lds_MU = off; off = al(off + (size_t)MB * a.ldmu * 4);
-    a.lds_B = off;  off = al(off + (size_t)(S::NT1 + S::NT2 + S::NT3) * 16 * 4);
+    a.lds_B = off;  off = al(off + ((size_t)(S::NT1 + S::NT2 + S::NT3) * 16 + 2 * RL * SPR) * 4);
     a.lds_bytes = off;
     if (off > LDS_LIMIT) return hipErrorInvalidConfiguration;
     if (P.KS[0] != S::KS1 || P.NT[0] != S::NT1 || P.NT[1] != S::NT2 || P.NT[2] != S::NT3 ||
@@ -832,11 +839,11 @@ hipError_t launch(RolloutArgs &a, hipStream_t st)
 // The launch configuration of a market of NS stocks with NI indicator
 // values per row and an actor with two hidden layers of width H:
 //  - J, the market batch: the largest of 3, 2, 1 whose J observation rows
-//    per env fit the LDS with h1, h2, mu and the biases, whose partial sums
-//    (J * NT1 accumulator registers per matrix wave) leave room for a ring
-//    of at least 16 fragments in 192 registers, and whose price rows (8 J
-//    registers) fit beside the indicator chunks (4 IPL) in the env waves'
-//    budget of 80;
+//    per env fit the LDS with h1, h2, mu, the biases and log sigma,
+//    whose partial sums (J * NT1 accumulator registers per matrix wave)
+//    leave room for a ring of at least 16 fragments in 192 registers, and
+//    whose price rows (8 J registers) fit beside the indicator chunks
+//    (4 IPL) in the env waves' budget of 92;
 //  - R, the ring depth: the largest in 16 .. 24 that divides the period of
 //    fragments (every fragment then has a fixed ring slot).
 template <int NS, int NI, int H>
@@ -849,7 +856,7 @@ struct Pick {
     {
         auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
         return al((size_t)J * MB * (KS1 * 32 + 8) * 2) + 2 * al((size_t)MB * (NT * 16 + 8) * 2) +
-               al((size_t)MB * (NT3 * 16 + 4) * 4) + al((size_t)(2 * NT + NT3) * 16 * 4);
+               al((size_t)MB * (NT3 * 16 + 4) * 4) + al(((size_t)(2 * NT + NT3) * 16 + 2 * RL * SPR) * 4);
     }
     template <int J>
     static constexpr int ring()
@@ -863,7 +870,7 @@ struct Pick {
     template <int J>
     static constexpr bool fits()
     {
-        return lds(J) <= LDS_LIMIT && J * NT <= 128 && 4 * IPL + 8 * J <= 80 && ring<J>() > 0;
+        return lds(J) <= LDS_LIMIT && J * NT <= 128 && 4 * IPL + 8 * J <= 92 && ring<J>() > 0;
     }
     static constexpr int J = fits<3>() ? 3 : (fits<2>() ? 2 : (fits<1>() ? 1 : 0));
     static_assert(J > 0, "no launch configuration fits this shape");
