@@ -117,6 +117,14 @@ def test_bf16_actor_of_another_shape():
     _run_case(W.get_config("dow30").with_(dtype="bf16"), 21, 120, rows=2521)
 
 
+def test_bf16_100_stock_actor_outside_the_role_split_shapes():
+    # unequal hidden widths (512-256) on the 100 x 8 market: the generic
+    # MFMA kernel takes it, with the same results contract
+    cfg = W.get_config("nasdaq100").with_(hidden=(512, 256))
+    pb = _run_case(cfg, 21, 30, rows=20 * 390 + 1)
+    assert tp.rollout_path(pb.mkt, pb.actor) == 0
+
+
 def test_deterministic_and_resumable():
     """Two identical runs are bitwise equal; rollout(L) equals rollout(j)
     followed by rollout(L-j, step0=j) from the saved state."""
