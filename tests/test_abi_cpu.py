@@ -144,6 +144,21 @@ def test_argument_errors_without_gpu():
     assert L.tp_rollout(C.byref(m), C.byref(cfg), C.byref(st), C.byref(a2), x, 1 << 30,
                         1, 0, 10, C.byref(tr), None) == tp.TP_EINVAL
     assert "match the market" in tp.last_error()
+    # empty inputs: no envs, or a rollout of no steps
+    st0 = tp.EnvState(x, x, x, 0)
+    assert L.tp_rollout(C.byref(m), C.byref(cfg), C.byref(st0), C.byref(a), x, 1 << 30,
+                        1, 0, 10, C.byref(tr), None) == tp.TP_EINVAL
+    assert "state.E" in tp.last_error()
+    assert L.tp_env_step(C.byref(m), C.byref(cfg), C.byref(st0), x, x, None, 0, 0, None) == tp.TP_EINVAL
+    assert L.tp_rollout(C.byref(m), C.byref(cfg), C.byref(st), C.byref(a), x, 1 << 30,
+                        1, 0, 0, C.byref(tr), None) == tp.TP_EINVAL
+    assert "L = 0" in tp.last_error()
+    # the largest market: n * n_ind = 1024 accepted, 1025 refused
+    big = tp.Market(x, x, 100, 128, 8)
+    too_big = tp.Market(x, x, 100, 125, 9)
+    ab = _nasdaq_actor(dims=(1 + 256 + 1024, 128, 128, 128))
+    assert L.tp_rollout_path(C.byref(big), C.byref(ab)) == 0
+    assert L.tp_rollout_path(C.byref(too_big), C.byref(ab)) == tp.TP_EUNSUPPORTED
 
 
 def _critic(dims=(1001, 512, 512), dtype=tp.TP_BF16, A=1, epa=4096):

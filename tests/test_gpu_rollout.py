@@ -117,6 +117,15 @@ def test_bf16_actor_of_another_shape():
     _run_case(W.get_config("dow30").with_(dtype="bf16"), 21, 120, rows=2521)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_largest_market(dtype):
+    # 128 stocks x 8 indicators (n * n_ind = 1024, the largest market the
+    # boundary takes; 1281 inputs) on the generic kernel, fp32 and bf16
+    cfg = W.get_config("tiny").with_(n=128, n_ind=8, dtype=dtype, hidden=(128, 128))
+    pb = _run_case(cfg, 20, 40)
+    assert tp.rollout_path(pb.mkt, pb.actor) == 0
+
+
 def test_bf16_100_stock_actor_outside_the_role_split_shapes():
     # unequal hidden widths (512-256) on the 100 x 8 market: the generic
     # MFMA kernel takes it, with the same results contract
