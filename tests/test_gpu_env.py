@@ -14,8 +14,15 @@ from paper_2111_05188_amd import problem, tp
 pytestmark = pytest.mark.gpu
 
 
+# the largest market the boundary takes: 128 stocks x 8 indicators
+_EXTRA = {
+    "largest_f32": W.get_config("tiny").with_(name="largest_f32", n=128, n_ind=8),
+    "largest_bf16": W.get_config("tiny").with_(name="largest_bf16", n=128, n_ind=8, dtype="bf16"),
+}
+
+
 def _setup(name, E, rows, seed):
-    cfg = W.get_config(name)
+    cfg = _EXTRA[name] if name in _EXTRA else W.get_config(name)
     mk = W.make_market(cfg, rows=(0, rows))
     rng = np.random.default_rng(seed)
     cash = np.concatenate([rng.uniform(0, 2e6, E - E // 4), rng.uniform(0, 200, E // 4)])
@@ -28,6 +35,7 @@ def _setup(name, E, rows, seed):
 
 
 @pytest.mark.parametrize("name,E,rows", [("tiny", 64, 257), ("tiny", 37, 257),
+                                         ("largest_f32", 40, 257), ("largest_bf16", 33, 257),
                                          ("dow30", 1000, 2521),
                                          ("nasdaq100", 515, 5000)])
 def test_env_step_teacher_forced(name, E, rows):
