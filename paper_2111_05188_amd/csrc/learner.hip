@@ -52,7 +52,7 @@ enum Epi : int {
     EPI_TANH = 0,   // h = tanh(acc + bias[col]) -> out[row][col], outT[col][row] (elem)
     EPI_BIAS = 1,   // out[row][col] = acc + bias[col]                   (fp32)
     EPI_GRAD = 2,   // gradient rows: row < gsplit -> g0, else g1; cols < gcols (fp32)
-    EPI_DTANH = 3,  // v = acc (1 - h[row][col]^2) -> out, outT            (elem)
+    EPI_DTANH = 3,  // v = acc (1 - h^2), h = hsrc[col][row] -> out, outT   (elem)
 };
 
 struct GemmProb {
@@ -70,7 +70,7 @@ struct GemmProb {
     float *g0, *g1;
     int64_t ldg;
     int gsplit, gcols;
-    const void *hsrc;
+    const void *hsrc;   // EPI_DTANH: the layer's activations, transposed ([col][row], 8-byte reads)
     int64_t ldh;
     int tiles_n, tile0;
 };
@@ -94,8 +94,10 @@ __device__ __forceinline__ bool gemm_slot(const GemmBatch &gb, int &agent, int &
     const int b = blockIdx.x, per = gridDim.x / 8;
     const int v = gb.na == 1 ? b : (b % 8) * per + b / 8;
     if (v >= gb.tiles * gb.na) return false;
-    agent = v / gb.tiles;
-    t = v % gb.tiles;
+    // uniform, but a division by a runtime value is computed on the vector
+    // unit: move the results to scalar registers
+    agent = __builtin_amdgcn_readfirstlane(v / gb.tiles);
+    t = __builtin_amdgcn_readfirstlane(v % gb.tiles);
     return true;
 }
 
@@ -169,7 +171,7 @@ __device__ __forceinline__ void epi4(const GemmProb &P, int row0, int col, const
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = min(row0 + i, P.M - 1);
-            const float y = (float)hs[(size_t)r * P.ldh + col];
+            const float y = (float)hs[(size_t)col * P.ldh + r];
             h[i] = to_elem<BF>(v[i] * (1.0f - y * y));
         }
     }
@@ -308,7 +310,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmBatch gb)
     const int pi = find_prob(gb, t);
     const GemmProb P = agent_prob(gb, pi, agent);
     t -= P.tile0;
-    const int tn = t % P.tiles_n, tm = t / P.tiles_n;
+    const int tn = __builtin_amdgcn_readfirstlane(t % P.tiles_n);
+    const int tm = __builtin_amdgcn_readfirstlane(t / P.tiles_n);
     const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
     const int m0 = tm * GT + (wave >> 1) * 32, n0 = tn * GT + (wave & 1) * 32;
     const int r16 = lane & 15, kq = lane >> 4;
@@ -362,6 +365,112 @@ typedef uint32_t v4u_t __attribute__((ext_vector_type(4)));
 
 constexpr int LWAVES = 8;              // waves per workgroup: 2 (rows) x 4 (columns)
 constexpr int LTHREADS = LWAVES * WAVE;
+
+// Epilogues staged through LDS.  In the MFMA layout a lane holds four rows
+// of one column, so stores straight from the accumulators give each
+// instruction 16 separate 32-byte pieces of bf16 (64-byte pieces of the
+// fp32 gradient rows).  Instead the fragments go into a 64 x 64 block in
+// LDS (row-major and transposed), and a group of G threads stores whole
+// rows of it: 128 contiguous bytes per bf16 row, 256 per fp32 row, 16
+// bytes a thread where the output's rows are 16-byte aligned, else one
+// element a thread, a row per 64 threads.  Same values as epi4, same bits.
+constexpr int ER = 64 + 8;   // LDS row of a staged bf16 block (elements)
+constexpr int EF = 64 + 4;   // LDS row of a staged fp32 block (floats)
+constexpr int STAGE_BYTES = 2 * 64 * ER * 2;   // one block: T and R (F is smaller)
+
+__device__ __forceinline__ bool rows16(const void *p, int64_t ld, int es)
+{
+    return (uintptr_t)p % 16 == 0 && (ld * es) % 16 == 0;
+}
+
+// Fragment piece (rows lr .. lr + 3, column lc of the block; global row0,
+// col) into the staged block: the gradient rows' fp32 values into F, or
+// the bf16 activation (EPI_TANH) or its pre-activation gradient
+// (EPI_DTANH) into R (row-major) and T (transposed).
+__device__ __forceinline__ void stage4(const GemmProb &P, const floatx4 &a, int row0, int col,
+                                       int lr, int lc, void *blk)
+{
+    if (P.mode == EPI_GRAD) {
+        float *F = (float *)blk;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) F[(lr + e) * EF + lc] = a[e];
+        return;
+    }
+    __bf16 *T = (__bf16 *)blk, *R = T + 64 * ER;
+    col = min(col, P.N - 1);   // columns past N are staged but never stored
+    __bf16 h[4];
+    if (P.mode == EPI_TANH) {
+        const float b = col < P.bsplit ? P.bias0[col] : P.bias1[col - P.bsplit];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) h[e] = to_bf16(fast_tanh(a[e] + b));
+    } else {
+        const __bf16 *hs = (const __bf16 *)P.hsrc + (size_t)col * P.ldh;
+        bf16x4 y4;
+        if (row0 + 3 < P.M) y4 = *(const bf16x4 *)(hs + row0);
+        else
+#pragma unroll
+            for (int e = 0; e < 4; ++e) y4[e] = hs[min(row0 + e, P.M - 1)];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float y = (float)y4[e];
+            h[e] = to_bf16(a[e] * (1.0f - y * y));
+        }
+    }
+    *(bf16x4 *)(T + lc * ER + lr) = bf16x4{h[0], h[1], h[2], h[3]};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) R[(lr + e) * ER + lc] = h[e];
+}
+
+// Threads gt = 0 .. G - 1 store the staged block of rows bm .., columns
+// bn .. (after a barrier that covers every write of stage4).
+template <int G>
+__device__ __forceinline__ void store_staged(const GemmProb &P, const void *blk, int bm, int bn,
+                                             int gt)
+{
+    const int nrow = min(64, P.M - bm);
+    if (P.mode == EPI_GRAD) {
+        const float *F = (const float *)blk;
+        const int ncol = min(64, min(P.N, P.gcols) - bn);
+        if (nrow <= 0 || ncol <= 0) return;
+        auto dst = [&](int r) {
+            const int gr = bm + r;
+            return gr < P.gsplit ? P.g0 + (size_t)gr * P.ldg : P.g1 + (size_t)(gr - P.gsplit) * P.ldg;
+        };
+        if (nrow == 64 && ncol == 64 && rows16(P.g0, P.ldg, 4) &&
+            (P.gsplit >= P.M || rows16(P.g1, P.ldg, 4))) {
+#pragma unroll
+            for (int s = 0; s < 1024 / G; ++s) {
+                const int r = (s * G + gt) / 16, c4 = (gt % 16) * 4;
+                *(floatx4 *)(dst(r) + bn + c4) = *(const floatx4 *)(F + r * EF + c4);
+            }
+        } else {
+            const int c = gt % 64;
+            for (int r = gt / 64; r < nrow; r += G / 64)
+                if (c < ncol) dst(r)[bn + c] = F[r * EF + c];
+        }
+        return;
+    }
+    const __bf16 *T = (const __bf16 *)blk, *R = T + 64 * ER;
+    const int ncol = min(64, P.N - bn);
+    if (nrow <= 0 || ncol <= 0) return;
+    const bool full = nrow == 64 && ncol == 64;
+    // block row (or column) x, 16-byte piece p8 of it
+    auto put = [&](__bf16 *o, int64_t ld, const __bf16 *src, int nx, int ny) {
+        if (full && rows16(o, ld, 2)) {
+#pragma unroll
+            for (int s = 0; s < 512 / G; ++s) {
+                const int x = (s * G + gt) / 8, p8 = (gt % 8) * 8;
+                *(v4u_t *)(o + (size_t)x * ld + p8) = *(const v4u_t *)(src + x * ER + p8);
+            }
+        } else {
+            const int y = gt % 64;
+            for (int x = gt / 64; x < nx; x += G / 64)
+                if (y < ny) o[(size_t)x * ld + y] = src[x * ER + y];
+        }
+    };
+    if (P.out) put((__bf16 *)P.out + (size_t)bm * P.ldo + bn, P.ldo, R, nrow, ncol);
+    if (P.outT) put((__bf16 *)P.outT + (size_t)bn * P.ldt + bm, P.ldt, T, ncol, nrow);
+}
 
 // Chunk loop: LTHREADS threads move a 64 x 128 chunk of A and one of B
 // (thread t: rows (t / 16) + 32 j, 16-byte piece t % 16); wave (wm, wn)
@@ -442,7 +551,8 @@ __global__ __launch_bounds__(LTHREADS, 2) void gemm_lds_kernel(GemmBatch gb)
     const int pi = find_prob(gb, t);
     const GemmProb P = agent_prob(gb, pi, agent);
     t -= P.tile0;
-    const int tn = t % P.tiles_n, tm = t / P.tiles_n;
+    const int tn = __builtin_amdgcn_readfirstlane(t % P.tiles_n);
+    const int tm = __builtin_amdgcn_readfirstlane(t / P.tiles_n);
     const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
     const int m0 = tm * GT, n0 = tn * GT;
     const int r16 = lane & 15, kq = lane >> 4;
@@ -459,11 +569,24 @@ __global__ __launch_bounds__(LTHREADS, 2) void gemm_lds_kernel(GemmBatch gb)
     default: break;   // the launcher routes other K to gemm_bf16_kernel
     }
     const int wm = m0 + (wave >> 2) * 32, wn = n0 + (wave & 3) * 16;
+    if (P.mode == EPI_BIAS) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const float v[4] = {acc[i][0], acc[i][1], acc[i][2], acc[i][3]};
-        epi4<true>(P, wm + i * 16 + kq * 4, wn + r16, v);
+        for (int i = 0; i < 2; ++i) {
+            const float v[4] = {acc[i][0], acc[i][1], acc[i][2], acc[i][3]};
+            epi4<true>(P, wm + i * 16 + kq * 4, wn + r16, v);
+        }
+        return;
     }
+    static_assert(STAGE_BYTES <= sizeof(smem), "the staged block fits");
+    // the eight waves stage the 64 x 64 tile in LDS (free once every wave has
+    // passed this barrier) and store it together
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+        stage4(P, acc[i], wm + i * 16 + kq * 4, wn + r16, wm - m0 + i * 16 + kq * 4, wn - n0 + r16,
+               smem);
+    __syncthreads();
+    store_staged<LTHREADS>(P, smem, m0, n0, threadIdx.x);
 }
 
 // Launches with many tiles (several agents): 128 x 128 workgroup tiles of
@@ -566,7 +689,8 @@ __global__ __launch_bounds__(256, 2) void gemm_big_kernel(GemmBatch gb)
     const int pi = find_prob(gb, t);
     const GemmProb P = agent_prob(gb, pi, agent);
     t -= P.tile0;
-    const int tn = t % P.tiles_n, tm = t / P.tiles_n;
+    const int tn = __builtin_amdgcn_readfirstlane(t % P.tiles_n);
+    const int tm = __builtin_amdgcn_readfirstlane(t / P.tiles_n);
     const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
     const int m0 = tm * BT, n0 = tn * BT;
     const int r16 = lane & 15, kq = lane >> 4;
@@ -586,13 +710,33 @@ __global__ __launch_bounds__(256, 2) void gemm_big_kernel(GemmBatch gb)
     }
     __builtin_amdgcn_sched_barrier(0);
     const int wm = m0 + (wave >> 1) * 64, wn = n0 + (wave & 1) * 64;
+    if (P.mode == EPI_BIAS) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+                epi4<true>(P, wm + i * 16 + kq * 4, wn + j * 16 + r16, v);
+            }
+        return;
+    }
+    // each wave stages its 64 x 64 block in LDS (free once every wave has
+    // passed this barrier: the last chunk's fragment reads are done) and
+    // stores it
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));   // keep these lane terms out of the chunk loop's live set
+    const int el = tid % WAVE, ew = tid / WAVE;
+    static_assert(4 * STAGE_BYTES <= sizeof(smem) && 64 * EF * 4 <= STAGE_BYTES, "staged blocks fit");
+    void *blk = (char *)smem + ew * STAGE_BYTES;
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-            epi4<true>(P, wm + i * 16 + kq * 4, wn + j * 16 + r16, v);
-        }
+        for (int j = 0; j < 4; ++j)
+            stage4(P, acc[i][j], wm + i * 16 + (el >> 4) * 4, wn + j * 16 + (el & 15),
+                   i * 16 + (el >> 4) * 4, j * 16 + (el & 15), blk);
+    __syncthreads();
+    store_staged<WAVE>(P, blk, wm, wn, el);
 }
 
 // fp32: 16x16 threads, each a 4x4 block of the 64x64 tile; k-slices of 16
@@ -606,7 +750,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmBatch gb)
     const int pi = find_prob(gb, t);
     const GemmProb P = agent_prob(gb, pi, agent);
     t -= P.tile0;
-    const int tn = t % P.tiles_n, tm = t / P.tiles_n;
+    const int tn = __builtin_amdgcn_readfirstlane(t % P.tiles_n);
+    const int tm = __builtin_amdgcn_readfirstlane(t / P.tiles_n);
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
     const float *A = (const float *)P.A, *B = (const float *)P.B;
     // loader: row lr = tid / 4 of the tile, k-quad lq = tid % 4
@@ -1561,8 +1706,8 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             g3.g0 = grad + L.oW3;
             g3.ldg = L.H2;
             GemmProb b3 = prob(dMU, L.n_pad, W(L.wW3t), L.n_pad, B, L.H2, L.n_pad, EPI_DTANH);
-            b3.hsrc = H2;
-            b3.ldh = L.H2;
+            b3.hsrc = H2t;
+            b3.ldh = B;
             b3.out = dZ2;
             b3.ldo = L.H2;
             b3.outT = dZ2t;
@@ -1571,8 +1716,8 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             gc2.g0 = grad + L.oWc2;
             gc2.ldg = L.C1;
             GemmProb bc2 = prob(dZc2, L.C2, W(L.wWc2t), L.C2, B, L.C1, L.C2, EPI_DTANH);
-            bc2.hsrc = at(H1, L.H1);
-            bc2.ldh = L.HC1;
+            bc2.hsrc = at(H1t, (size_t)L.H1 * B);
+            bc2.ldh = B;
             bc2.outT = at(dZ1t, (size_t)L.H1 * B);
             bc2.ldt = B;
             if ((e = run_gemms(bf, ag, {g3, b3, gc2, bc2}, s)) != hipSuccess) return e;
@@ -1583,8 +1728,8 @@ hipError_t launch_ppo_update(const PpoArgs &a, hipStream_t s)
             g2.g0 = grad + L.oW2;
             g2.ldg = L.H1;
             GemmProb b2 = prob(dZ2, L.H2, W(L.wW2t), L.H2, B, L.H1, L.H2, EPI_DTANH);
-            b2.hsrc = H1;
-            b2.ldh = L.HC1;
+            b2.hsrc = H1t;
+            b2.ldh = B;
             b2.outT = dZ1t;
             b2.ldt = B;
             if ((e = run_gemms(bf, ag, {g2, b2}, s)) != hipSuccess) return e;
