@@ -589,25 +589,31 @@ __global__ __launch_bounds__(LTHREADS, 2) void gemm_lds_kernel(GemmBatch gb)
     store_staged<LTHREADS>(P, smem, m0, n0, threadIdx.x);
 }
 
-// Launches with many tiles (several agents): 128 x 128 workgroup tiles of
-// four 64 x 64 waves, k-chunks of 64 staged through LDS.  A wave's 4 x 4
-// tiles of 16 x 16 use each fragment four times, 0.5 KiB of LDS reads per
-// MFMA against 1.5 KiB in the eight-wave kernel above, whose reads exceed
-// the LDS bandwidth once every CU is busy.  Rows padded by 32 bytes
-// (measured faster than 16; two workgroups fill the 160 KiB of LDS).
-constexpr int BT = 128;               // workgroup tile (rows and columns)
+// Launches with many tiles (several agents): 256 x 128 workgroup tiles of
+// eight 64 x 64 waves, k-chunks of 64 staged through LDS, one workgroup per
+// CU.  A wave's 4 x 4 tiles of 16 x 16 use each fragment four times, 0.5 KiB
+// of LDS reads per MFMA against 1.5 KiB in the eight-wave kernel above,
+// whose reads exceed the LDS bandwidth once every CU is busy.  The operand
+// loads bound this kernel (timing copies without them run 8% faster per
+// update, without the MFMAs no faster): 256 x 128 loads 48 KiB per chunk
+// for the work two 128 x 128 workgroups load 64 KiB for (measured 2% faster
+// per update).  Rows padded by 32 bytes (measured faster than 16).
+constexpr int BT = 128;               // workgroup tile: columns (rows of B)
+constexpr int BM = 256;               // workgroup tile: rows (rows of A)
+constexpr int BWAVES = 8;             // a 4 x 2 grid of 64 x 64 waves
+constexpr int BTHREADS = BWAVES * WAVE;
 #ifndef GEMM_BPAD
 #define GEMM_BPAD 16                  // LDS row padding (bf16 elements)
 #endif
 constexpr int BBK = 64;               // k per chunk
 constexpr int BROW = BBK + GEMM_BPAD; // padded LDS row (bf16)
-constexpr int BTILE = BT * BROW;      // one operand's chunk (bf16)
+constexpr int BBUF = (BM + BT) * BROW;   // one chunk of A and B (bf16)
 constexpr int BIG_MIN_TILES = 512;    // launches with fewer 128 x 128 tiles keep 64 x 64
 
-// Chunk loop: 256 threads move a 128 x 64 chunk of A and one of B (thread
-// t: rows (t / 8) + 32 j, 16-byte piece t % 8; a wave instruction reads
-// 8 rows x 128 contiguous bytes); wave (wm, wn) multiplies rows 64 wm ..
-// +63 by columns 64 wn .. +63.
+// Chunk loop: 512 threads move a 256 x 64 chunk of A and a 128 x 64 chunk
+// of B (thread t: rows (t / 8) + 64 j, 16-byte piece t % 8; a wave
+// instruction reads 8 rows x 128 contiguous bytes); wave (wm, wn)
+// multiplies rows 64 wm .. +63 by columns 64 wn .. +63.
 template <int NC>
 __device__ __forceinline__ void big_kloop(const __bf16 *const ga, const __bf16 *const gb,
                                           int64_t lda, int64_t ldb, int Mr, int Nr,
@@ -615,43 +621,42 @@ __device__ __forceinline__ void big_kloop(const __bf16 *const ga, const __bf16 *
 {
     const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
     const int r16 = lane & 15, kq = lane >> 4;
+    constexpr int RS = BTHREADS / 8, JA = BM / RS, JB = BT / RS;
     const int lrow = tid >> 3, lpiece = tid & 7;
-    const __bf16 *la[4], *lb[4];
+    const __bf16 *la[JA], *lb[JB];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        la[j] = ga + (size_t)min(lrow + 32 * j, Mr - 1) * lda + lpiece * 8;
-        lb[j] = gb + (size_t)min(lrow + 32 * j, Nr - 1) * ldb + lpiece * 8;
-    }
+    for (int j = 0; j < JA; ++j) la[j] = ga + (size_t)min(lrow + RS * j, Mr - 1) * lda + lpiece * 8;
+#pragma unroll
+    for (int j = 0; j < JB; ++j) lb[j] = gb + (size_t)min(lrow + RS * j, Nr - 1) * ldb + lpiece * 8;
     constexpr int D = NC < GEMM_LD ? NC : GEMM_LD;   // chunks in flight in registers
-    v4u_t ra[D][4], rb[D][4];
-    auto load = [&](v4u_t (&xa)[4], v4u_t (&xb)[4], int c) {
+    v4u_t ra[D][JA], rb[D][JB];
+    auto load = [&](v4u_t (&xa)[JA], v4u_t (&xb)[JB], int c) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            xa[j] = *(const v4u_t *)(la[j] + c * BBK);
-            xb[j] = *(const v4u_t *)(lb[j] + c * BBK);
-        }
+        for (int j = 0; j < JA; ++j) xa[j] = *(const v4u_t *)(la[j] + c * BBK);
+#pragma unroll
+        for (int j = 0; j < JB; ++j) xb[j] = *(const v4u_t *)(lb[j] + c * BBK);
     };
-    auto store = [&](const v4u_t (&xa)[4], const v4u_t (&xb)[4], int buf) {
-        __bf16 *As = smem + buf * 2 * BTILE, *Bs = As + BTILE;
+    auto store = [&](const v4u_t (&xa)[JA], const v4u_t (&xb)[JB], int buf) {
+        __bf16 *As = smem + buf * BBUF, *Bs = As + BM * BROW;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            *(v4u_t *)(As + (lrow + 32 * j) * BROW + lpiece * 8) = xa[j];
-            *(v4u_t *)(Bs + (lrow + 32 * j) * BROW + lpiece * 8) = xb[j];
-        }
+        for (int j = 0; j < JA; ++j) *(v4u_t *)(As + (lrow + RS * j) * BROW + lpiece * 8) = xa[j];
+#pragma unroll
+        for (int j = 0; j < JB; ++j) *(v4u_t *)(Bs + (lrow + RS * j) * BROW + lpiece * 8) = xb[j];
     };
     static_for<0, D>([&](auto c) { load(ra[c], rb[c], c); });
     store(ra[0], rb[0], 0);
     if constexpr (D < NC) load(ra[0], rb[0], D);
     __syncthreads();
     const int am = (wave >> 1) * 64, bn = (wave & 1) * 64;
-    // Per chunk c: read its fragments (both k-steps); store chunk c + 1 into
-    // the other LDS buffer (free since the last barrier: chunk c - 1's
-    // reads completed before it) and issue the load of chunk c + 1 + D;
-    // then the MFMAs, which overlap the stores and the second k-step's
-    // reads; one barrier.
+    // Per chunk c: read its fragments (both k-steps) and run its MFMAs; then
+    // store chunk c + 1 into the other LDS buffer (free since the last
+    // barrier: chunk c - 1's reads completed before it) and issue the load of
+    // chunk c + 1 + D; one barrier.  With the stores after the MFMAs, a
+    // chunk's loads have the MFMAs' time to land (measured 1% faster than
+    // storing between the reads and the MFMAs).
     static_for<0, NC>([&](auto c) {
         constexpr int buf = c & 1;
-        const __bf16 *As = smem + buf * 2 * BTILE, *Bs = As + BTILE;
+        const __bf16 *As = smem + buf * BBUF, *Bs = As + BM * BROW;
         bf16x8 fa[BBK / 32][4], fb[BBK / 32][4];
 #pragma unroll
         for (int q = 0; q < BBK / 32; ++q)
@@ -660,12 +665,6 @@ __device__ __forceinline__ void big_kloop(const __bf16 *const ga, const __bf16 *
                 fa[q][i] = *(const bf16x8 *)(As + (am + i * 16 + r16) * BROW + q * 32 + kq * 8);
                 fb[q][i] = *(const bf16x8 *)(Bs + (bn + i * 16 + r16) * BROW + q * 32 + kq * 8);
             }
-        if constexpr (c + 1 < NC) {
-            // chunk c + 1 sits in register set (c + 1) % D; refill it with c + 1 + D
-            constexpr int slot = (c + 1) % D;
-            store(ra[slot], rb[slot], (c + 1) & 1);
-            if constexpr (c + 1 + D < NC) load(ra[slot], rb[slot], c + 1 + D);
-        }
 #pragma unroll
         for (int q = 0; q < BBK / 32; ++q) {
             __builtin_amdgcn_sched_barrier(0);
@@ -677,13 +676,21 @@ __device__ __forceinline__ void big_kloop(const __bf16 *const ga, const __bf16 *
                                                                         acc[i][j], 0, 0, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
+        if constexpr (c + 1 < NC) {
+            // chunk c + 1 sits in register set (c + 1) % D; refill it with c + 1 + D
+            constexpr int slot = (c + 1) % D;
+            store(ra[slot], rb[slot], (c + 1) & 1);
+            if constexpr (c + 1 + D < NC) load(ra[slot], rb[slot], c + 1 + D);
+        }
+        __builtin_amdgcn_sched_barrier(0);
         if constexpr (c + 1 < NC) __syncthreads();
     });
 }
 
-__global__ __launch_bounds__(256, 2) void gemm_big_kernel(GemmBatch gb)
+__global__ __launch_bounds__(BTHREADS, 1) void gemm_big_kernel(GemmBatch gb)
 {
-    __shared__ __attribute__((aligned(16))) __bf16 smem[2 * 2 * BTILE];
+    constexpr int SM0 = 2 * BBUF, SM1 = BWAVES * STAGE_BYTES / 2;   // bf16 elements
+    __shared__ __attribute__((aligned(16))) __bf16 smem[SM0 > SM1 ? SM0 : SM1];
     int agent, t;
     if (!gemm_slot(gb, agent, t)) return;
     const int pi = find_prob(gb, t);
@@ -692,7 +699,7 @@ __global__ __launch_bounds__(256, 2) void gemm_big_kernel(GemmBatch gb)
     const int tn = __builtin_amdgcn_readfirstlane(t % P.tiles_n);
     const int tm = __builtin_amdgcn_readfirstlane(t / P.tiles_n);
     const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-    const int m0 = tm * BT, n0 = tn * BT;
+    const int m0 = tm * BM, n0 = tn * BT;
     const int r16 = lane & 15, kq = lane >> 4;
     const __bf16 *ga = (const __bf16 *)P.A + (size_t)m0 * P.lda;
     const __bf16 *gbp = (const __bf16 *)P.B + (size_t)n0 * P.ldb;
@@ -726,7 +733,7 @@ __global__ __launch_bounds__(256, 2) void gemm_big_kernel(GemmBatch gb)
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));   // keep these lane terms out of the chunk loop's live set
     const int el = tid % WAVE, ew = tid / WAVE;
-    static_assert(4 * STAGE_BYTES <= sizeof(smem) && 64 * EF * 4 <= STAGE_BYTES, "staged blocks fit");
+    static_assert(BWAVES * STAGE_BYTES <= sizeof(smem) && 64 * EF * 4 <= STAGE_BYTES, "staged blocks fit");
     void *blk = (char *)smem + ew * STAGE_BYTES;
     __syncthreads();
 #pragma unroll
@@ -1494,7 +1501,8 @@ hipError_t run_gemms(bool bf, const Agents &ag, std::initializer_list<GemmProb> 
     gb.aws = ag.aws;
     gb.aprm = ag.aprm;
     // kernel choice: bf16 products with K in {128, 512, 1024} go through
-    // LDS, in 128 x 128 tiles when the launch has enough of them
+    // LDS, in 256 x 128 tiles when the launch has at least BIG_MIN_TILES
+    // tiles' worth of 128 x 128
     bool staged = bf, big = bf;
     int tiles_big = 0;
     for (const GemmProb &p : ps) {
@@ -1505,19 +1513,19 @@ hipError_t run_gemms(bool bf, const Agents &ag, std::initializer_list<GemmProb> 
         tiles_big += cdiv(p.M, BT) * cdiv(p.N, BT);
     }
     big = big && tiles_big * ag.n >= BIG_MIN_TILES;
-    const int T = big ? BT : GT;
+    const int TN = big ? BT : GT, TM = big ? BM : GT;
     int tiles = 0;
     for (const GemmProb &p : ps) {
         GemmProb q = p;
-        q.tiles_n = cdiv(q.N, T);
+        q.tiles_n = cdiv(q.N, TN);
         q.tile0 = tiles;
-        tiles += q.tiles_n * cdiv(q.M, T);
+        tiles += q.tiles_n * cdiv(q.M, TM);
         gb.p[gb.np++] = q;
     }
     gb.tiles = tiles;
     gb.na = ag.n;
     const dim3 grid(8 * cdiv(tiles * ag.n, 8));
-    if (big) hipLaunchKernelGGL(gemm_big_kernel, grid, dim3(256), 0, s, gb);
+    if (big) hipLaunchKernelGGL(gemm_big_kernel, grid, dim3(BTHREADS), 0, s, gb);
     else if (staged) hipLaunchKernelGGL(gemm_lds_kernel, grid, dim3(LTHREADS), 0, s, gb);
     else if (bf) hipLaunchKernelGGL(gemm_bf16_kernel, grid, dim3(256), 0, s, gb);
     else hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, gb);
