@@ -329,3 +329,61 @@ def test_critic_widths_other_than_the_actors(dtype):
     _, _, _, _, g_o = ppo.update(flat.astype(np.float64), np.zeros(P), np.zeros(P), 1, dims,
                                  batch, bf16=bf)
     _check_grad(dims, grad.cpu().numpy(), g_o, GRAD_TOL[dtype], f"critic 96-32 {dtype}")
+
+
+def test_partial_column_blocks_in_staged_products():
+    """A second actor layer 480 wide (1001-512-480-100 bf16 with a 512-512
+    critic, batch 512): the forward of layer 2 and the first backward group
+    take the LDS-staged product kernels, and their 480 columns end in a
+    32-wide block, which the staged epilogue stores element by element.  One
+    learner (64 x 64 tiles) is compared with the oracle per element; 16
+    learners in one call (256 x 128 tiles for those launches) must give the
+    single call's bits, parameters and moments included."""
+    cfg = W.get_config("nasdaq100")
+    S, H1, _, n = cfg.dims
+    dims = (S, H1, 480, n, H1, H1)
+    rows, B, A = 2048, 512, 16
+    rng = np.random.default_rng(91)
+    parts = []
+    for name, shape in ppo.layout(*dims):
+        if name == "log_std":
+            parts.append(np.full(shape, -0.5))
+        elif len(shape) == 2:
+            parts.append(rng.uniform(-1, 1, shape) / np.sqrt(shape[1]))
+        else:
+            parts.append(rng.uniform(-0.1, 0.1, shape))
+    flat = np.concatenate([p.reshape(-1) for p in parts]).astype(np.float32)
+    obs, action, adv, ret, which = W.make_learner_data(cfg, rows)
+    obs_t = torch.from_numpy(obs).to(torch.bfloat16)
+    obs_vals = obs_t.float().numpy()
+    p = ppo.unflatten(flat.astype(np.float64), dims)
+    f = ppo.forward(p, obs_vals[:, :S], bf16=True)
+    logp = (ppo.log_prob(action, f["mu"], p["log_std"])
+            - np.asarray(W.LOG_RATIO_OFFSETS)[which]).astype(np.float32)
+    c = tp.ppo_cfg(dims, tp.TP_BF16, B)
+    P = tp.ppo_param_count(c)
+    assert P == flat.shape[0]
+    idx = rng.choice(rows, B, replace=False)
+    dev = [torch.from_numpy(x).cuda() for x in (action, logp, adv, ret)]
+    say(f"[ppo] 1001-512-480-100 bf16, 512-512 critic, B={B}, P={P}, one learner then {A}")
+    prm = torch.from_numpy(flat.copy()).cuda()
+    m, v = torch.zeros(P, device="cuda"), torch.zeros(P, device="cuda")
+    grad = torch.empty(P, device="cuda")
+    tp.ppo_update(c, prm, m, v, 1, obs_t.cuda(), *dev, torch.from_numpy(idx[None]).cuda(),
+                  tp.ppo_workspace(c), grad=grad)
+    torch.cuda.synchronize()
+    batch = ppo.gather(obs_vals, action, logp, adv, ret, idx, S)
+    _, _, _, _, g_o = ppo.update(flat.astype(np.float64), np.zeros(P), np.zeros(P), 1, dims,
+                                 batch, bf16=True)
+    _check_grad(dims, grad.cpu().numpy(), g_o, GRAD_TOL["bf16"], "1001-512-480-100 bf16")
+    # the same minibatch for every learner: each must reproduce the single call
+    pa = torch.from_numpy(np.tile(flat, (A, 1))).cuda()
+    ma, va = torch.zeros(A, P, device="cuda"), torch.zeros(A, P, device="cuda")
+    ga = torch.empty(A, P, device="cuda")
+    tp.ppo_update_agents(c, pa, ma, va, 1, obs_t.cuda(), *dev,
+                         torch.from_numpy(np.tile(idx, (A, 1, 1))).cuda(),
+                         tp.ppo_workspace(c, n_agents=A), grad=ga)
+    torch.cuda.synchronize()
+    for a in range(A):
+        assert torch.equal(ga[a], grad), a
+        assert torch.equal(pa[a], prm) and torch.equal(ma[a], m) and torch.equal(va[a], v), a
