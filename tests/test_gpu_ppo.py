@@ -202,16 +202,17 @@ def test_minimal_batch_and_rollout_rows():
 
 
 @pytest.mark.parametrize("name,rows,B,A", [("tiny", 512, 64, 3), ("nasdaq100", 4096, 1024, 3),
-                                            ("nasdaq100", 4096, 1024, 8)])
+                                            ("nasdaq100", 4096, 1024, 8),
+                                            ("nasdaq100", 4096, 1024, 11)])
 def test_agents_in_one_call_equal_single_calls(name, rows, B, A):
     """tp_ppo_update_agents: A agents with their own parameters, moments
     and minibatches, laid out with a stride wider than P, give bit for bit
     what A tp_ppo_update calls give (two updates, so the second reads
     moments the first wrote); the padding between agents is left alone.
-    With eight 1001-512-512-100 agents the launches with at least 512
-    tiles of 128 x 128 (layer 1, the first backward group, the weight
-    gradient of layer 1) run the 128 x 128 product kernel, which keeps the
-    k order of the 64 x 64 one, so the bits still agree."""
+    With eight or eleven 1001-512-512-100 agents the launches with at
+    least 512 tiles' worth of 128 x 128 run the 256 x 128 product kernel,
+    which keeps the k order of the 64 x 64 one, so the bits still agree;
+    eleven agents leave padding slots in its XCD-aware dealing."""
     cfg = W.get_config(name)
     dims, bf, c, host, dev = _setup(cfg, rows, B)
     P = tp.ppo_param_count(c)
